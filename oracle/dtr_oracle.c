@@ -1,0 +1,750 @@
+/*
+ * dtr_oracle.c -- plain, slow, CPU reference of Dynamic Tensor
+ * Rematerialization's greedy eviction loop (Kirisame et al., ICLR 2021).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library.  It shares no code,
+ * header, table or helper with the GPU path; the two meet only in the input
+ * arrays produced by the workload generators.
+ *
+ * What it computes, step by step in the paper's order:
+ *   - operator call (Section 2, Figure 1 prose; Appendix C.4
+ *     "(Re)materialization"): lock every input, rematerialize evicted inputs
+ *     recursively through their parent operation, allocate the output
+ *     (evicting while memory is insufficient), advance the clock by the
+ *     operator cost, unlock;
+ *   - eviction (Appendix C.4 "Eviction and banishing"): the evictable pool is
+ *     resident storages with no locks (Appendix C.1); the lowest score is
+ *     evicted (Appendix C.4 "Runtime state");
+ *   - eager eviction on deallocation (Section 2 "Deallocation";
+ *     Appendix C.5 "Banishing and eager eviction");
+ *   - heuristics of Section 4.1 and Appendix C.3: h_DTR with the exact
+ *     evicted neighbourhood e* (Appendix C.2), h_DTR^eq with the union-find
+ *     relaxation and its split approximation (Appendix C.2), h_DTR^local,
+ *     h_LRU, h_size, h_rand; plus h_{e*} of Appendix A.3 (no staleness);
+ *   - output condition: tensors the program still holds at the end are
+ *     rematerialized and locked (Appendix C.6 log semantics).
+ *
+ * No caching, no incremental data structure beyond the paper's own
+ * union-find: every eviction rescans every tensor and every h_DTR score
+ * walks its evicted neighbourhood from scratch.  Native recursion.
+ *
+ * Readings where the paper is silent (each is also a documented design
+ * decision of the build): ties on score go to the smaller tensor id; the
+ * clock is in integer cost units and last_access is stamped before the clock
+ * advances, so staleness is >= 1 for every candidate; the pool excludes
+ * constants; dead (released) tensors stay in the graph as evicted nodes and
+ * count in e* and in union-find components; h_rand draws a fresh 64-bit
+ * value per (seed, budget-eviction number, tensor id) from the SplitMix64
+ * finaliser; the clock guard stops a simulation once the clock reaches 2^40.
+ *
+ * All quantities are integers; scores N/D are compared exactly by 128-bit
+ * cross-multiplication.
+ */
+#define _GNU_SOURCE
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#include <pthread.h>
+
+#define O_FLAG_CONSTANT 1u
+#define O_FLAG_REQUIRED 2u
+
+enum { ST_UNCOMPUTED = 0, ST_RESIDENT = 1, ST_EVICTED = 2 };
+enum { OH_DTR = 0, OH_EQ = 1, OH_LOCAL = 2, OH_LRU = 3, OH_SIZE = 4, OH_RAND = 5, OH_ESTAR = 6 };
+enum { OS_OK = 0, OS_OOM = 1, OS_CLOCK_OVERFLOW = 2, OS_STOPPED = 100 };
+
+#define CLOCK_LIMIT ((int64_t)1 << 40)
+
+typedef unsigned __int128 u128;
+
+/* one trace, as handed over by the caller (arrays are borrowed) */
+typedef struct {
+    int32_t n_tensors, n_ops;
+    const int64_t *tensor_size;
+    const uint8_t *tensor_flags;
+    const int32_t *op_output;
+    const int64_t *op_cost;
+    const int64_t *op_input_offsets;
+    const int32_t *op_inputs;
+} oracle_trace;
+
+typedef struct { int32_t trace, heuristic; int64_t budget; uint64_t seed; } oracle_spec;
+
+/* result fields (int64 each) */
+enum {
+    R_TOTAL_COST, R_BASE_COST, R_REMAT_COST, R_PEAK, R_FINAL_MEM, R_EXECUTED, R_REMATS,
+    R_EVICTIONS, R_EAGER, R_SCORES, R_NBR_VISITS, R_ADJ_VISITS, R_STATUS, R_FAILED_OP, R_NFIELDS
+};
+
+/* optional probes used by tests */
+typedef struct {
+    int64_t stop_after_op;        /* >=0: stop once this op (incl. its releases) is done */
+    int64_t stop_at_eviction;     /* >=0: stop at the start of this budget-eviction decision */
+    uint8_t *state_out;           /* [n_tensors] state at the stop point (or at the end) */
+    int32_t *locks_out;           /* [n_tensors] */
+    int64_t *last_out;            /* [n_tensors] */
+    uint64_t *score_n_out;        /* [n_tensors] N of each candidate at stop_at_eviction */
+    uint64_t *score_d_lo_out;     /* [n_tensors] low 64 bits of D */
+    uint64_t *score_d_hi_out;     /* [n_tensors] high 64 bits of D */
+    uint8_t *candidate_out;       /* [n_tensors] 1 if in the pool at stop_at_eviction */
+    int64_t *clock_out;           /* [1] clock at the stop point */
+    int32_t *evict_log;           /* budget-evicted ids in order */
+    int64_t evict_log_cap;
+    int64_t *evict_log_len;
+    int32_t *remat_log;           /* rematerialized ids in order */
+    int64_t remat_log_cap;
+    int64_t *remat_log_len;
+    int64_t *uf_cost_sum_out;     /* [1] sum of running costs over union-find roots */
+} oracle_probe;
+
+/* ---------------------------------------------------------------- graph -- */
+
+typedef struct {
+    const oracle_trace *tr;
+    int32_t *producer;       /* op producing tensor t, -1 for constants            */
+    int64_t *c0;             /* cost of the producing op (0 for constants)         */
+    int64_t *ch_off;         /* children(t): outputs of ops that read t            */
+    int32_t *ch;
+    int64_t *rel_off;        /* tensors released after op o, ascending id          */
+    int32_t *rel;
+} graph;
+
+static void graph_free(graph *g)
+{
+    free(g->producer); free(g->c0); free(g->ch_off); free(g->ch); free(g->rel_off); free(g->rel);
+}
+
+/* parents(t) = inputs of t's parent operation (Appendix C.2 "Data dependencies");
+ * children(t) = tensors whose parent operation reads t (the dependents, deps^T);
+ * a tensor whose last external reference goes away after op o is released
+ * after o (reference counting, Appendix A.2) unless it is a constant or a
+ * required output. */
+static int graph_build(graph *g, const oracle_trace *tr)
+{
+    int32_t n = tr->n_tensors, F = tr->n_ops;
+    memset(g, 0, sizeof(*g));
+    g->tr = tr;
+    g->producer = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    g->c0 = calloc((size_t)(n > 0 ? n : 1), sizeof(int64_t));
+    g->ch_off = calloc((size_t)n + 1, sizeof(int64_t));
+    g->rel_off = calloc((size_t)F + 1, sizeof(int64_t));
+    int64_t E = tr->op_input_offsets[F];
+    g->ch = malloc(sizeof(int32_t) * (size_t)(E > 0 ? E : 1));
+    g->rel = malloc(sizeof(int32_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *last = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t *fill = malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    if (!g->producer || !g->c0 || !g->ch_off || !g->rel_off || !g->ch || !g->rel || !last || !fill) {
+        free(last); free(fill); graph_free(g); return -1;
+    }
+    for (int32_t t = 0; t < n; t++) { g->producer[t] = -1; last[t] = -1; }
+    for (int32_t o = 0; o < F; o++) {
+        int32_t t = tr->op_output[o];
+        g->producer[t] = o;
+        g->c0[t] = tr->op_cost[o];
+        if (last[t] < o) last[t] = o;
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
+            int32_t u = tr->op_inputs[e];
+            g->ch_off[u + 1]++;
+            if (last[u] < o) last[u] = o;
+        }
+    }
+    for (int32_t t = 0; t < n; t++) g->ch_off[t + 1] += g->ch_off[t];
+    for (int32_t t = 0; t < n; t++) fill[t] = g->ch_off[t];
+    for (int32_t o = 0; o < F; o++)
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
+            int32_t u = tr->op_inputs[e];
+            g->ch[fill[u]++] = tr->op_output[o];
+        }
+    /* release lists: ascending id within an op */
+    for (int32_t t = 0; t < n; t++) {
+        if (tr->tensor_flags[t] & (O_FLAG_CONSTANT | O_FLAG_REQUIRED)) continue;
+        if (last[t] >= 0) g->rel_off[last[t] + 1]++;
+    }
+    for (int32_t o = 0; o < F; o++) g->rel_off[o + 1] += g->rel_off[o];
+    int64_t *rfill = malloc(sizeof(int64_t) * (size_t)(F > 0 ? F : 1));
+    if (!rfill) { free(last); free(fill); graph_free(g); return -1; }
+    for (int32_t o = 0; o < F; o++) rfill[o] = g->rel_off[o];
+    for (int32_t t = 0; t < n; t++) {   /* ascending t gives ascending ids per list */
+        if (tr->tensor_flags[t] & (O_FLAG_CONSTANT | O_FLAG_REQUIRED)) continue;
+        if (last[t] >= 0) g->rel[rfill[last[t]]++] = t;
+    }
+    free(rfill); free(last); free(fill);
+    return 0;
+}
+
+/* ------------------------------------------------------------ simulator -- */
+
+typedef struct {
+    const graph *g;
+    const oracle_trace *tr;
+    int heuristic;
+    int64_t budget;
+    uint64_t seed;
+
+    uint8_t *state;
+    int32_t *locks;
+    int64_t *last_access;
+    int64_t clock, memory, peak;
+    int64_t r[R_NFIELDS];
+    int64_t eviction_no;          /* budget evictions so far (h_rand key) */
+    int stopped;
+    int64_t cur_op;
+
+    /* union-find over evicted components (h_DTR^eq), Appendix C.2 */
+    int32_t *node_of;             /* current UF node of each tensor     */
+    int32_t *uf_parent;
+    int64_t *uf_cost;
+    int64_t *uf_mark;             /* epoch stamps per UF node (root dedup) */
+    int64_t uf_n, uf_cap;
+
+    /* scratch for neighbourhood walks */
+    int64_t *mark;                /* epoch stamps */
+    int64_t epoch;
+    int32_t *queue;
+
+    oracle_probe *probe;
+} sim;
+
+static int32_t uf_new(sim *s)
+{
+    if (s->uf_n == s->uf_cap) {
+        int64_t cap = s->uf_cap ? 2 * s->uf_cap : 1024;
+        int32_t *p = realloc(s->uf_parent, sizeof(int32_t) * (size_t)cap);
+        if (!p) return -1;
+        s->uf_parent = p;
+        int64_t *c = realloc(s->uf_cost, sizeof(int64_t) * (size_t)cap);
+        if (!c) return -1;
+        s->uf_cost = c;
+        int64_t *m = realloc(s->uf_mark, sizeof(int64_t) * (size_t)cap);
+        if (!m) return -1;
+        memset(m + s->uf_cap, 0, sizeof(int64_t) * (size_t)(cap - s->uf_cap));
+        s->uf_mark = m;
+        s->uf_cap = cap;
+    }
+    int32_t id = (int32_t)s->uf_n++;
+    s->uf_parent[id] = id;
+    s->uf_cost[id] = 0;
+    return id;
+}
+
+static int32_t uf_find(sim *s, int32_t x)
+{
+    int32_t root = x;
+    while (s->uf_parent[root] != root) root = s->uf_parent[root];
+    while (s->uf_parent[x] != root) {          /* path compression */
+        int32_t next = s->uf_parent[x];
+        s->uf_parent[x] = root;
+        x = next;
+    }
+    return root;
+}
+
+static int32_t uf_union(sim *s, int32_t a, int32_t b)
+{
+    a = uf_find(s, a);
+    b = uf_find(s, b);
+    if (a == b) return a;
+    s->uf_parent[b] = a;
+    s->uf_cost[a] += s->uf_cost[b];
+    return a;
+}
+
+static void lock(sim *s, int32_t t) { s->locks[t]++; }
+static void unlock(sim *s, int32_t t) { s->locks[t]--; }
+
+static int is_evictable(const sim *s, int32_t t)
+{
+    return s->state[t] == ST_RESIDENT && s->locks[t] == 0 &&
+           !(s->tr->tensor_flags[t] & O_FLAG_CONSTANT);
+}
+
+/* Exact evicted neighbourhood e*(x) (Appendix C.2): evicted tensors reachable
+ * from x through evicted parents only (ancestors), together with evicted
+ * tensors reachable through evicted children only (descendants).  Returns the
+ * sum of their local costs; the set size goes to *count. */
+static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
+{
+    const graph *g = s->g;
+    const oracle_trace *tr = s->tr;
+    int64_t sum = 0, cnt = 0;
+    s->epoch++;
+    /* ancestors */
+    int64_t head = 0, tail = 0;
+    s->queue[tail++] = x;
+    while (head < tail) {
+        int32_t u = s->queue[head++];
+        int32_t o = g->producer[u];
+        if (o < 0) continue;
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
+            int32_t p = tr->op_inputs[e];
+            if (s->state[p] != ST_EVICTED || s->mark[p] == s->epoch) continue;
+            s->mark[p] = s->epoch;
+            sum += g->c0[p];
+            cnt++;
+            s->queue[tail++] = p;
+        }
+    }
+    /* descendants */
+    head = tail = 0;
+    s->queue[tail++] = x;
+    while (head < tail) {
+        int32_t u = s->queue[head++];
+        for (int64_t e = g->ch_off[u]; e < g->ch_off[u + 1]; e++) {
+            int32_t c = g->ch[e];
+            if (s->state[c] != ST_EVICTED || s->mark[c] == s->epoch) continue;
+            s->mark[c] = s->epoch;
+            sum += g->c0[c];
+            cnt++;
+            s->queue[tail++] = c;
+        }
+    }
+    *count = cnt;
+    return sum;
+}
+
+/* Relaxed neighbourhood cost (Appendix C.2): the union of the union-find sets
+ * of x's evicted parents and evicted children, each distinct set counted once,
+ * merged only for the query (no union is performed). */
+static int64_t eq_cost(sim *s, int32_t x, int64_t *count)
+{
+    const graph *g = s->g;
+    const oracle_trace *tr = s->tr;
+    int64_t sum = 0, cnt = 0;
+    s->epoch++;
+    int32_t o = g->producer[x];
+    if (o >= 0)
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
+            int32_t p = tr->op_inputs[e];
+            if (s->state[p] != ST_EVICTED) continue;
+            cnt++;
+            int32_t r = uf_find(s, s->node_of[p]);
+            if (s->uf_mark[r] == s->epoch) continue;
+            s->uf_mark[r] = s->epoch;
+            sum += s->uf_cost[r];
+        }
+    for (int64_t e = g->ch_off[x]; e < g->ch_off[x + 1]; e++) {
+        int32_t c = g->ch[e];
+        if (s->state[c] != ST_EVICTED) continue;
+        cnt++;
+        int32_t r = uf_find(s, s->node_of[c]);
+        if (s->uf_mark[r] == s->epoch) continue;
+        s->uf_mark[r] = s->epoch;
+        sum += s->uf_cost[r];
+    }
+    *count = cnt;
+    return sum;
+}
+
+static int64_t degree(const sim *s, int32_t x)
+{
+    int32_t o = s->g->producer[x];
+    int64_t d = s->g->ch_off[x + 1] - s->g->ch_off[x];
+    if (o >= 0) d += s->tr->op_input_offsets[o + 1] - s->tr->op_input_offsets[o];
+    return d;
+}
+
+/* SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): state advanced by the
+ * golden-ratio gamma, then the variant-13 output mix. */
+static uint64_t splitmix64_mix(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+/* score N/D of candidate x (Section 4.1 and Appendix C.3; h_{e*} from A.3) */
+static void score(sim *s, int32_t x, uint64_t *N, u128 *D)
+{
+    int64_t stale = s->clock - s->last_access[x];   /* >= 1 by construction */
+    int64_t m = s->tr->tensor_size[x];
+    int64_t c0 = s->g->c0[x];
+    int64_t cnt = 0;
+    if (stale < 1) abort();
+    switch (s->heuristic) {
+    case OH_DTR:
+        *N = (uint64_t)(c0 + estar_cost(s, x, &cnt));
+        *D = (u128)(uint64_t)m * (u128)(uint64_t)stale;
+        s->r[R_NBR_VISITS] += cnt;
+        s->r[R_ADJ_VISITS] += degree(s, x);
+        break;
+    case OH_ESTAR:
+        *N = (uint64_t)(c0 + estar_cost(s, x, &cnt));
+        *D = (u128)(uint64_t)m;
+        s->r[R_NBR_VISITS] += cnt;
+        s->r[R_ADJ_VISITS] += degree(s, x);
+        break;
+    case OH_EQ:
+        *N = (uint64_t)(c0 + eq_cost(s, x, &cnt));
+        *D = (u128)(uint64_t)m * (u128)(uint64_t)stale;
+        s->r[R_NBR_VISITS] += cnt;
+        s->r[R_ADJ_VISITS] += degree(s, x);
+        break;
+    case OH_LOCAL:
+        *N = (uint64_t)c0;
+        *D = (u128)(uint64_t)m * (u128)(uint64_t)stale;
+        break;
+    case OH_LRU:
+        *N = 1;
+        *D = (u128)(uint64_t)stale;
+        break;
+    case OH_SIZE:
+        *N = 1;
+        *D = (u128)(uint64_t)m;
+        break;
+    case OH_RAND: {
+        uint64_t key = ((uint64_t)s->eviction_no << 32) + (uint64_t)(uint32_t)x;
+        *N = splitmix64_mix(s->seed + 0x9E3779B97F4A7C15ull * key);
+        *D = 1;
+        break;
+    }
+    default:
+        abort();
+    }
+}
+
+/* a strictly better than b: N_a/D_a < N_b/D_b, ties to the smaller id */
+static int better(uint64_t na, u128 da, int32_t ia, uint64_t nb, u128 db, int32_t ib)
+{
+    u128 l = (u128)na * db, r = (u128)nb * da;
+    if (l != r) return l < r;
+    return ia < ib;
+}
+
+static void evict(sim *s, int32_t v, int eager)
+{
+    s->state[v] = ST_EVICTED;
+    s->memory -= s->tr->tensor_size[v];
+    if (eager) s->r[R_EAGER]++;
+    else s->r[R_EVICTIONS]++;
+    if (s->heuristic == OH_EQ) {
+        /* add c0(v) to its component, then union with every evicted neighbour */
+        int32_t r = uf_find(s, s->node_of[v]);
+        s->uf_cost[r] += s->g->c0[v];
+        int32_t o = s->g->producer[v];
+        if (o >= 0)
+            for (int64_t e = s->tr->op_input_offsets[o]; e < s->tr->op_input_offsets[o + 1]; e++) {
+                int32_t p = s->tr->op_inputs[e];
+                if (s->state[p] == ST_EVICTED) r = uf_union(s, r, s->node_of[p]);
+            }
+        for (int64_t e = s->g->ch_off[v]; e < s->g->ch_off[v + 1]; e++) {
+            int32_t c = s->g->ch[e];
+            if (s->state[c] == ST_EVICTED) r = uf_union(s, r, s->node_of[c]);
+        }
+    }
+}
+
+static void dump_state(sim *s)
+{
+    oracle_probe *p = s->probe;
+    if (!p) return;
+    int32_t n = s->tr->n_tensors;
+    if (p->state_out) memcpy(p->state_out, s->state, (size_t)n);
+    if (p->locks_out) memcpy(p->locks_out, s->locks, sizeof(int32_t) * (size_t)n);
+    if (p->last_out) memcpy(p->last_out, s->last_access, sizeof(int64_t) * (size_t)n);
+    if (p->clock_out) p->clock_out[0] = s->clock;
+    if (p->uf_cost_sum_out) {
+        int64_t sum = 0;
+        for (int64_t i = 0; i < s->uf_n; i++)
+            if (s->uf_parent[i] == (int32_t)i) sum += s->uf_cost[i];
+        p->uf_cost_sum_out[0] = sum;
+    }
+}
+
+/* while memory is insufficient, evict the lowest-scored evictable tensor */
+static void allocate(sim *s, int64_t size)
+{
+    int32_t n = s->tr->n_tensors;
+    while (s->memory + size > s->budget) {
+        oracle_probe *p = s->probe;
+        int dumping = p && p->stop_at_eviction >= 0 && s->eviction_no == p->stop_at_eviction;
+        int32_t best = -1;
+        uint64_t bn = 0;
+        u128 bd = 0;
+        int64_t count = 0;
+        for (int32_t x = 0; x < n; x++) {
+            if (!is_evictable(s, x)) continue;
+            uint64_t N;
+            u128 D;
+            score(s, x, &N, &D);
+            count++;
+            if (dumping) {
+                if (p->score_n_out) p->score_n_out[x] = N;
+                if (p->score_d_lo_out) p->score_d_lo_out[x] = (uint64_t)D;
+                if (p->score_d_hi_out) p->score_d_hi_out[x] = (uint64_t)(D >> 64);
+                if (p->candidate_out) p->candidate_out[x] = 1;
+            }
+            if (best < 0 || better(N, D, x, bn, bd, best)) { best = x; bn = N; bd = D; }
+        }
+        if (dumping) { dump_state(s); s->stopped = OS_STOPPED; s->r[R_STATUS] = OS_STOPPED; return; }
+        if (best < 0) { s->r[R_STATUS] = OS_OOM; s->stopped = OS_OOM; return; }
+        s->r[R_SCORES] += count;
+        if (p && p->evict_log && *p->evict_log_len < p->evict_log_cap)
+            p->evict_log[(*p->evict_log_len)++] = best;
+        evict(s, best, 0);
+        s->eviction_no++;
+    }
+}
+
+/* run op o producing t: stamp last_access, advance the clock by the op cost */
+static void execute(sim *s, int32_t o, int32_t t, int remat)
+{
+    const oracle_trace *tr = s->tr;
+    for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
+        s->last_access[tr->op_inputs[e]] = s->clock;
+    s->last_access[t] = s->clock;
+    int64_t c = tr->op_cost[o];
+    s->clock += c;
+    s->r[R_TOTAL_COST] += c;
+    s->r[R_EXECUTED]++;
+    if (remat) { s->r[R_REMATS]++; s->r[R_REMAT_COST] += c; }
+    else s->r[R_BASE_COST] += c;
+    s->memory += tr->tensor_size[t];
+    if (s->memory > s->peak) s->peak = s->memory;
+    s->state[t] = ST_RESIDENT;
+    if (s->heuristic == OH_EQ) {
+        if (remat) {
+            /* split approximation: subtract c0 from the old set, move t to a fresh empty set */
+            int32_t r = uf_find(s, s->node_of[t]);
+            s->uf_cost[r] -= s->g->c0[t];
+        }
+        int32_t nd = uf_new(s);
+        if (nd < 0) abort();
+        s->node_of[t] = nd;
+    }
+    if (s->clock >= CLOCK_LIMIT) { s->r[R_STATUS] = OS_CLOCK_OVERFLOW; s->stopped = OS_CLOCK_OVERFLOW; }
+}
+
+/* rematerialize evicted u by replaying its parent operation (recursive) */
+static void remat(sim *s, int32_t u)
+{
+    const oracle_trace *tr = s->tr;
+    int32_t o = s->g->producer[u];
+    oracle_probe *p = s->probe;
+    if (p && p->remat_log && *p->remat_log_len < p->remat_log_cap)
+        p->remat_log[(*p->remat_log_len)++] = u;
+    for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
+        lock(s, tr->op_inputs[e]);
+    for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
+        int32_t q = tr->op_inputs[e];
+        if (s->state[q] == ST_EVICTED) {
+            remat(s, q);
+            if (s->stopped) return;
+        }
+    }
+    allocate(s, tr->tensor_size[u]);
+    if (s->stopped) return;
+    execute(s, o, u, 1);
+    if (s->stopped) return;
+    for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
+        unlock(s, tr->op_inputs[e]);
+}
+
+static void sim_run(sim *s)
+{
+    const oracle_trace *tr = s->tr;
+    const graph *g = s->g;
+    int32_t n = tr->n_tensors;
+    s->r[R_FAILED_OP] = -1;
+    s->cur_op = 0;
+    /* constants: resident from time 0, never evictable */
+    for (int32_t t = 0; t < n; t++) {
+        if (!(tr->tensor_flags[t] & O_FLAG_CONSTANT)) continue;
+        s->state[t] = ST_RESIDENT;
+        s->memory += tr->tensor_size[t];
+        if (s->memory > s->peak) s->peak = s->memory;
+    }
+    if (s->memory > s->budget) { s->r[R_STATUS] = OS_OOM; s->stopped = OS_OOM; goto done; }
+
+    for (int32_t o = 0; o < tr->n_ops; o++) {
+        s->cur_op = o;
+        int32_t t = tr->op_output[o];
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
+            lock(s, tr->op_inputs[e]);
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
+            int32_t u = tr->op_inputs[e];
+            if (s->state[u] == ST_EVICTED) {
+                remat(s, u);
+                if (s->stopped) goto done;
+            }
+        }
+        allocate(s, tr->tensor_size[t]);
+        if (s->stopped) goto done;
+        execute(s, o, t, 0);
+        if (s->stopped) goto done;
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
+            unlock(s, tr->op_inputs[e]);
+        for (int64_t e = g->rel_off[o]; e < g->rel_off[o + 1]; e++) {
+            int32_t r = g->rel[e];
+            if (is_evictable(s, r)) evict(s, r, 1);
+        }
+        if (s->probe && s->probe->stop_after_op == o) {
+            dump_state(s);
+            s->stopped = OS_STOPPED;
+            s->r[R_STATUS] = OS_STOPPED;
+            goto done;
+        }
+    }
+    /* output condition: every required output resident (and held) at the end */
+    s->cur_op = tr->n_ops;
+    for (int32_t t = 0; t < n; t++) {
+        if (!(tr->tensor_flags[t] & O_FLAG_REQUIRED)) continue;
+        lock(s, t);
+        if (s->state[t] == ST_EVICTED) {
+            remat(s, t);
+            if (s->stopped) goto done;
+        }
+    }
+    dump_state(s);
+done:
+    if (s->stopped == OS_OOM || s->stopped == OS_CLOCK_OVERFLOW) s->r[R_FAILED_OP] = s->cur_op;
+    s->r[R_PEAK] = s->peak;
+    s->r[R_FINAL_MEM] = s->memory;
+}
+
+static int run_one(const oracle_trace *tr, const graph *g, const oracle_spec *sp,
+                   int64_t *result, oracle_probe *probe)
+{
+    int32_t n = tr->n_tensors;
+    sim s;
+    memset(&s, 0, sizeof(s));
+    s.g = g;
+    s.tr = tr;
+    s.heuristic = sp->heuristic;
+    s.budget = sp->budget;
+    s.seed = sp->seed;
+    s.probe = probe;
+    size_t nn = (size_t)(n > 0 ? n : 1);
+    s.state = calloc(nn, 1);
+    s.locks = calloc(nn, sizeof(int32_t));
+    s.last_access = calloc(nn, sizeof(int64_t));
+    s.node_of = malloc(sizeof(int32_t) * nn);
+    s.queue = malloc(sizeof(int32_t) * nn);
+    s.mark = calloc(nn, sizeof(int64_t));
+    int rc = 0;
+    if (!s.state || !s.locks || !s.last_access || !s.node_of || !s.queue || !s.mark) rc = -1;
+    else {
+        for (int32_t t = 0; t < n; t++) s.node_of[t] = -1;
+        sim_run(&s);
+        for (int i = 0; i < R_NFIELDS; i++) result[i] = s.r[i];
+    }
+    free(s.state); free(s.locks); free(s.last_access); free(s.node_of); free(s.queue); free(s.mark);
+    free(s.uf_parent); free(s.uf_cost); free(s.uf_mark);
+    return rc;
+}
+
+/* ------------------------------------------------------------ public API -- */
+
+/* Deep rematerialization chains recurse once per level, so every simulation
+ * runs on a worker thread with a large stack. */
+#define WORKER_STACK ((size_t)512 << 20)
+
+typedef struct {
+    const oracle_trace *traces;
+    const graph *graphs;
+    const oracle_spec *specs;
+    int64_t *results;
+    oracle_probe *probe;
+    int32_t n_sims;
+    int32_t next;                 /* shared cursor */
+    pthread_mutex_t mu;
+    int rc;
+} batch;
+
+static void *worker(void *arg)
+{
+    batch *b = arg;
+    for (;;) {
+        pthread_mutex_lock(&b->mu);
+        int32_t i = b->next++;
+        pthread_mutex_unlock(&b->mu);
+        if (i >= b->n_sims) break;
+        const oracle_spec *sp = &b->specs[i];
+        int rc = run_one(&b->traces[sp->trace], &b->graphs[sp->trace], sp,
+                         b->results + (int64_t)i * R_NFIELDS, b->probe);
+        if (rc) { pthread_mutex_lock(&b->mu); b->rc = rc; pthread_mutex_unlock(&b->mu); }
+    }
+    return NULL;
+}
+
+int oracle_result_fields(void) { return R_NFIELDS; }
+
+/* Run n_sims simulations over n_traces traces on n_threads threads.
+ * results: int64 [n_sims * oracle_result_fields()].  probe may be NULL; with a
+ * probe, n_sims must be 1.  Returns 0, or -1 on allocation failure, -2 on a
+ * bad argument. */
+int oracle_run(const oracle_trace *traces, int32_t n_traces, const oracle_spec *specs,
+               int32_t n_sims, int64_t *results, int32_t n_threads, oracle_probe *probe)
+{
+    if (n_traces < 0 || n_sims < 0 || (probe && n_sims != 1)) return -2;
+    for (int32_t i = 0; i < n_sims; i++)
+        if (specs[i].trace < 0 || specs[i].trace >= n_traces || specs[i].heuristic < 0 ||
+            specs[i].heuristic > OH_ESTAR)
+            return -2;
+    graph *graphs = calloc((size_t)(n_traces > 0 ? n_traces : 1), sizeof(graph));
+    if (!graphs) return -1;
+    int rc = 0;
+    int32_t built = 0;
+    for (; built < n_traces; built++)
+        if (graph_build(&graphs[built], &traces[built])) { rc = -1; break; }
+    if (rc == 0) {
+        batch b;
+        memset(&b, 0, sizeof(b));
+        b.traces = traces; b.graphs = graphs; b.specs = specs; b.results = results;
+        b.probe = probe; b.n_sims = n_sims;
+        pthread_mutex_init(&b.mu, NULL);
+        if (n_threads < 1) n_threads = 1;
+        if (n_threads > n_sims) n_threads = n_sims > 0 ? n_sims : 1;
+        pthread_t *th = calloc((size_t)n_threads, sizeof(pthread_t));
+        pthread_attr_t attr;
+        pthread_attr_init(&attr);
+        pthread_attr_setstacksize(&attr, WORKER_STACK);
+        int started = 0;
+        for (int i = 0; th && i < n_threads; i++)
+            if (pthread_create(&th[i], &attr, worker, &b) == 0) started++;
+        if (started == 0) rc = -1;
+        for (int i = 0; i < started; i++) pthread_join(th[i], NULL);
+        pthread_attr_destroy(&attr);
+        pthread_mutex_destroy(&b.mu);
+        free(th);
+        if (b.rc) rc = b.rc;
+    }
+    for (int32_t i = 0; i < built; i++) graph_free(&graphs[i]);
+    free(graphs);
+    return rc;
+}
+
+/* Test hook: exact evicted-neighbourhood cost of x under a given state vector
+ * (0 uncomputed, 1 resident, 2 evicted).  Returns sum of c0 over e*(x) and
+ * writes |e*(x)| to *count and the membership to member_out (optional). */
+int64_t oracle_estar(const oracle_trace *tr, const uint8_t *state, int32_t x, int64_t *count,
+                     uint8_t *member_out)
+{
+    graph g;
+    if (graph_build(&g, tr)) return -1;
+    sim s;
+    memset(&s, 0, sizeof(s));
+    s.g = &g;
+    s.tr = tr;
+    size_t nn = (size_t)(tr->n_tensors > 0 ? tr->n_tensors : 1);
+    s.state = malloc(nn);
+    s.mark = calloc(nn, sizeof(int64_t));
+    s.queue = malloc(sizeof(int32_t) * nn);
+    int64_t sum = -1;
+    if (s.state && s.mark && s.queue) {
+        memcpy(s.state, state, (size_t)tr->n_tensors);
+        sum = estar_cost(&s, x, count);
+        if (member_out)
+            for (int32_t t = 0; t < tr->n_tensors; t++) member_out[t] = (s.mark[t] == s.epoch);
+    }
+    free(s.state); free(s.mark); free(s.queue);
+    graph_free(&g);
+    return sum;
+}
+
+/* Test hook: the SplitMix64 draw used by h_rand for (seed, eviction number, id). */
+uint64_t oracle_rand_key(uint64_t seed, int64_t eviction_no, int32_t x)
+{
+    uint64_t key = ((uint64_t)eviction_no << 32) + (uint64_t)(uint32_t)x;
+    return splitmix64_mix(seed + 0x9E3779B97F4A7C15ull * key);
+}

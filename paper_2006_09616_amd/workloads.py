@@ -1,0 +1,520 @@
+"""Seeded synthetic operator traces and simulation batches for the DTR eviction loop.
+
+This module only builds *programs*: operators with input tensor ids, integer
+output sizes and integer compute costs, plus flags (constant, required output).
+It holds no part of the eviction method itself.  The one derived quantity it
+computes is a program's natural peak memory when every tensor is freed right
+after its last use (reference counting, no eviction), because the workloads
+space their memory budgets as fractions of that peak.
+
+Both the HIP path and the CPU oracle consume exactly these arrays, so the
+floating-point draws used for sizes (log-normal) cannot break parity: they are
+taken once, here, and rounded to integers.
+
+Trace model (single output per operator, as the method assumes in Section 2):
+  * tensors 0..n_tensors-1; operators 0..n_ops-1 in execution order;
+  * op o produces tensor ``op_output[o]`` from ``op_inputs[off[o]:off[o+1]]``;
+  * a tensor flagged CONSTANT has no producer and is resident from time 0;
+  * a tensor flagged REQUIRED_OUTPUT is never released and must be resident
+    when the program ends.
+
+The backward pass follows the gradient program of Appendix A (network
+definition): for each forward operator f_j, visited in reverse, the gradient
+operator reads f_j's inputs and the gradients of every operator that consumed
+f_j's output, and produces a gradient of the same size as that output.
+"""
+from __future__ import annotations
+
+import hashlib
+import math
+from dataclasses import dataclass, field
+
+import numpy as np
+
+FLAG_CONSTANT = 1
+FLAG_REQUIRED = 2
+
+# heuristic ids (shared numbering with the C-ABI; the numbers carry no arithmetic)
+H_DTR, H_EQ, H_LOCAL, H_LRU, H_SIZE, H_RAND, H_ESTAR = range(7)
+HEURISTIC_NAMES = ["dtr", "eq", "local", "lru", "size", "rand", "estar"]
+
+BUDGET_UNLIMITED = (1 << 63) - 1
+
+SPEC_DTYPE = np.dtype([("trace", "<i4"), ("heuristic", "<i4"),
+                       ("budget", "<i8"), ("seed", "<u8")])
+
+
+@dataclass
+class Trace:
+    name: str
+    tensor_size: np.ndarray        # int64 [n_tensors]
+    tensor_flags: np.ndarray       # uint8 [n_tensors]
+    op_output: np.ndarray          # int32 [n_ops]
+    op_cost: np.ndarray            # int64 [n_ops]
+    op_input_offsets: np.ndarray   # int64 [n_ops + 1]
+    op_inputs: np.ndarray          # int32 [n_edges]
+    meta: dict = field(default_factory=dict)
+
+    def __post_init__(self):
+        self.tensor_size = np.ascontiguousarray(self.tensor_size, dtype=np.int64)
+        self.tensor_flags = np.ascontiguousarray(self.tensor_flags, dtype=np.uint8)
+        self.op_output = np.ascontiguousarray(self.op_output, dtype=np.int32)
+        self.op_cost = np.ascontiguousarray(self.op_cost, dtype=np.int64)
+        self.op_input_offsets = np.ascontiguousarray(self.op_input_offsets, dtype=np.int64)
+        self.op_inputs = np.ascontiguousarray(self.op_inputs, dtype=np.int32)
+
+    @property
+    def n_tensors(self) -> int:
+        return int(self.tensor_size.shape[0])
+
+    @property
+    def n_ops(self) -> int:
+        return int(self.op_output.shape[0])
+
+    def inputs(self, o: int) -> np.ndarray:
+        return self.op_inputs[self.op_input_offsets[o]:self.op_input_offsets[o + 1]]
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for a in (self.tensor_size, self.tensor_flags, self.op_output, self.op_cost,
+                  self.op_input_offsets, self.op_inputs):
+            h.update(np.ascontiguousarray(a).tobytes())
+        return h.hexdigest()
+
+
+@dataclass
+class Workload:
+    name: str
+    traces: list
+    specs: np.ndarray              # SPEC_DTYPE [n_sims]
+    peaks: list                    # natural peak per trace
+    description: str = ""
+
+    @property
+    def n_sims(self) -> int:
+        return int(self.specs.shape[0])
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for t in self.traces:
+            h.update(t.digest().encode())
+        h.update(self.specs.tobytes())
+        return h.hexdigest()
+
+
+# ----------------------------------------------------------------------------
+# program construction helpers
+# ----------------------------------------------------------------------------
+
+def _csr(lists):
+    lens = np.fromiter((len(x) for x in lists), dtype=np.int64, count=len(lists))
+    off = np.zeros(len(lists) + 1, dtype=np.int64)
+    np.cumsum(lens, out=off[1:])
+    flat = np.fromiter((v for x in lists for v in x), dtype=np.int32, count=int(off[-1]))
+    return off, flat
+
+
+def _segment_gather(starts, lens):
+    """Indices of the concatenation of ranges [starts[i], starts[i]+lens[i])."""
+    lens = np.asarray(lens, dtype=np.int64)
+    total = int(lens.sum())
+    if total == 0:
+        return np.zeros(0, dtype=np.int64)
+    seg_off = np.zeros(len(lens), dtype=np.int64)
+    np.cumsum(lens[:-1], out=seg_off[1:])
+    return np.repeat(np.asarray(starts, dtype=np.int64) - seg_off, lens) + np.arange(total, dtype=np.int64)
+
+
+def with_backward(fwd_off, fwd_in, fwd_size, fwd_cost, bwd_cost, name="", meta=None):
+    """Forward program (tensor id == op index) followed by its gradient program.
+
+    Gradient operator for f_j (emitted for j = F-1 down to 0) reads
+    inputs(f_j) in their listed order, then the gradients of f_j's consumers
+    in ascending consumer order; it outputs a tensor of size(y_j).  Gradients
+    of nullary forward operators are the program's required outputs.
+    """
+    fwd_off = np.asarray(fwd_off, dtype=np.int64)
+    fwd_in = np.asarray(fwd_in, dtype=np.int64)
+    F = len(fwd_off) - 1
+    n_in = np.diff(fwd_off)
+    reader = np.repeat(np.arange(F, dtype=np.int64), n_in)          # consumer op of each edge
+    order = np.lexsort((reader, fwd_in))                            # by producer j, then consumer c
+    cons_c = reader[order]
+    n_cons = np.bincount(fwd_in, minlength=F).astype(np.int64)
+    cons_off = np.zeros(F + 1, dtype=np.int64)
+    np.cumsum(n_cons, out=cons_off[1:])
+
+    js = np.arange(F - 1, -1, -1, dtype=np.int64)                   # backward op b handles j = F-1-b
+    len1 = n_in[js]
+    len2 = n_cons[js]
+    blen = len1 + len2
+    boff = np.zeros(F + 1, dtype=np.int64)
+    np.cumsum(blen, out=boff[1:])
+    bin_ = np.empty(int(boff[-1]), dtype=np.int64)
+    pos1 = _segment_gather(boff[:-1], len1)
+    bin_[pos1] = fwd_in[_segment_gather(fwd_off[js], len1)]
+    pos2 = _segment_gather(boff[:-1] + len1, len2)
+    bin_[pos2] = F + (F - 1 - cons_c[_segment_gather(cons_off[js], len2)])
+
+    n = 2 * F
+    size = np.empty(n, dtype=np.int64)
+    size[:F] = fwd_size
+    size[F:] = np.asarray(fwd_size, dtype=np.int64)[js]
+    cost = np.empty(n, dtype=np.int64)
+    cost[:F] = fwd_cost
+    cost[F:] = bwd_cost
+    flags = np.zeros(n, dtype=np.uint8)
+    nullary = np.nonzero(n_in == 0)[0]
+    flags[F + (F - 1 - nullary)] |= FLAG_REQUIRED
+    off = np.concatenate([fwd_off, fwd_off[-1] + boff[1:]])
+    inp = np.concatenate([fwd_in, bin_]).astype(np.int32)
+    return Trace(name, size, flags, np.arange(n, dtype=np.int32), cost, off, inp,
+                 meta=dict(meta or {}, n_forward=F))
+
+
+def natural_peak(tr: Trace) -> int:
+    """Peak memory of the program when each tensor is freed right after its
+    last reader (or right after it is produced, if nothing reads it); constants
+    and required outputs are never freed.  No eviction is involved: this is the
+    program's own memory profile, used to space budgets."""
+    n, F = tr.n_tensors, tr.n_ops
+    last = np.full(n, -1, dtype=np.int64)
+    prod = np.full(n, -1, dtype=np.int64)
+    prod[tr.op_output] = np.arange(F)
+    reader = np.repeat(np.arange(F, dtype=np.int64), np.diff(tr.op_input_offsets))
+    np.maximum.at(last, tr.op_inputs.astype(np.int64), reader)
+    last = np.maximum(last, prod)
+    const = (tr.tensor_flags & FLAG_CONSTANT) != 0
+    keep = const | ((tr.tensor_flags & FLAG_REQUIRED) != 0)
+    freed = ~keep & (last >= 0)
+    free_at = np.zeros(F, dtype=np.int64)
+    np.add.at(free_at, last[freed], tr.tensor_size[freed])
+    alloc = tr.tensor_size[tr.op_output]
+    base = int(tr.tensor_size[const].sum())
+    before_free = base + np.cumsum(alloc) - np.concatenate([[0], np.cumsum(free_at)[:-1]])
+    return int(max(base, int(before_free.max()) if F else base))
+
+
+def linear_budgets(peak: int, lo_pct: int, hi_pct: int, k_count: int):
+    """k_count budgets linearly spaced from lo_pct% to hi_pct% of peak, each
+    rounded down, in exact integer arithmetic."""
+    if k_count == 1:
+        return [peak * hi_pct // 100]
+    den = 100 * (k_count - 1)
+    return [peak * (lo_pct * (k_count - 1) + (hi_pct - lo_pct) * k) // den for k in range(k_count)]
+
+
+def splitmix64(x: int) -> int:
+    """SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014): one
+    increment by the golden-ratio gamma, then the variant-13 finaliser.  Used
+    here only to derive per-tree seeds."""
+    m = (1 << 64) - 1
+    z = (x + 0x9E3779B97F4A7C15) & m
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & m
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & m
+    return z ^ (z >> 31)
+
+
+def _specs(rows):
+    a = np.zeros(len(rows), dtype=SPEC_DTYPE)
+    for i, (t, h, b, s) in enumerate(rows):
+        a[i] = (t, h, b, s)
+    return a
+
+
+# ----------------------------------------------------------------------------
+# workload 1: linear feed-forward chain (Appendix A network)
+# ----------------------------------------------------------------------------
+
+def chain_trace(N: int, size: int = 1, cost: int = 1) -> Trace:
+    """f_1 nullary, f_i(t_{i-1}); gradient ops as in Appendix A.  Tensor ids:
+    t_i -> i-1, gradient of f_i -> N + (N - i)."""
+    off = np.arange(N + 1, dtype=np.int64) - 1
+    off[0] = 0
+    inp = np.arange(N - 1, dtype=np.int64)        # f_{i+1} reads t_i  (id i-1)
+    return with_backward(off, inp, np.full(N, size, np.int64), np.full(N, cost, np.int64),
+                         np.full(N, cost, np.int64), name=f"chain{N}", meta=dict(N=N))
+
+
+def config_chain(N: int = 32) -> Workload:
+    tr = chain_trace(N)
+    peak = natural_peak(tr)
+    budgets = [math.ceil(2 * math.sqrt(N)), 16, 32, 64, BUDGET_UNLIMITED]
+    specs = _specs([(0, H_DTR, b, (1 << 32) + i) for i, b in enumerate(budgets)])
+    return Workload("chain32", [tr], specs, [peak],
+                    f"linear chain N={N}, unit sizes/costs, h_DTR at 5 budgets")
+
+
+# ----------------------------------------------------------------------------
+# workload 2: ResNet-like residual stack
+# ----------------------------------------------------------------------------
+
+MiB = 1 << 20
+
+
+def resnet_trace(seed: int = 2, blocks: int = 50) -> Trace:
+    rng = np.random.Generator(np.random.PCG64(seed))
+    ins = [[]]                                    # op 0: network input (nullary)
+    for b in range(blocks):
+        x = len(ins) - 1
+        base = len(ins)
+        ins.append([x])                           # conv1
+        ins.append([base])                        # bn1
+        ins.append([base + 1])                    # relu
+        ins.append([base + 2])                    # conv2
+        ins.append([base + 3])                    # bn2
+        ins.append([base + 4, x])                 # add(bn2, block input)
+    ins.append([len(ins) - 1])                    # loss
+    F = len(ins)
+    off, flat = _csr(ins)
+    size = np.maximum(1, np.rint(rng.lognormal(math.log(4 * MiB), 1.0, size=F - 1))).astype(np.int64)
+    size = np.concatenate([size, [4]])
+    fcost = np.maximum(1, size // 4096) * rng.integers(1, 5, size=F)
+    fcost[-1] = 1
+    bsize = size[::-1]
+    bcost = np.maximum(1, bsize // 4096) * rng.integers(1, 5, size=F)
+    return with_backward(off, flat, size, fcost, bcost, name=f"resnet{blocks}",
+                         meta=dict(seed=seed, blocks=blocks))
+
+
+def config_resnet() -> Workload:
+    tr = resnet_trace()
+    peak = natural_peak(tr)
+    budgets = linear_budgets(peak, 10, 100, 256)
+    rows = []
+    for h in (H_DTR, H_EQ, H_LOCAL, H_LRU, H_SIZE, H_RAND):
+        for b in budgets:
+            rows.append((0, h, b, 2 * (1 << 32) + len(rows)))
+    return Workload("resnet50blk", [tr], _specs(rows), [peak],
+                    "ResNet-like 50 residual blocks, 256 budgets x 6 heuristics")
+
+
+# ----------------------------------------------------------------------------
+# workload 3: transformer encoder
+# ----------------------------------------------------------------------------
+
+def transformer_trace(layers=12, hidden=768, seq=512, batch=8, heads=12, elem=2) -> Trace:
+    B, S, H = batch, seq, hidden
+    d = H // heads
+    M = B * S
+
+    def cst(flops):
+        return max(1, int(round(flops / 1e6)))
+
+    ins, size, cost = [], [], []
+
+    def op(inputs, nbytes, c):
+        ins.append(list(inputs))
+        size.append(int(nbytes))
+        cost.append(int(c))
+        return len(ins) - 1
+
+    x = op([], M * H * elem, cst(M * H))                                  # embedding
+    for _ in range(layers):
+        ln1 = op([x], M * H * elem, cst(8 * M * H))
+        qkv = op([ln1], M * 3 * H * elem, cst(2 * M * H * 3 * H))
+        ctxs = []
+        for _h in range(heads):
+            sc = op([qkv], B * S * S * elem, cst(2 * B * S * S * d))
+            sm = op([sc], B * S * S * elem, cst(5 * B * S * S))
+            ctxs.append(op([sm, qkv], M * d * elem, cst(2 * B * S * S * d)))
+        cat = op(ctxs, M * H * elem, cst(M * H))
+        proj = op([cat], M * H * elem, cst(2 * M * H * H))
+        add1 = op([proj, x], M * H * elem, cst(M * H))
+        ln2 = op([add1], M * H * elem, cst(8 * M * H))
+        mlp1 = op([ln2], M * 4 * H * elem, cst(2 * M * H * 4 * H))
+        gelu = op([mlp1], M * 4 * H * elem, cst(8 * M * 4 * H))
+        mlp2 = op([gelu], M * H * elem, cst(2 * M * 4 * H * H))
+        x = op([mlp2, add1], M * H * elem, cst(M * H))
+    op([x], 4, cst(M * H))                                               # loss
+    off, flat = _csr(ins)
+    fcost = np.asarray(cost, dtype=np.int64)
+    return with_backward(off, flat, np.asarray(size, np.int64), fcost, 2 * fcost[::-1],
+                         name=f"transformer{layers}",
+                         meta=dict(layers=layers, hidden=H, seq=S, batch=B, heads=heads))
+
+
+def config_transformer() -> Workload:
+    tr = transformer_trace()
+    peak = natural_peak(tr)
+    budgets = linear_budgets(peak, 15, 100, 512)
+    rows = []
+    for h in (H_DTR, H_EQ, H_LRU):
+        for b in budgets:
+            rows.append((0, h, b, 3 * (1 << 32) + len(rows)))
+    return Workload("transformer12", [tr], _specs(rows), [peak],
+                    "transformer encoder 12 layers, 512 budgets x 3 heuristics")
+
+
+# ----------------------------------------------------------------------------
+# workload 4: TreeLSTM over random binary trees
+# ----------------------------------------------------------------------------
+
+def treelstm_trace(seed: int, hidden: int = 256, min_leaves=64, max_leaves=512) -> Trace:
+    rng = np.random.Generator(np.random.PCG64(seed))
+    L = int(rng.integers(min_leaves, max_leaves + 1))
+    H = hidden
+    g_bytes, h_bytes = 5 * H * 4, H * 4
+    ins, size, cost = [], [], []
+
+    def op(inputs, nbytes, c):
+        ins.append(inputs)
+        size.append(nbytes)
+        cost.append(c)
+        return len(ins) - 1
+
+    def cst(flops):
+        return max(1, int(round(flops / 1e3)))
+
+    # shape: pre-order split draws, post-order emission
+    def build(n_leaves):
+        if n_leaves == 1:
+            g = op([], g_bytes, cst(2 * 5 * H * H))
+            a = op([g], g_bytes, cst(4 * 5 * H))
+            c = op([a], h_bytes, cst(5 * H))
+            tc = op([c], h_bytes, cst(H))
+            h = op([a, tc], h_bytes, cst(H))
+            return h, c
+        k = int(rng.integers(1, n_leaves))
+        hl, cl = build(k)
+        hr, cr = build(n_leaves - k)
+        g = op([hl, hr], g_bytes, cst(2 * 5 * H * 2 * H))
+        a = op([g], g_bytes, cst(4 * 5 * H))
+        c = op([a, cl, cr], h_bytes, cst(5 * H))
+        tc = op([c], h_bytes, cst(H))
+        h = op([a, tc], h_bytes, cst(H))
+        return h, c
+
+    hroot, _ = build(L)
+    op([hroot], 4, 1)                                                    # loss
+    off, flat = _csr(ins)
+    fcost = np.asarray(cost, dtype=np.int64)
+    return with_backward(off, flat, np.asarray(size, np.int64), fcost, 2 * fcost[::-1],
+                         name=f"treelstm_L{L}", meta=dict(seed=seed, leaves=L, hidden=H))
+
+
+def config_treelstm(n_trees: int = 4096, budgets_per_tree: int = 8) -> Workload:
+    import sys
+    old = sys.getrecursionlimit()
+    sys.setrecursionlimit(max(old, 5000))
+    try:
+        traces = [treelstm_trace(splitmix64(4 * (1 << 32) + i)) for i in range(n_trees)]
+    finally:
+        sys.setrecursionlimit(old)
+    peaks = [natural_peak(t) for t in traces]
+    rows = []
+    for i, p in enumerate(peaks):
+        for b in linear_budgets(p, 20, 100, budgets_per_tree):
+            rows.append((i, H_EQ, b, 4 * (1 << 32) + len(rows)))
+    return Workload(f"treelstm{n_trees}", traces, _specs(rows), peaks,
+                    f"{n_trees} TreeLSTM traces x {budgets_per_tree} budgets, h_DTR^eq")
+
+
+# ----------------------------------------------------------------------------
+# workload 5: large random DAG with a locality window
+# ----------------------------------------------------------------------------
+
+def random_dag_trace(seed: int = 5, n_forward: int = 100_000, window: int = 64,
+                     max_in: int = 3, median_bytes: int = MiB, sigma: float = 1.5,
+                     cost_mult: int = 8) -> Trace:
+    rng = np.random.Generator(np.random.PCG64(seed))
+    ins = [[]]
+    for k in range(1, n_forward):
+        lo = max(0, k - window)
+        w = k - lo
+        n = min(int(rng.integers(1, max_in + 1)), k)
+        pick = rng.choice(w, size=n, replace=False) + lo
+        ins.append(sorted(int(v) for v in pick))
+    off, flat = _csr(ins)
+    size = np.maximum(1, np.rint(rng.lognormal(math.log(median_bytes), sigma, size=n_forward))).astype(np.int64)
+    fcost = np.maximum(1, size // 4096) * rng.integers(1, cost_mult + 1, size=n_forward)
+    bsize = size[::-1]
+    bcost = np.maximum(1, bsize // 4096) * rng.integers(1, cost_mult + 1, size=n_forward)
+    return with_backward(off, flat, size, fcost, bcost, name=f"randdag{n_forward}",
+                         meta=dict(seed=seed, n_forward=n_forward, window=window))
+
+
+def config_random_dag(n_forward: int = 100_000, n_budgets: int = 1024, lo_pct: int = 5) -> Workload:
+    tr = random_dag_trace(n_forward=n_forward)
+    peak = natural_peak(tr)
+    rows = [(0, H_DTR, b, 5 * (1 << 32) + i)
+            for i, b in enumerate(linear_budgets(peak, lo_pct, 100, n_budgets))]
+    return Workload(f"randdag{n_forward}", [tr], _specs(rows), [peak],
+                    f"random DAG {n_forward} fwd ops, {n_budgets} budgets, h_DTR")
+
+
+# ----------------------------------------------------------------------------
+# small random programs for differential tests
+# ----------------------------------------------------------------------------
+
+def random_program(seed: int, n_ops: int, n_const: int = 0, max_in: int = 3,
+                   max_size: int = 8, max_cost: int = 5, p_required: float = 0.1,
+                   backward: bool = False, window: int | None = None,
+                   permute_ids: bool = True) -> Trace:
+    """Random DAG program.  Constants and operator outputs are interleaved in
+    execution order, then tensor ids are optionally shuffled, so id order and
+    execution order differ (this exercises the id tie-break and id mapping)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if backward:
+        ins = [[]]
+        for k in range(1, n_ops):
+            lo = 0 if window is None else max(0, k - window)
+            w = k - lo
+            n = int(rng.integers(0, min(max_in, w) + 1))
+            pick = rng.choice(w, size=n, replace=False) + lo if n else []
+            ins.append(sorted(int(v) for v in pick))
+        off, flat = _csr(ins)
+        size = rng.integers(1, max_size + 1, size=n_ops)
+        fcost = rng.integers(1, max_cost + 1, size=n_ops)
+        bcost = rng.integers(1, max_cost + 1, size=n_ops)
+        tr = with_backward(off, flat, size, fcost, bcost, name=f"rand_bwd{seed}")
+        sizes, flags = tr.tensor_size.copy(), tr.tensor_flags.copy()
+        outs, costs = tr.op_output.copy(), tr.op_cost.copy()
+        off2, inp2 = tr.op_input_offsets.copy(), tr.op_inputs.copy()
+    else:
+        # execution order over "slots": each slot is a constant or an operator output
+        kinds = np.array([1] * n_const + [0] * n_ops)
+        rng.shuffle(kinds)
+        sizes = rng.integers(1, max_size + 1, size=len(kinds)).astype(np.int64)
+        flags = np.where(kinds == 1, FLAG_CONSTANT, 0).astype(np.uint8)
+        outs, costs, lists = [], [], []
+        for slot, k in enumerate(kinds):
+            if k == 1:
+                continue
+            lo = 0 if window is None else max(0, slot - window)
+            avail = np.arange(lo, slot)
+            n = int(rng.integers(0, min(max_in, len(avail)) + 1))
+            pick = sorted(int(v) for v in rng.choice(avail, size=n, replace=False)) if n else []
+            lists.append(pick)
+            outs.append(slot)
+            costs.append(int(rng.integers(1, max_cost + 1)))
+        req = rng.random(len(kinds)) < p_required
+        flags[(kinds == 0) & req] |= FLAG_REQUIRED
+        off2, inp2 = _csr(lists)
+        outs = np.asarray(outs, np.int32)
+        costs = np.asarray(costs, np.int64)
+    if permute_ids:
+        n = len(sizes)
+        perm = rng.permutation(n)            # old id -> new id
+        new_sizes = np.empty_like(sizes)
+        new_flags = np.empty_like(flags)
+        new_sizes[perm] = sizes
+        new_flags[perm] = flags
+        sizes, flags = new_sizes, new_flags
+        outs = perm[np.asarray(outs)]
+        inp2 = perm[np.asarray(inp2)] if len(inp2) else np.asarray(inp2)
+        # the gradient op may list inputs in any order; keep listed order
+    return Trace(f"rand{seed}", sizes, flags, outs, costs, off2, inp2, meta=dict(seed=seed))
+
+
+CONFIGS = {
+    "chain32": config_chain,
+    "resnet50blk": config_resnet,
+    "transformer12": config_transformer,
+    "treelstm4096": config_treelstm,
+    "randdag100k": config_random_dag,
+}
+
+
+def make_config(name: str, **kw) -> Workload:
+    return CONFIGS[name](**kw)
