@@ -1,0 +1,166 @@
+/*
+ * dtr_sim.h -- C ABI of the batched Dynamic Tensor Rematerialization
+ * eviction-loop simulator for AMD Instinct MI355X (gfx950).
+ *
+ * The library replays operator traces under DTR's greedy online policy
+ * (Kirisame et al., "Dynamic Tensor Rematerialization", ICLR 2021):
+ *   - operator call (Section 2; Appendix C.4 "(Re)materialization"): lock the
+ *     inputs, rematerialize evicted inputs recursively by replaying their
+ *     parent operation, allocate the output, evicting while memory is
+ *     insufficient, advance the clock by the operator cost, unlock;
+ *   - eviction (Appendix C.4): the evictable pool is every resident tensor
+ *     with no locks (Appendix C.1); every pool member is scored and the
+ *     lowest score is evicted;
+ *   - eager eviction when the program drops its last reference (Section 2
+ *     "Deallocation", Appendix C.5);
+ *   - output condition (Appendix C.6): required outputs are rematerialized
+ *     and locked at the end.
+ * Each simulation is one (trace, heuristic, budget, seed).  Thousands run as
+ * independent work items on one GPU; all quantities are integers and every
+ * result is exact (bit-identical to a plain sequential implementation).
+ *
+ * Conventions used by every entry point:
+ *   - host pointers are read only during the call unless stated otherwise;
+ *   - the device workspace is caller-owned device memory (for example a
+ *     torch uint8 tensor); it must stay allocated while the handle lives;
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream);
+ *   - functions return DTR_OK (0) or a negative DTR_E* code; the message of
+ *     the last error on the calling thread is in dtr_sim_last_error();
+ *   - a handle is not thread-safe; distinct handles are independent.
+ */
+#ifndef DTR_SIM_H
+#define DTR_SIM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes (return values) ---------------------------------------- */
+#define DTR_OK      0
+#define DTR_EINVAL  (-1)   /* null pointer, bad count, workspace too small      */
+#define DTR_ETRACE  (-2)   /* trace or simulation spec fails validation         */
+#define DTR_EHIP    (-3)   /* a HIP runtime call failed                         */
+#define DTR_ESTATE  (-4)   /* call out of order (results before run)            */
+
+/* ---- tensor flags ---------------------------------------------------------- */
+#define DTR_FLAG_CONSTANT 1u  /* no producer; resident from time 0; never evicted
+                                 (Section 2: constants cannot be evicted)         */
+#define DTR_FLAG_REQUIRED 2u  /* never released; must be resident at the end
+                                 (Appendix C.6 output condition)                  */
+
+/* ---- heuristics (score = N/D, lowest evicted; Section 4.1, Appendix C.3) --- */
+#define DTR_H_DTR   0  /* (c0 + sum c0 over e*) / (m s), exact evicted neighbourhood   */
+#define DTR_H_EQ    1  /* (c0 + union-find neighbourhood cost) / (m s), split approx.  */
+#define DTR_H_LOCAL 2  /* c0 / (m s)                                                  */
+#define DTR_H_LRU   3  /* 1 / s                                                       */
+#define DTR_H_SIZE  4  /* 1 / m                                                       */
+#define DTR_H_RAND  5  /* fresh SplitMix64 draw per (seed, eviction number, id)       */
+#define DTR_H_ESTAR 6  /* (c0 + sum c0 over e*) / m, the h_{e*} of Appendix A.3       */
+
+#define DTR_BUDGET_UNLIMITED INT64_MAX
+
+/* ---- per-simulation status (a result, not an error) ------------------------ */
+#define DTR_STATUS_OK             0
+#define DTR_STATUS_OOM            1  /* nothing evictable while memory is short    */
+#define DTR_STATUS_CLOCK_OVERFLOW 2  /* clock reached 2^40 cost units              */
+#define DTR_STATUS_CAPACITY       3  /* internal capacity exceeded (never expected) */
+
+/*
+ * An operator trace.  Tensors are 0..n_tensors-1, operators 0..n_ops-1 in
+ * execution order; every operator produces exactly one tensor (Section 2
+ * assumptions).  Layout: plain host arrays.
+ *   tensor_size[n_tensors]     bytes (or units), 1 <= size < 2^36
+ *   tensor_flags[n_tensors]    DTR_FLAG_* bits
+ *   op_output[n_ops]           tensor produced by each op; every non-constant
+ *                              tensor is produced exactly once, constants never
+ *   op_cost[n_ops]             integer cost, 1 <= cost <= 2^28; sum < 2^50
+ *   op_input_offsets[n_ops+1]  CSR offsets into op_inputs (first 0, non-decreasing)
+ *   op_inputs[...]             input tensor ids; each must be a constant or the
+ *                              output of an earlier op; no duplicates per op
+ * A tensor is released after the last op that reads it (after the op that
+ * produces it, if nothing reads it), unless it is CONSTANT or REQUIRED.
+ */
+typedef struct {
+    int32_t n_tensors, n_ops;
+    const int64_t *tensor_size;
+    const uint8_t *tensor_flags;
+    const int32_t *op_output;
+    const int64_t *op_cost;
+    const int64_t *op_input_offsets;
+    const int32_t *op_inputs;
+} dtr_trace;
+
+/* One simulation: trace index, DTR_H_* heuristic, memory budget (same unit as
+ * tensor_size; DTR_BUDGET_UNLIMITED for none), seed (used by DTR_H_RAND). */
+typedef struct {
+    int32_t trace;
+    int32_t heuristic;
+    int64_t budget;
+    uint64_t seed;
+} dtr_sim_spec;
+
+/* Result of one simulation (104 bytes). */
+typedef struct {
+    int64_t total_cost;        /* base_cost + remat_cost                                */
+    int64_t base_cost;         /* cost of trace ops executed                            */
+    int64_t remat_cost;        /* cost of rematerializations                            */
+    int64_t peak_memory;       /* maximum memory in use                                 */
+    int64_t final_memory;      /* memory in use when the run ended                      */
+    int64_t n_executed_ops;    /* trace ops + rematerializations executed               */
+    int64_t n_remats;          /* rematerializations                                    */
+    int64_t n_evictions;       /* budget-driven evictions                               */
+    int64_t n_eager_evictions; /* evictions on release                                  */
+    int64_t n_scores;          /* candidates scored, summed over budget evictions       */
+    int64_t n_nbr_visits;      /* h_DTR/h_ESTAR: sum of |e*|; h_EQ: evicted neighbours;
+                                  summed over scored candidates; else 0                 */
+    int64_t n_adj_visits;      /* h_DTR/h_EQ/h_ESTAR: sum of candidate degrees; else 0  */
+    int32_t status;            /* DTR_STATUS_*                                          */
+    int32_t failed_op;         /* op index being run when status != OK (n_ops while the
+                                  output condition runs); -1 otherwise                  */
+} dtr_sim_result;
+
+/* Launch options (NULL = defaults). */
+typedef struct {
+    int32_t slots;   /* simulations resident on the GPU at once (0 = 16 per CU) */
+    int32_t flags;   /* reserved, must be 0                                     */
+} dtr_sim_options;
+
+typedef struct dtr_sim dtr_sim;
+
+/* Device workspace size for this batch on the current device.  Validates the
+ * traces and specs (DTR_ETRACE names the trace, op or sim and the reason). */
+int dtr_sim_workspace_bytes(const dtr_trace *traces, int32_t n_traces,
+                            const dtr_sim_spec *sims, int32_t n_sims,
+                            const dtr_sim_options *options, size_t *bytes);
+
+/* Validate, derive per-trace tables (producers, children, release lists),
+ * lay out and upload everything into device_workspace on `stream`.  Host
+ * arrays are copied; the caller may free them on return.  *out receives an
+ * owned handle (free with dtr_sim_destroy). */
+int dtr_sim_create(const dtr_trace *traces, int32_t n_traces,
+                   const dtr_sim_spec *sims, int32_t n_sims,
+                   const dtr_sim_options *options,
+                   void *device_workspace, size_t workspace_bytes,
+                   void *stream, dtr_sim **out);
+
+/* Enqueue every simulation on `stream` (asynchronous, stream-ordered).  May be
+ * called again; each call recomputes all results. */
+int dtr_sim_run(dtr_sim *sim, void *stream);
+
+/* Copy n_sims results (== the batch size) into host_out, after synchronizing
+ * the stream of the last run.  DTR_ESTATE if no run was enqueued. */
+int dtr_sim_results(dtr_sim *sim, dtr_sim_result *host_out, int32_t n_sims);
+
+/* Release the handle (not the caller's workspace).  NULL is ignored. */
+void dtr_sim_destroy(dtr_sim *sim);
+
+/* Message of the last failing call on this thread ("" if none). */
+const char *dtr_sim_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DTR_SIM_H */

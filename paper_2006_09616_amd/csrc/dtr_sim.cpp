@@ -1,0 +1,430 @@
+// dtr_sim.cpp -- host side of the C ABI declared in include/dtr_sim.h:
+// validation, per-trace derivation, workspace layout, upload and launch.
+//
+// Derivation (once per trace, host): the parent operation of every tensor
+// and its cost c0 (Appendix C.2 "Cost"), children (the dependents deps^T of
+// Appendix C.2 "Data dependencies"), the undirected neighbourhood used by the
+// union-find relaxation, the release point of every tensor (after its last
+// reader, from reference counting as in Appendix A.2 "Liveness"), required
+// outputs and constants.  All tables are uploaded once into the caller's
+// device workspace and shared read-only by every simulation of the trace.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <numeric>
+#include <string>
+#include <vector>
+
+#include "../../include/dtr_sim.h"
+#include "layout.h"
+
+extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream);
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char *fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+constexpr int64_t MAX_SIZE = int64_t(1) << 36;
+constexpr int64_t MAX_COST = int64_t(1) << 28;
+constexpr int64_t MAX_TOTAL_COST = int64_t(1) << 50;
+constexpr size_t ALIGN = 256;
+
+size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
+
+struct Derived {
+    int32_t n = 0, F = 0;
+    std::vector<int64_t> size, c0, cost;
+    std::vector<uint8_t> flags;
+    std::vector<int32_t> producer, out, in_off, in, ch_off, ch, adj_off, adj, rel_off, rel, req, consts;
+    int64_t const_mem = 0;
+};
+
+int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
+{
+    if (tr.n_tensors < 0 || tr.n_ops < 0)
+        return fail(DTR_ETRACE, "trace %d: negative n_tensors or n_ops", index);
+    if ((tr.n_tensors > 0 && (!tr.tensor_size || !tr.tensor_flags)) ||
+        (tr.n_ops > 0 && (!tr.op_output || !tr.op_cost || !tr.op_inputs)) || !tr.op_input_offsets)
+        return fail(DTR_EINVAL, "trace %d: null array", index);
+    const int32_t n = tr.n_tensors, F = tr.n_ops;
+    d.n = n;
+    d.F = F;
+    d.size.assign(tr.tensor_size, tr.tensor_size + n);
+    d.flags.assign(tr.tensor_flags, tr.tensor_flags + n);
+    for (int32_t t = 0; t < n; t++) {
+        if (d.size[t] < 1 || d.size[t] >= MAX_SIZE)
+            return fail(DTR_ETRACE, "trace %d: tensor %d size %lld outside [1, 2^36)", index, t,
+                        (long long)d.size[t]);
+        if (d.flags[t] & ~(DTR_FLAG_CONSTANT | DTR_FLAG_REQUIRED))
+            return fail(DTR_ETRACE, "trace %d: tensor %d has unknown flag bits", index, t);
+    }
+    if (tr.op_input_offsets[0] != 0) return fail(DTR_ETRACE, "trace %d: op_input_offsets[0] != 0", index);
+    const int64_t E = tr.op_input_offsets[F];
+    if (E < 0 || E > (int64_t(1) << 30)) return fail(DTR_ETRACE, "trace %d: %lld edges", index, (long long)E);
+    d.producer.assign(n, -1);
+    d.c0.assign(n, 0);
+    d.out.assign(tr.op_output, tr.op_output + F);
+    d.cost.assign(tr.op_cost, tr.op_cost + F);
+    d.in_off.resize(F + 1);
+    d.in.resize(E);
+    std::vector<uint8_t> defined(n, 0);
+    std::vector<int32_t> seen(n, -1);
+    for (int32_t t = 0; t < n; t++) defined[t] = (d.flags[t] & DTR_FLAG_CONSTANT) ? 1 : 0;
+    int64_t total = 0;
+    std::vector<int32_t> last(n, -1);
+    for (int32_t o = 0; o < F; o++) {
+        const int64_t b = tr.op_input_offsets[o], e = tr.op_input_offsets[o + 1];
+        if (e < b || e > E) return fail(DTR_ETRACE, "trace %d: op %d: offsets not monotone", index, o);
+        const int64_t c = d.cost[o];
+        if (c < 1 || c > MAX_COST)
+            return fail(DTR_ETRACE, "trace %d: op %d: cost %lld outside [1, 2^28]", index, o, (long long)c);
+        total += c;
+        if (total >= MAX_TOTAL_COST) return fail(DTR_ETRACE, "trace %d: total cost reaches 2^50", index);
+        d.in_off[o] = (int32_t)b;
+        for (int64_t k = b; k < e; k++) {
+            const int32_t u = tr.op_inputs[k];
+            if (u < 0 || u >= n) return fail(DTR_ETRACE, "trace %d: op %d: input %d out of range", index, o, u);
+            if (!defined[u])
+                return fail(DTR_ETRACE, "trace %d: op %d: input %d is not defined before use", index, o, u);
+            if (seen[u] == o) return fail(DTR_ETRACE, "trace %d: op %d: duplicate input %d", index, o, u);
+            seen[u] = o;
+            d.in[k] = u;
+            last[u] = o;
+        }
+        const int32_t t = d.out[o];
+        if (t < 0 || t >= n) return fail(DTR_ETRACE, "trace %d: op %d: output %d out of range", index, o, t);
+        if (defined[t])
+            return fail(DTR_ETRACE, "trace %d: op %d: tensor %d is a constant or already produced", index, o, t);
+        defined[t] = 1;
+        d.producer[t] = o;
+        d.c0[t] = c;
+        if (last[t] < o) last[t] = o;
+    }
+    d.in_off[F] = (int32_t)E;
+    for (int32_t t = 0; t < n; t++)
+        if (!defined[t]) return fail(DTR_ETRACE, "trace %d: tensor %d is never produced", index, t);
+
+    // children CSR (ascending consumer op order)
+    d.ch_off.assign(n + 1, 0);
+    for (int64_t k = 0; k < E; k++) d.ch_off[d.in[k] + 1]++;
+    for (int32_t t = 0; t < n; t++) d.ch_off[t + 1] += d.ch_off[t];
+    d.ch.resize(E);
+    {
+        std::vector<int32_t> fill(d.ch_off.begin(), d.ch_off.end() - 1);
+        for (int32_t o = 0; o < F; o++)
+            for (int32_t k = d.in_off[o]; k < d.in_off[o + 1]; k++) d.ch[fill[d.in[k]]++] = d.out[o];
+    }
+    // undirected neighbourhood: parents then children
+    d.adj_off.assign(n + 1, 0);
+    for (int32_t t = 0; t < n; t++) {
+        const int32_t o = d.producer[t];
+        const int32_t np = o >= 0 ? d.in_off[o + 1] - d.in_off[o] : 0;
+        d.adj_off[t + 1] = d.adj_off[t] + np + (d.ch_off[t + 1] - d.ch_off[t]);
+    }
+    d.adj.resize(d.adj_off[n]);
+    for (int32_t t = 0; t < n; t++) {
+        int32_t w = d.adj_off[t];
+        const int32_t o = d.producer[t];
+        if (o >= 0)
+            for (int32_t k = d.in_off[o]; k < d.in_off[o + 1]; k++) d.adj[w++] = d.in[k];
+        for (int32_t k = d.ch_off[t]; k < d.ch_off[t + 1]; k++) d.adj[w++] = d.ch[k];
+    }
+    // release lists, ascending id
+    d.rel_off.assign(F + 1, 0);
+    for (int32_t t = 0; t < n; t++)
+        if (!(d.flags[t] & (DTR_FLAG_CONSTANT | DTR_FLAG_REQUIRED)) && last[t] >= 0) d.rel_off[last[t] + 1]++;
+    for (int32_t o = 0; o < F; o++) d.rel_off[o + 1] += d.rel_off[o];
+    d.rel.resize(d.rel_off[F]);
+    {
+        std::vector<int32_t> fill(d.rel_off.begin(), d.rel_off.end() - 1);
+        for (int32_t t = 0; t < n; t++)
+            if (!(d.flags[t] & (DTR_FLAG_CONSTANT | DTR_FLAG_REQUIRED)) && last[t] >= 0) d.rel[fill[last[t]]++] = t;
+    }
+    for (int32_t t = 0; t < n; t++) {
+        if (d.flags[t] & DTR_FLAG_REQUIRED) d.req.push_back(t);
+        if (d.flags[t] & DTR_FLAG_CONSTANT) {
+            d.consts.push_back(t);
+            d.const_mem += d.size[t];
+        }
+    }
+    return DTR_OK;
+}
+
+// workspace: [header | trace tables | trace descriptors | specs | order | results | slots]
+struct Plan {
+    std::vector<Derived> traces;
+    std::vector<size_t> trace_off;   // start of each trace's tables
+    size_t desc_off = 0, spec_off = 0, order_off = 0, result_off = 0, slot_off = 0;
+    size_t tables_bytes = 0;         // everything before the slots (uploaded)
+    size_t total = 0;
+    dtr::SlotLayout L{};
+    int32_t n_slots = 0;
+    std::vector<int32_t> order;
+};
+
+template <class T>
+size_t bytes_of(const std::vector<T> &v) { return align_up(v.size() * sizeof(T)); }
+
+size_t trace_bytes(const Derived &d)
+{
+    return bytes_of(d.size) + bytes_of(d.c0) + bytes_of(d.flags) + bytes_of(d.producer) + bytes_of(d.out) +
+           bytes_of(d.cost) + bytes_of(d.in_off) + bytes_of(d.in) + bytes_of(d.ch_off) + bytes_of(d.ch) +
+           bytes_of(d.adj_off) + bytes_of(d.adj) + bytes_of(d.rel_off) + bytes_of(d.rel) + bytes_of(d.req) +
+           bytes_of(d.consts) + 8 * ALIGN;
+}
+
+int device_cus(int32_t *cus)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(DTR_EHIP, "hipGetDevice failed");
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return fail(DTR_EHIP, "hipDeviceGetAttribute(multiProcessorCount) failed");
+    *cus = v;
+    return DTR_OK;
+}
+
+int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sims, int32_t n_sims,
+              const dtr_sim_options *opt, Plan &p)
+{
+    if (n_traces < 0 || n_sims < 0) return fail(DTR_EINVAL, "negative n_traces or n_sims");
+    if ((n_traces > 0 && !traces) || (n_sims > 0 && !sims)) return fail(DTR_EINVAL, "null traces or sims");
+    if (opt && (opt->slots < 0 || opt->flags != 0)) return fail(DTR_EINVAL, "bad options");
+    p.traces.resize(n_traces);
+    for (int32_t i = 0; i < n_traces; i++) {
+        int rc = validate_and_derive(traces[i], i, p.traces[i]);
+        if (rc) return rc;
+    }
+    bool need_uf = false, need_walk = false;
+    int32_t n_max = 1;
+    for (int32_t i = 0; i < n_sims; i++) {
+        const dtr_sim_spec &s = sims[i];
+        if (s.trace < 0 || s.trace >= n_traces)
+            return fail(DTR_ETRACE, "sim %d: trace index %d out of range", i, s.trace);
+        if (s.heuristic < DTR_H_DTR || s.heuristic > DTR_H_ESTAR)
+            return fail(DTR_ETRACE, "sim %d: unknown heuristic %d", i, s.heuristic);
+        if (s.budget < 0) return fail(DTR_ETRACE, "sim %d: negative budget", i);
+        need_uf |= s.heuristic == DTR_H_EQ;
+        need_walk |= s.heuristic == DTR_H_DTR || s.heuristic == DTR_H_ESTAR;
+        n_max = std::max(n_max, p.traces[s.trace].n);
+    }
+    // slot layout
+    dtr::SlotLayout &L = p.L;
+    size_t o = 0;
+    auto take = [&](int64_t &field, size_t bytes) { field = (int64_t)o; o += align_up(bytes); };
+    const size_t n = (size_t)n_max;
+    L.n_max = n_max;
+    take(L.sw, 4 * n);
+    take(L.locks, 4 * n);
+    take(L.last, 8 * n);
+    take(L.pos, 4 * n);
+    take(L.pool_id, 4 * n);
+    take(L.pool_last, 8 * n);
+    take(L.pool_size, 8 * n);
+    take(L.pool_c0, 8 * n);
+    take(L.stack, 8 * (n + 1));
+    L.uf_cap = need_uf ? (int64_t)(2 * n + 64) : 0;
+    take(L.uf_parent, 4 * (size_t)L.uf_cap);
+    take(L.uf_cost, 8 * (size_t)L.uf_cap);
+    take(L.uf_size, 4 * (size_t)L.uf_cap);
+    take(L.uf_remap, 4 * (size_t)L.uf_cap);
+    take(L.stamp, need_walk ? 4 * n * dtr::WAVE : 0);
+    take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);
+    L.bytes = (int64_t)o;
+
+    int32_t cus = 0;
+    int rc = device_cus(&cus);
+    if (rc) return rc;
+    int64_t slots = opt && opt->slots > 0 ? opt->slots : (int64_t)cus * 16;
+    const int64_t cap_bytes = int64_t(48) << 30;     // bound slot memory
+    slots = std::min<int64_t>(slots, std::max<int64_t>(1, cap_bytes / std::max<int64_t>(1, L.bytes)));
+    slots = std::min<int64_t>(slots, std::max<int32_t>(1, n_sims));
+    p.n_slots = (int32_t)std::max<int64_t>(1, slots);
+
+    // longest first: ops of the trace, then lower budget first
+    p.order.resize(n_sims);
+    std::iota(p.order.begin(), p.order.end(), 0);
+    std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {
+        const int32_t fa = p.traces[sims[a].trace].F, fb = p.traces[sims[b].trace].F;
+        if (fa != fb) return fa > fb;
+        return sims[a].budget < sims[b].budget;
+    });
+
+    size_t w = align_up(64);   // header: work counter
+    p.trace_off.resize(n_traces);
+    for (int32_t i = 0; i < n_traces; i++) {
+        p.trace_off[i] = w;
+        w += trace_bytes(p.traces[i]);
+    }
+    p.desc_off = w;
+    w += align_up(sizeof(dtr::TraceDev) * std::max(1, n_traces));
+    p.spec_off = w;
+    w += align_up(sizeof(dtr::SpecDev) * std::max(1, n_sims));
+    p.order_off = w;
+    w += align_up(sizeof(int32_t) * std::max(1, n_sims));
+    p.tables_bytes = w;
+    p.result_off = w;
+    w += align_up(sizeof(dtr::ResultDev) * std::max(1, n_sims));
+    p.slot_off = w;
+    w += (size_t)L.bytes * (size_t)p.n_slots;
+    p.total = w;
+    return DTR_OK;
+}
+
+}  // namespace
+
+struct dtr_sim {
+    Plan plan;
+    uint8_t *ws = nullptr;
+    size_t ws_bytes = 0;
+    std::vector<uint8_t> staging;
+    hipStream_t last_stream = nullptr;
+    bool ran = false;
+    int32_t n_sims = 0;
+};
+
+extern "C" {
+
+const char *dtr_sim_last_error(void) { return g_err.c_str(); }
+
+int dtr_sim_workspace_bytes(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sims, int32_t n_sims,
+                            const dtr_sim_options *options, size_t *bytes)
+{
+    g_err.clear();
+    if (!bytes) return fail(DTR_EINVAL, "null bytes");
+    Plan p;
+    int rc = make_plan(traces, n_traces, sims, n_sims, options, p);
+    if (rc) return rc;
+    *bytes = p.total;
+    return DTR_OK;
+}
+
+int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sims, int32_t n_sims,
+                   const dtr_sim_options *options, void *device_workspace, size_t workspace_bytes, void *stream,
+                   dtr_sim **out)
+{
+    g_err.clear();
+    if (!out) return fail(DTR_EINVAL, "null out");
+    *out = nullptr;
+    if (!device_workspace) return fail(DTR_EINVAL, "null device workspace");
+    if ((uintptr_t)device_workspace % ALIGN) return fail(DTR_EINVAL, "workspace must be 256-byte aligned");
+    dtr_sim *h = new dtr_sim();
+    int rc = make_plan(traces, n_traces, sims, n_sims, options, h->plan);
+    if (rc) { delete h; return rc; }
+    Plan &p = h->plan;
+    if (workspace_bytes < p.total) {
+        rc = fail(DTR_EINVAL, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, p.total);
+        delete h;
+        return rc;
+    }
+    h->ws = (uint8_t *)device_workspace;
+    h->ws_bytes = workspace_bytes;
+    h->n_sims = n_sims;
+    h->staging.assign(p.tables_bytes, 0);
+    uint8_t *H = h->staging.data();
+    std::vector<dtr::TraceDev> descs(std::max(1, n_traces));
+    for (int32_t i = 0; i < n_traces; i++) {
+        const Derived &d = p.traces[i];
+        size_t w = p.trace_off[i];
+        auto put = [&](const auto &v) {
+            using T = typename std::decay_t<decltype(v)>::value_type;
+            size_t at = w;
+            if (!v.empty()) std::memcpy(H + at, v.data(), v.size() * sizeof(T));
+            w += bytes_of(v);
+            return (const T *)(h->ws + at);
+        };
+        dtr::TraceDev &D = descs[i];
+        D.n = d.n;
+        D.F = d.F;
+        D.n_req = (int32_t)d.req.size();
+        D.n_const = (int32_t)d.consts.size();
+        D.const_mem = d.const_mem;
+        D.size = put(d.size);
+        D.c0 = put(d.c0);
+        D.flags = put(d.flags);
+        D.producer = put(d.producer);
+        D.out = put(d.out);
+        D.cost = put(d.cost);
+        D.in_off = put(d.in_off);
+        D.in = put(d.in);
+        D.ch_off = put(d.ch_off);
+        D.ch = put(d.ch);
+        D.adj_off = put(d.adj_off);
+        D.adj = put(d.adj);
+        D.rel_off = put(d.rel_off);
+        D.rel = put(d.rel);
+        D.req = put(d.req);
+        D.consts = put(d.consts);
+    }
+    std::memcpy(H + p.desc_off, descs.data(), sizeof(dtr::TraceDev) * n_traces);
+    for (int32_t i = 0; i < n_sims; i++) {
+        dtr::SpecDev s{sims[i].trace, sims[i].heuristic, sims[i].budget, sims[i].seed};
+        std::memcpy(H + p.spec_off + i * sizeof(dtr::SpecDev), &s, sizeof(s));
+    }
+    if (n_sims) std::memcpy(H + p.order_off, p.order.data(), sizeof(int32_t) * n_sims);
+    hipStream_t st = (hipStream_t)stream;
+    if (hipMemcpyAsync(h->ws, H, p.tables_bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
+        hipStreamSynchronize(st) != hipSuccess) {
+        rc = fail(DTR_EHIP, "upload of %zu bytes failed", p.tables_bytes);
+        delete h;
+        return rc;
+    }
+    *out = h;
+    return DTR_OK;
+}
+
+int dtr_sim_run(dtr_sim *h, void *stream)
+{
+    g_err.clear();
+    if (!h) return fail(DTR_EINVAL, "null handle");
+    const Plan &p = h->plan;
+    if (h->n_sims == 0) { h->ran = true; h->last_stream = (hipStream_t)stream; return DTR_OK; }
+    dtr::KernelArgs a;
+    a.traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
+    a.specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
+    a.order = (const int32_t *)(h->ws + p.order_off);
+    a.results = (dtr::ResultDev *)(h->ws + p.result_off);
+    a.queue = (uint32_t *)h->ws;
+    a.slots = h->ws + p.slot_off;
+    a.L = p.L;
+    a.n_sims = h->n_sims;
+    a.n_slots = p.n_slots;
+    hipError_t e = dtr_launch_replay(&a, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+    h->ran = true;
+    h->last_stream = (hipStream_t)stream;
+    return DTR_OK;
+}
+
+int dtr_sim_results(dtr_sim *h, dtr_sim_result *host_out, int32_t n_sims)
+{
+    g_err.clear();
+    if (!h || (!host_out && n_sims > 0)) return fail(DTR_EINVAL, "null handle or output");
+    if (n_sims != h->n_sims) return fail(DTR_EINVAL, "n_sims %d does not match the batch (%d)", n_sims, h->n_sims);
+    if (!h->ran) return fail(DTR_ESTATE, "no run enqueued");
+    if (n_sims == 0) return DTR_OK;
+    static_assert(sizeof(dtr_sim_result) == sizeof(dtr::ResultDev), "result layout");
+    if (hipMemcpyAsync(host_out, h->ws + h->plan.result_off, sizeof(dtr_sim_result) * n_sims,
+                       hipMemcpyDeviceToHost, h->last_stream) != hipSuccess ||
+        hipStreamSynchronize(h->last_stream) != hipSuccess)
+        return fail(DTR_EHIP, "result copy failed");
+    return DTR_OK;
+}
+
+void dtr_sim_destroy(dtr_sim *h) { delete h; }
+
+}  // extern "C"

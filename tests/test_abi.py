@@ -1,0 +1,104 @@
+"""C-ABI library: loads, exports what include/dtr_sim.h declares, and
+validates traces on the host (no GPU needed for any of these)."""
+import ctypes as C
+
+import numpy as np
+import pytest
+
+from paper_2006_09616_amd import dtr as D
+from paper_2006_09616_amd import workloads as W
+
+
+def test_library_exports_every_declared_function():
+    names = D.header_functions()
+    assert set(names) >= {"dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run",
+                          "dtr_sim_results", "dtr_sim_destroy", "dtr_sim_last_error"}
+    lib = D.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_struct_sizes_match_header():
+    assert C.sizeof(D._Trace) == 8 + 6 * 8
+    assert W.SPEC_DTYPE.itemsize == 24
+    assert D.RESULT_DTYPE.itemsize == 104
+
+
+def _spec(h=W.H_LRU, b=10, trace=0):
+    s = np.zeros(1, W.SPEC_DTYPE)
+    s[0] = (trace, h, b, 0)
+    return s
+
+
+def _expect(code, traces, specs, match):
+    with pytest.raises(D.DtrError) as e:
+        D.dtr_sim_workspace_bytes(traces, specs)
+    assert e.value.code == code
+    assert match in str(e.value)
+
+
+def test_validation_rejects_malformed_traces():
+    good = W.chain_trace(4)
+
+    def mod(**kw):
+        t = W.Trace("m", good.tensor_size.copy(), good.tensor_flags.copy(), good.op_output.copy(),
+                    good.op_cost.copy(), good.op_input_offsets.copy(), good.op_inputs.copy())
+        for k, v in kw.items():
+            getattr(t, k)[...] = v
+        return t
+
+    t = mod()
+    t.op_cost[2] = 0
+    _expect(D.DTR_ETRACE, [t], _spec(), "op 2: cost 0")
+    t = mod()
+    t.tensor_size[1] = 0
+    _expect(D.DTR_ETRACE, [t], _spec(), "tensor 1 size 0")
+    t = mod()
+    t.op_inputs[0] = 3                       # op 1 reads a tensor produced later
+    _expect(D.DTR_ETRACE, [t], _spec(), "op 1: input 3 is not defined before use")
+    t = mod()
+    t.op_output[3] = 2                       # produced twice
+    _expect(D.DTR_ETRACE, [t], _spec(), "already produced")
+    t = mod()
+    t.tensor_flags[0] = W.FLAG_CONSTANT      # constant that an op also produces
+    _expect(D.DTR_ETRACE, [t], _spec(), "op 0: tensor 0 is a constant")
+    t = mod()
+    t.tensor_flags[2] = 8
+    _expect(D.DTR_ETRACE, [t], _spec(), "unknown flag")
+    _expect(D.DTR_ETRACE, [good], _spec(h=9), "unknown heuristic 9")
+    _expect(D.DTR_ETRACE, [good], _spec(trace=1), "trace index 1 out of range")
+    _expect(D.DTR_ETRACE, [good], _spec(b=-1), "negative budget")
+
+
+def test_duplicate_input_rejected():
+    ins = [[], [0], [0, 1, 1]]
+    off = np.array([0, 0, 1, 4], np.int64)
+    t = W.Trace("dup", np.ones(3, np.int64), np.zeros(3, np.uint8), np.arange(3, dtype=np.int32),
+                np.ones(3, np.int64), off, np.array([0, 0, 1, 1], np.int32))
+    _expect(D.DTR_ETRACE, [t], _spec(), "duplicate input 1")
+
+
+def test_cost_sum_guard():
+    n = 8
+    t = W.Trace("big", np.ones(n, np.int64), np.zeros(n, np.uint8), np.arange(n, dtype=np.int32),
+                np.full(n, 1 << 28, np.int64), np.zeros(n + 1, np.int64), np.zeros(0, np.int32))
+    big = [t] * 1
+    # 8 * 2^28 < 2^50: accepted by validation (may then fail only for lack of a GPU)
+    try:
+        D.dtr_sim_workspace_bytes(big, _spec())
+    except D.DtrError as e:
+        assert e.code == D.DTR_EHIP
+    t2 = W.Trace("big", np.ones(n, np.int64), np.zeros(n, np.uint8), np.arange(n, dtype=np.int32),
+                 np.full(n, (1 << 28) + 1, np.int64), np.zeros(n + 1, np.int64), np.zeros(0, np.int32))
+    _expect(D.DTR_ETRACE, [t2], _spec(), "outside [1, 2^28]")
+
+
+def test_null_arguments():
+    lib = D.lib()
+    assert lib.dtr_sim_workspace_bytes(None, 0, None, 0, None, None) == D.DTR_EINVAL
+    assert lib.dtr_sim_run(None, None) == D.DTR_EINVAL
+    assert lib.dtr_sim_results(None, None, 0) == D.DTR_EINVAL
+    lib.dtr_sim_destroy(None)
+    h = C.c_void_p()
+    assert lib.dtr_sim_create(None, 0, None, 0, None, None, 0, None, C.byref(h)) == D.DTR_EINVAL
+    assert "null" in D.dtr_sim_last_error()

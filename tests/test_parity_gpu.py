@@ -1,0 +1,122 @@
+"""GPU parity: the HIP path, called through the C ABI, against the CPU oracle,
+field by field and bit-exact (every quantity is an integer)."""
+import os
+
+import numpy as np
+import pytest
+
+from paper_2006_09616_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+FIELDS = ["total_cost", "base_cost", "remat_cost", "peak_memory", "final_memory", "n_executed_ops",
+          "n_remats", "n_evictions", "n_eager_evictions", "n_scores", "n_nbr_visits", "n_adj_visits",
+          "status", "failed_op"]
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2006_09616_amd import dtr as D
+    D.lib()
+    return D
+
+
+def compare(gpu_res, ref, specs, label):
+    bad = []
+    for k in range(len(specs)):
+        for f in FIELDS:
+            if int(gpu_res[f][k]) != int(ref[f][k]):
+                bad.append((k, f, int(gpu_res[f][k]), int(ref[f][k]), tuple(specs[k])))
+                break
+    assert not bad, f"{label}: {len(bad)}/{len(specs)} differ; first: {bad[:4]}"
+
+
+def specs_of(rows):
+    s = np.zeros(len(rows), W.SPEC_DTYPE)
+    for i, r in enumerate(rows):
+        s[i] = r
+    return s
+
+
+def test_chain_all_heuristics(gpu, oracle_lib):
+    traces = [W.chain_trace(N) for N in (2, 3, 8, 32, 100)]
+    rows = []
+    for i, tr in enumerate(traces):
+        N = tr.n_ops // 2
+        for h in range(7):
+            for B in sorted({1, 2, 3, 4, max(3, N // 4), N, 2 * N, W.BUDGET_UNLIMITED}):
+                rows.append((i, h, B, 77 + len(rows)))
+    specs = specs_of(rows)
+    print(f"chain batch: {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "chains")
+
+
+@pytest.mark.parametrize("seed0", [0, 1000])
+def test_random_programs(gpu, oracle_lib, seed0):
+    traces = []
+    rows = []
+    for s in range(seed0, seed0 + 60):
+        tr = W.random_program(s, n_ops=5 + (s * 7) % 120, n_const=s % 5, backward=s % 2 == 0,
+                              max_in=1 + s % 5, max_size=1 + s % 30, max_cost=1 + s % 9,
+                              window=None if s % 3 else 16)
+        traces.append(tr)
+        peak = W.natural_peak(tr)
+        for h in range(7):
+            for frac in (0.2, 0.35, 0.5, 0.75, 1.0):
+                rows.append((len(traces) - 1, h, max(1, int(peak * frac)), s * 131 + h))
+    specs = specs_of(rows)
+    print(f"random batch: {len(traces)} traces, {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "random")
+
+
+def test_empty_and_degenerate(gpu, oracle_lib):
+    empty = W.Trace("empty", np.zeros(0, np.int64), np.zeros(0, np.uint8), np.zeros(0, np.int32),
+                    np.zeros(0, np.int64), np.zeros(1, np.int64), np.zeros(0, np.int32))
+    consts = W.Trace("consts", np.array([5, 7], np.int64), np.array([1, 3], np.uint8),
+                     np.zeros(0, np.int32), np.zeros(0, np.int64), np.zeros(1, np.int64),
+                     np.zeros(0, np.int32))
+    single = W.Trace("single", np.array([4], np.int64), np.array([2], np.uint8), np.array([0], np.int32),
+                     np.array([3], np.int64), np.array([0, 0], np.int64), np.zeros(0, np.int32))
+    traces = [empty, consts, single, W.chain_trace(1)]
+    rows = []
+    for i in range(len(traces)):
+        for h in range(7):
+            for b in (0, 1, 4, 11, 12, W.BUDGET_UNLIMITED):
+                rows.append((i, h, b, 5))
+    specs = specs_of(rows)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "degenerate")
+    assert len(gpu.run(traces, specs[:0])) == 0
+
+
+def test_chain32_config(gpu, oracle_lib):
+    w = W.make_config("chain32")
+    compare(gpu.run(w.traces, w.specs), oracle_lib.run(w.traces, w.specs), w.specs, "chain32")
+
+
+def test_resnet_config(gpu, oracle_lib):
+    w = W.make_config("resnet50blk")
+    print(f"resnet: {w.n_sims} sims", flush=True)
+    compare(gpu.run(w.traces, w.specs), oracle_lib.run(w.traces, w.specs), w.specs, "resnet")
+
+
+def test_transformer_config(gpu, oracle_lib):
+    w = W.make_config("transformer12")
+    print(f"transformer: {w.n_sims} sims", flush=True)
+    compare(gpu.run(w.traces, w.specs), oracle_lib.run(w.traces, w.specs), w.specs, "transformer")
+
+
+def test_treelstm_subset(gpu, oracle_lib):
+    w = W.make_config("treelstm4096", n_trees=128)
+    print(f"treelstm subset: {w.n_sims} sims", flush=True)
+    compare(gpu.run(w.traces, w.specs), oracle_lib.run(w.traces, w.specs), w.specs, "treelstm128")
+
+
+def test_determinism_across_slot_counts(gpu):
+    w = W.make_config("resnet50blk")
+    a = gpu.run(w.traces, w.specs, slots=7)
+    b = gpu.run(w.traces, w.specs, slots=1000)
+    c = gpu.run(w.traces, w.specs)
+    assert a.tobytes() == b.tobytes() == c.tobytes()
