@@ -42,6 +42,8 @@ constexpr int64_t MAX_SIZE = int64_t(1) << 36;
 constexpr int64_t MAX_COST = int64_t(1) << 28;
 constexpr int64_t MAX_TOTAL_COST = int64_t(1) << 50;
 constexpr size_t ALIGN = 256;
+constexpr int32_t MAX_TENSORS = 8000000;       // pool positions are packed in 24 bits
+constexpr int32_t MAX_DEGREE = (1 << 23) - 1;  // degrees are packed in 23 bits
 
 size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
@@ -50,6 +52,7 @@ struct Derived {
     std::vector<int64_t> size, c0, cost;
     std::vector<uint8_t> flags;
     std::vector<int32_t> producer, out, in_off, in, ch_off, ch, adj_off, adj, rel_off, rel, req, consts;
+    std::vector<dtr::TRec> rec;
     int64_t const_mem = 0;
 };
 
@@ -57,6 +60,8 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
 {
     if (tr.n_tensors < 0 || tr.n_ops < 0)
         return fail(DTR_ETRACE, "trace %d: negative n_tensors or n_ops", index);
+    if (tr.n_tensors > MAX_TENSORS)
+        return fail(DTR_ETRACE, "trace %d: %d tensors exceed the limit of %d", index, tr.n_tensors, MAX_TENSORS);
     if ((tr.n_tensors > 0 && (!tr.tensor_size || !tr.tensor_flags)) ||
         (tr.n_ops > 0 && (!tr.op_output || !tr.op_cost || !tr.op_inputs)) || !tr.op_input_offsets)
         return fail(DTR_EINVAL, "trace %d: null array", index);
@@ -135,6 +140,9 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
         const int32_t np = o >= 0 ? d.in_off[o + 1] - d.in_off[o] : 0;
         d.adj_off[t + 1] = d.adj_off[t] + np + (d.ch_off[t + 1] - d.ch_off[t]);
     }
+    for (int32_t t = 0; t < n; t++)
+        if (d.adj_off[t + 1] - d.adj_off[t] > MAX_DEGREE)
+            return fail(DTR_ETRACE, "trace %d: tensor %d has more than %d neighbours", index, t, MAX_DEGREE);
     d.adj.resize(d.adj_off[n]);
     for (int32_t t = 0; t < n; t++) {
         int32_t w = d.adj_off[t];
@@ -154,6 +162,18 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
         for (int32_t t = 0; t < n; t++)
             if (!(d.flags[t] & (DTR_FLAG_CONSTANT | DTR_FLAG_REQUIRED)) && last[t] >= 0) d.rel[fill[last[t]]++] = t;
     }
+    d.rec.resize(n);
+    for (int32_t t = 0; t < n; t++) {
+        dtr::TRec &r = d.rec[t];
+        const int32_t o = d.producer[t];
+        r.size = d.size[t];
+        r.c0 = (int32_t)d.c0[t];
+        r.producer = o;
+        r.in_b = o >= 0 ? d.in_off[o] : 0;
+        r.in_e = o >= 0 ? d.in_off[o + 1] : 0;
+        r.adj_b = d.adj_off[t];
+        r.adj_e = d.adj_off[t + 1];
+    }
     for (int32_t t = 0; t < n; t++) {
         if (d.flags[t] & DTR_FLAG_REQUIRED) d.req.push_back(t);
         if (d.flags[t] & DTR_FLAG_CONSTANT) {
@@ -168,12 +188,13 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
 struct Plan {
     std::vector<Derived> traces;
     std::vector<size_t> trace_off;   // start of each trace's tables
-    size_t desc_off = 0, spec_off = 0, order_off = 0, result_off = 0, slot_off = 0;
+    size_t desc_off = 0, spec_off = 0, order_off = 0, result_off = 0, slot_off = 0, prof_off = 0;
     size_t tables_bytes = 0;         // everything before the slots (uploaded)
     size_t total = 0;
     dtr::SlotLayout L{};
     int32_t n_slots = 0;
     std::vector<int32_t> order;
+    int32_t class_count[3] = {0, 0, 0};
 };
 
 template <class T>
@@ -184,7 +205,7 @@ size_t trace_bytes(const Derived &d)
     return bytes_of(d.size) + bytes_of(d.c0) + bytes_of(d.flags) + bytes_of(d.producer) + bytes_of(d.out) +
            bytes_of(d.cost) + bytes_of(d.in_off) + bytes_of(d.in) + bytes_of(d.ch_off) + bytes_of(d.ch) +
            bytes_of(d.adj_off) + bytes_of(d.adj) + bytes_of(d.rel_off) + bytes_of(d.rel) + bytes_of(d.req) +
-           bytes_of(d.consts) + 8 * ALIGN;
+           bytes_of(d.consts) + bytes_of(d.rec) + 8 * ALIGN;
 }
 
 int device_cus(int32_t *cus)
@@ -228,20 +249,19 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     auto take = [&](int64_t &field, size_t bytes) { field = (int64_t)o; o += align_up(bytes); };
     const size_t n = (size_t)n_max;
     L.n_max = n_max;
-    take(L.sw, 4 * n);
-    take(L.locks, 4 * n);
-    take(L.last, 8 * n);
-    take(L.pos, 4 * n);
-    take(L.pool_id, 4 * n);
-    take(L.pool_last, 8 * n);
-    take(L.pool_size, 8 * n);
-    take(L.pool_c0, 8 * n);
+    L.pcap = 2 * (int64_t)n + 128;
+    L.ucap = need_uf ? 2 * (int64_t)n + 64 : 0;
+    const size_t pc = (size_t)L.pcap;
+    take(L.tst, 8 * n);
+    take(L.pid, 4 * pc);
+    take(L.plast, 8 * pc);
+    take(L.psize, 8 * pc);
+    take(L.pc0, 8 * pc);
+    take(L.pdeg, 4 * pc);
+    take(L.pnb, need_uf ? 4 * pc * dtr::NB_CACHE : 0);
+    take(L.nodes, sizeof(dtr::UfNode) * (size_t)L.ucap);
+    take(L.uf_remap, 4 * (size_t)L.ucap);
     take(L.stack, 8 * (n + 1));
-    L.uf_cap = need_uf ? (int64_t)(2 * n + 64) : 0;
-    take(L.uf_parent, 4 * (size_t)L.uf_cap);
-    take(L.uf_cost, 8 * (size_t)L.uf_cap);
-    take(L.uf_size, 4 * (size_t)L.uf_cap);
-    take(L.uf_remap, 4 * (size_t)L.uf_cap);
     take(L.stamp, need_walk ? 4 * n * dtr::WAVE : 0);
     take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);
     L.bytes = (int64_t)o;
@@ -255,14 +275,22 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     slots = std::min<int64_t>(slots, std::max<int32_t>(1, n_sims));
     p.n_slots = (int32_t)std::max<int64_t>(1, slots);
 
+    // grouped by heuristic class (one kernel specialisation each), then
     // longest first: ops of the trace, then lower budget first
+    auto cls = [&](int32_t i) {
+        const int32_t hh = sims[i].heuristic;
+        return hh == DTR_H_EQ ? 0 : (hh == DTR_H_DTR || hh == DTR_H_ESTAR) ? 1 : 2;
+    };
     p.order.resize(n_sims);
     std::iota(p.order.begin(), p.order.end(), 0);
     std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {
+        if (cls(a) != cls(b)) return cls(a) < cls(b);
         const int32_t fa = p.traces[sims[a].trace].F, fb = p.traces[sims[b].trace].F;
         if (fa != fb) return fa > fb;
         return sims[a].budget < sims[b].budget;
     });
+    for (int c = 0; c < 3; c++) p.class_count[c] = 0;
+    for (int32_t i = 0; i < n_sims; i++) p.class_count[cls(i)]++;
 
     size_t w = align_up(64);   // header: work counter
     p.trace_off.resize(n_traces);
@@ -279,6 +307,10 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     p.tables_bytes = w;
     p.result_off = w;
     w += align_up(sizeof(dtr::ResultDev) * std::max(1, n_sims));
+#ifdef DTR_PROFILE
+    p.prof_off = w;
+    w += align_up(sizeof(int64_t) * dtr::PROF_FIELDS * std::max(1, n_sims));
+#endif
     p.slot_off = w;
     w += (size_t)L.bytes * (size_t)p.n_slots;
     p.total = w;
@@ -369,6 +401,7 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec
         D.rel = put(d.rel);
         D.req = put(d.req);
         D.consts = put(d.consts);
+        D.rec = put(d.rec);
     }
     std::memcpy(H + p.desc_off, descs.data(), sizeof(dtr::TraceDev) * n_traces);
     for (int32_t i = 0; i < n_sims; i++) {
@@ -393,17 +426,25 @@ int dtr_sim_run(dtr_sim *h, void *stream)
     if (!h) return fail(DTR_EINVAL, "null handle");
     const Plan &p = h->plan;
     if (h->n_sims == 0) { h->ran = true; h->last_stream = (hipStream_t)stream; return DTR_OK; }
-    dtr::KernelArgs a;
-    a.traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
-    a.specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
-    a.order = (const int32_t *)(h->ws + p.order_off);
-    a.results = (dtr::ResultDev *)(h->ws + p.result_off);
-    a.queue = (uint32_t *)h->ws;
-    a.slots = h->ws + p.slot_off;
-    a.L = p.L;
-    a.n_sims = h->n_sims;
-    a.n_slots = p.n_slots;
-    hipError_t e = dtr_launch_replay(&a, (hipStream_t)stream);
+    dtr::KernelArgs a[3];
+    int32_t first = 0;
+    for (int c = 0; c < 3; c++) {
+        a[c].traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
+        a[c].specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
+        a[c].order = (const int32_t *)(h->ws + p.order_off) + first;
+        a[c].results = (dtr::ResultDev *)(h->ws + p.result_off);
+        a[c].queue = (uint32_t *)h->ws + c;
+        a[c].slots = h->ws + p.slot_off;
+        a[c].L = p.L;
+        a[c].n_sims = p.class_count[c];
+        a[c].n_slots = std::max(1, std::min(p.n_slots, p.class_count[c]));
+        a[c].prof = nullptr;
+#ifdef DTR_PROFILE
+        a[c].prof = (int64_t *)(h->ws + p.prof_off);
+#endif
+        first += p.class_count[c];
+    }
+    hipError_t e = dtr_launch_replay(a, (hipStream_t)stream);
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     h->ran = true;
     h->last_stream = (hipStream_t)stream;
@@ -426,5 +467,19 @@ int dtr_sim_results(dtr_sim *h, dtr_sim_result *host_out, int32_t n_sims)
 }
 
 void dtr_sim_destroy(dtr_sim *h) { delete h; }
+
+#ifdef DTR_PROFILE
+// Phase timers of the last run (DTR_PROFILE builds only; not part of the
+// public header): PROF_FIELDS int64 per simulation.
+int dtr_sim_profile(dtr_sim *h, int64_t *host_out, int32_t n_sims)
+{
+    if (!h || n_sims != h->n_sims || !h->ran) return fail(DTR_EINVAL, "bad profile request");
+    if (hipMemcpyAsync(host_out, h->ws + h->plan.prof_off, sizeof(int64_t) * dtr::PROF_FIELDS * n_sims,
+                       hipMemcpyDeviceToHost, h->last_stream) != hipSuccess ||
+        hipStreamSynchronize(h->last_stream) != hipSuccess)
+        return fail(DTR_EHIP, "profile copy failed");
+    return DTR_OK;
+}
+#endif
 
 }  // extern "C"

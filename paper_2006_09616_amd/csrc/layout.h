@@ -22,6 +22,17 @@ constexpr int WAVE = 64;
 //   ch               children: tensors whose parent operation reads the tensor
 //   rel              tensors released after each op (last reader), ascending id
 //   req / consts     required outputs and constants, ascending id
+// Per-tensor static record, one scalar load (32 bytes): size, c0, parent
+// operation, its input range in `in`, and the tensor's neighbour range in `adj`.
+struct TRec {
+    int64_t size;
+    int32_t c0;              // cost of the parent operation (<= 2^28), 0 for constants
+    int32_t producer;        // -1 for constants
+    int32_t in_b, in_e;      // inputs of the parent operation
+    int32_t adj_b, adj_e;    // parents then children
+};
+static_assert(sizeof(TRec) == 32, "tensor record layout");
+
 struct TraceDev {
     int32_t n;               // tensors
     int32_t F;               // ops
@@ -43,6 +54,7 @@ struct TraceDev {
     const int32_t *rel;      // [<= n]
     const int32_t *req;      // [n_req]
     const int32_t *consts;   // [n_const]
+    const TRec *rec;         // [n]
 };
 
 struct SpecDev {
@@ -59,18 +71,35 @@ struct ResultDev {
 };
 static_assert(sizeof(ResultDev) == 104, "result layout");
 
-// Per-slot working memory: one slot per resident simulation.  Column arrays
-// sized for the largest trace of the batch (n_max tensors).  Offsets in bytes
-// from the slot base, each 256-byte aligned.
+// Per-slot working memory: one slot per resident simulation, sized for the
+// largest trace of the batch (n_max tensors).  Offsets in bytes from the slot
+// base, each 256-byte aligned.
+//   tst       per-tensor state word: state/union-find node (32 bits), pool
+//             position (24 bits), lock count (8 bits)
+//   pool      evictable tensors, struct of arrays over pcap slots (dead slots
+//             are tombstoned and squeezed out when the array fills):
+//             id, last access, size, c0, packed (degree << 8 | n), and for
+//             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
+//             neighbours (n = NB_CACHE + 1 marks an overflowed list)
+//   nodes     union-find nodes {running cost, parent, size}
+//   stack     rematerialization frames (tensor, next input)
+//   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
+constexpr int NB_CACHE = 4;
+
 struct SlotLayout {
     int64_t bytes;           // stride between slots
-    int64_t sw, locks, last, pos;            // per tensor
-    int64_t pool_id, pool_last, pool_size, pool_c0;   // pool columns
-    int64_t stack;           // remat frames: (tensor, cursor) int32 pairs
-    int64_t uf_parent, uf_cost, uf_size, uf_remap;    // union-find (h_DTR^eq)
-    int64_t uf_cap;          // nodes
-    int64_t stamp, queue;    // per-lane neighbourhood walk (h_DTR, h_ESTAR)
-    int64_t n_max;
+    int64_t tst;
+    int64_t pid, plast, psize, pc0, pdeg, pnb;
+    int64_t nodes, uf_remap;
+    int64_t stack;
+    int64_t stamp, queue;
+    int64_t pcap, ucap, n_max;
+};
+
+struct __attribute__((aligned(16))) UfNode {
+    int64_t cost;
+    int32_t parent;
+    int32_t size;
 };
 
 struct KernelArgs {
@@ -83,6 +112,11 @@ struct KernelArgs {
     SlotLayout L;
     int32_t n_sims;
     int32_t n_slots;
+    int64_t *prof;           // DTR_PROFILE builds: PROF_FIELDS counters per sim
 };
+
+// In-kernel phase timers (DTR_PROFILE builds only): cycles spent per sim in
+// the whole replay and in the eviction scans, and the number of scans.
+constexpr int PROF_FIELDS = 4;   // total cycles, scan cycles, scans, scan rounds
 
 }  // namespace dtr

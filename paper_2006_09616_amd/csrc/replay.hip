@@ -1,25 +1,38 @@
 // replay.hip -- gfx950 kernels of the batched DTR eviction-loop simulator.
 //
 // One wavefront (64 lanes, one workgroup) owns one simulation at a time and
-// pulls the next one from a global work counter (persistent grid).  The
-// sequential part of DTR's operator call (Section 2; Appendix C.4) runs
-// wave-uniformly: every lane holds the same clock, memory and counters.  The
-// data-parallel part -- scoring every evictable tensor when memory runs out
-// (Appendix C.4 "Runtime state": the lowest score is evicted) -- is spread
-// over the lanes: each lane scores a strided slice of the pool, keeps its own
-// lexicographic (score, id) minimum, and a cross-lane reduction yields the
-// victim.  Scores N/D are compared exactly by 128-bit cross-multiplication.
+// pulls the next one from a global work counter (persistent grid, longest
+// traces first).  DTR's operator call (Section 2; Appendix C.4) is a chain of
+// dependent steps, so the kernel is organised around memory latency: every
+// step is arranged so that independent reads are issued together and the
+// number of dependent memory round trips per operation stays small.
 //
-// Neighbourhood costs:
-//   h_DTR^eq  union-find over evicted components with a running cost per set;
-//             a tensor's new node is created when it is evicted and unioned
-//             with its evicted neighbours' sets; rematerialization subtracts
-//             c0 from the set and detaches the tensor (split approximation,
-//             Appendix C.2).  A query sums the distinct sets of the evicted
-//             parents and children without merging them.
-//   h_DTR     e* (Appendix C.2): each lane walks evicted ancestors and
-//             evicted descendants of its candidate with lane-private epoch
-//             stamps (set semantics, nothing counted twice).
+//  * wave-uniform control: clock, memory, counters and the current frame are
+//    identical in every lane; read-only trace tables are read through the
+//    scalar cache (one 32-byte record per tensor);
+//  * lane-parallel bookkeeping: the inputs of an operation are locked,
+//    checked and unlocked by one lane each, with their state kept in
+//    registers for the life of the frame; release lists are checked in
+//    parallel;
+//  * the evictable pool (Appendix C.4 "Runtime state") is a tombstoned
+//    struct of arrays read coalesced; each lane scores U candidates per
+//    round with all slot reads issued at once, and the exact (score, id)
+//    minimum is reduced across lanes;
+//  * h_DTR^eq (Appendix C.2): each pool slot caches the union-find nodes of
+//    its candidate's evicted neighbours, kept current as neighbours are
+//    evicted and rematerialized, so a score needs one dependent node read
+//    (two if the node is no longer a root); union-find nodes are created at
+//    eviction and carry the running cost of their set; all sets adjacent to
+//    an evicted tensor are found in parallel and merged at once;
+//    rematerialization subtracts c0 and detaches the tensor (split
+//    approximation); the node pool is compacted when full;
+//  * h_DTR / h_{e*}: each lane walks its candidate's evicted ancestors and
+//    descendants (e*, Appendix C.2) with lane-private epoch stamps.
+//
+// Scores N/D are compared exactly by 128-bit cross-multiplication; ties go to
+// the smaller tensor id.  Last-access times are not kept per tensor: a tensor
+// joins the pool right after the operation that last referenced it, so the
+// pool slot receives that operation's start time.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -32,7 +45,19 @@ typedef unsigned __int128 u128;
 enum { H_DTR = 0, H_EQ = 1, H_LOCAL = 2, H_LRU = 3, H_SIZE = 4, H_RAND = 5, H_ESTAR = 6 };
 enum { ST_OK = 0, ST_OOM = 1, ST_CLOCK = 2, ST_CAPACITY = 3 };
 
+// state word values (low 32 bits of a tensor's state); >= 0: evicted (node)
+constexpr int32_t S_CONST = -3;
+constexpr int32_t S_UNCOMPUTED = -2;
+constexpr int32_t S_RESIDENT = -1;
+constexpr uint32_t MAX_LOCKS = 255;
 constexpr uint8_t FLAG_CONST = 1;
+constexpr int U = 2;             // candidates per lane per scan round
+constexpr int K = NB_CACHE;
+constexpr int LB = 8;            // neighbour reads issued together when building a cache
+// kernel specialisations by heuristic class (register budgets differ widely)
+enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2 };
+
+// ------------------------------------------------------------- helpers --
 
 __device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
 
@@ -42,6 +67,30 @@ __device__ __forceinline__ int64_t uni64(int64_t v)
     uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
     return (int64_t)(((uint64_t)hi << 32) | lo);
 }
+
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int32_t j)
+{
+    return __shfl(v, j, WAVE);
+}
+
+// read-only trace tables: constant address space, so uniform reads become
+// scalar loads
+template <class T>
+__device__ __forceinline__ T cld(const T *p) { return *(const __attribute__((address_space(4))) T *)p; }
+
+__device__ __forceinline__ int32_t lane_rank(uint64_t mask)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
+}
+
+__device__ __forceinline__ uint64_t ts_make(int32_t sw, uint32_t pos, uint32_t locks)
+{
+    return (uint64_t)(uint32_t)sw | ((uint64_t)(pos & 0xFFFFFFu) << 32) | ((uint64_t)locks << 56);
+}
+__device__ __forceinline__ int32_t ts_sw(uint64_t w) { return (int32_t)(uint32_t)w; }
+__device__ __forceinline__ uint32_t ts_pos(uint64_t w) { return (uint32_t)(w >> 32) & 0xFFFFFFu; }
+__device__ __forceinline__ uint32_t ts_locks(uint64_t w) { return (uint32_t)(w >> 56); }
+__device__ __forceinline__ bool ts_in_pool(uint64_t w) { return ts_sw(w) == S_RESIDENT && ts_locks(w) == 0; }
 
 // SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014)
 __device__ __forceinline__ uint64_t mix64(uint64_t z)
@@ -61,39 +110,37 @@ __device__ __forceinline__ bool better(uint64_t na, u128 da, int32_t ia, uint64_
 }
 
 struct Slot {
-    int32_t *sw, *locks, *pos;
-    int64_t *last;
-    int32_t *pool_id;
-    int64_t *pool_last, *pool_size, *pool_c0;
-    int32_t *stack;
-    int32_t *uf_parent, *uf_size, *uf_remap;
-    int64_t *uf_cost;
+    uint64_t *tst;
+    int32_t *pid;
+    int64_t *plast, *psize, *pc0;
+    int32_t *pdeg;     // degree << 8 | cached neighbour count
+    int32_t *pnb;      // K columns of pcap
+    UfNode *nodes;
+    int32_t *remap;
+    int2 *stack;
     uint32_t *stamp;
     int32_t *queue;
-    int64_t uf_cap;
-    int32_t n_max;
+    int32_t pcap, ucap, n_max;
 };
 
 __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
 {
     uint8_t *b = a.slots + (size_t)k * (size_t)a.L.bytes;
     Slot S;
-    S.sw = (int32_t *)(b + a.L.sw);
-    S.locks = (int32_t *)(b + a.L.locks);
-    S.last = (int64_t *)(b + a.L.last);
-    S.pos = (int32_t *)(b + a.L.pos);
-    S.pool_id = (int32_t *)(b + a.L.pool_id);
-    S.pool_last = (int64_t *)(b + a.L.pool_last);
-    S.pool_size = (int64_t *)(b + a.L.pool_size);
-    S.pool_c0 = (int64_t *)(b + a.L.pool_c0);
-    S.stack = (int32_t *)(b + a.L.stack);
-    S.uf_parent = (int32_t *)(b + a.L.uf_parent);
-    S.uf_cost = (int64_t *)(b + a.L.uf_cost);
-    S.uf_size = (int32_t *)(b + a.L.uf_size);
-    S.uf_remap = (int32_t *)(b + a.L.uf_remap);
+    S.tst = (uint64_t *)(b + a.L.tst);
+    S.pid = (int32_t *)(b + a.L.pid);
+    S.plast = (int64_t *)(b + a.L.plast);
+    S.psize = (int64_t *)(b + a.L.psize);
+    S.pc0 = (int64_t *)(b + a.L.pc0);
+    S.pdeg = (int32_t *)(b + a.L.pdeg);
+    S.pnb = (int32_t *)(b + a.L.pnb);
+    S.nodes = (UfNode *)(b + a.L.nodes);
+    S.remap = (int32_t *)(b + a.L.uf_remap);
+    S.stack = (int2 *)(b + a.L.stack);
     S.stamp = (uint32_t *)(b + a.L.stamp);
     S.queue = (int32_t *)(b + a.L.queue);
-    S.uf_cap = a.L.uf_cap;
+    S.pcap = (int32_t)a.L.pcap;
+    S.ucap = (int32_t)a.L.ucap;
     S.n_max = (int32_t)a.L.n_max;
     return S;
 }
@@ -107,211 +154,395 @@ struct Sim {
     int64_t budget;
     uint64_t seed;
     int64_t T, mem, peak;
-    int32_t pool_n;
+    int32_t pool_end, pool_live;
     int32_t uf_n;
     int32_t status, cur_op;
     uint32_t epoch;
     int64_t evict_no;
     int64_t total, base, remat_cost, executed, remats, evictions, eager, scores;
     int64_t nbr, adj;     // per-lane partial sums, reduced at the end
+#ifdef DTR_PROFILE
+    int64_t prof_scan_cycles, prof_scans, prof_rounds;
+#endif
 };
 
-// ---------------------------------------------------------------- pool ----
-
-__device__ __forceinline__ void pool_add(Sim &s, int32_t x)
+__device__ __forceinline__ void set_status(Sim &s, int32_t st)
 {
-    if (s.pool_n >= s.S.n_max) { s.status = ST_CAPACITY; return; }   // a tensor joins at most once
-    int32_t i = s.pool_n++;
-    s.S.pool_id[i] = x;
-    s.S.pool_last[i] = s.S.last[x];
-    s.S.pool_size[i] = s.t.size[x];
-    s.S.pool_c0[i] = s.t.c0[x];
-    s.S.pos[x] = i;
+    if (s.status == ST_OK) s.status = st;
 }
 
-__device__ __forceinline__ void pool_remove(Sim &s, int32_t x)
+// uniform read of a tensor's static record (two 16-byte scalar loads)
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ TRec rec_u(const Sim &s, int32_t x)
 {
-    int32_t i = uni(s.S.pos[x]);
-    int32_t j = --s.pool_n;
-    if (i != j) {
-        int32_t y = uni(s.S.pool_id[j]);
-        int64_t l = s.S.pool_last[j], z = s.S.pool_size[j], c = s.S.pool_c0[j];
-        s.S.pool_id[i] = y;
-        s.S.pool_last[i] = l;
-        s.S.pool_size[i] = z;
-        s.S.pool_c0[i] = c;
-        s.S.pos[y] = i;
+    const __attribute__((address_space(4))) u32x4 *p =
+        (const __attribute__((address_space(4))) u32x4 *)(s.t.rec + x);
+    const u32x4 a = p[0], b = p[1];
+    TRec r;
+    r.size = (int64_t)((uint64_t)a.x | ((uint64_t)a.y << 32));
+    r.c0 = (int32_t)a.z;
+    r.producer = (int32_t)a.w;
+    r.in_b = (int32_t)b.x;
+    r.in_e = (int32_t)b.y;
+    r.adj_b = (int32_t)b.z;
+    r.adj_e = (int32_t)b.w;
+    return r;
+}
+
+// ------------------------------------------------------ neighbour cache --
+
+// This lane's cache of evicted-neighbour nodes for tensor x (neighbour range
+// [b, e)), written to slot i.  Neighbour states are read LB at a time.
+__device__ __forceinline__ void list_build(const Sim &s, int32_t b, int32_t e, int32_t i)
+{
+    int32_t cnt = 0;
+    int32_t *col = s.S.pnb;
+    const int32_t pcap = s.S.pcap;
+    for (int32_t k0 = b; k0 < e; k0 += LB) {
+        int32_t w[LB];
+        int32_t q[LB];
+#pragma unroll
+        for (int j = 0; j < LB; j++) w[j] = k0 + j < e ? s.t.adj[k0 + j] : 0;
+#pragma unroll
+        for (int j = 0; j < LB; j++) q[j] = ts_sw(s.S.tst[w[j]]);
+#pragma unroll
+        for (int j = 0; j < LB; j++) {
+            if (k0 + j >= e || q[j] < 0) continue;
+            if (cnt < K) col[(size_t)cnt * pcap + i] = q[j];
+            cnt++;
+        }
     }
+    if (cnt > K) cnt = K + 1;
+    s.S.pdeg[i] = ((e - b) << 8) | cnt;
 }
 
-__device__ __forceinline__ bool evictable_resident(const Sim &s, int32_t x)
+__device__ __forceinline__ void list_add(const Sim &s, int32_t i, int32_t nd)
 {
-    return s.S.sw[x] == SW_RESIDENT && s.S.locks[x] == 0 && !(s.t.flags[x] & FLAG_CONST);
+    const int32_t pd = s.S.pdeg[i];
+    const int32_t c = pd & 0xFF;
+    if (c > K) return;
+    if (c < K) s.S.pnb[(size_t)c * s.S.pcap + i] = nd;
+    s.S.pdeg[i] = (pd & ~0xFF) | (c + 1);
 }
 
-__device__ __forceinline__ void lock(Sim &s, int32_t u)
+// returns false if nd was not cached (cannot happen while the caches are consistent)
+__device__ __forceinline__ bool list_remove(const Sim &s, int32_t i, int32_t nd)
 {
-    int32_t l = uni(s.S.locks[u]) + 1;
-    s.S.locks[u] = l;
-    if (l == 1 && uni(s.S.sw[u]) == SW_RESIDENT && !(s.t.flags[u] & FLAG_CONST)) pool_remove(s, u);
+    int32_t *col = s.S.pnb;
+    const int32_t pcap = s.S.pcap;
+    const int32_t pd = s.S.pdeg[i];
+    int32_t v[K];
+#pragma unroll
+    for (int k = 0; k < K; k++) v[k] = col[(size_t)k * pcap + i];
+    const int32_t c = pd & 0xFF;
+    if (c > K) return true;
+    int32_t at = -1;
+#pragma unroll
+    for (int k = 0; k < K; k++)
+        if (k < c && v[k] == nd) at = k;
+    if (at < 0) return false;
+    int32_t lastv = v[0];
+#pragma unroll
+    for (int k = 0; k < K; k++)
+        if (k == c - 1) lastv = v[k];
+    col[(size_t)at * pcap + i] = lastv;
+    s.S.pdeg[i] = (pd & ~0xFF) | (c - 1);
+    return true;
 }
 
-__device__ __forceinline__ void unlock(Sim &s, int32_t u)
+// ---------------------------------------------------------------- pool --
+
+// Squeeze tombstones out of the pool (order preserved; positions updated).
+template <int HC>
+__device__ __forceinline__ void pool_compact(Sim &s)
 {
-    int32_t l = uni(s.S.locks[u]) - 1;
-    s.S.locks[u] = l;
-    if (l == 0 && uni(s.S.sw[u]) == SW_RESIDENT && !(s.t.flags[u] & FLAG_CONST)) pool_add(s, u);
+    const int32_t lane = s.lane;
+    const int32_t pcap = s.S.pcap;
+    int32_t kept = 0;
+    __syncthreads();
+    for (int32_t base = 0; base < s.pool_end; base += WAVE) {
+        const int32_t i = base + lane;
+        const int32_t ii = i < s.pool_end ? i : 0;
+        const int32_t x0 = s.S.pid[ii];
+        const int64_t l = s.S.plast[ii], z = s.S.psize[ii], c = s.S.pc0[ii];
+        const int32_t d = s.S.pdeg[ii];
+        int32_t nb[K];
+        if (HC == HC_EQ) {
+#pragma unroll
+            for (int k = 0; k < K; k++) nb[k] = s.S.pnb[(size_t)k * pcap + ii];
+        }
+        const int32_t x = i < s.pool_end ? x0 : -1;
+        const bool keep = x >= 0;
+        const uint64_t m = __ballot(keep);
+        __syncthreads();
+        if (keep) {
+            const int32_t j = kept + lane_rank(m);
+            s.S.pid[j] = x;
+            s.S.plast[j] = l;
+            s.S.psize[j] = z;
+            s.S.pc0[j] = c;
+            s.S.pdeg[j] = d;
+            if (HC == HC_EQ) {
+#pragma unroll
+                for (int k = 0; k < K; k++) s.S.pnb[(size_t)k * pcap + j] = nb[k];
+            }
+            s.S.tst[x] = ts_make(S_RESIDENT, (uint32_t)j, 0);
+        }
+        kept += __popcll(m);
+        __syncthreads();
+    }
+    s.pool_end = kept;
 }
 
-// ---------------------------------------------------------- union-find ----
+// Every lane with `want` appends tensor x (resident, unlocked) with last
+// access `last`; returns its slot (or -1).  The caller stores x's new state.
+template <int HC>
+__device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int64_t last)
+{
+    const uint64_t m = __ballot(want);
+    if (!m) return -1;
+    const int32_t cnt = __popcll(m);
+    if (s.pool_end + cnt > s.S.pcap) {
+        pool_compact<HC>(s);
+        if (s.pool_end + cnt > s.S.pcap) { set_status(s, ST_CAPACITY); return -1; }
+    }
+    int32_t i = -1;
+    if (want) {
+        i = s.pool_end + lane_rank(m);
+        const TRec r = s.t.rec[x];
+        s.S.pid[i] = x;
+        s.S.plast[i] = last;
+        s.S.psize[i] = r.size;
+        s.S.pc0[i] = r.c0;
+        if (HC == HC_EQ) list_build(s, r.adj_b, r.adj_e, i);
+        else s.S.pdeg[i] = (r.adj_e - r.adj_b) << 8;
+    }
+    s.pool_end += cnt;
+    s.pool_live += cnt;
+    return i;
+}
 
-__device__ __forceinline__ int32_t find_ro(const int32_t *parent, int32_t x, int32_t limit)
+// ---------------------------------------------------------- union-find --
+
+__device__ __forceinline__ int32_t find_ro(const UfNode *nodes, int32_t x, int32_t limit)
 {
     for (int32_t k = 0; k <= limit; k++) {
-        int32_t p = parent[x];
+        const int32_t p = nodes[x].parent;
         if (p == x) return x;
         x = p;
     }
     return -1;   // not a forest: reported as a capacity error
 }
 
+// uniform find with path compression (used where one set is touched)
 __device__ __forceinline__ int32_t find_compress(Sim &s, int32_t x)
 {
-    int32_t *P = s.S.uf_parent;
+    UfNode *N = s.S.nodes;
     int32_t root = x;
     for (int32_t k = 0;; k++) {
-        int32_t p = uni(P[root]);
+        const int32_t p = uni(N[root].parent);
         if (p == root) break;
-        if (k > s.uf_n) { s.status = ST_CAPACITY; return x; }
+        if (k > s.uf_n) { set_status(s, ST_CAPACITY); return x; }
         root = p;
     }
     while (x != root) {
-        int32_t nx = uni(P[x]);
-        P[x] = root;
+        const int32_t nx = uni(N[x].parent);
+        N[x].parent = root;
         x = nx;
     }
     return root;
 }
 
+__device__ __forceinline__ int32_t unite(Sim &s, int32_t a, int32_t b)
+{
+    if (a == b) return a;
+    UfNode *N = s.S.nodes;
+    int32_t sa = uni(N[a].size), sb = uni(N[b].size);
+    if (sa < sb) { int32_t t = a; a = b; b = t; int32_t u = sa; sa = sb; sb = u; }
+    const int64_t cost = uni64(N[a].cost) + uni64(N[b].cost);
+    N[b].parent = a;
+    N[a].size = sa + sb;
+    N[a].cost = cost;
+    return a;
+}
+
 // Rebuild the node pool: one node per distinct set that still holds an
 // evicted tensor (sets left with phantom members only are unreachable).
-// Membership and running costs are unchanged, so every later query is too.
+// Membership and running costs are unchanged, so every later score is too;
+// the neighbour caches are rebuilt with the new node ids.
 __device__ __forceinline__ void uf_compact(Sim &s)
 {
     const int32_t lane = s.lane, n = s.t.n;
-    int32_t *P = s.S.uf_parent, *R = s.S.uf_remap, *sw = s.S.sw, *tmp = s.S.pos;
+    UfNode *N = s.S.nodes;
+    int32_t *R = s.S.remap;
+    __syncthreads();
     for (int32_t i = lane; i < s.uf_n; i += WAVE) R[i] = -1;
     __syncthreads();
     for (int32_t x = lane; x < n; x += WAVE) {
-        int32_t v = sw[x];
+        const uint64_t w = s.S.tst[x];
+        const int32_t v = ts_sw(w);
         if (v >= 0) {
-            int32_t r = find_ro(P, v, s.uf_n);
-            if (r < 0) r = v;    // cannot happen in a forest; keeps indices in range
-            tmp[x] = r;          // pos[] is unused while a tensor is evicted
+            int32_t r = find_ro(N, v, s.uf_n);
+            if (r < 0) r = v;        // cannot happen in a forest; keeps indices in range
+            s.S.tst[x] = ts_make(v, (uint32_t)r, ts_locks(w));   // pos is unused while evicted
             R[r] = 0;
         }
     }
     __syncthreads();
     int32_t kept = 0;
     for (int32_t base = 0; base < s.uf_n; base += WAVE) {
-        int32_t i = base + lane;
-        bool keep = i < s.uf_n && R[i] == 0;
-        int64_t c = keep ? s.S.uf_cost[i] : 0;
-        uint64_t m = __ballot(keep);
-        int32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+        const int32_t i = base + lane;
+        const bool keep = i < s.uf_n && R[i] == 0;
+        const int64_t c = keep ? N[i].cost : 0;
+        const uint64_t m = __ballot(keep);
         __syncthreads();
         if (keep) {
-            int32_t ni = kept + rank;
+            const int32_t ni = kept + lane_rank(m);
             R[i] = ni;
-            s.S.uf_cost[ni] = c;
-            P[ni] = ni;
-            s.S.uf_size[ni] = 1;
+            UfNode nd;
+            nd.cost = c;
+            nd.parent = ni;
+            nd.size = 1;
+            N[ni] = nd;
         }
         kept += __popcll(m);
         __syncthreads();
     }
     for (int32_t x = lane; x < n; x += WAVE) {
-        if (sw[x] >= 0) sw[x] = R[tmp[x]];
+        const uint64_t w = s.S.tst[x];
+        if (ts_sw(w) >= 0) s.S.tst[x] = ts_make(R[ts_pos(w)], 0, ts_locks(w));
     }
     __syncthreads();
     s.uf_n = kept;
-}
-
-__device__ __forceinline__ int32_t unite(Sim &s, int32_t a, int32_t b)
-{
-    if (a == b) return a;
-    int32_t sa = uni(s.S.uf_size[a]), sb = uni(s.S.uf_size[b]);
-    if (sa < sb) { int32_t t = a; a = b; b = t; }
-    int64_t cb = uni64(s.S.uf_cost[b]);
-    int64_t ca = uni64(s.S.uf_cost[a]);
-    s.S.uf_parent[b] = a;
-    s.S.uf_size[a] = sa + sb;
-    s.S.uf_cost[a] = ca + cb;
-    return a;
-}
-
-// ------------------------------------------------------------ eviction ----
-
-__device__ __forceinline__ bool evict(Sim &s, int32_t v, bool eager)
-{
-    if (s.h == H_EQ) {
-        if (s.uf_n >= s.S.uf_cap) {
-            uf_compact(s);
-            if (s.uf_n >= s.S.uf_cap) { s.status = ST_CAPACITY; return false; }
+    for (int32_t i = lane; i < s.pool_end; i += WAVE) {
+        const int32_t x = s.S.pid[i];
+        if (x >= 0) {
+            const TRec r = s.t.rec[x];
+            list_build(s, r.adj_b, r.adj_e, i);
         }
-        int32_t nd = s.uf_n++;
-        s.S.uf_parent[nd] = nd;
-        s.S.uf_size[nd] = 1;
-        s.S.uf_cost[nd] = s.t.c0[v];
-        int32_t r = nd;
-        const int32_t b = s.t.adj_off[v], e = s.t.adj_off[v + 1];
-        for (int32_t k = b; k < e; k++) {
-            int32_t w = s.t.adj[k];
-            int32_t q = uni(s.S.sw[w]);
-            if (q >= 0) r = unite(s, r, find_compress(s, q));
-        }
-        s.S.sw[v] = nd;
-    } else {
-        s.S.sw[v] = 0;
     }
-    s.mem -= s.t.size[v];
-    pool_remove(s, v);
+    __syncthreads();
+}
+
+// ------------------------------------------------------------ eviction --
+
+// Evict v (resident, unlocked, in pool slot `slot`).  Under h_DTR^eq, v gets a
+// fresh node holding c0(v), which is merged with the sets of all its evicted
+// neighbours (found in parallel, merged under the largest), and every
+// neighbour waiting in the pool caches the new node.
+template <int HC>
+__device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eager)
+{
+    s.S.pid[slot] = -1;
+    s.pool_live--;
+    const TRec rv = rec_u(s, v);
+    s.mem -= rv.size;
     if (eager) s.eager++;
     else s.evictions++;
+    if (HC != HC_EQ) {
+        s.S.tst[v] = ts_make(0, 0, 0);
+        return true;
+    }
+    if (s.uf_n >= s.S.ucap) {
+        uf_compact(s);
+        if (s.uf_n >= s.S.ucap) { set_status(s, ST_CAPACITY); return false; }
+    }
+    UfNode *N = s.S.nodes;
+    const int32_t nd = s.uf_n++;
+    int32_t R = nd;               // current root of v's set
+    int64_t Rcost = rv.c0;
+    int32_t Rsize = 1;
+    UfNode node;
+    node.cost = rv.c0;
+    node.parent = nd;
+    node.size = 1;
+    if (s.lane == 0) N[nd] = node;
+    bool bad = false;
+    for (int32_t k0 = rv.adj_b; k0 < rv.adj_e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        int32_t q = -1, r = -1;
+        if (k < rv.adj_e) {
+            const uint64_t w = s.S.tst[s.t.adj[k]];
+            q = ts_sw(w);
+            if (ts_in_pool(w)) list_add(s, (int32_t)ts_pos(w), nd);
+            if (q >= 0) {
+                r = find_ro(N, q, s.uf_n);
+                if (r < 0) { bad = true; r = -1; q = -1; }
+            }
+        }
+        // first lane holding each distinct root contributes it
+        bool first = r >= 0;
+        uint64_t m = __ballot(r >= 0);
+        while (m) {
+            const int32_t j = __ffsll((long long)m) - 1;
+            m &= m - 1;
+            const int32_t rj = __shfl(r, j, WAVE);
+            if (r == rj && s.lane > j) first = false;
+        }
+        if (!first || r == R) r = -1;
+        int64_t rc = 0;
+        int32_t rs = 0;
+        if (r >= 0) {
+            const UfNode x = N[r];
+            rc = x.cost;
+            rs = x.size;
+        }
+        // merge every distinct root into the largest (ties: the earliest)
+        uint64_t mr = __ballot(r >= 0);
+        int32_t big = R, bigsize = Rsize;
+        int64_t sumc = Rcost;
+        int32_t sums = Rsize;
+        uint64_t mm = mr;
+        while (mm) {
+            const int32_t j = __ffsll((long long)mm) - 1;
+            mm &= mm - 1;
+            const int32_t rj = uni(__shfl(r, j, WAVE));
+            const int32_t sj = uni(__shfl(rs, j, WAVE));
+            sumc += uni64((int64_t)shfl64((uint64_t)rc, j));
+            sums += sj;
+            if (sj > bigsize) { big = rj; bigsize = sj; }
+        }
+        if (mr) {
+            if (r >= 0 && r != big) N[r].parent = big;
+            if (q >= 0 && q != big) N[q].parent = big;     // compress the neighbour's path
+            if (s.lane == 0 && R != big) N[R].parent = big;
+            R = big;
+            Rcost = sumc;
+            Rsize = sums;
+        }
+    }
+    if (__ballot(bad)) { set_status(s, ST_CAPACITY); return false; }
+    if (s.lane == 0) {
+        N[R].cost = Rcost;
+        N[R].size = Rsize;
+        if (nd != R) N[nd].parent = R;
+    }
+    s.S.tst[v] = ts_make(nd, 0, 0);
     return true;
 }
 
-// ---------------------------------------------------------------- scan ----
+// ---------------------------------------------------------------- scan --
 
-// Neighbourhood cost of candidate x under h_DTR^eq: distinct sets of the
-// evicted parents and children.  The last eight distinct roots are kept in
-// registers; past eight the earlier neighbours are re-checked.
-__device__ __forceinline__ int64_t eq_cost(const Sim &s, int32_t x, int64_t &ev_count, bool &bad)
+// Neighbourhood cost of x under h_DTR^eq from the full adjacency (used when
+// the slot's cache overflowed): distinct sets of the evicted parents and
+// children.
+__device__ __forceinline__ int64_t eq_cost_slow(const Sim &s, int32_t x, int64_t &ev_count, bool &bad)
 {
-    const int32_t b = s.t.adj_off[x], e = s.t.adj_off[x + 1];
-    const int32_t *P = s.S.uf_parent;
-    int32_t r0 = -1, r1 = -1, r2 = -1, r3 = -1, r4 = -1, r5 = -1, r6 = -1, r7 = -1;
-    int32_t distinct = 0;
+    const TRec rx = s.t.rec[x];
+    const int32_t b = rx.adj_b, e = rx.adj_e;
     int64_t sum = 0, cnt = 0;
     for (int32_t k = b; k < e; k++) {
-        int32_t w = s.t.adj[k];
-        int32_t q = s.S.sw[w];
+        const int32_t q = ts_sw(s.S.tst[s.t.adj[k]]);
         if (q < 0) continue;
         cnt++;
-        int32_t r = find_ro(P, q, s.uf_n);
+        const int32_t r = find_ro(s.S.nodes, q, s.uf_n);
         if (r < 0) { bad = true; break; }
-        bool dup = (r == r0) | (r == r1) | (r == r2) | (r == r3) | (r == r4) | (r == r5) | (r == r6) | (r == r7);
-        if (!dup && distinct > 8) {
-            for (int32_t j = b; j < k && !dup; j++) {
-                int32_t q2 = s.S.sw[s.t.adj[j]];
-                if (q2 >= 0 && find_ro(P, q2, s.uf_n) == r) dup = true;
-            }
+        bool dup = false;
+        for (int32_t j = b; j < k && !dup; j++) {
+            const int32_t q2 = ts_sw(s.S.tst[s.t.adj[j]]);
+            if (q2 >= 0 && find_ro(s.S.nodes, q2, s.uf_n) == r) dup = true;
         }
-        if (!dup) {
-            sum += s.S.uf_cost[r];
-            r7 = r6; r6 = r5; r5 = r4; r4 = r3; r3 = r2; r2 = r1; r1 = r0; r0 = r;
-            distinct++;
-        }
+        if (!dup) sum += s.S.nodes[r].cost;
     }
     ev_count = cnt;
     return sum;
@@ -328,16 +559,15 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
     int32_t head = 0, tail = 0;
     q[(size_t)tail++ * WAVE + lane] = x;
     while (head < tail) {
-        int32_t u = q[(size_t)head++ * WAVE + lane];
-        int32_t o = s.t.producer[u];
-        if (o < 0) continue;
-        for (int32_t k = s.t.in_off[o], e = s.t.in_off[o + 1]; k < e; k++) {
-            int32_t p = s.t.in[k];
-            if (s.S.sw[p] < 0) continue;
-            size_t sp = (size_t)p * WAVE + lane;
+        const int32_t u = q[(size_t)head++ * WAVE + lane];
+        const TRec ru = s.t.rec[u];
+        for (int32_t k = ru.in_b; k < ru.in_e; k++) {
+            const int32_t p = s.t.in[k];
+            if (ts_sw(s.S.tst[p]) < 0) continue;
+            const size_t sp = (size_t)p * WAVE + lane;
             if (st[sp] == ep) continue;
             st[sp] = ep;
-            sum += s.t.c0[p];
+            sum += s.t.rec[p].c0;
             cnt++;
             q[(size_t)tail++ * WAVE + lane] = p;
         }
@@ -345,14 +575,14 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
     head = tail = 0;
     q[(size_t)tail++ * WAVE + lane] = x;
     while (head < tail) {
-        int32_t u = q[(size_t)head++ * WAVE + lane];
+        const int32_t u = q[(size_t)head++ * WAVE + lane];
         for (int32_t k = s.t.ch_off[u], e = s.t.ch_off[u + 1]; k < e; k++) {
-            int32_t c = s.t.ch[k];
-            if (s.S.sw[c] < 0) continue;
-            size_t sc = (size_t)c * WAVE + lane;
+            const int32_t c = s.t.ch[k];
+            if (ts_sw(s.S.tst[c]) < 0) continue;
+            const size_t sc = (size_t)c * WAVE + lane;
             if (st[sc] == ep) continue;
             st[sc] = ep;
-            sum += s.t.c0[c];
+            sum += s.t.rec[c].c0;
             cnt++;
             q[(size_t)tail++ * WAVE + lane] = c;
         }
@@ -363,179 +593,419 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
 
 __device__ __forceinline__ void clear_stamps(Sim &s)
 {
+    __syncthreads();
     for (size_t i = s.lane; i < (size_t)s.t.n * WAVE; i += WAVE) s.S.stamp[i] = 0;
     __syncthreads();
     s.epoch = 0;
 }
 
-// Score every pool entry; return the victim (uniform), or -1 if the pool is empty.
-__device__ __forceinline__ int32_t scan(Sim &s)
+struct Best {
+    uint64_t N;
+    u128 D;
+    int32_t id, slot, have;
+};
+
+// keep (N, D, id) if valid and better than the current best (selects, no branch)
+__device__ __forceinline__ void take(Best &b, bool valid, uint64_t N, u128 D, int32_t id, int32_t slot)
 {
-    const int32_t n_pool = s.pool_n;
-    const int32_t lane = s.lane;
-    const int64_t T = s.T;
-    bool have = false, bad = false;
-    uint64_t bN = 0;
-    u128 bD = 1;
-    int32_t bid = 0x7fffffff;
-    if ((s.h == H_DTR || s.h == H_ESTAR) &&
-        (uint64_t)s.epoch + (uint64_t)(n_pool / WAVE) + 2 >= 0xffffffffull)
-        clear_stamps(s);
-    for (int32_t i0 = 0; i0 < n_pool; i0 += WAVE) {
-        const int32_t i = i0 + lane;
-        const uint32_t ep = ++s.epoch;   // uniform; one walk per lane per round
-        if (i >= n_pool) continue;
-        const int32_t x = s.S.pool_id[i];
-        uint64_t N;
-        u128 D;
-        switch (s.h) {
-        case H_LRU: {
-            N = 1;
-            D = (u128)(uint64_t)(T - s.S.pool_last[i]);
-            break;
-        }
-        case H_SIZE: {
-            N = 1;
-            D = (u128)(uint64_t)s.S.pool_size[i];
-            break;
-        }
-        case H_RAND: {
-            uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)x;
-            N = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
-            D = 1;
-            break;
-        }
-        case H_LOCAL: {
-            N = (uint64_t)s.S.pool_c0[i];
-            D = (u128)(uint64_t)s.S.pool_size[i] * (u128)(uint64_t)(T - s.S.pool_last[i]);
-            break;
-        }
-        case H_EQ: {
-            int64_t ev;
-            N = (uint64_t)(s.S.pool_c0[i] + eq_cost(s, x, ev, bad));
-            D = (u128)(uint64_t)s.S.pool_size[i] * (u128)(uint64_t)(T - s.S.pool_last[i]);
-            s.nbr += ev;
-            s.adj += s.t.adj_off[x + 1] - s.t.adj_off[x];
-            break;
-        }
-        default: {   // H_DTR, H_ESTAR
-            int64_t cnt;
-            N = (uint64_t)(s.S.pool_c0[i] + estar_cost(s, x, ep, cnt));
-            if (s.h == H_DTR)
-                D = (u128)(uint64_t)s.S.pool_size[i] * (u128)(uint64_t)(T - s.S.pool_last[i]);
-            else
-                D = (u128)(uint64_t)s.S.pool_size[i];
-            s.nbr += cnt;
-            s.adj += s.t.adj_off[x + 1] - s.t.adj_off[x];
-            break;
-        }
-        }
-        if (!have || better(N, D, x, bN, bD, bid)) {
-            have = true;
-            bN = N;
-            bD = D;
-            bid = x;
-        }
-    }
-    // cross-lane lexicographic minimum
-    int32_t hv = have ? 1 : 0;
-    for (int off = WAVE / 2; off >= 1; off >>= 1) {
-        uint64_t oN = __shfl_xor(bN, off, WAVE);
-        uint64_t oDl = __shfl_xor((uint64_t)bD, off, WAVE);
-        uint64_t oDh = __shfl_xor((uint64_t)(bD >> 64), off, WAVE);
-        int32_t oid = __shfl_xor(bid, off, WAVE);
-        int32_t oh = __shfl_xor(hv, off, WAVE);
-        u128 oD = ((u128)oDh << 64) | oDl;
-        if (oh && (!hv || better(oN, oD, oid, bN, bD, bid))) {
-            hv = 1;
-            bN = oN;
-            bD = oD;
-            bid = oid;
-        }
-    }
-    if (__ballot(bad)) { s.status = ST_CAPACITY; return -1; }
-    return uni(hv) ? uni(bid) : -1;
+    const bool t = valid && (!b.have || better(N, D, id, b.N, b.D, b.id));
+    b.N = t ? N : b.N;
+    b.D = t ? D : b.D;
+    b.id = t ? id : b.id;
+    b.slot = t ? slot : b.slot;
+    b.have = t ? 1 : b.have;
 }
 
-// ----------------------------------------------------- operator calls ----
+// Score every pool entry; return the victim (uniform) and its slot, or -1.
+template <int HC>
+__device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
+{
+    const int32_t end = s.pool_end;
+    const int32_t lane = s.lane;
+    const int32_t pcap = s.S.pcap;
+    const int64_t T = s.T;
+    const int32_t h = s.h;
+    bool bad = false;
+    Best best;
+    best.N = 0;
+    best.D = 1;
+    best.id = 0x7fffffff;
+    best.slot = -1;
+    best.have = 0;
+    if (HC == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
+        clear_stamps(s);
+    for (int32_t base = 0; base < end; base += WAVE * U) {
+        int32_t idx[U], id[U], pd[U];
+        int64_t last[U], size[U], c0[U];
+        int32_t nb[U][K];
+        // level 1: every slot column at once (index clamped into the array)
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int32_t i = base + u * WAVE + lane;
+            idx[u] = i < end ? i : 0;
+            id[u] = s.S.pid[idx[u]];
+            last[u] = s.S.plast[idx[u]];
+            size[u] = s.S.psize[idx[u]];
+            c0[u] = s.S.pc0[idx[u]];
+            pd[u] = s.S.pdeg[idx[u]];
+            if (HC == HC_EQ) {
+#pragma unroll
+                for (int k = 0; k < K; k++) nb[u][k] = s.S.pnb[(size_t)k * pcap + idx[u]];
+            }
+            if (i >= end) id[u] = -1;
+        }
+        uint64_t N[U];
+        u128 D[U];
+        bool ok[U];
+#pragma unroll
+        for (int u = 0; u < U; u++) ok[u] = id[u] >= 0;
+        if (HC == HC_EQ) {
+            // level 2: every cached neighbour node at once (unused entries read node 0)
+            int64_t ncost[U][K];
+            int32_t npar[U][K];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int32_t c = pd[u] & 0xFF;
+#pragma unroll
+                for (int k = 0; k < K; k++) {
+                    const bool use = ok[u] && k < c && c <= K;
+                    const UfNode nd = s.S.nodes[use ? nb[u][k] : 0];
+                    ncost[u][k] = use ? nd.cost : 0;
+                    npar[u][k] = use ? nd.parent : nb[u][k];
+                }
+            }
+            // level 3 (rare): cached node is no longer a root
+            bool deep = false;
+#pragma unroll
+            for (int u = 0; u < U; u++)
+#pragma unroll
+                for (int k = 0; k < K; k++) deep |= npar[u][k] != nb[u][k];
+            if (deep) {
+#pragma unroll
+                for (int u = 0; u < U; u++)
+#pragma unroll
+                    for (int k = 0; k < K; k++) {
+                        if (npar[u][k] == nb[u][k]) continue;
+                        int32_t q = find_ro(s.S.nodes, npar[u][k], s.uf_n);
+                        if (q < 0) { bad = true; q = nb[u][k]; }
+                        nb[u][k] = q;
+                        ncost[u][k] = s.S.nodes[q].cost;
+                    }
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int32_t c = pd[u] & 0xFF;
+                // distinct roots among the cached entries (branch-free)
+                int64_t sum = 0;
+#pragma unroll
+                for (int k = 0; k < K; k++) {
+                    bool dup = false;
+#pragma unroll
+                    for (int j = 0; j < k; j++) dup |= nb[u][j] == nb[u][k];
+                    sum += (k < c && !dup) ? ncost[u][k] : 0;
+                }
+                int64_t ev = c;
+                if (ok[u] && c > K) sum = eq_cost_slow(s, id[u], ev, bad);   // overflowed cache (rare)
+                N[u] = (uint64_t)(c0[u] + sum);
+                D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
+                s.nbr += ok[u] ? ev : 0;
+                s.adj += ok[u] ? (pd[u] >> 8) : 0;
+            }
+        } else if (HC == HC_WALK) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                N[u] = 0;
+                D[u] = 1;
+                if (!ok[u]) continue;
+                int64_t cnt;
+                const uint32_t ep = s.epoch + 1 + (uint32_t)u;
+                N[u] = (uint64_t)(c0[u] + estar_cost(s, id[u], ep, cnt));
+                if (h == H_DTR)
+                    D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
+                else
+                    D[u] = (u128)(uint64_t)size[u];
+                s.nbr += cnt;
+                s.adj += pd[u] >> 8;
+            }
+            s.epoch += U;
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                switch (h) {
+                case H_LRU:
+                    N[u] = 1;
+                    D[u] = (u128)(uint64_t)(T - last[u]);
+                    break;
+                case H_SIZE:
+                    N[u] = 1;
+                    D[u] = (u128)(uint64_t)size[u];
+                    break;
+                case H_RAND: {
+                    const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
+                    N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
+                    D[u] = 1;
+                    break;
+                }
+                default:     // H_LOCAL
+                    N[u] = (uint64_t)c0[u];
+                    D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
+                    break;
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) take(best, ok[u], N[u], D[u], id[u], idx[u]);
+    }
+    // cross-lane lexicographic minimum
+    for (int off = WAVE / 2; off >= 1; off >>= 1) {
+        const uint64_t oN = __shfl_xor(best.N, off, WAVE);
+        const uint64_t oDl = __shfl_xor((uint64_t)best.D, off, WAVE);
+        const uint64_t oDh = __shfl_xor((uint64_t)(best.D >> 64), off, WAVE);
+        const int32_t oid = __shfl_xor(best.id, off, WAVE);
+        const int32_t oslot = __shfl_xor(best.slot, off, WAVE);
+        const int32_t oh = __shfl_xor(best.have, off, WAVE);
+        take(best, oh != 0, oN, ((u128)oDh << 64) | oDl, oid, oslot);
+    }
+    if (__ballot(bad)) { set_status(s, ST_CAPACITY); return -1; }
+    if (!uni(best.have)) return -1;
+    victim_slot = uni(best.slot);
+    return uni(best.id);
+}
 
+// ----------------------------------------------------- operator calls --
+
+template <int HC>
 __device__ __forceinline__ bool allocate(Sim &s, int64_t sz)
 {
     while (s.mem + sz > s.budget) {
-        if (s.pool_n == 0) { s.status = ST_OOM; return false; }
-        int32_t v = scan(s);
-        if (s.status != ST_OK) return false;
-        s.scores += s.pool_n;
-        if (!evict(s, v, false)) return false;
+        if (s.pool_live == 0) { set_status(s, ST_OOM); return false; }
+        // keep the scanned range at most about twice the live pool
+        if (s.pool_end > 2 * s.pool_live + WAVE * U) pool_compact<HC>(s);
+#ifdef DTR_PROFILE
+        const int64_t c0_ = (int64_t)__builtin_readcyclecounter();
+        s.prof_scans++;
+        s.prof_rounds += (s.pool_end + WAVE * U - 1) / (WAVE * U);
+#endif
+        int32_t slot = -1;
+        const int32_t v = scan<HC>(s, slot);
+#ifdef DTR_PROFILE
+        s.prof_scan_cycles += (int64_t)__builtin_readcyclecounter() - c0_;
+#endif
+        if (v < 0) { set_status(s, ST_CAPACITY); return false; }
+        s.scores += s.pool_live;
+        if (!evict<HC>(s, v, slot, false)) return false;
         s.evict_no++;
     }
     return true;
 }
 
-__device__ __forceinline__ bool execute(Sim &s, int32_t o, int32_t t, bool remat)
+// Frame of the explicit rematerialization stack: while a frame is current,
+// lane k holds input k's id and state word (operations with more inputs than
+// lanes use the chunked path).
+struct Frame {
+    int32_t u;        // this lane's input (or -1)
+    uint64_t w;       // its state word, lock included
+};
+
+// lock inputs ids[b..e) (one lane per input); tensors that were evictable
+// leave the pool.  Fills f for single-chunk operations.
+__device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t b, int32_t e, Frame &f)
 {
-    const int32_t b = s.t.in_off[o], e = s.t.in_off[o + 1];
-    for (int32_t k = b; k < e; k++) s.S.last[s.t.in[k]] = s.T;
-    s.S.last[t] = s.T;
-    const int64_t c = s.t.cost[o];
+    for (int32_t k0 = b; k0 < e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        bool killed = false, over = false;
+        int32_t u = -1;
+        uint64_t nw = 0;
+        if (k < e) {
+            u = ids[k];
+            const uint64_t w = s.S.tst[u];
+            const uint32_t l = ts_locks(w);
+            nw = ts_make(ts_sw(w), ts_pos(w), l + 1);
+            if (l >= MAX_LOCKS) over = true;
+            else {
+                if (ts_in_pool(w)) {
+                    s.S.pid[ts_pos(w)] = -1;
+                    killed = true;
+                }
+                s.S.tst[u] = nw;
+            }
+        }
+        if (k0 == b) {
+            f.u = u;
+            f.w = nw;
+        }
+        s.pool_live -= __popcll(__ballot(killed));
+        if (__ballot(over)) set_status(s, ST_CAPACITY);
+    }
+}
+
+// reload a frame's inputs after returning from nested rematerializations
+__device__ __forceinline__ void reload_frame(const Sim &s, int32_t b, int32_t e, Frame &f)
+{
+    const int32_t k = b + s.lane;
+    f.u = k < e ? s.t.in[k] : -1;
+    f.w = f.u >= 0 ? s.S.tst[f.u] : 0;
+}
+
+// unlock inputs [b, e); tensors left unlocked and resident rejoin the pool
+// with last access `last`
+template <int HC>
+__device__ __forceinline__ void unlock_inputs(Sim &s, int32_t b, int32_t e, int64_t last, const Frame &f)
+{
+    for (int32_t k0 = b; k0 < e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        int32_t u = -1;
+        uint64_t w = 0;
+        if (k < e) {
+            if (k0 == b) {
+                u = f.u;
+                w = f.w;
+            } else {
+                u = s.t.in[k];
+                w = s.S.tst[u];
+            }
+        }
+        const bool join = k < e && ts_locks(w) == 1 && ts_sw(w) == S_RESIDENT;
+        const int32_t slot = pool_append<HC>(s, join, u, last);
+        if (k < e) s.S.tst[u] = ts_make(ts_sw(w), join ? (uint32_t)slot : ts_pos(w), ts_locks(w) - 1);
+    }
+}
+
+// index (relative to b) of the first evicted input at or after `from`, or e - b
+__device__ __forceinline__ int32_t next_evicted(const Sim &s, int32_t b, int32_t e, int32_t from, const Frame &f)
+{
+    const bool ev0 = s.lane >= from && b + s.lane < e && ts_sw(f.w) >= 0;
+    const uint64_t m0 = __ballot(ev0);
+    if (m0) return __ffsll((long long)m0) - 1;
+    for (int32_t k0 = b + WAVE; k0 < e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        bool ev = false;
+        if (k < e && k - b >= from) ev = ts_sw(s.S.tst[s.t.in[k]]) >= 0;
+        const uint64_t m = __ballot(ev);
+        if (m) return k0 - b + __ffsll((long long)m) - 1;
+    }
+    return e - b;
+}
+
+// run the parent operation of t (record rt); its start time is the last
+// access of its inputs and output
+template <int HC>
+__device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool remat, uint32_t locks)
+{
+    const int64_t c = rt.c0;
     s.T += c;
     s.total += c;
     s.executed++;
     if (remat) { s.remats++; s.remat_cost += c; }
     else s.base += c;
-    s.mem += s.t.size[t];
+    s.mem += rt.size;
     if (s.mem > s.peak) s.peak = s.mem;
-    if (s.h == H_EQ && remat) {
-        int32_t r = find_compress(s, uni(s.S.sw[t]));
-        s.S.uf_cost[r] = uni64(s.S.uf_cost[r]) - s.t.c0[t];
+    if (HC == HC_EQ && remat) {
+        // split approximation: the set loses c0(t); t leaves it (its node stays as a phantom)
+        const int32_t old = uni(ts_sw(s.S.tst[t]));
+        const int32_t r = find_compress(s, old);
+        s.S.nodes[r].cost = uni64(s.S.nodes[r].cost) - c;
+        bool lost = false;
+        for (int32_t k0 = rt.adj_b; k0 < rt.adj_e; k0 += WAVE) {
+            const int32_t k = k0 + s.lane;
+            if (k < rt.adj_e) {
+                const uint64_t wx = s.S.tst[s.t.adj[k]];
+                if (ts_in_pool(wx) && !list_remove(s, (int32_t)ts_pos(wx), old)) lost = true;
+            }
+        }
+        if (__ballot(lost)) set_status(s, ST_CAPACITY);
     }
-    s.S.sw[t] = SW_RESIDENT;
-    if (s.T >= CLOCK_LIMIT) { s.status = ST_CLOCK; return false; }
-    return true;
+    s.S.tst[t] = ts_make(S_RESIDENT, 0, locks);
+    if (s.T >= CLOCK_LIMIT) { set_status(s, ST_CLOCK); return false; }
+    return s.status == ST_OK;
 }
 
 // Run the operation producing `root` together with every rematerialization it
 // needs (explicit stack instead of recursion).  root_remat: the root itself is
-// a rematerialization (output condition).  Returns false once the simulation
-// has stopped.
-__device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat)
+// a rematerialization held by the output condition.  Returns false once the
+// simulation has stopped.
+template <int HC>
+__device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint32_t root_locks)
 {
     int32_t sp = 0;
     int32_t tt = root, cur = -1;
+    uint32_t tlocks = root_locks;     // locks held on tt by the frame below
     bool remat = root_remat;
+    Frame f;
+    f.u = -1;
+    f.w = 0;
     for (;;) {
-        const int32_t o = uni(s.t.producer[tt]);
-        const int32_t b = uni(s.t.in_off[o]), e = uni(s.t.in_off[o + 1]);
+        const TRec rt = rec_u(s, tt);
+        const int32_t b = rt.in_b, e = rt.in_e;
         if (cur < 0) {
-            for (int32_t k = b; k < e; k++) lock(s, uni(s.t.in[k]));
+            lock_inputs(s, s.t.in, b, e, f);
+            if (s.status != ST_OK) return false;
             cur = 0;
         }
-        if (cur < e - b) {
-            const int32_t u = uni(s.t.in[b + cur]);
-            cur++;
-            if (uni(s.S.sw[u]) >= 0) {
-                if (sp + 1 >= s.S.n_max) { s.status = ST_CAPACITY; return false; }
-                s.S.stack[2 * sp] = tt;
-                s.S.stack[2 * sp + 1] = cur;
-                sp++;
-                tt = u;
-                cur = -1;
-                remat = true;
-            }
+        const int32_t j = uni(next_evicted(s, b, e, cur, f));
+        if (j < e - b) {
+            if (sp + 1 >= s.S.n_max) { set_status(s, ST_CAPACITY); return false; }
+            const int32_t child = uni(j < WAVE ? __shfl(f.u, j, WAVE) : cld(s.t.in + b + j));
+            const uint32_t clocks = j < WAVE ? (uint32_t)uni((int32_t)ts_locks(shfl64(f.w, j)))
+                                             : (uint32_t)uni((int32_t)ts_locks(s.S.tst[child]));
+            s.S.stack[sp] = make_int2(tt, j + 1);
+            sp++;
+            tt = child;
+            tlocks = clocks;
+            cur = -1;
+            remat = true;
             continue;
         }
-        if (s.status != ST_OK || !allocate(s, s.t.size[tt])) return false;
-        if (!execute(s, o, tt, remat)) return false;
-        for (int32_t k = b; k < e; k++) unlock(s, uni(s.t.in[k]));
-        if (uni(s.S.locks[tt]) == 0) pool_add(s, tt);
+        if (!allocate<HC>(s, rt.size)) return false;
+        const int64_t start = s.T;
+        if (!execute<HC>(s, tt, rt, remat, tlocks)) return false;
+        unlock_inputs<HC>(s, b, e, start, f);
+        if (!remat) {
+            // a trace operation's output is unlocked: it joins the pool at once
+            const int32_t slot = uni(pool_append<HC>(s, s.lane == 0, tt, start));
+            s.S.tst[tt] = ts_make(S_RESIDENT, (uint32_t)slot, 0);
+        }
+        if (s.status != ST_OK) return false;
         if (sp == 0) return true;
         sp--;
-        tt = uni(s.S.stack[2 * sp]);
-        cur = uni(s.S.stack[2 * sp + 1]);
+        const int2 fr = s.S.stack[sp];
+        tt = uni(fr.x);
+        cur = uni(fr.y);
         remat = sp > 0 ? true : root_remat;
+        const TRec rp = rec_u(s, tt);
+        reload_frame(s, rp.in_b, rp.in_e, f);
+        // locks on the resumed frame's output: none for a trace operation,
+        // else whatever its consumers (or the output condition) hold
+        tlocks = remat ? (uint32_t)uni((int32_t)ts_locks(s.S.tst[tt])) : 0u;
     }
 }
 
+// eager eviction of the tensors released after op o (ascending id)
+template <int HC>
+__device__ __forceinline__ bool release(Sim &s, int32_t o)
+{
+    const int32_t b = uni(cld(s.t.rel_off + o)), e = uni(cld(s.t.rel_off + o + 1));
+    for (int32_t k0 = b; k0 < e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        int32_t r = -1, pos = 0;
+        bool ev = false;
+        if (k < e) {
+            r = s.t.rel[k];
+            const uint64_t w = s.S.tst[r];
+            ev = ts_in_pool(w);
+            pos = (int32_t)ts_pos(w);
+        }
+        uint64_t m = __ballot(ev);
+        while (m) {
+            const int32_t j = __ffsll((long long)m) - 1;
+            m &= m - 1;
+            if (!evict<HC>(s, uni(__shfl(r, j, WAVE)), uni(__shfl(pos, j, WAVE)), true)) return false;
+        }
+    }
+    return true;
+}
+
+template <int HC>
 __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const Slot &S, int32_t lane)
 {
     Sim s;
@@ -547,7 +1017,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.budget = sp.budget;
     s.seed = sp.seed;
     s.T = 0;
-    s.pool_n = 0;
+    s.pool_end = s.pool_live = 0;
     s.uf_n = 0;
     s.status = ST_OK;
     s.cur_op = 0;
@@ -555,35 +1025,35 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.evict_no = 0;
     s.total = s.base = s.remat_cost = s.executed = s.remats = s.evictions = s.eager = s.scores = 0;
     s.nbr = s.adj = 0;
+#ifdef DTR_PROFILE
+    const int64_t t_start = (int64_t)__builtin_readcyclecounter();
+    s.prof_scan_cycles = s.prof_scans = s.prof_rounds = 0;
+#endif
 
     const int32_t n = s.t.n;
-    for (int32_t x = lane; x < n; x += WAVE) {
-        s.S.sw[x] = (s.t.flags[x] & FLAG_CONST) ? SW_RESIDENT : SW_UNCOMPUTED;
-        s.S.locks[x] = 0;
-        s.S.last[x] = 0;
-    }
-    if (s.h == H_DTR || s.h == H_ESTAR) clear_stamps(s);
+    for (int32_t x = lane; x < n; x += WAVE)
+        s.S.tst[x] = ts_make((s.t.flags[x] & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
+    if (HC == HC_WALK) clear_stamps(s);
     __syncthreads();
     s.mem = s.t.const_mem;
     s.peak = s.mem;
 
     bool ok = true;
-    if (s.mem > s.budget) { s.status = ST_OOM; ok = false; }
+    if (s.mem > s.budget) { set_status(s, ST_OOM); ok = false; }
     for (int32_t o = 0; ok && o < s.t.F; o++) {
         s.cur_op = o;
-        if (!call(s, uni(s.t.out[o]), false) || s.status != ST_OK) { ok = false; break; }
-        for (int32_t k = uni(s.t.rel_off[o]), e = uni(s.t.rel_off[o + 1]); ok && k < e; k++) {
-            const int32_t r = uni(s.t.rel[k]);
-            if (evictable_resident(s, r) && !evict(s, r, true)) ok = false;
-        }
-        if (s.status != ST_OK) ok = false;
+        if (!call<HC>(s, uni(cld(s.t.out + o)), false, 0) || !release<HC>(s, o) || s.status != ST_OK) ok = false;
     }
     if (ok) {
+        // output condition: lock each required output, rematerialize it if evicted
         s.cur_op = s.t.F;
-        for (int32_t k = 0; k < s.t.n_req; k++) {
-            const int32_t r = uni(s.t.req[k]);
-            lock(s, r);
-            if (uni(s.S.sw[r]) >= 0 && !call(s, r, true)) { ok = false; break; }
+        for (int32_t k = 0; ok && k < s.t.n_req; k++) {
+            Frame f;
+            lock_inputs(s, s.t.req, k, k + 1, f);
+            const int32_t r = uni(cld(s.t.req + k));
+            const uint64_t w = shfl64(f.w, 0);
+            if (s.status != ST_OK) ok = false;
+            else if (ts_sw(w) >= 0 && !call<HC>(s, r, true, (uint32_t)uni((int32_t)ts_locks(w)))) ok = false;
         }
     }
 
@@ -592,6 +1062,15 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
         nbr += __shfl_xor(nbr, off, WAVE);
         adj += __shfl_xor(adj, off, WAVE);
     }
+#ifdef DTR_PROFILE
+    if (lane == 0 && a.prof) {
+        int64_t *pr = a.prof + (size_t)sim * PROF_FIELDS;
+        pr[0] = (int64_t)__builtin_readcyclecounter() - t_start;
+        pr[1] = s.prof_scan_cycles;
+        pr[2] = s.prof_scans;
+        pr[3] = s.prof_rounds;
+    }
+#endif
     if (lane == 0) {
         ResultDev r;
         r.total_cost = s.total;
@@ -613,6 +1092,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     __syncthreads();
 }
 
+template <int HC>
 __global__ void __launch_bounds__(WAVE) replay_kernel(KernelArgs a)
 {
     const int32_t lane = threadIdx.x;
@@ -622,21 +1102,28 @@ __global__ void __launch_bounds__(WAVE) replay_kernel(KernelArgs a)
         if (lane == 0) k = atomicAdd(a.queue, 1u);
         k = (uint32_t)uni((int32_t)k);
         if (k >= (uint32_t)a.n_sims) break;
-        run_sim(a, a.order[k], S, lane);
+        run_sim<HC>(a, a.order[k], S, lane);
     }
 }
 
-__global__ void reset_kernel(uint32_t *queue)
+__global__ void reset_kernel(uint32_t *queue, int32_t n)
 {
-    if (threadIdx.x == 0) *queue = 0;
+    if ((int32_t)threadIdx.x < n) queue[threadIdx.x] = 0;
 }
 
 }  // namespace dtr
 
-// launch entry used by the host library (same shared object)
+// Launch entry used by the host library (same shared object): args[c] holds
+// the simulations of heuristic class c (h_DTR^eq; h_DTR and h_{e*}; the
+// rest), each with its own work counter; empty classes are skipped.
 extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream)
 {
-    hipLaunchKernelGGL(dtr::reset_kernel, dim3(1), dim3(dtr::WAVE), 0, stream, args->queue);
-    hipLaunchKernelGGL(dtr::replay_kernel, dim3(args->n_slots), dim3(dtr::WAVE), 0, stream, *args);
+    hipLaunchKernelGGL(dtr::reset_kernel, dim3(1), dim3(dtr::WAVE), 0, stream, args[0].queue, 3);
+    if (args[0].n_sims > 0)
+        hipLaunchKernelGGL(dtr::replay_kernel<dtr::HC_EQ>, dim3(args[0].n_slots), dim3(dtr::WAVE), 0, stream, args[0]);
+    if (args[1].n_sims > 0)
+        hipLaunchKernelGGL(dtr::replay_kernel<dtr::HC_WALK>, dim3(args[1].n_slots), dim3(dtr::WAVE), 0, stream, args[1]);
+    if (args[2].n_sims > 0)
+        hipLaunchKernelGGL(dtr::replay_kernel<dtr::HC_SIMPLE>, dim3(args[2].n_slots), dim3(dtr::WAVE), 0, stream, args[2]);
     return hipGetLastError();
 }
