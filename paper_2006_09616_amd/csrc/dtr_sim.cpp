@@ -253,14 +253,9 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     L.ucap = need_uf ? 2 * (int64_t)n + 64 : 0;
     const size_t pc = (size_t)L.pcap;
     take(L.tst, 8 * n);
-    take(L.pid, 4 * pc);
-    take(L.plast, 8 * pc);
-    take(L.psize, 8 * pc);
-    take(L.pc0, 8 * pc);
-    take(L.pdeg, 4 * pc);
-    take(L.pnb, need_uf ? 4 * pc * dtr::NB_CACHE : 0);
+    take(L.pool, sizeof(dtr::PoolSlot) * pc);
     take(L.nodes, sizeof(dtr::UfNode) * (size_t)L.ucap);
-    take(L.uf_remap, 4 * (size_t)L.ucap);
+    take(L.uf_remap, need_uf ? 4 * ((size_t)L.ucap + dtr::UF_LDS) : 0);
     take(L.stack, 8 * (n + 1));
     take(L.stamp, need_walk ? 4 * n * dtr::WAVE : 0);
     take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);

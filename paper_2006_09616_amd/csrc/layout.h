@@ -76,25 +76,38 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 // base, each 256-byte aligned.
 //   tst       per-tensor state word: state/union-find node (32 bits), pool
 //             position (24 bits), lock count (8 bits)
-//   pool      evictable tensors, struct of arrays over pcap slots (dead slots
-//             are tombstoned and squeezed out when the array fills):
-//             id, last access, size, c0, packed (degree << 8 | n), and for
-//             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
-//             neighbours (n = NB_CACHE + 1 marks an overflowed list)
+//   pool      evictable tensors, pcap 48-byte slots (dead slots are
+//             tombstoned and squeezed out): id, packed (degree << 8 | n), last
+//             access, size, c0, and for h_DTR^eq the union-find nodes of up
+//             to NB_CACHE evicted neighbours (n = NB_CACHE + 1 marks an
+//             overflowed cache)
 //   nodes     union-find nodes {running cost, parent, size}
 //   stack     rematerialization frames (tensor, next input)
 //   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
 constexpr int NB_CACHE = 4;
+// union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
+// the rest in the slot's global node array
+constexpr int UF_LDS = 1024;
 
 struct SlotLayout {
     int64_t bytes;           // stride between slots
     int64_t tst;
-    int64_t pid, plast, psize, pc0, pdeg, pnb;
+    int64_t pool;
     int64_t nodes, uf_remap;
     int64_t stack;
     int64_t stamp, queue;
     int64_t pcap, ucap, n_max;
 };
+
+struct __attribute__((aligned(16))) PoolSlot {
+    int32_t id;              // tensor; -1 marks a dead slot
+    int32_t deg;             // degree << 8 | cached neighbour count
+    int64_t last;            // last access
+    int64_t size;
+    int64_t c0;
+    int32_t nb[NB_CACHE];    // cached union-find nodes of evicted neighbours
+};
+static_assert(sizeof(PoolSlot) == 48, "pool slot layout");
 
 struct __attribute__((aligned(16))) UfNode {
     int64_t cost;

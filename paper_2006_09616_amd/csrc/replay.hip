@@ -109,13 +109,21 @@ __device__ __forceinline__ bool better(uint64_t na, u128 da, int32_t ia, uint64_
     return ia < ib;
 }
 
+// Union-find node store: ids below UF_LDS in this wavefront's LDS array, the
+// rest in the slot's global array; one id space, read through flat pointers.
+struct NodeStore {
+    UfNode *lds;
+    UfNode *glob;
+    __device__ __forceinline__ UfNode &operator[](int32_t id) const
+    {
+        return id < UF_LDS ? lds[id] : glob[id - UF_LDS];
+    }
+};
+
 struct Slot {
     uint64_t *tst;
-    int32_t *pid;
-    int64_t *plast, *psize, *pc0;
-    int32_t *pdeg;     // degree << 8 | cached neighbour count
-    int32_t *pnb;      // K columns of pcap
-    UfNode *nodes;
+    PoolSlot *pool;
+    NodeStore nodes;
     int32_t *remap;
     int2 *stack;
     uint32_t *stamp;
@@ -128,13 +136,9 @@ __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
     uint8_t *b = a.slots + (size_t)k * (size_t)a.L.bytes;
     Slot S;
     S.tst = (uint64_t *)(b + a.L.tst);
-    S.pid = (int32_t *)(b + a.L.pid);
-    S.plast = (int64_t *)(b + a.L.plast);
-    S.psize = (int64_t *)(b + a.L.psize);
-    S.pc0 = (int64_t *)(b + a.L.pc0);
-    S.pdeg = (int32_t *)(b + a.L.pdeg);
-    S.pnb = (int32_t *)(b + a.L.pnb);
-    S.nodes = (UfNode *)(b + a.L.nodes);
+    S.pool = (PoolSlot *)(b + a.L.pool);
+    S.nodes.lds = nullptr;
+    S.nodes.glob = (UfNode *)(b + a.L.nodes);
     S.remap = (int32_t *)(b + a.L.uf_remap);
     S.stack = (int2 *)(b + a.L.stack);
     S.stamp = (uint32_t *)(b + a.L.stamp);
@@ -155,7 +159,7 @@ struct Sim {
     uint64_t seed;
     int64_t T, mem, peak;
     int32_t pool_end, pool_live;
-    int32_t uf_n;
+    int32_t uf_n, uf_limit;      // nodes in use; count that triggers a compaction
     int32_t status, cur_op;
     uint32_t epoch;
     int64_t evict_no;
@@ -196,8 +200,7 @@ __device__ __forceinline__ TRec rec_u(const Sim &s, int32_t x)
 __device__ __forceinline__ void list_build(const Sim &s, int32_t b, int32_t e, int32_t i)
 {
     int32_t cnt = 0;
-    int32_t *col = s.S.pnb;
-    const int32_t pcap = s.S.pcap;
+    int32_t *col = s.S.pool[i].nb;
     for (int32_t k0 = b; k0 < e; k0 += LB) {
         int32_t w[LB];
         int32_t q[LB];
@@ -208,32 +211,34 @@ __device__ __forceinline__ void list_build(const Sim &s, int32_t b, int32_t e, i
 #pragma unroll
         for (int j = 0; j < LB; j++) {
             if (k0 + j >= e || q[j] < 0) continue;
-            if (cnt < K) col[(size_t)cnt * pcap + i] = q[j];
+            if (cnt < K) col[cnt] = q[j];
             cnt++;
         }
     }
+#pragma unroll
+    for (int k = 0; k < K; k++)
+        if (k >= cnt) col[k] = 0;      // node 0: the null node (cost 0, its own root)
     if (cnt > K) cnt = K + 1;
-    s.S.pdeg[i] = ((e - b) << 8) | cnt;
+    s.S.pool[i].deg = ((e - b) << 8) | cnt;
 }
 
 __device__ __forceinline__ void list_add(const Sim &s, int32_t i, int32_t nd)
 {
-    const int32_t pd = s.S.pdeg[i];
+    PoolSlot &ps = s.S.pool[i];
+    const int32_t pd = ps.deg;
     const int32_t c = pd & 0xFF;
     if (c > K) return;
-    if (c < K) s.S.pnb[(size_t)c * s.S.pcap + i] = nd;
-    s.S.pdeg[i] = (pd & ~0xFF) | (c + 1);
+    if (c < K) ps.nb[c] = nd;
+    ps.deg = (pd & ~0xFF) | (c + 1);
 }
 
 // returns false if nd was not cached (cannot happen while the caches are consistent)
 __device__ __forceinline__ bool list_remove(const Sim &s, int32_t i, int32_t nd)
 {
-    int32_t *col = s.S.pnb;
-    const int32_t pcap = s.S.pcap;
-    const int32_t pd = s.S.pdeg[i];
-    int32_t v[K];
-#pragma unroll
-    for (int k = 0; k < K; k++) v[k] = col[(size_t)k * pcap + i];
+    PoolSlot &ps = s.S.pool[i];
+    const int4 nb4 = *(const int4 *)ps.nb;
+    const int32_t pd = ps.deg;
+    const int32_t v[K] = {nb4.x, nb4.y, nb4.z, nb4.w};
     const int32_t c = pd & 0xFF;
     if (c > K) return true;
     int32_t at = -1;
@@ -245,8 +250,9 @@ __device__ __forceinline__ bool list_remove(const Sim &s, int32_t i, int32_t nd)
 #pragma unroll
     for (int k = 0; k < K; k++)
         if (k == c - 1) lastv = v[k];
-    col[(size_t)at * pcap + i] = lastv;
-    s.S.pdeg[i] = (pd & ~0xFF) | (c - 1);
+    ps.nb[at] = lastv;
+    ps.nb[c - 1] = 0;
+    ps.deg = (pd & ~0xFF) | (c - 1);
     return true;
 }
 
@@ -257,36 +263,25 @@ template <int HC>
 __device__ __forceinline__ void pool_compact(Sim &s)
 {
     const int32_t lane = s.lane;
-    const int32_t pcap = s.S.pcap;
     int32_t kept = 0;
+    int4 *P4 = (int4 *)s.S.pool;
     __syncthreads();
     for (int32_t base = 0; base < s.pool_end; base += WAVE) {
         const int32_t i = base + lane;
-        const int32_t ii = i < s.pool_end ? i : 0;
-        const int32_t x0 = s.S.pid[ii];
-        const int64_t l = s.S.plast[ii], z = s.S.psize[ii], c = s.S.pc0[ii];
-        const int32_t d = s.S.pdeg[ii];
-        int32_t nb[K];
-        if (HC == HC_EQ) {
-#pragma unroll
-            for (int k = 0; k < K; k++) nb[k] = s.S.pnb[(size_t)k * pcap + ii];
-        }
-        const int32_t x = i < s.pool_end ? x0 : -1;
+        const uint32_t ii = (uint32_t)(i < s.pool_end ? i : 0);
+        const int4 q0 = P4[3 * ii], q1 = P4[3 * ii + 1];
+        int4 q2 = make_int4(0, 0, 0, 0);
+        if (HC == HC_EQ) q2 = P4[3 * ii + 2];
+        const int32_t x = i < s.pool_end ? q0.x : -1;
         const bool keep = x >= 0;
         const uint64_t m = __ballot(keep);
         __syncthreads();
         if (keep) {
-            const int32_t j = kept + lane_rank(m);
-            s.S.pid[j] = x;
-            s.S.plast[j] = l;
-            s.S.psize[j] = z;
-            s.S.pc0[j] = c;
-            s.S.pdeg[j] = d;
-            if (HC == HC_EQ) {
-#pragma unroll
-                for (int k = 0; k < K; k++) s.S.pnb[(size_t)k * pcap + j] = nb[k];
-            }
-            s.S.tst[x] = ts_make(S_RESIDENT, (uint32_t)j, 0);
+            const uint32_t j = (uint32_t)(kept + lane_rank(m));
+            P4[3 * j] = q0;
+            P4[3 * j + 1] = q1;
+            if (HC == HC_EQ) P4[3 * j + 2] = q2;
+            s.S.tst[x] = ts_make(S_RESIDENT, j, 0);
         }
         kept += __popcll(m);
         __syncthreads();
@@ -310,12 +305,13 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
     if (want) {
         i = s.pool_end + lane_rank(m);
         const TRec r = s.t.rec[x];
-        s.S.pid[i] = x;
-        s.S.plast[i] = last;
-        s.S.psize[i] = r.size;
-        s.S.pc0[i] = r.c0;
+        PoolSlot &ps = s.S.pool[i];
+        ps.id = x;
+        ps.last = last;
+        ps.size = r.size;
+        ps.c0 = r.c0;
         if (HC == HC_EQ) list_build(s, r.adj_b, r.adj_e, i);
-        else s.S.pdeg[i] = (r.adj_e - r.adj_b) << 8;
+        else ps.deg = (r.adj_e - r.adj_b) << 8;
     }
     s.pool_end += cnt;
     s.pool_live += cnt;
@@ -324,7 +320,7 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
 
 // ---------------------------------------------------------- union-find --
 
-__device__ __forceinline__ int32_t find_ro(const UfNode *nodes, int32_t x, int32_t limit)
+__device__ __forceinline__ int32_t find_ro(const NodeStore &nodes, int32_t x, int32_t limit)
 {
     for (int32_t k = 0; k <= limit; k++) {
         const int32_t p = nodes[x].parent;
@@ -337,7 +333,7 @@ __device__ __forceinline__ int32_t find_ro(const UfNode *nodes, int32_t x, int32
 // uniform find with path compression (used where one set is touched)
 __device__ __forceinline__ int32_t find_compress(Sim &s, int32_t x)
 {
-    UfNode *N = s.S.nodes;
+    const NodeStore &N = s.S.nodes;
     int32_t root = x;
     for (int32_t k = 0;; k++) {
         const int32_t p = uni(N[root].parent);
@@ -356,7 +352,7 @@ __device__ __forceinline__ int32_t find_compress(Sim &s, int32_t x)
 __device__ __forceinline__ int32_t unite(Sim &s, int32_t a, int32_t b)
 {
     if (a == b) return a;
-    UfNode *N = s.S.nodes;
+    const NodeStore &N = s.S.nodes;
     int32_t sa = uni(N[a].size), sb = uni(N[b].size);
     if (sa < sb) { int32_t t = a; a = b; b = t; int32_t u = sa; sa = sb; sb = u; }
     const int64_t cost = uni64(N[a].cost) + uni64(N[b].cost);
@@ -373,7 +369,7 @@ __device__ __forceinline__ int32_t unite(Sim &s, int32_t a, int32_t b)
 __device__ __forceinline__ void uf_compact(Sim &s)
 {
     const int32_t lane = s.lane, n = s.t.n;
-    UfNode *N = s.S.nodes;
+    const NodeStore &N = s.S.nodes;
     int32_t *R = s.S.remap;
     __syncthreads();
     for (int32_t i = lane; i < s.uf_n; i += WAVE) R[i] = -1;
@@ -389,10 +385,10 @@ __device__ __forceinline__ void uf_compact(Sim &s)
         }
     }
     __syncthreads();
-    int32_t kept = 0;
+    int32_t kept = 1;                    // node 0 stays the null node
     for (int32_t base = 0; base < s.uf_n; base += WAVE) {
         const int32_t i = base + lane;
-        const bool keep = i < s.uf_n && R[i] == 0;
+        const bool keep = i > 0 && i < s.uf_n && R[i] == 0;
         const int64_t c = keep ? N[i].cost : 0;
         const uint64_t m = __ballot(keep);
         __syncthreads();
@@ -414,8 +410,10 @@ __device__ __forceinline__ void uf_compact(Sim &s)
     }
     __syncthreads();
     s.uf_n = kept;
+    // stay inside LDS while the live sets fit comfortably, else double
+    s.uf_limit = kept + 256 <= UF_LDS ? UF_LDS : min(UF_LDS + s.S.ucap, 2 * kept + 256);
     for (int32_t i = lane; i < s.pool_end; i += WAVE) {
-        const int32_t x = s.S.pid[i];
+        const int32_t x = s.S.pool[i].id;
         if (x >= 0) {
             const TRec r = s.t.rec[x];
             list_build(s, r.adj_b, r.adj_e, i);
@@ -433,7 +431,7 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 template <int HC>
 __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eager)
 {
-    s.S.pid[slot] = -1;
+    s.S.pool[slot].id = -1;
     s.pool_live--;
     const TRec rv = rec_u(s, v);
     s.mem -= rv.size;
@@ -443,11 +441,11 @@ __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eage
         s.S.tst[v] = ts_make(0, 0, 0);
         return true;
     }
-    if (s.uf_n >= s.S.ucap) {
+    if (s.uf_n >= s.uf_limit) {
         uf_compact(s);
-        if (s.uf_n >= s.S.ucap) { set_status(s, ST_CAPACITY); return false; }
+        if (s.uf_n >= UF_LDS + s.S.ucap) { set_status(s, ST_CAPACITY); return false; }
     }
-    UfNode *N = s.S.nodes;
+    const NodeStore &N = s.S.nodes;
     const int32_t nd = s.uf_n++;
     int32_t R = nd;               // current root of v's set
     int64_t Rcost = rv.c0;
@@ -537,6 +535,7 @@ __device__ __forceinline__ int64_t eq_cost_slow(const Sim &s, int32_t x, int64_t
         cnt++;
         const int32_t r = find_ro(s.S.nodes, q, s.uf_n);
         if (r < 0) { bad = true; break; }
+        if (r != q) s.S.nodes[q].parent = r;    // same value from every lane that gets here
         bool dup = false;
         for (int32_t j = b; j < k && !dup; j++) {
             const int32_t q2 = ts_sw(s.S.tst[s.t.adj[j]]);
@@ -622,9 +621,9 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
 {
     const int32_t end = s.pool_end;
     const int32_t lane = s.lane;
-    const int32_t pcap = s.S.pcap;
     const int64_t T = s.T;
     const int32_t h = s.h;
+    const int4 *P4 = (const int4 *)s.S.pool;
     bool bad = false;
     Best best;
     best.N = 0;
@@ -635,80 +634,81 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
     if (HC == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
         clear_stamps(s);
     for (int32_t base = 0; base < end; base += WAVE * U) {
-        int32_t idx[U], id[U], pd[U];
+        int32_t id[U], pd[U];
+        uint32_t slot[U];
         int64_t last[U], size[U], c0[U];
         int32_t nb[U][K];
-        // level 1: every slot column at once (index clamped into the array)
+        bool ok[U];
+        // level 1: three 16-byte quads per slot, all issued together
 #pragma unroll
         for (int u = 0; u < U; u++) {
             const int32_t i = base + u * WAVE + lane;
-            idx[u] = i < end ? i : 0;
-            id[u] = s.S.pid[idx[u]];
-            last[u] = s.S.plast[idx[u]];
-            size[u] = s.S.psize[idx[u]];
-            c0[u] = s.S.pc0[idx[u]];
-            pd[u] = s.S.pdeg[idx[u]];
-            if (HC == HC_EQ) {
-#pragma unroll
-                for (int k = 0; k < K; k++) nb[u][k] = s.S.pnb[(size_t)k * pcap + idx[u]];
-            }
-            if (i >= end) id[u] = -1;
+            slot[u] = (uint32_t)(i < end ? i : 0);
+            const int4 q0 = P4[3 * slot[u]];
+            const int4 q1 = P4[3 * slot[u] + 1];
+            int4 q2 = make_int4(0, 0, 0, 0);
+            if (HC == HC_EQ) q2 = P4[3 * slot[u] + 2];
+            id[u] = i < end ? q0.x : -1;
+            pd[u] = q0.y;
+            last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
+            size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
+            c0[u] = (int64_t)(((uint64_t)(uint32_t)q1.w << 32) | (uint32_t)q1.z);
+            nb[u][0] = q2.x;
+            nb[u][1] = q2.y;
+            nb[u][2] = q2.z;
+            nb[u][3] = q2.w;
+            ok[u] = id[u] >= 0;
         }
         uint64_t N[U];
         u128 D[U];
-        bool ok[U];
-#pragma unroll
-        for (int u = 0; u < U; u++) ok[u] = id[u] >= 0;
         if (HC == HC_EQ) {
-            // level 2: every cached neighbour node at once (unused entries read node 0)
-            int64_t ncost[U][K];
-            int32_t npar[U][K];
+            // level 2: every cached node (unused entries hold node 0, the null
+            // node); level 3: its parent, so nodes one merge away resolve too
+            int64_t sum[U], ev[U];
+            bool slow[U];
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 const int32_t c = pd[u] & 0xFF;
+                // roots are their own parent, so the node two hops along (n2)
+                // is the set root whenever the cached node is at most one
+                // merge away from it; its cost is used unconditionally
+                int32_t r[K];
+#pragma unroll
+                for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
+                int64_t cost[K];
+                bool deep = false;
 #pragma unroll
                 for (int k = 0; k < K; k++) {
-                    const bool use = ok[u] && k < c && c <= K;
-                    const UfNode nd = s.S.nodes[use ? nb[u][k] : 0];
-                    ncost[u][k] = use ? nd.cost : 0;
-                    npar[u][k] = use ? nd.parent : nb[u][k];
+                    const UfNode n2 = s.S.nodes[r[k]];
+                    cost[k] = n2.cost;
+                    deep |= n2.parent != r[k];
                 }
-            }
-            // level 3 (rare): cached node is no longer a root
-            bool deep = false;
-#pragma unroll
-            for (int u = 0; u < U; u++)
-#pragma unroll
-                for (int k = 0; k < K; k++) deep |= npar[u][k] != nb[u][k];
-            if (deep) {
-#pragma unroll
-                for (int u = 0; u < U; u++)
-#pragma unroll
-                    for (int k = 0; k < K; k++) {
-                        if (npar[u][k] == nb[u][k]) continue;
-                        int32_t q = find_ro(s.S.nodes, npar[u][k], s.uf_n);
-                        if (q < 0) { bad = true; q = nb[u][k]; }
-                        nb[u][k] = q;
-                        ncost[u][k] = s.S.nodes[q].cost;
-                    }
-            }
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                const int32_t c = pd[u] & 0xFF;
-                // distinct roots among the cached entries (branch-free)
-                int64_t sum = 0;
+                int64_t t = 0;
 #pragma unroll
                 for (int k = 0; k < K; k++) {
                     bool dup = false;
 #pragma unroll
-                    for (int j = 0; j < k; j++) dup |= nb[u][j] == nb[u][k];
-                    sum += (k < c && !dup) ? ncost[u][k] : 0;
+                    for (int j = 0; j < k; j++) dup |= r[j] == r[k];
+                    t += dup ? 0 : cost[k];
                 }
-                int64_t ev = c;
-                if (ok[u] && c > K) sum = eq_cost_slow(s, id[u], ev, bad);   // overflowed cache (rare)
-                N[u] = (uint64_t)(c0[u] + sum);
+                sum[u] = t;
+                ev[u] = c;
+                slow[u] = ok[u] && (c > K || deep);
+            }
+            // rare: overflowed cache or a merged-away node -- exact recount
+            bool any_slow = false;
+#pragma unroll
+            for (int u = 0; u < U; u++) any_slow |= slow[u];
+            if (__ballot(any_slow)) {
+#pragma unroll
+                for (int u = 0; u < U; u++)
+                    if (slow[u]) sum[u] = eq_cost_slow(s, id[u], ev[u], bad);
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                N[u] = (uint64_t)(c0[u] + sum[u]);
                 D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
-                s.nbr += ok[u] ? ev : 0;
+                s.nbr += ok[u] ? ev[u] : 0;
                 s.adj += ok[u] ? (pd[u] >> 8) : 0;
             }
         } else if (HC == HC_WALK) {
@@ -754,7 +754,7 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
             }
         }
 #pragma unroll
-        for (int u = 0; u < U; u++) take(best, ok[u], N[u], D[u], id[u], idx[u]);
+        for (int u = 0; u < U; u++) take(best, ok[u], N[u], D[u], id[u], (int32_t)slot[u]);
     }
     // cross-lane lexicographic minimum
     for (int off = WAVE / 2; off >= 1; off >>= 1) {
@@ -779,8 +779,8 @@ __device__ __forceinline__ bool allocate(Sim &s, int64_t sz)
 {
     while (s.mem + sz > s.budget) {
         if (s.pool_live == 0) { set_status(s, ST_OOM); return false; }
-        // keep the scanned range at most about twice the live pool
-        if (s.pool_end > 2 * s.pool_live + WAVE * U) pool_compact<HC>(s);
+        // keep the scanned range within half a round of the live pool
+        if (s.pool_end > s.pool_live + WAVE * U / 2) pool_compact<HC>(s);
 #ifdef DTR_PROFILE
         const int64_t c0_ = (int64_t)__builtin_readcyclecounter();
         s.prof_scans++;
@@ -824,7 +824,7 @@ __device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t 
             if (l >= MAX_LOCKS) over = true;
             else {
                 if (ts_in_pool(w)) {
-                    s.S.pid[ts_pos(w)] = -1;
+                    s.S.pool[ts_pos(w)].id = -1;
                     killed = true;
                 }
                 s.S.tst[u] = nw;
@@ -1018,7 +1018,8 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.seed = sp.seed;
     s.T = 0;
     s.pool_end = s.pool_live = 0;
-    s.uf_n = 0;
+    s.uf_n = 1;                          // node 0: the null node (h_DTR^eq)
+    s.uf_limit = UF_LDS;
     s.status = ST_OK;
     s.cur_op = 0;
     s.epoch = 0;
@@ -1034,6 +1035,13 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     for (int32_t x = lane; x < n; x += WAVE)
         s.S.tst[x] = ts_make((s.t.flags[x] & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
     if (HC == HC_WALK) clear_stamps(s);
+    if (HC == HC_EQ && lane == 0) {
+        UfNode z;
+        z.cost = 0;
+        z.parent = 0;
+        z.size = 1;
+        s.S.nodes[0] = z;
+    }
     __syncthreads();
     s.mem = s.t.const_mem;
     s.peak = s.mem;
@@ -1095,8 +1103,10 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
 template <int HC>
 __global__ void __launch_bounds__(WAVE) replay_kernel(KernelArgs a)
 {
+    __shared__ UfNode lds_nodes[HC == HC_EQ ? UF_LDS : 1];
     const int32_t lane = threadIdx.x;
-    const Slot S = slot_at(a, blockIdx.x);
+    Slot S = slot_at(a, blockIdx.x);
+    S.nodes.lds = lds_nodes;
     for (;;) {
         uint32_t k = 0;
         if (lane == 0) k = atomicAdd(a.queue, 1u);
