@@ -120,3 +120,23 @@ def test_determinism_across_slot_counts(gpu):
     b = gpu.run(w.traces, w.specs, slots=1000)
     c = gpu.run(w.traces, w.specs)
     assert a.tobytes() == b.tobytes() == c.tobytes()
+
+
+def test_random_dag_replica_all_budgets(gpu, oracle_lib):
+    """Random-DAG recipe (1-3 inputs from the previous 64 outputs, log-normal
+    sizes) at 1000 forward ops, h_DTR at 12 budgets from 5% to 100%: the
+    budget range of the full workload on a trace the oracle finishes."""
+    w = W.config_random_dag(n_forward=1000, n_budgets=12)
+    print(f"random dag replica: {w.n_sims} sims", flush=True)
+    compare(gpu.run(w.traces, w.specs), oracle_lib.run(w.traces, w.specs), w.specs, "randdag1k")
+
+
+def test_random_dag_full_size_sampled(gpu, oracle_lib):
+    """The full 100k-forward-op trace (200k ops), in the launch configuration of
+    the full batch, on the sampled budgets the exact-e* oracle finishes in
+    seconds (the top of the 1024-budget range)."""
+    w = W.make_config("randdag100k")
+    pick = np.array([1023, 1012, 1000])
+    specs = w.specs[pick]
+    print(f"random dag full size: sims {pick.tolist()}", flush=True)
+    compare(gpu.run(w.traces, specs), oracle_lib.run(w.traces, specs), specs, "randdag100k-sampled")
