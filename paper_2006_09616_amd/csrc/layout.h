@@ -78,16 +78,19 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 //             position (24 bits), lock count (8 bits)
 //   pool      evictable tensors, pcap 48-byte slots (dead slots are
 //             tombstoned and squeezed out): id, packed (degree << 8 | n), last
-//             access, size, c0, and for h_DTR^eq the union-find nodes of up
-//             to NB_CACHE evicted neighbours (n = NB_CACHE + 1 marks an
-//             overflowed cache)
+//             access, size, c0, start of the neighbour range, and for
+//             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
+//             neighbours (n = NB_CACHE + 1 marks an overflowed cache)
 //   nodes     union-find nodes {running cost, parent, size}
 //   stack     rematerialization frames (tensor, next input)
 //   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
 constexpr int NB_CACHE = 4;
 // union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
 // the rest in the slot's global node array
-constexpr int UF_LDS = 1024;
+constexpr int UF_LDS = 512;
+// pool slots below POOL_LDS live in LDS (48 bytes each per wavefront), the
+// rest in the slot's global pool array (which keeps the same indices)
+constexpr int POOL_LDS = 256;
 
 struct SlotLayout {
     int64_t bytes;           // stride between slots
@@ -104,7 +107,8 @@ struct __attribute__((aligned(16))) PoolSlot {
     int32_t deg;             // degree << 8 | cached neighbour count
     int64_t last;            // last access
     int64_t size;
-    int64_t c0;
+    int32_t c0;              // <= 2^28
+    int32_t adj_b;           // start of the tensor's neighbour range
     int32_t nb[NB_CACHE];    // cached union-find nodes of evicted neighbours
 };
 static_assert(sizeof(PoolSlot) == 48, "pool slot layout");
@@ -130,6 +134,7 @@ struct KernelArgs {
 
 // In-kernel phase timers (DTR_PROFILE builds only): cycles spent per sim in
 // the whole replay and in the eviction scans, and the number of scans.
-constexpr int PROF_FIELDS = 4;   // total cycles, scan cycles, scans, scan rounds
+constexpr int PROF_FIELDS = 8;   // total cycles, scan cycles, scans, scan rounds, slow
+                                 // recounts, scans over global nodes, node and pool compactions
 
 }  // namespace dtr

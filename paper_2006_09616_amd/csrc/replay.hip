@@ -54,6 +54,7 @@ constexpr uint8_t FLAG_CONST = 1;
 constexpr int U = 2;             // candidates per lane per scan round
 constexpr int K = NB_CACHE;
 constexpr int LB = 8;            // neighbour reads issued together when building a cache
+static_assert(POOL_LDS % (WAVE * U) == 0, "a scan round lies wholly in LDS or wholly in global memory");
 // kernel specialisations by heuristic class (register budgets differ widely)
 enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2 };
 
@@ -73,10 +74,17 @@ __device__ __forceinline__ uint64_t shfl64(uint64_t v, int32_t j)
     return __shfl(v, j, WAVE);
 }
 
+#define GAS __attribute__((address_space(1)))    // global memory
+#define LAS __attribute__((address_space(3)))    // LDS
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+
 // read-only trace tables: constant address space, so uniform reads become
 // scalar loads
 template <class T>
 __device__ __forceinline__ T cld(const T *p) { return *(const __attribute__((address_space(4))) T *)p; }
+// per-lane reads of the same tables: global loads (never flat)
+template <class T>
+__device__ __forceinline__ T gld(const T *p) { return *(const GAS T *)p; }
 
 __device__ __forceinline__ int32_t lane_rank(uint64_t mask)
 {
@@ -110,9 +118,11 @@ __device__ __forceinline__ bool better(uint64_t na, u128 da, int32_t ia, uint64_
 }
 
 // Union-find node store: ids below UF_LDS in this wavefront's LDS array, the
-// rest in the slot's global array; one id space, read through flat pointers.
+// rest in the slot's global array; one id space, read through flat pointers
+// (or straight from LDS while every node id is below UF_LDS).
 struct NodeStore {
     UfNode *lds;
+    LAS UfNode *lds_l;
     UfNode *glob;
     __device__ __forceinline__ UfNode &operator[](int32_t id) const
     {
@@ -120,29 +130,40 @@ struct NodeStore {
     }
 };
 
+// Evictable pool: slots below POOL_LDS in this wavefront's LDS array, the
+// rest in the slot's global array (same indices).
 struct Slot {
-    uint64_t *tst;
-    PoolSlot *pool;
+    GAS uint64_t *tst;
+    PoolSlot *lpool;              // flat view of the LDS head
+    LAS PoolSlot *lpool_l;
+    GAS PoolSlot *gpool;
     NodeStore nodes;
-    int32_t *remap;
+    GAS int32_t *remap;
     int2 *stack;
-    uint32_t *stamp;
-    int32_t *queue;
+    GAS uint32_t *stamp;
+    GAS int32_t *queue;
     int32_t pcap, ucap, n_max;
+    __device__ __forceinline__ PoolSlot &pool(int32_t i) const
+    {
+        return i < POOL_LDS ? lpool[i] : *(PoolSlot *)(gpool + i);
+    }
 };
 
 __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
 {
     uint8_t *b = a.slots + (size_t)k * (size_t)a.L.bytes;
     Slot S;
-    S.tst = (uint64_t *)(b + a.L.tst);
-    S.pool = (PoolSlot *)(b + a.L.pool);
+    S.tst = (GAS uint64_t *)(b + a.L.tst);
+    S.lpool = nullptr;
+    S.lpool_l = nullptr;
+    S.gpool = (GAS PoolSlot *)(b + a.L.pool);
     S.nodes.lds = nullptr;
+    S.nodes.lds_l = nullptr;
     S.nodes.glob = (UfNode *)(b + a.L.nodes);
-    S.remap = (int32_t *)(b + a.L.uf_remap);
+    S.remap = (GAS int32_t *)(b + a.L.uf_remap);
     S.stack = (int2 *)(b + a.L.stack);
-    S.stamp = (uint32_t *)(b + a.L.stamp);
-    S.queue = (int32_t *)(b + a.L.queue);
+    S.stamp = (GAS uint32_t *)(b + a.L.stamp);
+    S.queue = (GAS int32_t *)(b + a.L.queue);
     S.pcap = (int32_t)a.L.pcap;
     S.ucap = (int32_t)a.L.ucap;
     S.n_max = (int32_t)a.L.n_max;
@@ -167,6 +188,7 @@ struct Sim {
     int64_t nbr, adj;     // per-lane partial sums, reduced at the end
 #ifdef DTR_PROFILE
     int64_t prof_scan_cycles, prof_scans, prof_rounds;
+    int64_t prof_slow, prof_global_nodes, prof_uf_compact, prof_pool_compact;
 #endif
 };
 
@@ -193,38 +215,62 @@ __device__ __forceinline__ TRec rec_u(const Sim &s, int32_t x)
     return r;
 }
 
+// per-lane read of a tensor's static record (two 16-byte global loads)
+__device__ __forceinline__ TRec rec_v(const Sim &s, int32_t x)
+{
+    const GAS u32x4 *p = (const GAS u32x4 *)(s.t.rec + x);
+    const u32x4 a = p[0], b = p[1];
+    TRec r;
+    r.size = (int64_t)((uint64_t)a.x | ((uint64_t)a.y << 32));
+    r.c0 = (int32_t)a.z;
+    r.producer = (int32_t)a.w;
+    r.in_b = (int32_t)b.x;
+    r.in_e = (int32_t)b.y;
+    r.adj_b = (int32_t)b.z;
+    r.adj_e = (int32_t)b.w;
+    return r;
+}
+
 // ------------------------------------------------------ neighbour cache --
 
-// This lane's cache of evicted-neighbour nodes for tensor x (neighbour range
-// [b, e)), written to slot i.  Neighbour states are read LB at a time.
-__device__ __forceinline__ void list_build(const Sim &s, int32_t b, int32_t e, int32_t i)
+// This lane's cache of evicted-neighbour nodes for a tensor with neighbour
+// range [b, e), built in registers: the first K evicted neighbours' nodes
+// (unused entries hold node 0, the null node: cost 0, its own root).  Returns
+// the cache; `deg` receives (degree << 8) | count (K + 1: overflowed).
+// Neighbour states are read LB at a time, all loads unconditional.
+__device__ __forceinline__ i32x4 list_build(const Sim &s, int32_t b, int32_t e, int32_t &deg)
 {
+    int32_t c[K];
+#pragma unroll
+    for (int k = 0; k < K; k++) c[k] = 0;
     int32_t cnt = 0;
-    int32_t *col = s.S.pool[i].nb;
     for (int32_t k0 = b; k0 < e; k0 += LB) {
         int32_t w[LB];
         int32_t q[LB];
 #pragma unroll
-        for (int j = 0; j < LB; j++) w[j] = k0 + j < e ? s.t.adj[k0 + j] : 0;
+        for (int j = 0; j < LB; j++) w[j] = gld(s.t.adj + (k0 + j < e ? k0 + j : k0));
 #pragma unroll
         for (int j = 0; j < LB; j++) q[j] = ts_sw(s.S.tst[w[j]]);
 #pragma unroll
         for (int j = 0; j < LB; j++) {
-            if (k0 + j >= e || q[j] < 0) continue;
-            if (cnt < K) col[cnt] = q[j];
-            cnt++;
+            const bool v = k0 + j < e && q[j] >= 0;
+#pragma unroll
+            for (int k = 0; k < K; k++) c[k] = v && cnt == k ? q[j] : c[k];
+            cnt += v ? 1 : 0;
         }
     }
-#pragma unroll
-    for (int k = 0; k < K; k++)
-        if (k >= cnt) col[k] = 0;      // node 0: the null node (cost 0, its own root)
-    if (cnt > K) cnt = K + 1;
-    s.S.pool[i].deg = ((e - b) << 8) | cnt;
+    deg = ((e - b) << 8) | (cnt > K ? K + 1 : cnt);
+    i32x4 r;
+    r.x = c[0];
+    r.y = c[1];
+    r.z = c[2];
+    r.w = c[3];
+    return r;
 }
 
 __device__ __forceinline__ void list_add(const Sim &s, int32_t i, int32_t nd)
 {
-    PoolSlot &ps = s.S.pool[i];
+    PoolSlot &ps = s.S.pool(i);
     const int32_t pd = ps.deg;
     const int32_t c = pd & 0xFF;
     if (c > K) return;
@@ -235,8 +281,8 @@ __device__ __forceinline__ void list_add(const Sim &s, int32_t i, int32_t nd)
 // returns false if nd was not cached (cannot happen while the caches are consistent)
 __device__ __forceinline__ bool list_remove(const Sim &s, int32_t i, int32_t nd)
 {
-    PoolSlot &ps = s.S.pool[i];
-    const int4 nb4 = *(const int4 *)ps.nb;
+    PoolSlot &ps = s.S.pool(i);
+    const i32x4 nb4 = *(const i32x4 *)ps.nb;
     const int32_t pd = ps.deg;
     const int32_t v[K] = {nb4.x, nb4.y, nb4.z, nb4.w};
     const int32_t c = pd & 0xFF;
@@ -264,24 +310,27 @@ __device__ __forceinline__ void pool_compact(Sim &s)
 {
     const int32_t lane = s.lane;
     int32_t kept = 0;
-    int4 *P4 = (int4 *)s.S.pool;
+#ifdef DTR_PROFILE
+    s.prof_pool_compact++;
+#endif
     __syncthreads();
     for (int32_t base = 0; base < s.pool_end; base += WAVE) {
         const int32_t i = base + lane;
-        const uint32_t ii = (uint32_t)(i < s.pool_end ? i : 0);
-        const int4 q0 = P4[3 * ii], q1 = P4[3 * ii + 1];
-        int4 q2 = make_int4(0, 0, 0, 0);
-        if (HC == HC_EQ) q2 = P4[3 * ii + 2];
+        const i32x4 *P = (const i32x4 *)&s.S.pool(i < s.pool_end ? i : 0);
+        const i32x4 q0 = P[0], q1 = P[1];
+        i32x4 q2 = 0;
+        if (HC == HC_EQ) q2 = P[2];
         const int32_t x = i < s.pool_end ? q0.x : -1;
         const bool keep = x >= 0;
         const uint64_t m = __ballot(keep);
         __syncthreads();
         if (keep) {
-            const uint32_t j = (uint32_t)(kept + lane_rank(m));
-            P4[3 * j] = q0;
-            P4[3 * j + 1] = q1;
-            if (HC == HC_EQ) P4[3 * j + 2] = q2;
-            s.S.tst[x] = ts_make(S_RESIDENT, j, 0);
+            const int32_t j = kept + lane_rank(m);
+            i32x4 *Q = (i32x4 *)&s.S.pool(j);
+            Q[0] = q0;
+            Q[1] = q1;
+            if (HC == HC_EQ) Q[2] = q2;
+            s.S.tst[x] = ts_make(S_RESIDENT, (uint32_t)j, 0);
         }
         kept += __popcll(m);
         __syncthreads();
@@ -304,14 +353,23 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
     int32_t i = -1;
     if (want) {
         i = s.pool_end + lane_rank(m);
-        const TRec r = s.t.rec[x];
-        PoolSlot &ps = s.S.pool[i];
-        ps.id = x;
-        ps.last = last;
-        ps.size = r.size;
-        ps.c0 = r.c0;
-        if (HC == HC_EQ) list_build(s, r.adj_b, r.adj_e, i);
-        else ps.deg = (r.adj_e - r.adj_b) << 8;
+        const TRec r = rec_v(s, x);
+        int32_t deg = (r.adj_e - r.adj_b) << 8;
+        i32x4 nb = 0;
+        if (HC == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg);
+        i32x4 q0, q1;
+        q0.x = x;
+        q0.y = deg;
+        q0.z = (int32_t)(uint32_t)(uint64_t)last;
+        q0.w = (int32_t)(uint32_t)((uint64_t)last >> 32);
+        q1.x = (int32_t)(uint32_t)(uint64_t)r.size;
+        q1.y = (int32_t)(uint32_t)((uint64_t)r.size >> 32);
+        q1.z = r.c0;
+        q1.w = r.adj_b;
+        i32x4 *Q = (i32x4 *)&s.S.pool(i);
+        Q[0] = q0;
+        Q[1] = q1;
+        if (HC == HC_EQ) Q[2] = nb;
     }
     s.pool_end += cnt;
     s.pool_live += cnt;
@@ -370,7 +428,10 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 {
     const int32_t lane = s.lane, n = s.t.n;
     const NodeStore &N = s.S.nodes;
-    int32_t *R = s.S.remap;
+    GAS int32_t *R = s.S.remap;
+#ifdef DTR_PROFILE
+    s.prof_uf_compact++;
+#endif
     __syncthreads();
     for (int32_t i = lane; i < s.uf_n; i += WAVE) R[i] = -1;
     __syncthreads();
@@ -413,10 +474,13 @@ __device__ __forceinline__ void uf_compact(Sim &s)
     // stay inside LDS while the live sets fit comfortably, else double
     s.uf_limit = kept + 256 <= UF_LDS ? UF_LDS : min(UF_LDS + s.S.ucap, 2 * kept + 256);
     for (int32_t i = lane; i < s.pool_end; i += WAVE) {
-        const int32_t x = s.S.pool[i].id;
+        PoolSlot &ps = s.S.pool(i);
+        const int32_t x = ps.id;
         if (x >= 0) {
-            const TRec r = s.t.rec[x];
-            list_build(s, r.adj_b, r.adj_e, i);
+            const TRec r = rec_v(s, x);
+            int32_t deg;
+            *(i32x4 *)ps.nb = list_build(s, r.adj_b, r.adj_e, deg);
+            ps.deg = deg;
         }
     }
     __syncthreads();
@@ -431,7 +495,7 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 template <int HC>
 __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eager)
 {
-    s.S.pool[slot].id = -1;
+    s.S.pool(slot).id = -1;
     s.pool_live--;
     const TRec rv = rec_u(s, v);
     s.mem -= rv.size;
@@ -460,7 +524,7 @@ __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eage
         const int32_t k = k0 + s.lane;
         int32_t q = -1, r = -1;
         if (k < rv.adj_e) {
-            const uint64_t w = s.S.tst[s.t.adj[k]];
+            const uint64_t w = s.S.tst[gld(s.t.adj + k)];
             q = ts_sw(w);
             if (ts_in_pool(w)) list_add(s, (int32_t)ts_pos(w), nd);
             if (q >= 0) {
@@ -521,27 +585,94 @@ __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eage
 
 // ---------------------------------------------------------------- scan --
 
-// Neighbourhood cost of x under h_DTR^eq from the full adjacency (used when
-// the slot's cache overflowed): distinct sets of the evicted parents and
-// children.
-__device__ __forceinline__ int64_t eq_cost_slow(const Sim &s, int32_t x, int64_t &ev_count, bool &bad)
+// Union-find node reads for the full-adjacency recount: straight from LDS
+// while every node id is below UF_LDS, else through the hybrid store.
+struct LdsNodes {
+    LAS UfNode *p;
+    __device__ __forceinline__ int32_t parent(int32_t i) const { return p[i].parent; }
+    __device__ __forceinline__ void set_parent(int32_t i, int32_t v) const { p[i].parent = v; }
+    __device__ __forceinline__ int64_t cost(int32_t i) const { return p[i].cost; }
+};
+struct AnyNodes {
+    NodeStore n;
+    __device__ __forceinline__ int32_t parent(int32_t i) const { return n[i].parent; }
+    __device__ __forceinline__ void set_parent(int32_t i, int32_t v) const { n[i].parent = v; }
+    __device__ __forceinline__ int64_t cost(int32_t i) const { return n[i].cost; }
+};
+
+// Set roots of the neighbours k0 .. k0+LB-1 (below e) of a candidate: r[j] is
+// the root of neighbour k0+j if it is evicted, else -1.  All neighbour and
+// state reads are issued together; the finds then advance in lockstep, with
+// the first hop compressed (every lane writes the same root).  Returns the
+// number of evicted neighbours in the chunk; `bad` is set on a broken forest.
+template <class NS>
+__device__ __forceinline__ int32_t chunk_roots(const Sim &s, const NS &N, int32_t k0, int32_t e, int32_t (&r)[LB],
+                                               bool &bad)
 {
-    const TRec rx = s.t.rec[x];
-    const int32_t b = rx.adj_b, e = rx.adj_e;
-    int64_t sum = 0, cnt = 0;
-    for (int32_t k = b; k < e; k++) {
-        const int32_t q = ts_sw(s.S.tst[s.t.adj[k]]);
-        if (q < 0) continue;
-        cnt++;
-        const int32_t r = find_ro(s.S.nodes, q, s.uf_n);
-        if (r < 0) { bad = true; break; }
-        if (r != q) s.S.nodes[q].parent = r;    // same value from every lane that gets here
-        bool dup = false;
-        for (int32_t j = b; j < k && !dup; j++) {
-            const int32_t q2 = ts_sw(s.S.tst[s.t.adj[j]]);
-            if (q2 >= 0 && find_ro(s.S.nodes, q2, s.uf_n) == r) dup = true;
+    int32_t w[LB], q[LB];
+#pragma unroll
+    for (int j = 0; j < LB; j++) w[j] = gld(s.t.adj + (k0 + j < e ? k0 + j : k0));
+#pragma unroll
+    for (int j = 0; j < LB; j++) q[j] = ts_sw(s.S.tst[w[j]]);
+    int32_t cnt = 0;
+#pragma unroll
+    for (int j = 0; j < LB; j++) {
+        const bool v = k0 + j < e && q[j] >= 0;
+        q[j] = v ? q[j] : 0;            // node 0: the null node, its own root
+        r[j] = q[j];
+        cnt += v ? 1 : 0;
+    }
+    for (int32_t it = 0;; it++) {
+        int32_t p[LB];
+        bool more = false;
+#pragma unroll
+        for (int j = 0; j < LB; j++) {
+            p[j] = N.parent(r[j]);
+            more |= p[j] != r[j];
         }
-        if (!dup) sum += s.S.nodes[r].cost;
+        if (!more) break;
+        if (it > s.uf_n) { bad = true; break; }
+#pragma unroll
+        for (int j = 0; j < LB; j++) r[j] = p[j];
+    }
+#pragma unroll
+    for (int j = 0; j < LB; j++) {
+        if (q[j] != 0 && r[j] != q[j]) N.set_parent(q[j], r[j]);
+        r[j] = q[j] != 0 ? r[j] : -1;
+    }
+    return cnt;
+}
+
+// Neighbourhood cost under h_DTR^eq from the full adjacency [b, e) (used when
+// the candidate's cache overflowed or a cached node sits deep in its set):
+// summed running costs of the distinct sets of its evicted neighbours.  A
+// set counts at its first neighbour; chunks after the first compare against
+// the roots of the chunks before them.
+template <class NS>
+__device__ __forceinline__ int64_t eq_cost_full(const Sim &s, const NS &N, int32_t b, int32_t e, int64_t &ev_count,
+                                                bool &bad)
+{
+    int64_t sum = 0, cnt = 0;
+    for (int32_t k0 = b; k0 < e; k0 += LB) {
+        int32_t r[LB];
+        cnt += chunk_roots(s, N, k0, e, r, bad);
+        bool keep[LB];
+#pragma unroll
+        for (int j = 0; j < LB; j++) {
+            keep[j] = r[j] >= 0;
+#pragma unroll
+            for (int i = 0; i < j; i++) keep[j] = keep[j] && r[i] != r[j];
+        }
+        for (int32_t p0 = b; p0 < k0; p0 += LB) {
+            int32_t rp[LB];
+            chunk_roots(s, N, p0, e, rp, bad);
+#pragma unroll
+            for (int j = 0; j < LB; j++)
+#pragma unroll
+                for (int i = 0; i < LB; i++) keep[j] = keep[j] && rp[i] != r[j];
+        }
+#pragma unroll
+        for (int j = 0; j < LB; j++) sum += keep[j] ? N.cost(r[j]) : 0;
     }
     ev_count = cnt;
     return sum;
@@ -552,21 +683,21 @@ __device__ __forceinline__ int64_t eq_cost_slow(const Sim &s, int32_t x, int64_t
 __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t ep, int64_t &count)
 {
     const int32_t lane = s.lane;
-    uint32_t *st = s.S.stamp;
-    int32_t *q = s.S.queue;
+    GAS uint32_t *st = s.S.stamp;
+    GAS int32_t *q = s.S.queue;
     int64_t sum = 0, cnt = 0;
     int32_t head = 0, tail = 0;
     q[(size_t)tail++ * WAVE + lane] = x;
     while (head < tail) {
         const int32_t u = q[(size_t)head++ * WAVE + lane];
-        const TRec ru = s.t.rec[u];
+        const TRec ru = rec_v(s, u);
         for (int32_t k = ru.in_b; k < ru.in_e; k++) {
-            const int32_t p = s.t.in[k];
+            const int32_t p = gld(s.t.in + k);
             if (ts_sw(s.S.tst[p]) < 0) continue;
             const size_t sp = (size_t)p * WAVE + lane;
             if (st[sp] == ep) continue;
             st[sp] = ep;
-            sum += s.t.rec[p].c0;
+            sum += gld(&s.t.rec[p].c0);
             cnt++;
             q[(size_t)tail++ * WAVE + lane] = p;
         }
@@ -575,13 +706,13 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
     q[(size_t)tail++ * WAVE + lane] = x;
     while (head < tail) {
         const int32_t u = q[(size_t)head++ * WAVE + lane];
-        for (int32_t k = s.t.ch_off[u], e = s.t.ch_off[u + 1]; k < e; k++) {
-            const int32_t c = s.t.ch[k];
+        for (int32_t k = gld(s.t.ch_off + u), e = gld(s.t.ch_off + u + 1); k < e; k++) {
+            const int32_t c = gld(s.t.ch + k);
             if (ts_sw(s.S.tst[c]) < 0) continue;
             const size_t sc = (size_t)c * WAVE + lane;
             if (st[sc] == ep) continue;
             st[sc] = ep;
-            sum += s.t.rec[c].c0;
+            sum += gld(&s.t.rec[c].c0);
             cnt++;
             q[(size_t)tail++ * WAVE + lane] = c;
         }
@@ -623,7 +754,8 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
     const int32_t lane = s.lane;
     const int64_t T = s.T;
     const int32_t h = s.h;
-    const int4 *P4 = (const int4 *)s.S.pool;
+    const LAS i32x4 *L4 = (const LAS i32x4 *)s.S.lpool_l;
+    const GAS i32x4 *G4 = (const GAS i32x4 *)s.S.gpool;
     bool bad = false;
     Best best;
     best.N = 0;
@@ -637,22 +769,44 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
         int32_t id[U], pd[U];
         uint32_t slot[U];
         int64_t last[U], size[U], c0[U];
+        int32_t ab[U];
         int32_t nb[U][K];
         bool ok[U];
-        // level 1: three 16-byte quads per slot, all issued together
+        // level 1: three 16-byte quads per slot, all issued together, from
+        // LDS or global memory (a round never straddles the two)
+        i32x4 Q0[U], Q1[U], Q2[U];
 #pragma unroll
         for (int u = 0; u < U; u++) {
             const int32_t i = base + u * WAVE + lane;
-            slot[u] = (uint32_t)(i < end ? i : 0);
-            const int4 q0 = P4[3 * slot[u]];
-            const int4 q1 = P4[3 * slot[u] + 1];
-            int4 q2 = make_int4(0, 0, 0, 0);
-            if (HC == HC_EQ) q2 = P4[3 * slot[u] + 2];
+            slot[u] = (uint32_t)(i < end ? i : base);
+        }
+        if (base < POOL_LDS) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                Q0[u] = L4[3 * slot[u]];
+                Q1[u] = L4[3 * slot[u] + 1];
+                Q2[u] = 0;
+                if (HC == HC_EQ) Q2[u] = L4[3 * slot[u] + 2];
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                Q0[u] = G4[3 * slot[u]];
+                Q1[u] = G4[3 * slot[u] + 1];
+                Q2[u] = 0;
+                if (HC == HC_EQ) Q2[u] = G4[3 * slot[u] + 2];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int32_t i = base + u * WAVE + lane;
+            const i32x4 q0 = Q0[u], q1 = Q1[u], q2 = Q2[u];
             id[u] = i < end ? q0.x : -1;
             pd[u] = q0.y;
             last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
             size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
-            c0[u] = (int64_t)(((uint64_t)(uint32_t)q1.w << 32) | (uint32_t)q1.z);
+            c0[u] = (int64_t)q1.z;
+            ab[u] = q1.w;
             nb[u][0] = q2.x;
             nb[u][1] = q2.y;
             nb[u][2] = q2.z;
@@ -662,6 +816,7 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
         uint64_t N[U];
         u128 D[U];
         if (HC == HC_EQ) {
+            const bool lds_nodes = s.uf_n <= UF_LDS;
             // level 2: every cached node (unused entries hold node 0, the null
             // node); level 3: its parent, so nodes one merge away resolve too
             int64_t sum[U], ev[U];
@@ -673,15 +828,26 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 // is the set root whenever the cached node is at most one
                 // merge away from it; its cost is used unconditionally
                 int32_t r[K];
-#pragma unroll
-                for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
                 int64_t cost[K];
                 bool deep = false;
+                if (lds_nodes) {
+                    const LAS UfNode *NL = s.S.nodes.lds_l;
 #pragma unroll
-                for (int k = 0; k < K; k++) {
-                    const UfNode n2 = s.S.nodes[r[k]];
-                    cost[k] = n2.cost;
-                    deep |= n2.parent != r[k];
+                    for (int k = 0; k < K; k++) r[k] = NL[nb[u][k]].parent;
+#pragma unroll
+                    for (int k = 0; k < K; k++) {
+                        cost[k] = NL[r[k]].cost;
+                        deep |= NL[r[k]].parent != r[k];
+                    }
+                } else {
+#pragma unroll
+                    for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
+#pragma unroll
+                    for (int k = 0; k < K; k++) {
+                        const UfNode n2 = s.S.nodes[r[k]];
+                        cost[k] = n2.cost;
+                        deep |= n2.parent != r[k];
+                    }
                 }
                 int64_t t = 0;
 #pragma unroll
@@ -699,10 +865,29 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
             bool any_slow = false;
 #pragma unroll
             for (int u = 0; u < U; u++) any_slow |= slow[u];
-            if (__ballot(any_slow)) {
+#ifdef DTR_PROFILE
+            {
+                int32_t ns = 0;
 #pragma unroll
-                for (int u = 0; u < U; u++)
-                    if (slow[u]) sum[u] = eq_cost_slow(s, id[u], ev[u], bad);
+                for (int u = 0; u < U; u++) ns += slow[u] ? 1 : 0;
+                s.prof_slow += ns;     // per lane; reduced at the end
+                for (int u = 0; u < U; u++) s.prof_global_nodes += ok[u] && (pd[u] & 0xFF) > K ? 1 : 0;
+            }
+#endif
+            if (__ballot(any_slow)) {
+                if (lds_nodes) {
+                    LdsNodes NL;
+                    NL.p = s.S.nodes.lds_l;
+#pragma unroll
+                    for (int u = 0; u < U; u++)
+                        if (slow[u]) sum[u] = eq_cost_full(s, NL, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+                } else {
+                    AnyNodes NA;
+                    NA.n = s.S.nodes;
+#pragma unroll
+                    for (int u = 0; u < U; u++)
+                        if (slow[u]) sum[u] = eq_cost_full(s, NA, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+                }
             }
 #pragma unroll
             for (int u = 0; u < U; u++) {
@@ -817,14 +1002,14 @@ __device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t 
         int32_t u = -1;
         uint64_t nw = 0;
         if (k < e) {
-            u = ids[k];
+            u = gld(ids + k);
             const uint64_t w = s.S.tst[u];
             const uint32_t l = ts_locks(w);
             nw = ts_make(ts_sw(w), ts_pos(w), l + 1);
             if (l >= MAX_LOCKS) over = true;
             else {
                 if (ts_in_pool(w)) {
-                    s.S.pool[ts_pos(w)].id = -1;
+                    s.S.pool((int32_t)ts_pos(w)).id = -1;
                     killed = true;
                 }
                 s.S.tst[u] = nw;
@@ -843,7 +1028,7 @@ __device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t 
 __device__ __forceinline__ void reload_frame(const Sim &s, int32_t b, int32_t e, Frame &f)
 {
     const int32_t k = b + s.lane;
-    f.u = k < e ? s.t.in[k] : -1;
+    f.u = k < e ? gld(s.t.in + k) : -1;
     f.w = f.u >= 0 ? s.S.tst[f.u] : 0;
 }
 
@@ -861,7 +1046,7 @@ __device__ __forceinline__ void unlock_inputs(Sim &s, int32_t b, int32_t e, int6
                 u = f.u;
                 w = f.w;
             } else {
-                u = s.t.in[k];
+                u = gld(s.t.in + k);
                 w = s.S.tst[u];
             }
         }
@@ -880,7 +1065,7 @@ __device__ __forceinline__ int32_t next_evicted(const Sim &s, int32_t b, int32_t
     for (int32_t k0 = b + WAVE; k0 < e; k0 += WAVE) {
         const int32_t k = k0 + s.lane;
         bool ev = false;
-        if (k < e && k - b >= from) ev = ts_sw(s.S.tst[s.t.in[k]]) >= 0;
+        if (k < e && k - b >= from) ev = ts_sw(s.S.tst[gld(s.t.in + k)]) >= 0;
         const uint64_t m = __ballot(ev);
         if (m) return k0 - b + __ffsll((long long)m) - 1;
     }
@@ -909,7 +1094,7 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
         for (int32_t k0 = rt.adj_b; k0 < rt.adj_e; k0 += WAVE) {
             const int32_t k = k0 + s.lane;
             if (k < rt.adj_e) {
-                const uint64_t wx = s.S.tst[s.t.adj[k]];
+                const uint64_t wx = s.S.tst[gld(s.t.adj + k)];
                 if (ts_in_pool(wx) && !list_remove(s, (int32_t)ts_pos(wx), old)) lost = true;
             }
         }
@@ -990,7 +1175,7 @@ __device__ __forceinline__ bool release(Sim &s, int32_t o)
         int32_t r = -1, pos = 0;
         bool ev = false;
         if (k < e) {
-            r = s.t.rel[k];
+            r = gld(s.t.rel + k);
             const uint64_t w = s.S.tst[r];
             ev = ts_in_pool(w);
             pos = (int32_t)ts_pos(w);
@@ -1029,11 +1214,12 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
 #ifdef DTR_PROFILE
     const int64_t t_start = (int64_t)__builtin_readcyclecounter();
     s.prof_scan_cycles = s.prof_scans = s.prof_rounds = 0;
+    s.prof_slow = s.prof_global_nodes = s.prof_uf_compact = s.prof_pool_compact = 0;
 #endif
 
     const int32_t n = s.t.n;
     for (int32_t x = lane; x < n; x += WAVE)
-        s.S.tst[x] = ts_make((s.t.flags[x] & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
+        s.S.tst[x] = ts_make((gld(s.t.flags + x) & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
     if (HC == HC_WALK) clear_stamps(s);
     if (HC == HC_EQ && lane == 0) {
         UfNode z;
@@ -1071,12 +1257,20 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
         adj += __shfl_xor(adj, off, WAVE);
     }
 #ifdef DTR_PROFILE
+    for (int off = WAVE / 2; off >= 1; off >>= 1) {
+        s.prof_slow += __shfl_xor(s.prof_slow, off, WAVE);
+        s.prof_global_nodes += __shfl_xor(s.prof_global_nodes, off, WAVE);
+    }
     if (lane == 0 && a.prof) {
         int64_t *pr = a.prof + (size_t)sim * PROF_FIELDS;
         pr[0] = (int64_t)__builtin_readcyclecounter() - t_start;
         pr[1] = s.prof_scan_cycles;
         pr[2] = s.prof_scans;
         pr[3] = s.prof_rounds;
+        pr[4] = s.prof_slow;
+        pr[5] = s.prof_global_nodes;
+        pr[6] = s.prof_uf_compact;
+        pr[7] = s.prof_pool_compact;
     }
 #endif
     if (lane == 0) {
@@ -1104,9 +1298,13 @@ template <int HC>
 __global__ void __launch_bounds__(WAVE) replay_kernel(KernelArgs a)
 {
     __shared__ UfNode lds_nodes[HC == HC_EQ ? UF_LDS : 1];
+    __shared__ PoolSlot lds_pool[POOL_LDS];
     const int32_t lane = threadIdx.x;
     Slot S = slot_at(a, blockIdx.x);
     S.nodes.lds = lds_nodes;
+    S.nodes.lds_l = (LAS UfNode *)lds_nodes;
+    S.lpool = lds_pool;
+    S.lpool_l = (LAS PoolSlot *)lds_pool;
     for (;;) {
         uint32_t k = 0;
         if (lane == 0) k = atomicAdd(a.queue, 1u);
