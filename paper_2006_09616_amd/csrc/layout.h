@@ -76,7 +76,7 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 // base, each 256-byte aligned.
 //   tst       per-tensor state word: state/union-find node (32 bits), pool
 //             position (24 bits), lock count (8 bits)
-//   pool      evictable tensors, pcap 48-byte slots (dead slots are
+//   pool      evictable tensors, pcap 64-byte slots (dead slots are
 //             tombstoned and squeezed out): id, packed (degree << 8 | n), last
 //             access, size, c0, start of the neighbour range, and for
 //             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
@@ -84,11 +84,11 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 //   nodes     union-find nodes {running cost, parent, size}
 //   stack     rematerialization frames (tensor, next input)
 //   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
-constexpr int NB_CACHE = 4;
+constexpr int NB_CACHE = 8;
 // union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
 // the rest in the slot's global node array
 constexpr int UF_LDS = 512;
-// pool slots below POOL_LDS live in LDS (48 bytes each per wavefront), the
+// pool slots below POOL_LDS live in LDS (64 bytes each per wavefront), the
 // rest in the slot's global pool array (which keeps the same indices)
 constexpr int POOL_LDS = 256;
 
@@ -111,7 +111,7 @@ struct __attribute__((aligned(16))) PoolSlot {
     int32_t adj_b;           // start of the tensor's neighbour range
     int32_t nb[NB_CACHE];    // cached union-find nodes of evicted neighbours
 };
-static_assert(sizeof(PoolSlot) == 48, "pool slot layout");
+static_assert(sizeof(PoolSlot) == 64, "pool slot layout");
 
 struct __attribute__((aligned(16))) UfNode {
     int64_t cost;
@@ -134,7 +134,9 @@ struct KernelArgs {
 
 // In-kernel phase timers (DTR_PROFILE builds only): cycles spent per sim in
 // the whole replay and in the eviction scans, and the number of scans.
-constexpr int PROF_FIELDS = 8;   // total cycles, scan cycles, scans, scan rounds, slow
-                                 // recounts, scans over global nodes, node and pool compactions
+constexpr int PROF_PHASES = 8;   // evict, execute, unlock, lock, release, resume, output, descend
+constexpr int PROF_FIELDS = 8 + PROF_PHASES;   // total cycles, scan cycles, scans, scan rounds,
+                                               // recounts, overflowed caches, node and pool
+                                               // compactions, then cycles per phase
 
 }  // namespace dtr

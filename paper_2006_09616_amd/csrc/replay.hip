@@ -15,7 +15,7 @@
 //    registers for the life of the frame; release lists are checked in
 //    parallel;
 //  * the evictable pool (Appendix C.4 "Runtime state") is a tombstoned
-//    struct of arrays read coalesced; each lane scores U candidates per
+//    struct of arrays read coalesced; each lane scores one or two candidates per
 //    round with all slot reads issued at once, and the exact (score, id)
 //    minimum is reduced across lanes;
 //  * h_DTR^eq (Appendix C.2): each pool slot caches the union-find nodes of
@@ -51,12 +51,20 @@ constexpr int32_t S_UNCOMPUTED = -2;
 constexpr int32_t S_RESIDENT = -1;
 constexpr uint32_t MAX_LOCKS = 255;
 constexpr uint8_t FLAG_CONST = 1;
-constexpr int U = 2;             // candidates per lane per scan round
 constexpr int K = NB_CACHE;
+constexpr int KQ = K / 4;        // 16-byte quads of cached nodes per pool slot
+constexpr int PQ = (int)(sizeof(PoolSlot) / 16);   // quads per pool slot
+static_assert(K % 4 == 0 && PQ == 2 + KQ, "pool slot: two header quads, then the cache");
 constexpr int LB = 8;            // neighbour reads issued together when building a cache
-static_assert(POOL_LDS % (WAVE * U) == 0, "a scan round lies wholly in LDS or wholly in global memory");
 // kernel specialisations by heuristic class (register budgets differ widely)
 enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2 };
+// candidates per lane per scan round (h_DTR^eq reads K cached nodes per
+// candidate, so one fits the register budget there)
+template <int HC>
+struct Round {
+    static constexpr int value = HC == HC_EQ ? 1 : 2;
+    static_assert(POOL_LDS % (WAVE * value) == 0, "a scan round lies wholly in LDS or wholly in global memory");
+};
 
 // ------------------------------------------------------------- helpers --
 
@@ -72,6 +80,14 @@ __device__ __forceinline__ int64_t uni64(int64_t v)
 __device__ __forceinline__ uint64_t shfl64(uint64_t v, int32_t j)
 {
     return __shfl(v, j, WAVE);
+}
+
+// lane j's value (j wave-uniform)
+__device__ __forceinline__ uint64_t readlane64(uint64_t v, int32_t j)
+{
+    const uint32_t lo = __builtin_amdgcn_readlane((uint32_t)v, j);
+    const uint32_t hi = __builtin_amdgcn_readlane((uint32_t)(v >> 32), j);
+    return ((uint64_t)hi << 32) | lo;
 }
 
 #define GAS __attribute__((address_space(1)))    // global memory
@@ -189,8 +205,19 @@ struct Sim {
 #ifdef DTR_PROFILE
     int64_t prof_scan_cycles, prof_scans, prof_rounds;
     int64_t prof_slow, prof_global_nodes, prof_uf_compact, prof_pool_compact;
+    int64_t prof_ph[PROF_PHASES];
 #endif
 };
+
+// phase timers (DTR_PROFILE builds only)
+#ifdef DTR_PROFILE
+#define PROF_T0(v) const int64_t v = (int64_t)__builtin_readcyclecounter()
+#define PROF_ADD(k, v) s.prof_ph[k] += (int64_t)__builtin_readcyclecounter() - (v)
+#else
+#define PROF_T0(v)
+#define PROF_ADD(k, v)
+#endif
+enum { PH_EVICT = 0, PH_EXECUTE, PH_UNLOCK, PH_LOCK, PH_RELEASE, PH_RESUME, PH_OUTPUT, PH_DESCEND };
 
 __device__ __forceinline__ void set_status(Sim &s, int32_t st)
 {
@@ -238,7 +265,11 @@ __device__ __forceinline__ TRec rec_v(const Sim &s, int32_t x)
 // (unused entries hold node 0, the null node: cost 0, its own root).  Returns
 // the cache; `deg` receives (degree << 8) | count (K + 1: overflowed).
 // Neighbour states are read LB at a time, all loads unconditional.
-__device__ __forceinline__ i32x4 list_build(const Sim &s, int32_t b, int32_t e, int32_t &deg)
+struct NbCache {
+    i32x4 q[KQ];
+};
+
+__device__ __forceinline__ NbCache list_build(const Sim &s, int32_t b, int32_t e, int32_t &deg)
 {
     int32_t c[K];
 #pragma unroll
@@ -260,12 +291,21 @@ __device__ __forceinline__ i32x4 list_build(const Sim &s, int32_t b, int32_t e, 
         }
     }
     deg = ((e - b) << 8) | (cnt > K ? K + 1 : cnt);
-    i32x4 r;
-    r.x = c[0];
-    r.y = c[1];
-    r.z = c[2];
-    r.w = c[3];
+    NbCache r;
+#pragma unroll
+    for (int k = 0; k < KQ; k++) {
+        r.q[k].x = c[4 * k];
+        r.q[k].y = c[4 * k + 1];
+        r.q[k].z = c[4 * k + 2];
+        r.q[k].w = c[4 * k + 3];
+    }
     return r;
+}
+
+__device__ __forceinline__ void cache_store(PoolSlot &ps, const NbCache &c)
+{
+#pragma unroll
+    for (int k = 0; k < KQ; k++) ((i32x4 *)ps.nb)[k] = c.q[k];
 }
 
 __device__ __forceinline__ void list_add(const Sim &s, int32_t i, int32_t nd)
@@ -282,9 +322,16 @@ __device__ __forceinline__ void list_add(const Sim &s, int32_t i, int32_t nd)
 __device__ __forceinline__ bool list_remove(const Sim &s, int32_t i, int32_t nd)
 {
     PoolSlot &ps = s.S.pool(i);
-    const i32x4 nb4 = *(const i32x4 *)ps.nb;
+    int32_t v[K];
+#pragma unroll
+    for (int k = 0; k < KQ; k++) {
+        const i32x4 q = ((const i32x4 *)ps.nb)[k];
+        v[4 * k] = q.x;
+        v[4 * k + 1] = q.y;
+        v[4 * k + 2] = q.z;
+        v[4 * k + 3] = q.w;
+    }
     const int32_t pd = ps.deg;
-    const int32_t v[K] = {nb4.x, nb4.y, nb4.z, nb4.w};
     const int32_t c = pd & 0xFF;
     if (c > K) return true;
     int32_t at = -1;
@@ -318,8 +365,9 @@ __device__ __forceinline__ void pool_compact(Sim &s)
         const int32_t i = base + lane;
         const i32x4 *P = (const i32x4 *)&s.S.pool(i < s.pool_end ? i : 0);
         const i32x4 q0 = P[0], q1 = P[1];
-        i32x4 q2 = 0;
-        if (HC == HC_EQ) q2 = P[2];
+        i32x4 qc[KQ];
+#pragma unroll
+        for (int k = 0; k < KQ; k++) qc[k] = HC == HC_EQ ? P[2 + k] : 0;
         const int32_t x = i < s.pool_end ? q0.x : -1;
         const bool keep = x >= 0;
         const uint64_t m = __ballot(keep);
@@ -329,7 +377,9 @@ __device__ __forceinline__ void pool_compact(Sim &s)
             i32x4 *Q = (i32x4 *)&s.S.pool(j);
             Q[0] = q0;
             Q[1] = q1;
-            if (HC == HC_EQ) Q[2] = q2;
+            if (HC == HC_EQ)
+#pragma unroll
+                for (int k = 0; k < KQ; k++) Q[2 + k] = qc[k];
             s.S.tst[x] = ts_make(S_RESIDENT, (uint32_t)j, 0);
         }
         kept += __popcll(m);
@@ -355,7 +405,7 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
         i = s.pool_end + lane_rank(m);
         const TRec r = rec_v(s, x);
         int32_t deg = (r.adj_e - r.adj_b) << 8;
-        i32x4 nb = 0;
+        NbCache nb;
         if (HC == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg);
         i32x4 q0, q1;
         q0.x = x;
@@ -369,7 +419,7 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
         i32x4 *Q = (i32x4 *)&s.S.pool(i);
         Q[0] = q0;
         Q[1] = q1;
-        if (HC == HC_EQ) Q[2] = nb;
+        if (HC == HC_EQ) cache_store(s.S.pool(i), nb);
     }
     s.pool_end += cnt;
     s.pool_live += cnt;
@@ -479,7 +529,7 @@ __device__ __forceinline__ void uf_compact(Sim &s)
         if (x >= 0) {
             const TRec r = rec_v(s, x);
             int32_t deg;
-            *(i32x4 *)ps.nb = list_build(s, r.adj_b, r.adj_e, deg);
+            cache_store(ps, list_build(s, r.adj_b, r.adj_e, deg));
             ps.deg = deg;
         }
     }
@@ -729,18 +779,53 @@ __device__ __forceinline__ void clear_stamps(Sim &s)
     s.epoch = 0;
 }
 
+// Scores are N / (da * db) with N < 2^64 and da * db < 2^76.  A float
+// estimate (relative error below 2^-21) decides every comparison whose two
+// estimates differ by more than a factor 1 -+ 2^-16; the rest (near ties,
+// exact ties, 0/0) are decided exactly by 128-bit cross-multiplication, so
+// the outcome is always that of the exact comparison.
+constexpr float FILTER_LO = 1.0f - 0x1p-16f;
+constexpr float FILTER_HI = 1.0f + 0x1p-16f;
+
+__device__ __forceinline__ float u64f(uint64_t x)
+{
+    return fmaf((float)(uint32_t)(x >> 32), 4294967296.0f, (float)(uint32_t)x);
+}
+
+__device__ __forceinline__ float score_est(uint64_t N, uint64_t da, uint64_t db)
+{
+    return u64f(N) * __builtin_amdgcn_rcpf(u64f(da) * u64f(db));   // 0 -> inf, 0/0 -> NaN
+}
+
+__device__ __forceinline__ bool better_exact(uint64_t na, uint64_t daa, uint64_t dba, int32_t ia, uint64_t nb,
+                                             uint64_t dab, uint64_t dbb, int32_t ib)
+{
+    return better(na, (u128)daa * dba, ia, nb, (u128)dab * dbb, ib);
+}
+
 struct Best {
-    uint64_t N;
-    u128 D;
+    float sc, lo, hi;    // estimated score of the best and its decision bounds
+    uint64_t N, da, db;
     int32_t id, slot, have;
 };
 
-// keep (N, D, id) if valid and better than the current best (selects, no branch)
-__device__ __forceinline__ void take(Best &b, bool valid, uint64_t N, u128 D, int32_t id, int32_t slot)
+// keep the candidate if valid and better than the current best
+__device__ __forceinline__ void take(Best &b, bool valid, float sc, uint64_t N, uint64_t da, uint64_t db, int32_t id,
+                                     int32_t slot)
 {
-    const bool t = valid && (!b.have || better(N, D, id, b.N, b.D, b.id));
+    const bool dec_better = sc < b.lo;
+    const bool dec_worse = sc > b.hi;
+    bool t = valid && (!b.have || dec_better);
+    const bool close = valid && b.have && !dec_better && !dec_worse;
+    if (__ballot(close)) {
+        if (close) t = better_exact(N, da, db, id, b.N, b.da, b.db, b.id);
+    }
+    b.sc = t ? sc : b.sc;
+    b.lo = t ? sc * FILTER_LO : b.lo;
+    b.hi = t ? sc * FILTER_HI : b.hi;
     b.N = t ? N : b.N;
-    b.D = t ? D : b.D;
+    b.da = t ? da : b.da;
+    b.db = t ? db : b.db;
     b.id = t ? id : b.id;
     b.slot = t ? slot : b.slot;
     b.have = t ? 1 : b.have;
@@ -758,11 +843,13 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
     const GAS i32x4 *G4 = (const GAS i32x4 *)s.S.gpool;
     bool bad = false;
     Best best;
+    best.sc = best.lo = best.hi = 0.0f;
     best.N = 0;
-    best.D = 1;
+    best.da = best.db = 1;
     best.id = 0x7fffffff;
     best.slot = -1;
     best.have = 0;
+    constexpr int U = Round<HC>::value;
     if (HC == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
         clear_stamps(s);
     for (int32_t base = 0; base < end; base += WAVE * U) {
@@ -772,9 +859,9 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
         int32_t ab[U];
         int32_t nb[U][K];
         bool ok[U];
-        // level 1: three 16-byte quads per slot, all issued together, from
+        // level 1: the 16-byte quads of each slot, all issued together, from
         // LDS or global memory (a round never straddles the two)
-        i32x4 Q0[U], Q1[U], Q2[U];
+        i32x4 Q0[U], Q1[U], QC[U][KQ];
 #pragma unroll
         for (int u = 0; u < U; u++) {
             const int32_t i = base + u * WAVE + lane;
@@ -783,38 +870,40 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
         if (base < POOL_LDS) {
 #pragma unroll
             for (int u = 0; u < U; u++) {
-                Q0[u] = L4[3 * slot[u]];
-                Q1[u] = L4[3 * slot[u] + 1];
-                Q2[u] = 0;
-                if (HC == HC_EQ) Q2[u] = L4[3 * slot[u] + 2];
+                Q0[u] = L4[PQ * slot[u]];
+                Q1[u] = L4[PQ * slot[u] + 1];
+#pragma unroll
+                for (int k = 0; k < KQ; k++) QC[u][k] = HC == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
             }
         } else {
 #pragma unroll
             for (int u = 0; u < U; u++) {
-                Q0[u] = G4[3 * slot[u]];
-                Q1[u] = G4[3 * slot[u] + 1];
-                Q2[u] = 0;
-                if (HC == HC_EQ) Q2[u] = G4[3 * slot[u] + 2];
+                Q0[u] = G4[PQ * slot[u]];
+                Q1[u] = G4[PQ * slot[u] + 1];
+#pragma unroll
+                for (int k = 0; k < KQ; k++) QC[u][k] = HC == HC_EQ ? G4[PQ * slot[u] + 2 + k] : 0;
             }
         }
 #pragma unroll
         for (int u = 0; u < U; u++) {
             const int32_t i = base + u * WAVE + lane;
-            const i32x4 q0 = Q0[u], q1 = Q1[u], q2 = Q2[u];
+            const i32x4 q0 = Q0[u], q1 = Q1[u];
             id[u] = i < end ? q0.x : -1;
             pd[u] = q0.y;
             last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
             size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
             c0[u] = (int64_t)q1.z;
             ab[u] = q1.w;
-            nb[u][0] = q2.x;
-            nb[u][1] = q2.y;
-            nb[u][2] = q2.z;
-            nb[u][3] = q2.w;
+#pragma unroll
+            for (int k = 0; k < KQ; k++) {
+                nb[u][4 * k] = QC[u][k].x;
+                nb[u][4 * k + 1] = QC[u][k].y;
+                nb[u][4 * k + 2] = QC[u][k].z;
+                nb[u][4 * k + 3] = QC[u][k].w;
+            }
             ok[u] = id[u] >= 0;
         }
-        uint64_t N[U];
-        u128 D[U];
+        uint64_t N[U], DA[U], DB[U];
         if (HC == HC_EQ) {
             const bool lds_nodes = s.uf_n <= UF_LDS;
             // level 2: every cached node (unused entries hold node 0, the null
@@ -832,12 +921,14 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 bool deep = false;
                 if (lds_nodes) {
                     const LAS UfNode *NL = s.S.nodes.lds_l;
+                    const LAS i32x4 *NQ = (const LAS i32x4 *)NL;    // {cost lo, cost hi, parent, size}
 #pragma unroll
                     for (int k = 0; k < K; k++) r[k] = NL[nb[u][k]].parent;
 #pragma unroll
                     for (int k = 0; k < K; k++) {
-                        cost[k] = NL[r[k]].cost;
-                        deep |= NL[r[k]].parent != r[k];
+                        const i32x4 n2 = NQ[r[k]];
+                        cost[k] = (int64_t)(((uint64_t)(uint32_t)n2.y << 32) | (uint32_t)n2.x);
+                        deep |= n2.z != r[k];
                     }
                 } else {
 #pragma unroll
@@ -892,7 +983,8 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 N[u] = (uint64_t)(c0[u] + sum[u]);
-                D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
+                DA[u] = (uint64_t)size[u];
+                DB[u] = (uint64_t)(T - last[u]);
                 s.nbr += ok[u] ? ev[u] : 0;
                 s.adj += ok[u] ? (pd[u] >> 8) : 0;
             }
@@ -900,15 +992,13 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 N[u] = 0;
-                D[u] = 1;
+                DA[u] = DB[u] = 1;
                 if (!ok[u]) continue;
                 int64_t cnt;
                 const uint32_t ep = s.epoch + 1 + (uint32_t)u;
                 N[u] = (uint64_t)(c0[u] + estar_cost(s, id[u], ep, cnt));
-                if (h == H_DTR)
-                    D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
-                else
-                    D[u] = (u128)(uint64_t)size[u];
+                DA[u] = (uint64_t)size[u];
+                DB[u] = h == H_DTR ? (uint64_t)(T - last[u]) : 1;
                 s.nbr += cnt;
                 s.adj += pd[u] >> 8;
             }
@@ -919,42 +1009,59 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 switch (h) {
                 case H_LRU:
                     N[u] = 1;
-                    D[u] = (u128)(uint64_t)(T - last[u]);
+                    DA[u] = 1;
+                    DB[u] = (uint64_t)(T - last[u]);
                     break;
                 case H_SIZE:
                     N[u] = 1;
-                    D[u] = (u128)(uint64_t)size[u];
+                    DA[u] = (uint64_t)size[u];
+                    DB[u] = 1;
                     break;
                 case H_RAND: {
                     const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
                     N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
-                    D[u] = 1;
+                    DA[u] = DB[u] = 1;
                     break;
                 }
                 default:     // H_LOCAL
                     N[u] = (uint64_t)c0[u];
-                    D[u] = (u128)(uint64_t)size[u] * (u128)(uint64_t)(T - last[u]);
+                    DA[u] = (uint64_t)size[u];
+                    DB[u] = (uint64_t)(T - last[u]);
                     break;
                 }
             }
         }
 #pragma unroll
-        for (int u = 0; u < U; u++) take(best, ok[u], N[u], D[u], id[u], (int32_t)slot[u]);
-    }
-    // cross-lane lexicographic minimum
-    for (int off = WAVE / 2; off >= 1; off >>= 1) {
-        const uint64_t oN = __shfl_xor(best.N, off, WAVE);
-        const uint64_t oDl = __shfl_xor((uint64_t)best.D, off, WAVE);
-        const uint64_t oDh = __shfl_xor((uint64_t)(best.D >> 64), off, WAVE);
-        const int32_t oid = __shfl_xor(best.id, off, WAVE);
-        const int32_t oslot = __shfl_xor(best.slot, off, WAVE);
-        const int32_t oh = __shfl_xor(best.have, off, WAVE);
-        take(best, oh != 0, oN, ((u128)oDh << 64) | oDl, oid, oslot);
+        for (int u = 0; u < U; u++)
+            take(best, ok[u], score_est(N[u], DA[u], DB[u]), N[u], DA[u], DB[u], id[u], (int32_t)slot[u]);
     }
     if (__ballot(bad)) { set_status(s, ST_CAPACITY); return -1; }
-    if (!uni(best.have)) return -1;
-    victim_slot = uni(best.slot);
-    return uni(best.id);
+    // cross-lane minimum: the smallest estimate bounds the winner; only the
+    // lanes within the filter margin of it (usually one) are compared exactly
+    float mn = best.have ? best.sc : __builtin_inff();
+    for (int off = WAVE / 2; off >= 1; off >>= 1) mn = fminf(mn, __shfl_xor(mn, off, WAVE));
+    const float thr = mn * FILTER_HI;
+    uint64_t m = __ballot(best.have && !(best.sc > thr));     // NaN estimates stay in
+    if (!m) return -1;
+    int32_t j = __ffsll((long long)m) - 1;
+    m &= m - 1;
+    uint64_t wN = readlane64(best.N, j), wda = readlane64(best.da, j), wdb = readlane64(best.db, j);
+    int32_t wid = __builtin_amdgcn_readlane(best.id, j), wslot = __builtin_amdgcn_readlane(best.slot, j);
+    while (m) {
+        j = __ffsll((long long)m) - 1;
+        m &= m - 1;
+        const uint64_t cN = readlane64(best.N, j), cda = readlane64(best.da, j), cdb = readlane64(best.db, j);
+        const int32_t cid = __builtin_amdgcn_readlane(best.id, j), cslot = __builtin_amdgcn_readlane(best.slot, j);
+        if (better_exact(cN, cda, cdb, cid, wN, wda, wdb, wid)) {
+            wN = cN;
+            wda = cda;
+            wdb = cdb;
+            wid = cid;
+            wslot = cslot;
+        }
+    }
+    victim_slot = wslot;
+    return wid;
 }
 
 // ----------------------------------------------------- operator calls --
@@ -965,11 +1072,11 @@ __device__ __forceinline__ bool allocate(Sim &s, int64_t sz)
     while (s.mem + sz > s.budget) {
         if (s.pool_live == 0) { set_status(s, ST_OOM); return false; }
         // keep the scanned range within half a round of the live pool
-        if (s.pool_end > s.pool_live + WAVE * U / 2) pool_compact<HC>(s);
+        if (s.pool_end > s.pool_live + WAVE * Round<HC>::value / 2) pool_compact<HC>(s);
 #ifdef DTR_PROFILE
         const int64_t c0_ = (int64_t)__builtin_readcyclecounter();
         s.prof_scans++;
-        s.prof_rounds += (s.pool_end + WAVE * U - 1) / (WAVE * U);
+        s.prof_rounds += (s.pool_end + WAVE * Round<HC>::value - 1) / (WAVE * Round<HC>::value);
 #endif
         int32_t slot = -1;
         const int32_t v = scan<HC>(s, slot);
@@ -978,7 +1085,10 @@ __device__ __forceinline__ bool allocate(Sim &s, int64_t sz)
 #endif
         if (v < 0) { set_status(s, ST_CAPACITY); return false; }
         s.scores += s.pool_live;
-        if (!evict<HC>(s, v, slot, false)) return false;
+        PROF_T0(te);
+        const bool evicted = evict<HC>(s, v, slot, false);
+        PROF_ADD(PH_EVICT, te);
+        if (!evicted) return false;
         s.evict_no++;
     }
     return true;
@@ -1120,14 +1230,18 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
     f.u = -1;
     f.w = 0;
     for (;;) {
+        PROF_T0(td);
         const TRec rt = rec_u(s, tt);
         const int32_t b = rt.in_b, e = rt.in_e;
         if (cur < 0) {
+            PROF_T0(tl);
             lock_inputs(s, s.t.in, b, e, f);
+            PROF_ADD(PH_LOCK, tl);
             if (s.status != ST_OK) return false;
             cur = 0;
         }
         const int32_t j = uni(next_evicted(s, b, e, cur, f));
+        PROF_ADD(PH_DESCEND, td);
         if (j < e - b) {
             if (sp + 1 >= s.S.n_max) { set_status(s, ST_CAPACITY); return false; }
             const int32_t child = uni(j < WAVE ? __shfl(f.u, j, WAVE) : cld(s.t.in + b + j));
@@ -1143,15 +1257,23 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         }
         if (!allocate<HC>(s, rt.size)) return false;
         const int64_t start = s.T;
-        if (!execute<HC>(s, tt, rt, remat, tlocks)) return false;
+        PROF_T0(tx);
+        const bool done = execute<HC>(s, tt, rt, remat, tlocks);
+        PROF_ADD(PH_EXECUTE, tx);
+        if (!done) return false;
+        PROF_T0(tu);
         unlock_inputs<HC>(s, b, e, start, f);
+        PROF_ADD(PH_UNLOCK, tu);
         if (!remat) {
             // a trace operation's output is unlocked: it joins the pool at once
+            PROF_T0(to);
             const int32_t slot = uni(pool_append<HC>(s, s.lane == 0, tt, start));
             s.S.tst[tt] = ts_make(S_RESIDENT, (uint32_t)slot, 0);
+            PROF_ADD(PH_OUTPUT, to);
         }
         if (s.status != ST_OK) return false;
         if (sp == 0) return true;
+        PROF_T0(tr);
         sp--;
         const int2 fr = s.S.stack[sp];
         tt = uni(fr.x);
@@ -1162,6 +1284,7 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         // locks on the resumed frame's output: none for a trace operation,
         // else whatever its consumers (or the output condition) hold
         tlocks = remat ? (uint32_t)uni((int32_t)ts_locks(s.S.tst[tt])) : 0u;
+        PROF_ADD(PH_RESUME, tr);
     }
 }
 
@@ -1215,6 +1338,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     const int64_t t_start = (int64_t)__builtin_readcyclecounter();
     s.prof_scan_cycles = s.prof_scans = s.prof_rounds = 0;
     s.prof_slow = s.prof_global_nodes = s.prof_uf_compact = s.prof_pool_compact = 0;
+    for (int k = 0; k < PROF_PHASES; k++) s.prof_ph[k] = 0;
 #endif
 
     const int32_t n = s.t.n;
@@ -1236,7 +1360,10 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     if (s.mem > s.budget) { set_status(s, ST_OOM); ok = false; }
     for (int32_t o = 0; ok && o < s.t.F; o++) {
         s.cur_op = o;
-        if (!call<HC>(s, uni(cld(s.t.out + o)), false, 0) || !release<HC>(s, o) || s.status != ST_OK) ok = false;
+        if (!call<HC>(s, uni(cld(s.t.out + o)), false, 0)) ok = false;
+        PROF_T0(tr);
+        if (ok && (!release<HC>(s, o) || s.status != ST_OK)) ok = false;
+        PROF_ADD(PH_RELEASE, tr);
     }
     if (ok) {
         // output condition: lock each required output, rematerialize it if evicted
@@ -1271,6 +1398,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
         pr[5] = s.prof_global_nodes;
         pr[6] = s.prof_uf_compact;
         pr[7] = s.prof_pool_compact;
+        for (int k = 0; k < PROF_PHASES; k++) pr[8 + k] = s.prof_ph[k];
     }
 #endif
     if (lane == 0) {
