@@ -19,8 +19,10 @@ plain CPU oracle timed on a bounded, deterministic sample of the same batch.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -58,6 +60,46 @@ def scan_bytes(specs, res) -> int:
     return total
 
 
+# HBM traffic of the replay kernel, measured with rocprofv3 counter passes
+# (FETCH_SIZE, WRITE_SIZE) and scaled by the same counters on a plain device
+# copy of known size; valid only for the kernel sources it was measured on.
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "replay_kernel_eq_treelstm4096_traffic.md")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2006_09616_amd", "csrc", f) for f in ("replay.hip", "layout.h")]
+
+
+def kernel_source_digest() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per launch from the committed counter summary, or None when
+    there is none for this workload or the kernel changed since it was taken."""
+    if workload != "treelstm4096" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    text = open(TRAFFIC_FILE).read()
+    m_b = re.search(r"^traffic_bytes_per_launch:\s*(\d+)", text, re.M)
+    m_h = re.search(r"^kernel_source_sha256:\s*([0-9a-f]{64})", text, re.M)
+    if not m_b or not m_h or m_h.group(1) != kernel_source_digest():
+        return None
+    return int(m_b.group(1))
+
+
+def copy_probe(mib: int):
+    """A plain device-to-device copy of known size (counter calibration)."""
+    import torch
+    n = mib << 20
+    x = torch.ones(n, dtype=torch.uint8, device="cuda:0")
+    y = torch.empty_like(x)
+    for _ in range(3):
+        y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_probe_bytes": n, "copies": 3}))
+
+
 WORKLOADS = {
     "treelstm4096": lambda: W.make_config("treelstm4096"),
     "resnet50blk": lambda: W.make_config("resnet50blk"),
@@ -93,11 +135,17 @@ def main():
     ap.add_argument("--slots", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=32, help="oracle on every k-th simulation (0: skip)")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB MiB three times (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py measures one GPU: simulations are independent and this build runs on a "
               "single MI355X; sharding across GPUs is described in DESIGN.md, not run.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe > 0:
+        copy_probe(args.copy_probe)
+        return
 
     import torch
     from paper_2006_09616_amd import dtr as D
@@ -163,7 +211,7 @@ def main():
                    "trace_sha256": wl.digest()[:16]},
         "eviction_scores_per_s": scores / avg_s,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
                      "kernel": "replay_kernel", "algorithmic_bytes_per_launch": nbytes,
                      "avg_launch_ms": avg_s * 1e3},
         "cpu_baseline": cpu,
