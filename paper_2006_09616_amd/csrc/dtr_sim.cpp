@@ -256,7 +256,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     take(L.pool, sizeof(dtr::PoolSlot) * pc);
     take(L.nodes, sizeof(dtr::UfNode) * (size_t)L.ucap);
     take(L.uf_remap, need_uf ? 4 * ((size_t)L.ucap + dtr::UF_LDS) : 0);
-    take(L.stack, 8 * (n + 1));
+    take(L.stack, sizeof(dtr::StackFrame) * (size_t)(n + 1));
     take(L.stamp, need_walk ? 4 * n * dtr::WAVE : 0);
     take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);
     L.bytes = (int64_t)o;

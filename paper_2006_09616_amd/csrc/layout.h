@@ -82,7 +82,7 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 //             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
 //             neighbours (n = NB_CACHE + 1 marks an overflowed cache)
 //   nodes     union-find nodes {running cost, parent, size}
-//   stack     rematerialization frames (tensor, next input)
+//   stack     rematerialization frames (tensor, next input, the tensor's record)
 //   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
 constexpr int NB_CACHE = 8;
 // union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
@@ -112,6 +112,12 @@ struct __attribute__((aligned(16))) PoolSlot {
     int32_t nb[NB_CACHE];    // cached union-find nodes of evicted neighbours
 };
 static_assert(sizeof(PoolSlot) == 64, "pool slot layout");
+
+struct __attribute__((aligned(16))) StackFrame {
+    int32_t t, next, pad0, pad1;
+    TRec rec;
+};
+static_assert(sizeof(StackFrame) == 48, "stack frame layout");
 
 struct __attribute__((aligned(16))) UfNode {
     int64_t cost;

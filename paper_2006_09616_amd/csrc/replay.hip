@@ -15,7 +15,7 @@
 //    registers for the life of the frame; release lists are checked in
 //    parallel;
 //  * the evictable pool (Appendix C.4 "Runtime state") is a tombstoned
-//    struct of arrays read coalesced; each lane scores one or two candidates per
+//    array of 64-byte slots read as coalesced quads; each lane scores one or two candidates per
 //    round with all slot reads issued at once, and the exact (score, id)
 //    minimum is reduced across lanes;
 //  * h_DTR^eq (Appendix C.2): each pool slot caches the union-find nodes of
@@ -58,8 +58,9 @@ static_assert(K % 4 == 0 && PQ == 2 + KQ, "pool slot: two header quads, then the
 constexpr int LB = 8;            // neighbour reads issued together when building a cache
 // kernel specialisations by heuristic class (register budgets differ widely)
 enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2 };
-// candidates per lane per scan round (h_DTR^eq reads K cached nodes per
-// candidate, so one fits the register budget there)
+// candidates per lane per scan round (their reads are issued together); the
+// h_DTR^eq round is instruction-issue bound, so a second candidate per lane
+// only doubles the round
 template <int HC>
 struct Round {
     static constexpr int value = HC == HC_EQ ? 1 : 2;
@@ -75,11 +76,6 @@ __device__ __forceinline__ int64_t uni64(int64_t v)
     uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
     uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
     return (int64_t)(((uint64_t)hi << 32) | lo);
-}
-
-__device__ __forceinline__ uint64_t shfl64(uint64_t v, int32_t j)
-{
-    return __shfl(v, j, WAVE);
 }
 
 // lane j's value (j wave-uniform)
@@ -155,7 +151,7 @@ struct Slot {
     GAS PoolSlot *gpool;
     NodeStore nodes;
     GAS int32_t *remap;
-    int2 *stack;
+    GAS i32x4 *stack;             // StackFrame records, three quads each
     GAS uint32_t *stamp;
     GAS int32_t *queue;
     int32_t pcap, ucap, n_max;
@@ -177,7 +173,7 @@ __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
     S.nodes.lds_l = nullptr;
     S.nodes.glob = (UfNode *)(b + a.L.nodes);
     S.remap = (GAS int32_t *)(b + a.L.uf_remap);
-    S.stack = (int2 *)(b + a.L.stack);
+    S.stack = (GAS i32x4 *)(b + a.L.stack);
     S.stamp = (GAS uint32_t *)(b + a.L.stamp);
     S.queue = (GAS int32_t *)(b + a.L.queue);
     S.pcap = (int32_t)a.L.pcap;
@@ -428,6 +424,39 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
 
 // ---------------------------------------------------------- union-find --
 
+// Union-find node access: straight from LDS while every node id is below
+// UF_LDS, else through the hybrid store (flat pointers).
+struct LdsNodes {
+    LAS UfNode *p;
+    __device__ __forceinline__ int32_t parent(int32_t i) const { return p[i].parent; }
+    __device__ __forceinline__ int32_t size(int32_t i) const { return p[i].size; }
+    __device__ __forceinline__ int64_t cost(int32_t i) const { return p[i].cost; }
+    __device__ __forceinline__ void set_parent(int32_t i, int32_t v) const { p[i].parent = v; }
+    __device__ __forceinline__ void set_size(int32_t i, int32_t v) const { p[i].size = v; }
+    __device__ __forceinline__ void set_cost(int32_t i, int64_t v) const { p[i].cost = v; }
+};
+struct AnyNodes {
+    NodeStore n;
+    __device__ __forceinline__ int32_t parent(int32_t i) const { return n[i].parent; }
+    __device__ __forceinline__ int32_t size(int32_t i) const { return n[i].size; }
+    __device__ __forceinline__ int64_t cost(int32_t i) const { return n[i].cost; }
+    __device__ __forceinline__ void set_parent(int32_t i, int32_t v) const { n[i].parent = v; }
+    __device__ __forceinline__ void set_size(int32_t i, int32_t v) const { n[i].size = v; }
+    __device__ __forceinline__ void set_cost(int32_t i, int64_t v) const { n[i].cost = v; }
+};
+
+
+template <class NS>
+__device__ __forceinline__ int32_t find_in(const NS &N, int32_t x, int32_t limit)
+{
+    for (int32_t k = 0; k <= limit; k++) {
+        const int32_t p = N.parent(x);
+        if (p == x) return x;
+        x = p;
+    }
+    return -1;   // not a forest: reported as a capacity error
+}
+
 __device__ __forceinline__ int32_t find_ro(const NodeStore &nodes, int32_t x, int32_t limit)
 {
     for (int32_t k = 0; k <= limit; k++) {
@@ -439,35 +468,22 @@ __device__ __forceinline__ int32_t find_ro(const NodeStore &nodes, int32_t x, in
 }
 
 // uniform find with path compression (used where one set is touched)
-__device__ __forceinline__ int32_t find_compress(Sim &s, int32_t x)
+template <class NS>
+__device__ __forceinline__ int32_t find_compress(Sim &s, const NS &N, int32_t x)
 {
-    const NodeStore &N = s.S.nodes;
     int32_t root = x;
     for (int32_t k = 0;; k++) {
-        const int32_t p = uni(N[root].parent);
+        const int32_t p = uni(N.parent(root));
         if (p == root) break;
         if (k > s.uf_n) { set_status(s, ST_CAPACITY); return x; }
         root = p;
     }
     while (x != root) {
-        const int32_t nx = uni(N[x].parent);
-        N[x].parent = root;
+        const int32_t nx = uni(N.parent(x));
+        N.set_parent(x, root);
         x = nx;
     }
     return root;
-}
-
-__device__ __forceinline__ int32_t unite(Sim &s, int32_t a, int32_t b)
-{
-    if (a == b) return a;
-    const NodeStore &N = s.S.nodes;
-    int32_t sa = uni(N[a].size), sb = uni(N[b].size);
-    if (sa < sb) { int32_t t = a; a = b; b = t; int32_t u = sa; sa = sb; sb = u; }
-    const int64_t cost = uni64(N[a].cost) + uni64(N[b].cost);
-    N[b].parent = a;
-    N[a].size = sa + sb;
-    N[a].cost = cost;
-    return a;
 }
 
 // Rebuild the node pool: one node per distinct set that still holds an
@@ -538,6 +554,82 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 
 // ------------------------------------------------------------ eviction --
 
+// v's fresh node nd (cost c0(v)) joins the sets of all v's evicted neighbours
+// (found in parallel, merged under the largest; ties: the earliest), and every
+// neighbour waiting in the pool caches nd.
+template <class NS>
+__device__ __forceinline__ bool evict_merge(Sim &s, const NS &N, int32_t nd, const TRec &rv)
+{
+    int32_t R = nd;               // current root of v's set
+    int64_t Rcost = rv.c0;
+    int32_t Rsize = 1;
+    if (s.lane == 0) {
+        N.set_cost(nd, rv.c0);
+        N.set_parent(nd, nd);
+        N.set_size(nd, 1);
+    }
+    bool bad = false;
+    for (int32_t k0 = rv.adj_b; k0 < rv.adj_e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        int32_t q = -1, r = -1;
+        if (k < rv.adj_e) {
+            const uint64_t w = s.S.tst[gld(s.t.adj + k)];
+            q = ts_sw(w);
+            if (ts_in_pool(w)) list_add(s, (int32_t)ts_pos(w), nd);
+            if (q >= 0) {
+                r = find_in(N, q, s.uf_n);
+                if (r < 0) { bad = true; r = -1; q = -1; }
+            }
+        }
+        // first lane holding each distinct root contributes it
+        bool first = r >= 0;
+        uint64_t m = __ballot(r >= 0);
+        while (m) {
+            const int32_t j = __ffsll((long long)m) - 1;
+            m &= m - 1;
+            const int32_t rj = __builtin_amdgcn_readlane(r, j);
+            if (r == rj && s.lane > j) first = false;
+        }
+        if (!first || r == R) r = -1;
+        int64_t rc = 0;
+        int32_t rs = 0;
+        if (r >= 0) {
+            rc = N.cost(r);
+            rs = N.size(r);
+        }
+        // merge every distinct root into the largest (ties: the earliest)
+        uint64_t mr = __ballot(r >= 0);
+        int32_t big = R, bigsize = Rsize;
+        int64_t sumc = Rcost;
+        int32_t sums = Rsize;
+        uint64_t mm = mr;
+        while (mm) {
+            const int32_t j = __ffsll((long long)mm) - 1;
+            mm &= mm - 1;
+            const int32_t rj = __builtin_amdgcn_readlane(r, j);
+            const int32_t sj = __builtin_amdgcn_readlane(rs, j);
+            sumc += (int64_t)readlane64((uint64_t)rc, j);
+            sums += sj;
+            if (sj > bigsize) { big = rj; bigsize = sj; }
+        }
+        if (mr) {
+            if (r >= 0 && r != big) N.set_parent(r, big);
+            if (q >= 0 && q != big) N.set_parent(q, big);     // compress the neighbour's path
+            if (s.lane == 0 && R != big) N.set_parent(R, big);
+            R = big;
+            Rcost = sumc;
+            Rsize = sums;
+        }
+    }
+    if (__ballot(bad)) { set_status(s, ST_CAPACITY); return false; }
+    if (s.lane == 0) {
+        N.set_cost(R, Rcost);
+        N.set_size(R, Rsize);
+        if (nd != R) N.set_parent(nd, R);
+    }
+    return true;
+}
+
 // Evict v (resident, unlocked, in pool slot `slot`).  Under h_DTR^eq, v gets a
 // fresh node holding c0(v), which is merged with the sets of all its evicted
 // neighbours (found in parallel, merged under the largest), and every
@@ -545,9 +637,19 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 template <int HC>
 __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eager)
 {
+    // size, c0 and neighbour range come from v's pool slot (LDS for the pool
+    // head), not from the static record
+    TRec rv;
+    {
+        const i32x4 *P = (const i32x4 *)&s.S.pool(slot);
+        const i32x4 q0 = P[0], q1 = P[1];
+        rv.size = uni64((int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x));
+        rv.c0 = uni(q1.z);
+        rv.adj_b = uni(q1.w);
+        rv.adj_e = rv.adj_b + uni(q0.y >> 8);
+    }
     s.S.pool(slot).id = -1;
     s.pool_live--;
-    const TRec rv = rec_u(s, v);
     s.mem -= rv.size;
     if (eager) s.eager++;
     else s.evictions++;
@@ -559,96 +661,23 @@ __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eage
         uf_compact(s);
         if (s.uf_n >= UF_LDS + s.S.ucap) { set_status(s, ST_CAPACITY); return false; }
     }
-    const NodeStore &N = s.S.nodes;
     const int32_t nd = s.uf_n++;
-    int32_t R = nd;               // current root of v's set
-    int64_t Rcost = rv.c0;
-    int32_t Rsize = 1;
-    UfNode node;
-    node.cost = rv.c0;
-    node.parent = nd;
-    node.size = 1;
-    if (s.lane == 0) N[nd] = node;
-    bool bad = false;
-    for (int32_t k0 = rv.adj_b; k0 < rv.adj_e; k0 += WAVE) {
-        const int32_t k = k0 + s.lane;
-        int32_t q = -1, r = -1;
-        if (k < rv.adj_e) {
-            const uint64_t w = s.S.tst[gld(s.t.adj + k)];
-            q = ts_sw(w);
-            if (ts_in_pool(w)) list_add(s, (int32_t)ts_pos(w), nd);
-            if (q >= 0) {
-                r = find_ro(N, q, s.uf_n);
-                if (r < 0) { bad = true; r = -1; q = -1; }
-            }
-        }
-        // first lane holding each distinct root contributes it
-        bool first = r >= 0;
-        uint64_t m = __ballot(r >= 0);
-        while (m) {
-            const int32_t j = __ffsll((long long)m) - 1;
-            m &= m - 1;
-            const int32_t rj = __shfl(r, j, WAVE);
-            if (r == rj && s.lane > j) first = false;
-        }
-        if (!first || r == R) r = -1;
-        int64_t rc = 0;
-        int32_t rs = 0;
-        if (r >= 0) {
-            const UfNode x = N[r];
-            rc = x.cost;
-            rs = x.size;
-        }
-        // merge every distinct root into the largest (ties: the earliest)
-        uint64_t mr = __ballot(r >= 0);
-        int32_t big = R, bigsize = Rsize;
-        int64_t sumc = Rcost;
-        int32_t sums = Rsize;
-        uint64_t mm = mr;
-        while (mm) {
-            const int32_t j = __ffsll((long long)mm) - 1;
-            mm &= mm - 1;
-            const int32_t rj = uni(__shfl(r, j, WAVE));
-            const int32_t sj = uni(__shfl(rs, j, WAVE));
-            sumc += uni64((int64_t)shfl64((uint64_t)rc, j));
-            sums += sj;
-            if (sj > bigsize) { big = rj; bigsize = sj; }
-        }
-        if (mr) {
-            if (r >= 0 && r != big) N[r].parent = big;
-            if (q >= 0 && q != big) N[q].parent = big;     // compress the neighbour's path
-            if (s.lane == 0 && R != big) N[R].parent = big;
-            R = big;
-            Rcost = sumc;
-            Rsize = sums;
-        }
+    bool ok;
+    if (s.uf_n <= UF_LDS) {
+        LdsNodes NL;
+        NL.p = s.S.nodes.lds_l;
+        ok = evict_merge(s, NL, nd, rv);
+    } else {
+        AnyNodes NA;
+        NA.n = s.S.nodes;
+        ok = evict_merge(s, NA, nd, rv);
     }
-    if (__ballot(bad)) { set_status(s, ST_CAPACITY); return false; }
-    if (s.lane == 0) {
-        N[R].cost = Rcost;
-        N[R].size = Rsize;
-        if (nd != R) N[nd].parent = R;
-    }
+    if (!ok) return false;
     s.S.tst[v] = ts_make(nd, 0, 0);
     return true;
 }
 
 // ---------------------------------------------------------------- scan --
-
-// Union-find node reads for the full-adjacency recount: straight from LDS
-// while every node id is below UF_LDS, else through the hybrid store.
-struct LdsNodes {
-    LAS UfNode *p;
-    __device__ __forceinline__ int32_t parent(int32_t i) const { return p[i].parent; }
-    __device__ __forceinline__ void set_parent(int32_t i, int32_t v) const { p[i].parent = v; }
-    __device__ __forceinline__ int64_t cost(int32_t i) const { return p[i].cost; }
-};
-struct AnyNodes {
-    NodeStore n;
-    __device__ __forceinline__ int32_t parent(int32_t i) const { return n[i].parent; }
-    __device__ __forceinline__ void set_parent(int32_t i, int32_t v) const { n[i].parent = v; }
-    __device__ __forceinline__ int64_t cost(int32_t i) const { return n[i].cost; }
-};
 
 // Set roots of the neighbours k0 .. k0+LB-1 (below e) of a candidate: r[j] is
 // the root of neighbour k0+j if it is evicted, else -1.  All neighbour and
@@ -1198,8 +1227,17 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
     if (HC == HC_EQ && remat) {
         // split approximation: the set loses c0(t); t leaves it (its node stays as a phantom)
         const int32_t old = uni(ts_sw(s.S.tst[t]));
-        const int32_t r = find_compress(s, old);
-        s.S.nodes[r].cost = uni64(s.S.nodes[r].cost) - c;
+        if (s.uf_n <= UF_LDS) {
+            LdsNodes NL;
+            NL.p = s.S.nodes.lds_l;
+            const int32_t r = find_compress(s, NL, old);
+            NL.set_cost(r, uni64(NL.cost(r)) - c);
+        } else {
+            AnyNodes NA;
+            NA.n = s.S.nodes;
+            const int32_t r = find_compress(s, NA, old);
+            NA.set_cost(r, uni64(NA.cost(r)) - c);
+        }
         bool lost = false;
         for (int32_t k0 = rt.adj_b; k0 < rt.adj_e; k0 += WAVE) {
             const int32_t k = k0 + s.lane;
@@ -1213,6 +1251,41 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
     s.S.tst[t] = ts_make(S_RESIDENT, 0, locks);
     if (s.T >= CLOCK_LIMIT) { set_status(s, ST_CLOCK); return false; }
     return s.status == ST_OK;
+}
+
+__device__ __forceinline__ void stack_push(const Sim &s, int32_t sp, int32_t t, int32_t next, const TRec &r)
+{
+    GAS i32x4 *F = s.S.stack + 3 * (size_t)sp;
+    i32x4 a, b, c;
+    a.x = t;
+    a.y = next;
+    a.z = a.w = 0;
+    b.x = (int32_t)(uint32_t)(uint64_t)r.size;
+    b.y = (int32_t)(uint32_t)((uint64_t)r.size >> 32);
+    b.z = r.c0;
+    b.w = r.producer;
+    c.x = r.in_b;
+    c.y = r.in_e;
+    c.z = r.adj_b;
+    c.w = r.adj_e;
+    F[0] = a;
+    F[1] = b;
+    F[2] = c;
+}
+
+__device__ __forceinline__ void stack_pop(const Sim &s, int32_t sp, int32_t &t, int32_t &next, TRec &r)
+{
+    const GAS i32x4 *F = s.S.stack + 3 * (size_t)sp;
+    const i32x4 a = F[0], b = F[1], c = F[2];
+    t = uni(a.x);
+    next = uni(a.y);
+    r.size = uni64((int64_t)(((uint64_t)(uint32_t)b.y << 32) | (uint32_t)b.x));
+    r.c0 = uni(b.z);
+    r.producer = uni(b.w);
+    r.in_b = uni(c.x);
+    r.in_e = uni(c.y);
+    r.adj_b = uni(c.z);
+    r.adj_e = uni(c.w);
 }
 
 // Run the operation producing `root` together with every rematerialization it
@@ -1229,9 +1302,9 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
     Frame f;
     f.u = -1;
     f.w = 0;
+    TRec rt = rec_u(s, tt);           // record of the current frame's tensor
     for (;;) {
         PROF_T0(td);
-        const TRec rt = rec_u(s, tt);
         const int32_t b = rt.in_b, e = rt.in_e;
         if (cur < 0) {
             PROF_T0(tl);
@@ -1244,15 +1317,16 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         PROF_ADD(PH_DESCEND, td);
         if (j < e - b) {
             if (sp + 1 >= s.S.n_max) { set_status(s, ST_CAPACITY); return false; }
-            const int32_t child = uni(j < WAVE ? __shfl(f.u, j, WAVE) : cld(s.t.in + b + j));
-            const uint32_t clocks = j < WAVE ? (uint32_t)uni((int32_t)ts_locks(shfl64(f.w, j)))
+            const int32_t child = j < WAVE ? __builtin_amdgcn_readlane(f.u, j) : uni(cld(s.t.in + b + j));
+            const uint32_t clocks = j < WAVE ? ts_locks(readlane64(f.w, j))
                                              : (uint32_t)uni((int32_t)ts_locks(s.S.tst[child]));
-            s.S.stack[sp] = make_int2(tt, j + 1);
+            stack_push(s, sp, tt, j + 1, rt);
             sp++;
             tt = child;
             tlocks = clocks;
             cur = -1;
             remat = true;
+            rt = rec_u(s, tt);
             continue;
         }
         if (!allocate<HC>(s, rt.size)) return false;
@@ -1275,12 +1349,9 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         if (sp == 0) return true;
         PROF_T0(tr);
         sp--;
-        const int2 fr = s.S.stack[sp];
-        tt = uni(fr.x);
-        cur = uni(fr.y);
+        stack_pop(s, sp, tt, cur, rt);
         remat = sp > 0 ? true : root_remat;
-        const TRec rp = rec_u(s, tt);
-        reload_frame(s, rp.in_b, rp.in_e, f);
+        reload_frame(s, rt.in_b, rt.in_e, f);
         // locks on the resumed frame's output: none for a trace operation,
         // else whatever its consumers (or the output condition) hold
         tlocks = remat ? (uint32_t)uni((int32_t)ts_locks(s.S.tst[tt])) : 0u;
@@ -1307,7 +1378,7 @@ __device__ __forceinline__ bool release(Sim &s, int32_t o)
         while (m) {
             const int32_t j = __ffsll((long long)m) - 1;
             m &= m - 1;
-            if (!evict<HC>(s, uni(__shfl(r, j, WAVE)), uni(__shfl(pos, j, WAVE)), true)) return false;
+            if (!evict<HC>(s, __builtin_amdgcn_readlane(r, j), __builtin_amdgcn_readlane(pos, j), true)) return false;
         }
     }
     return true;
@@ -1372,7 +1443,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
             Frame f;
             lock_inputs(s, s.t.req, k, k + 1, f);
             const int32_t r = uni(cld(s.t.req + k));
-            const uint64_t w = shfl64(f.w, 0);
+            const uint64_t w = readlane64(f.w, 0);
             if (s.status != ST_OK) ok = false;
             else if (ts_sw(w) >= 0 && !call<HC>(s, r, true, (uint32_t)uni((int32_t)ts_locks(w)))) ok = false;
         }
