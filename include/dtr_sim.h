@@ -59,6 +59,18 @@ extern "C" {
 #define DTR_H_SIZE  4  /* 1 / m                                                       */
 #define DTR_H_RAND  5  /* fresh SplitMix64 draw per (seed, eviction number, id)       */
 #define DTR_H_ESTAR 6  /* (c0 + sum c0 over e*) / m, the h_{e*} of Appendix A.3       */
+#define DTR_H_MSPS  7  /* (c0 + sum c0 over e_R) / m, e_R = the evicted tensors that
+                          rematerializing the candidate would recompute (Section 4.1) */
+/* The ablation family of Appendix D: h'(s, m, c) = c / (m s), where staleness
+ * s and size m are each used (1) or ablated (0: the measure is 1), and c is
+ * one of the cost measures below.  DTR_H_FAMILY(DTR_C_ESTAR, 1, 1) is h_DTR,
+ * (DTR_C_EQCLASS, 1, 1) h_DTR^eq, (DTR_C_LOCAL, 1, 1) h_local, (DTR_C_NONE, 1,
+ * 0) h_LRU, (DTR_C_NONE, 0, 1) h_size and (DTR_C_ESTAR, 0, 1) h_{e*}. */
+#define DTR_C_ESTAR   0  /* c0 + sum c0 over e*                    */
+#define DTR_C_EQCLASS 1  /* c0 + union-find neighbourhood cost      */
+#define DTR_C_LOCAL   2  /* c0                                      */
+#define DTR_C_NONE    3  /* 1                                       */
+#define DTR_H_FAMILY(c, s, m) (16 + 4 * (c) + 2 * (s) + (m))
 
 #define DTR_BUDGET_UNLIMITED INT64_MAX
 

@@ -21,7 +21,11 @@
  *   - heuristics of Section 4.1 and Appendix C.3: h_DTR with the exact
  *     evicted neighbourhood e* (Appendix C.2), h_DTR^eq with the union-find
  *     relaxation and its split approximation (Appendix C.2), h_DTR^local,
- *     h_LRU, h_size, h_rand; plus h_{e*} of Appendix A.3 (no staleness);
+ *     h_LRU, h_size, h_rand, h_MSPS (cost of the evicted ancestors e_R over
+ *     size, Section 4.1); h_{e*} of Appendix A.3 (no staleness); and the
+ *     ablation family h'(s, m, c) = c / (m * s) of Appendix D, with staleness
+ *     s and size m each used or not, and c the full e* cost, the
+ *     equivalence-class cost, the local cost or none (c = 1);
  *   - output condition: tensors the program still holds at the end are
  *     rematerialized and locked (Appendix C.6 log semantics).
  *
@@ -51,7 +55,14 @@
 #define O_FLAG_REQUIRED 2u
 
 enum { ST_UNCOMPUTED = 0, ST_RESIDENT = 1, ST_EVICTED = 2 };
-enum { OH_DTR = 0, OH_EQ = 1, OH_LOCAL = 2, OH_LRU = 3, OH_SIZE = 4, OH_RAND = 5, OH_ESTAR = 6 };
+enum { OH_DTR = 0, OH_EQ = 1, OH_LOCAL = 2, OH_LRU = 3, OH_SIZE = 4, OH_RAND = 5, OH_ESTAR = 6, OH_MSPS = 7,
+       OH_FAMILY = 16 /* h'(s, m, c): 16 + 4c + 2s + m, s and m 1 = used */ };
+enum { OC_ESTAR = 0, OC_EQCLASS = 1, OC_LOCAL = 2, OC_NONE = 3 };
+
+static int family(int h) { return h >= OH_FAMILY && h < OH_FAMILY + 16; }
+static int family_c(int h) { return (h - OH_FAMILY) >> 2; }
+/* heuristics that keep the union-find components of Appendix C.2 */
+static int uses_uf(int h) { return h == OH_EQ || (family(h) && family_c(h) == OC_EQCLASS); }
 enum { OS_OK = 0, OS_OOM = 1, OS_CLOCK_OVERFLOW = 2, OS_STOPPED = 100 };
 
 #define CLOCK_LIMIT ((int64_t)1 << 40)
@@ -259,17 +270,15 @@ static int is_evictable(const sim *s, int32_t t)
            !(s->tr->tensor_flags[t] & O_FLAG_CONSTANT);
 }
 
-/* Exact evicted neighbourhood e*(x) (Appendix C.2): evicted tensors reachable
- * from x through evicted parents only (ancestors), together with evicted
- * tensors reachable through evicted children only (descendants).  Returns the
- * sum of their local costs; the set size goes to *count. */
-static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
+/* e_R(x) (Section 4.1): evicted tensors reachable from x through evicted
+ * parents only, i.e. those that rematerializing x would rematerialize.
+ * Returns the sum of their local costs; the set size goes to *count. */
+static int64_t ancestors_cost(sim *s, int32_t x, int64_t *count)
 {
     const graph *g = s->g;
     const oracle_trace *tr = s->tr;
     int64_t sum = 0, cnt = 0;
     s->epoch++;
-    /* ancestors */
     int64_t head = 0, tail = 0;
     s->queue[tail++] = x;
     while (head < tail) {
@@ -285,8 +294,22 @@ static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
             s->queue[tail++] = p;
         }
     }
-    /* descendants */
-    head = tail = 0;
+    *count = cnt;
+    return sum;
+}
+
+/* Exact evicted neighbourhood e*(x) (Appendix C.2): the evicted ancestors
+ * e_R(x), together with the evicted tensors reachable from x through evicted
+ * children only (descendants).  The two sets are disjoint (the graph is
+ * acyclic).  Returns the sum of their local costs; the set size goes to
+ * *count. */
+static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
+{
+    const graph *g = s->g;
+    int64_t cnt = 0;
+    int64_t sum = ancestors_cost(s, x, &cnt);
+    /* descendants (same epoch: a tensor is never on both sides) */
+    int64_t head = 0, tail = 0;
     s->queue[tail++] = x;
     while (head < tail) {
         int32_t u = s->queue[head++];
@@ -398,8 +421,37 @@ static void score(sim *s, int32_t x, uint64_t *N, u128 *D)
         *D = 1;
         break;
     }
-    default:
-        abort();
+    case OH_MSPS:
+        *N = (uint64_t)(c0 + ancestors_cost(s, x, &cnt));
+        *D = (u128)(uint64_t)m;
+        s->r[R_NBR_VISITS] += cnt;
+        s->r[R_ADJ_VISITS] += degree(s, x);
+        break;
+    default: {
+        if (!family(s->heuristic)) abort();
+        /* h'(s, m, c)(x) = c(x) / (m(x) * s(x)), an ablated measure being 1 */
+        const int h = s->heuristic - OH_FAMILY;
+        switch (h >> 2) {
+        case OC_ESTAR:
+            *N = (uint64_t)(c0 + estar_cost(s, x, &cnt));
+            s->r[R_NBR_VISITS] += cnt;
+            s->r[R_ADJ_VISITS] += degree(s, x);
+            break;
+        case OC_EQCLASS:
+            *N = (uint64_t)(c0 + eq_cost(s, x, &cnt));
+            s->r[R_NBR_VISITS] += cnt;
+            s->r[R_ADJ_VISITS] += degree(s, x);
+            break;
+        case OC_LOCAL:
+            *N = (uint64_t)c0;
+            break;
+        default:
+            *N = 1;
+            break;
+        }
+        *D = (u128)(uint64_t)((h & 1) ? m : 1) * (u128)(uint64_t)((h & 2) ? stale : 1);
+        break;
+    }
     }
 }
 
@@ -417,7 +469,7 @@ static void evict(sim *s, int32_t v, int eager)
     s->memory -= s->tr->tensor_size[v];
     if (eager) s->r[R_EAGER]++;
     else s->r[R_EVICTIONS]++;
-    if (s->heuristic == OH_EQ) {
+    if (uses_uf(s->heuristic)) {
         /* add c0(v) to its component, then union with every evicted neighbour */
         int32_t r = uf_find(s, s->node_of[v]);
         s->uf_cost[r] += s->g->c0[v];
@@ -502,7 +554,7 @@ static void execute(sim *s, int32_t o, int32_t t, int remat)
     s->memory += tr->tensor_size[t];
     if (s->memory > s->peak) s->peak = s->memory;
     s->state[t] = ST_RESIDENT;
-    if (s->heuristic == OH_EQ) {
+    if (uses_uf(s->heuristic)) {
         if (remat) {
             /* split approximation: subtract c0 from the old set, move t to a fresh empty set */
             int32_t r = uf_find(s, s->node_of[t]);
@@ -678,8 +730,8 @@ int oracle_run(const oracle_trace *traces, int32_t n_traces, const oracle_spec *
 {
     if (n_traces < 0 || n_sims < 0 || (probe && n_sims != 1)) return -2;
     for (int32_t i = 0; i < n_sims; i++)
-        if (specs[i].trace < 0 || specs[i].trace >= n_traces || specs[i].heuristic < 0 ||
-            specs[i].heuristic > OH_ESTAR)
+        if (specs[i].trace < 0 || specs[i].trace >= n_traces ||
+            !((specs[i].heuristic >= 0 && specs[i].heuristic <= OH_MSPS) || family(specs[i].heuristic)))
             return -2;
     graph *graphs = calloc((size_t)(n_traces > 0 ? n_traces : 1), sizeof(graph));
     if (!graphs) return -1;
@@ -715,10 +767,11 @@ int oracle_run(const oracle_trace *traces, int32_t n_traces, const oracle_spec *
 }
 
 /* Test hook: exact evicted-neighbourhood cost of x under a given state vector
- * (0 uncomputed, 1 resident, 2 evicted).  Returns sum of c0 over e*(x) and
- * writes |e*(x)| to *count and the membership to member_out (optional). */
+ * (0 uncomputed, 1 resident, 2 evicted).  Returns sum of c0 over e*(x), or
+ * over e_R(x) (the evicted ancestors only) when ancestors_only is set, and
+ * writes the set size to *count and the membership to member_out (optional). */
 int64_t oracle_estar(const oracle_trace *tr, const uint8_t *state, int32_t x, int64_t *count,
-                     uint8_t *member_out)
+                     uint8_t *member_out, int32_t ancestors_only)
 {
     graph g;
     if (graph_build(&g, tr)) return -1;
@@ -733,7 +786,7 @@ int64_t oracle_estar(const oracle_trace *tr, const uint8_t *state, int32_t x, in
     int64_t sum = -1;
     if (s.state && s.mark && s.queue) {
         memcpy(s.state, state, (size_t)tr->n_tensors);
-        sum = estar_cost(&s, x, count);
+        sum = ancestors_only ? ancestors_cost(&s, x, count) : estar_cost(&s, x, count);
         if (member_out)
             for (int32_t t = 0; t < tr->n_tensors; t++) member_out[t] = (s.mark[t] == s.epoch);
     }

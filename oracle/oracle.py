@@ -66,7 +66,7 @@ def lib():
                                     C.c_int32, C.c_void_p]
         _lib.oracle_run.restype = C.c_int
         _lib.oracle_result_fields.restype = C.c_int
-        _lib.oracle_estar.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p]
+        _lib.oracle_estar.argtypes = [C.c_void_p, C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_int32]
         _lib.oracle_estar.restype = C.c_int64
         _lib.oracle_rand_key.argtypes = [C.c_uint64, C.c_int64, C.c_int32]
         _lib.oracle_rand_key.restype = C.c_uint64
@@ -144,13 +144,14 @@ def run_probe(trace, spec, stop_after_op: int = -1, stop_at_eviction: int = -1,
                 uf_cost_sum=int(ufsum[0]))
 
 
-def estar(trace, state, x: int):
-    """Exact evicted neighbourhood of x under ``state``: (cost sum, members)."""
+def estar(trace, state, x: int, ancestors_only: bool = False):
+    """Exact evicted neighbourhood e*(x) under ``state`` (or e_R(x), the
+    evicted ancestors only): (cost sum, members)."""
     arr, keep = _pack([trace])
     state = np.ascontiguousarray(state, np.uint8)
     cnt = np.zeros(1, np.int64)
     member = np.zeros(trace.n_tensors, np.uint8)
-    s = lib().oracle_estar(C.addressof(arr), _ptr(state), int(x), _ptr(cnt), _ptr(member))
+    s = lib().oracle_estar(C.addressof(arr), _ptr(state), int(x), _ptr(cnt), _ptr(member), int(ancestors_only))
     del keep
     if s < 0:
         raise RuntimeError("oracle_estar failed")

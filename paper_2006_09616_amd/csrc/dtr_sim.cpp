@@ -38,6 +38,22 @@ int fail(int code, const char *fmt, ...)
     return code;
 }
 
+bool heuristic_known(int32_t h)
+{
+    return (h >= DTR_H_DTR && h <= DTR_H_MSPS) || (h >= DTR_H_FAMILY(0, 0, 0) && h <= DTR_H_FAMILY(3, 1, 1));
+}
+
+// kernel specialisation: 0 union-find neighbourhood, 1 neighbourhood walk
+// (e* or e_R), 2 no neighbourhood
+int32_t heuristic_class(int32_t h)
+{
+    if (h >= DTR_H_FAMILY(0, 0, 0)) {
+        const int32_t c = (h - DTR_H_FAMILY(0, 0, 0)) >> 2;
+        return c == DTR_C_EQCLASS ? 0 : c == DTR_C_ESTAR ? 1 : 2;
+    }
+    return h == DTR_H_EQ ? 0 : (h == DTR_H_DTR || h == DTR_H_ESTAR || h == DTR_H_MSPS) ? 1 : 2;
+}
+
 constexpr int64_t MAX_SIZE = int64_t(1) << 36;
 constexpr int64_t MAX_COST = int64_t(1) << 28;
 constexpr int64_t MAX_TOTAL_COST = int64_t(1) << 50;
@@ -236,11 +252,11 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
         const dtr_sim_spec &s = sims[i];
         if (s.trace < 0 || s.trace >= n_traces)
             return fail(DTR_ETRACE, "sim %d: trace index %d out of range", i, s.trace);
-        if (s.heuristic < DTR_H_DTR || s.heuristic > DTR_H_ESTAR)
+        if (!heuristic_known(s.heuristic))
             return fail(DTR_ETRACE, "sim %d: unknown heuristic %d", i, s.heuristic);
         if (s.budget < 0) return fail(DTR_ETRACE, "sim %d: negative budget", i);
-        need_uf |= s.heuristic == DTR_H_EQ;
-        need_walk |= s.heuristic == DTR_H_DTR || s.heuristic == DTR_H_ESTAR;
+        need_uf |= heuristic_class(s.heuristic) == 0;
+        need_walk |= heuristic_class(s.heuristic) == 1;
         n_max = std::max(n_max, p.traces[s.trace].n);
     }
     // slot layout
@@ -272,10 +288,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
 
     // grouped by heuristic class (one kernel specialisation each), then
     // longest first: ops of the trace, then lower budget first
-    auto cls = [&](int32_t i) {
-        const int32_t hh = sims[i].heuristic;
-        return hh == DTR_H_EQ ? 0 : (hh == DTR_H_DTR || hh == DTR_H_ESTAR) ? 1 : 2;
-    };
+    auto cls = [&](int32_t i) { return heuristic_class(sims[i].heuristic); };
     p.order.resize(n_sims);
     std::iota(p.order.begin(), p.order.end(), 0);
     std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {

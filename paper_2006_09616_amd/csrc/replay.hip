@@ -42,7 +42,12 @@ namespace dtr {
 
 typedef unsigned __int128 u128;
 
-enum { H_DTR = 0, H_EQ = 1, H_LOCAL = 2, H_LRU = 3, H_SIZE = 4, H_RAND = 5, H_ESTAR = 6 };
+enum { H_DTR = 0, H_EQ = 1, H_LOCAL = 2, H_LRU = 3, H_SIZE = 4, H_RAND = 5, H_ESTAR = 6, H_MSPS = 7,
+       H_FAMILY = 16 };
+// cost measure of a score N / (m^use_m * s^use_s): c0 + e* cost, c0 +
+// union-find neighbourhood cost, c0, 1, c0 + e_R cost (evicted ancestors
+// only), or a random draw
+enum { CM_ESTAR = 0, CM_EQCLASS = 1, CM_LOCAL = 2, CM_NONE = 3, CM_ANCESTORS = 4, CM_RAND = 5 };
 enum { ST_OK = 0, ST_OOM = 1, ST_CLOCK = 2, ST_CAPACITY = 3 };
 
 // state word values (low 32 bits of a tensor's state); >= 0: evicted (node)
@@ -187,6 +192,7 @@ struct Sim {
     TraceDev t;
     Slot S;
     int32_t h;
+    int32_t cmode, use_s, use_m;  // the heuristic as (cost measure, staleness used, size used)
     int32_t lane;
     int64_t budget;
     uint64_t seed;
@@ -757,9 +763,9 @@ __device__ __forceinline__ int64_t eq_cost_full(const Sim &s, const NS &N, int32
     return sum;
 }
 
-// e*(x): evicted ancestors through evicted parents, then evicted descendants
-// through evicted children; lane-private stamps make it a set.
-__device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t ep, int64_t &count)
+// e*(x): evicted ancestors through evicted parents, then (if `both`) evicted
+// descendants through evicted children; lane-private stamps make it a set.
+__device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t ep, int64_t &count, bool both)
 {
     const int32_t lane = s.lane;
     GAS uint32_t *st = s.S.stamp;
@@ -782,7 +788,7 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
         }
     }
     head = tail = 0;
-    q[(size_t)tail++ * WAVE + lane] = x;
+    if (both) q[(size_t)tail++ * WAVE + lane] = x;
     while (head < tail) {
         const int32_t u = q[(size_t)head++ * WAVE + lane];
         for (int32_t k = gld(s.t.ch_off + u), e = gld(s.t.ch_off + u + 1); k < e; k++) {
@@ -867,7 +873,6 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
     const int32_t end = s.pool_end;
     const int32_t lane = s.lane;
     const int64_t T = s.T;
-    const int32_t h = s.h;
     const LAS i32x4 *L4 = (const LAS i32x4 *)s.S.lpool_l;
     const GAS i32x4 *G4 = (const GAS i32x4 *)s.S.gpool;
     bool bad = false;
@@ -1012,8 +1017,8 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 N[u] = (uint64_t)(c0[u] + sum[u]);
-                DA[u] = (uint64_t)size[u];
-                DB[u] = (uint64_t)(T - last[u]);
+                DA[u] = s.use_m ? (uint64_t)size[u] : 1;
+                DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
                 s.nbr += ok[u] ? ev[u] : 0;
                 s.adj += ok[u] ? (pd[u] >> 8) : 0;
             }
@@ -1025,9 +1030,9 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 if (!ok[u]) continue;
                 int64_t cnt;
                 const uint32_t ep = s.epoch + 1 + (uint32_t)u;
-                N[u] = (uint64_t)(c0[u] + estar_cost(s, id[u], ep, cnt));
-                DA[u] = (uint64_t)size[u];
-                DB[u] = h == H_DTR ? (uint64_t)(T - last[u]) : 1;
+                N[u] = (uint64_t)(c0[u] + estar_cost(s, id[u], ep, cnt, s.cmode == CM_ESTAR));
+                DA[u] = s.use_m ? (uint64_t)size[u] : 1;
+                DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
                 s.nbr += cnt;
                 s.adj += pd[u] >> 8;
             }
@@ -1035,28 +1040,14 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
         } else {
 #pragma unroll
             for (int u = 0; u < U; u++) {
-                switch (h) {
-                case H_LRU:
-                    N[u] = 1;
-                    DA[u] = 1;
-                    DB[u] = (uint64_t)(T - last[u]);
-                    break;
-                case H_SIZE:
-                    N[u] = 1;
-                    DA[u] = (uint64_t)size[u];
-                    DB[u] = 1;
-                    break;
-                case H_RAND: {
+                if (s.cmode == CM_RAND) {
                     const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
                     N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
                     DA[u] = DB[u] = 1;
-                    break;
-                }
-                default:     // H_LOCAL
-                    N[u] = (uint64_t)c0[u];
-                    DA[u] = (uint64_t)size[u];
-                    DB[u] = (uint64_t)(T - last[u]);
-                    break;
+                } else {
+                    N[u] = s.cmode == CM_LOCAL ? (uint64_t)c0[u] : 1;
+                    DA[u] = s.use_m ? (uint64_t)size[u] : 1;
+                    DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
                 }
             }
         }
@@ -1392,6 +1383,22 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.t = a.traces[sp.trace];
     s.S = S;
     s.h = sp.heuristic;
+    if (s.h >= H_FAMILY) {             // h'(s, m, c) = 16 + 4c + 2s + m
+        s.cmode = (s.h - H_FAMILY) >> 2;
+        s.use_s = (s.h >> 1) & 1;
+        s.use_m = s.h & 1;
+    } else {
+        // the named heuristics as members of the family (Section 4.1, Appendix
+        // A.3), packed 3 bits of cost measure and one bit of each flag per id
+        constexpr uint32_t CM = CM_ESTAR | CM_EQCLASS << 3 | CM_LOCAL << 6 | CM_NONE << 9 | CM_NONE << 12 |
+                                CM_RAND << 15 | CM_ESTAR << 18 | CM_ANCESTORS << 21;
+        constexpr uint32_t US = 0x0F;    // h_DTR, h_eq, h_local, h_LRU use staleness
+        constexpr uint32_t UM = 0xD7;    // all but h_LRU and h_rand use size
+        const int32_t k = s.h & 7;
+        s.cmode = (int32_t)((CM >> (3 * k)) & 7);
+        s.use_s = (int32_t)((US >> k) & 1);
+        s.use_m = (int32_t)((UM >> k) & 1);
+    }
     s.lane = lane;
     s.budget = sp.budget;
     s.seed = sp.seed;

@@ -35,8 +35,20 @@ FLAG_CONSTANT = 1
 FLAG_REQUIRED = 2
 
 # heuristic ids (shared numbering with the C-ABI; the numbers carry no arithmetic)
-H_DTR, H_EQ, H_LOCAL, H_LRU, H_SIZE, H_RAND, H_ESTAR = range(7)
-HEURISTIC_NAMES = ["dtr", "eq", "local", "lru", "size", "rand", "estar"]
+H_DTR, H_EQ, H_LOCAL, H_LRU, H_SIZE, H_RAND, H_ESTAR, H_MSPS = range(8)
+HEURISTIC_NAMES = ["dtr", "eq", "local", "lru", "size", "rand", "estar", "msps"]
+# the ablation family h'(s, m, c): cost measure c, staleness s and size m each
+# used (1) or ablated (0); id = H_FAMILY + 4*c + 2*s + m
+C_ESTAR, C_EQCLASS, C_LOCAL, C_NONE = range(4)
+H_FAMILY = 16
+
+
+def h_family(c: int, s: int, m: int) -> int:
+    assert 0 <= c < 4 and s in (0, 1) and m in (0, 1)
+    return H_FAMILY + 4 * c + 2 * s + m
+
+
+ALL_FAMILY = [h_family(c, s, m) for c in range(4) for s in (0, 1) for m in (0, 1)]
 
 BUDGET_UNLIMITED = (1 << 63) - 1
 

@@ -306,6 +306,20 @@ def evicted_closure(prog, state, x):
     return seen
 
 
+def evicted_ancestors(prog, state, x):
+    """e_R(x): the evicted tensors that rematerializing x would recompute
+    (reachable from x through evicted parents)."""
+    seen = set()
+    stack = [x]
+    while stack:
+        u = stack.pop()
+        for v in prog.parents[u]:
+            if state[v] == EVICTED and v not in seen:
+                seen.add(v)
+                stack.append(v)
+    return seen
+
+
 def _mix64(z):
     z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & MASK64
     z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & MASK64
@@ -315,7 +329,9 @@ def _mix64(z):
 def simulate(trace, budget: int, heuristic: int, seed: int = 0) -> dict:
     """Heuristic-driven run of the same machine (h ids as in the C-ABI)."""
     prog = Program(trace)
-    m = Machine(prog, budget, track_uf=(heuristic == 1))
+    fam = heuristic >= 16
+    fc, fs, fm = ((heuristic - 16) >> 2, ((heuristic - 16) >> 1) & 1, (heuristic - 16) & 1) if fam else (-1, 0, 0)
+    m = Machine(prog, budget, track_uf=(heuristic == 1 or fc == 1))
     c = None if m.oom else m.run()
     while c is not None:
         best, bkey = None, None
@@ -335,6 +351,18 @@ def simulate(trace, budget: int, heuristic: int, seed: int = 0) -> dict:
                 key = Fraction(1, sz)
             elif heuristic == 5:
                 key = _mix64((seed + 0x9E3779B97F4A7C15 * ((m.evict_no << 32) + x)) & MASK64)
+            elif heuristic == 7:
+                key = Fraction(prog.c0[x] + sum(prog.c0[u] for u in evicted_ancestors(prog, m.state, x)), sz)
+            elif fam:
+                if fc == 0:
+                    num = prog.c0[x] + sum(prog.c0[u] for u in evicted_closure(prog, m.state, x))
+                elif fc == 1:
+                    num = prog.c0[x] + m.uf.neighbourhood_cost(x, m)
+                elif fc == 2:
+                    num = prog.c0[x]
+                else:
+                    num = 1
+                key = Fraction(num, (sz if fm else 1) * (s if fs else 1))
             else:
                 raise ValueError(heuristic)
             if bkey is None or key < bkey or (key == bkey and x < best):

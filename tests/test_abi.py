@@ -66,6 +66,8 @@ def test_validation_rejects_malformed_traces():
     t.tensor_flags[2] = 8
     _expect(D.DTR_ETRACE, [t], _spec(), "unknown flag")
     _expect(D.DTR_ETRACE, [good], _spec(h=9), "unknown heuristic 9")
+    for h in (8, 15, 32, -1):
+        _expect(D.DTR_ETRACE, [good], _spec(h=h), f"unknown heuristic {h}")
     _expect(D.DTR_ETRACE, [good], _spec(trace=1), "trace index 1 out of range")
     _expect(D.DTR_ETRACE, [good], _spec(b=-1), "negative budget")
 
@@ -102,3 +104,14 @@ def test_null_arguments():
     h = C.c_void_p()
     assert lib.dtr_sim_create(None, 0, None, 0, None, None, 0, None, C.byref(h)) == D.DTR_EINVAL
     assert "null" in D.dtr_sim_last_error()
+
+
+def test_family_and_msps_ids_accepted():
+    """Validation accepts h_MSPS and every family id (without a GPU the call
+    then stops at the device query, after validation)."""
+    good = W.chain_trace(4)
+    for h in [W.H_MSPS] + W.ALL_FAMILY:
+        try:
+            assert D.dtr_sim_workspace_bytes([good], np.array([(0, h, 4, 0)], dtype=W.SPEC_DTYPE)) > 0
+        except D.DtrError as e:
+            assert e.code == D.DTR_EHIP and "heuristic" not in str(e), (h, str(e))

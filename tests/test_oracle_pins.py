@@ -495,3 +495,103 @@ def test_matches_independent_python_machine(oracle_lib):
                 s = brute.simulate(tr, b, h, seed * 7 + 1)
                 for k, v in s.items():
                     assert int(r[k]) == v, (seed, h, b, k)
+
+
+# -------------------------------------------- h_MSPS and the ablation family --
+
+FAMILY_NAMED = [  # members of h'(s, m, c) that are the named heuristics (Section 4.1, Appendix D)
+    (W.H_DTR, W.h_family(W.C_ESTAR, 1, 1)),
+    (W.H_EQ, W.h_family(W.C_EQCLASS, 1, 1)),
+    (W.H_LOCAL, W.h_family(W.C_LOCAL, 1, 1)),
+    (W.H_LRU, W.h_family(W.C_NONE, 1, 0)),
+    (W.H_SIZE, W.h_family(W.C_NONE, 0, 1)),
+    (W.H_ESTAR, W.h_family(W.C_ESTAR, 0, 1)),
+]
+
+
+def test_ancestors_match_scipy_reachability(oracle_lib):
+    """e_R(x) of h_MSPS: evicted tensors reachable through evicted parents."""
+    O = oracle_lib
+    rng = np.random.default_rng(12)
+    for seed in range(20):
+        tr = W.random_program(seed, n_ops=80, n_const=5, backward=seed % 2 == 0, max_in=4)
+        adj_up = _adj(tr).T.tocsr()
+        prod_cost = np.zeros(tr.n_tensors, np.int64)
+        prod_cost[tr.op_output] = tr.op_cost
+        for _ in range(5):
+            state = rng.choice([O.RESIDENT, O.EVICTED], size=tr.n_tensors, p=[0.4, 0.6]).astype(np.uint8)
+            state[(tr.tensor_flags & W.FLAG_CONSTANT) != 0] = O.RESIDENT
+            ev = state == O.EVICTED
+            for x in rng.choice(np.nonzero(~ev)[0], size=5):
+                expect = _reach(adj_up, ev, x)
+                cost, mem = O.estar(tr, state, int(x), ancestors_only=True)
+                assert set(np.nonzero(mem)[0].tolist()) == expect
+                assert cost == int(prod_cost[list(expect)].sum())
+
+
+def test_msps_and_family_scores_match_scipy(oracle_lib):
+    """Scores at eviction decisions: h_MSPS N = c0 + c0(e_R), D = m; family
+    members N in {c0 + c0(e*), c0, 1}, D = (m or 1) * (staleness or 1)."""
+    O = oracle_lib
+    tr = W.resnet_trace(seed=7, blocks=6)
+    adj = _adj(tr)
+    c0 = np.zeros(tr.n_tensors, np.int64)
+    c0[tr.op_output] = tr.op_cost
+    peak = W.natural_peak(tr)
+    cases = [(W.H_MSPS, "anc", 0, 1), (W.h_family(W.C_ESTAR, 0, 0), "estar", 0, 0),
+             (W.h_family(W.C_ESTAR, 1, 0), "estar", 1, 0), (W.h_family(W.C_LOCAL, 0, 1), "local", 0, 1),
+             (W.h_family(W.C_NONE, 0, 0), "none", 0, 0), (W.h_family(W.C_LOCAL, 1, 0), "local", 1, 0)]
+    for h, cmode, use_s, use_m in cases:
+        checked = 0
+        for k in (0, 6, 19):
+            p = O.run_probe(tr, spec(h, peak // 4), stop_at_eviction=k)
+            if p["result"]["status"] != O.STATUS_STOPPED:
+                continue
+            checked += 1
+            ev = p["state"] == O.EVICTED
+            for x in np.nonzero(p["candidate"])[0]:
+                anc = _reach(adj.T.tocsr(), ev, x)
+                if cmode == "anc":
+                    n = int(c0[x]) + int(c0[list(anc)].sum())
+                elif cmode == "estar":
+                    n = int(c0[x]) + int(c0[list(anc | _reach(adj, ev, x))].sum())
+                elif cmode == "local":
+                    n = int(c0[x])
+                else:
+                    n = 1
+                stale = p["clock"] - int(p["last_access"][x])
+                d = (int(tr.tensor_size[x]) if use_m else 1) * (stale if use_s else 1)
+                assert p["score_n"][x] == n, (h, k, x)
+                assert p["score_d"][x] == d, (h, k, x)
+        assert checked >= 2, h
+
+
+def test_family_reproduces_named_heuristics(oracle_lib):
+    O = oracle_lib
+    for seed in range(12):
+        tr = W.random_program(seed, n_ops=40 + seed, n_const=seed % 3, backward=True, max_size=9, max_cost=6)
+        peak = W.natural_peak(tr)
+        specs = []
+        for named, fam in FAMILY_NAMED:
+            for b in (peak // 3, peak // 2, (3 * peak) // 4):
+                specs.append((0, named, b, seed))
+                specs.append((0, fam, b, seed))
+        arr = np.array(specs, dtype=W.SPEC_DTYPE)
+        res = O.run([tr], arr)
+        for i in range(0, len(arr), 2):
+            for f in O.RESULT_FIELDS:
+                assert int(res[f][i]) == int(res[f][i + 1]), (seed, arr[i], f)
+
+
+def test_msps_and_family_match_independent_python_machine(oracle_lib):
+    O = oracle_lib
+    hs = [W.H_MSPS] + W.ALL_FAMILY
+    for seed in range(40):
+        tr = W.random_program(seed, n_ops=6 + seed % 10, n_const=seed % 3, backward=seed % 2 == 0, max_size=6)
+        peak = W.natural_peak(tr)
+        for h in hs:
+            for b in sorted({max(1, peak // 3), max(1, 2 * peak // 3)}):
+                r = run1(O, tr, h, b, seed)
+                s = brute.simulate(tr, b, h, seed)
+                for k, v in s.items():
+                    assert int(r[k]) == v, (seed, h, b, k)

@@ -72,6 +72,24 @@ def test_random_programs(gpu, oracle_lib, seed0):
     compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "random")
 
 
+def test_msps_and_ablation_family(gpu, oracle_lib):
+    """h_MSPS and every member of h'(s, m, c) on random programs."""
+    traces = []
+    rows = []
+    hs = [W.H_MSPS] + W.ALL_FAMILY
+    for s in range(40):
+        tr = W.random_program(500 + s, n_ops=10 + (s * 13) % 90, n_const=s % 4, backward=s % 2 == 0,
+                              max_in=1 + s % 4, max_size=1 + s % 20, max_cost=1 + s % 7)
+        traces.append(tr)
+        peak = W.natural_peak(tr)
+        for h in hs:
+            for frac in (0.25, 0.5, 0.8):
+                rows.append((len(traces) - 1, h, max(1, int(peak * frac)), s * 37 + h))
+    specs = specs_of(rows)
+    print(f"family batch: {len(traces)} traces, {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "family")
+
+
 def test_empty_and_degenerate(gpu, oracle_lib):
     empty = W.Trace("empty", np.zeros(0, np.int64), np.zeros(0, np.uint8), np.zeros(0, np.int32),
                     np.zeros(0, np.int64), np.zeros(1, np.int64), np.zeros(0, np.int32))
