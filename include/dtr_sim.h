@@ -105,13 +105,29 @@ typedef struct {
     const int32_t *op_inputs;
 } dtr_trace;
 
-/* One simulation: trace index, DTR_H_* heuristic, memory budget (same unit as
- * tensor_size; DTR_BUDGET_UNLIMITED for none), seed (used by DTR_H_RAND). */
+/* ---- deallocation policies: what releasing a tensor after its last reader
+ * does (Section 2; Appendix C.4 and C.5; compared in Appendix D) ------------ */
+#define DTR_POLICY_EAGER  0  /* evict it if resident, unlocked and not a constant   */
+#define DTR_POLICY_IGNORE 1  /* nothing                                             */
+#define DTR_POLICY_BANISH 2  /* if no child is evicted and no operation in progress
+                                holds it: free it for good (constants included) and
+                                pin its resident children (never evictable again);
+                                else retry whenever one of its children is
+                                rematerialized.  Not defined for the union-find
+                                heuristics (DTR_H_EQ, DTR_C_EQCLASS): rejected.
+                                Banishments are counted in n_eager_evictions. */
+
+/* One simulation (32 bytes): trace index, DTR_H_* heuristic, memory budget
+ * (same unit as tensor_size; DTR_BUDGET_UNLIMITED for none), seed (used by
+ * DTR_H_RAND), DTR_POLICY_* deallocation policy, and a reserved word that
+ * must be 0. */
 typedef struct {
     int32_t trace;
     int32_t heuristic;
     int64_t budget;
     uint64_t seed;
+    int32_t policy;
+    int32_t reserved;
 } dtr_sim_spec;
 
 /* Result of one simulation (104 bytes). */

@@ -16,8 +16,13 @@
  *   - eviction (Appendix C.4 "Eviction and banishing"): the evictable pool is
  *     resident storages with no locks (Appendix C.1); the lowest score is
  *     evicted (Appendix C.4 "Runtime state");
- *   - eager eviction on deallocation (Section 2 "Deallocation";
- *     Appendix C.5 "Banishing and eager eviction");
+ *   - deallocation policies (Section 2 "Deallocation"; Appendix C.4
+ *     "Eviction and banishing"; Appendix C.5 "Banishing and eager eviction";
+ *     compared in Appendix D): eager eviction of a released tensor, ignoring
+ *     releases, or banishing -- a released tensor with no evicted child is
+ *     removed for good (constants included) and its children are pinned
+ *     (never evictable again); otherwise it is retried whenever one of its
+ *     children is rematerialized;
  *   - heuristics of Section 4.1 and Appendix C.3: h_DTR with the exact
  *     evicted neighbourhood e* (Appendix C.2), h_DTR^eq with the union-find
  *     relaxation and its split approximation (Appendix C.2), h_DTR^local,
@@ -54,7 +59,8 @@
 #define O_FLAG_CONSTANT 1u
 #define O_FLAG_REQUIRED 2u
 
-enum { ST_UNCOMPUTED = 0, ST_RESIDENT = 1, ST_EVICTED = 2 };
+enum { ST_UNCOMPUTED = 0, ST_RESIDENT = 1, ST_EVICTED = 2, ST_BANISHED = 3 };
+enum { OP_EAGER = 0, OP_IGNORE = 1, OP_BANISH = 2 };   /* deallocation policies */
 enum { OH_DTR = 0, OH_EQ = 1, OH_LOCAL = 2, OH_LRU = 3, OH_SIZE = 4, OH_RAND = 5, OH_ESTAR = 6, OH_MSPS = 7,
        OH_FAMILY = 16 /* h'(s, m, c): 16 + 4c + 2s + m, s and m 1 = used */ };
 enum { OC_ESTAR = 0, OC_EQCLASS = 1, OC_LOCAL = 2, OC_NONE = 3 };
@@ -80,7 +86,7 @@ typedef struct {
     const int32_t *op_inputs;
 } oracle_trace;
 
-typedef struct { int32_t trace, heuristic; int64_t budget; uint64_t seed; } oracle_spec;
+typedef struct { int32_t trace, heuristic; int64_t budget; uint64_t seed; int32_t policy, reserved; } oracle_spec;
 
 /* result fields (int64 each) */
 enum {
@@ -129,8 +135,9 @@ static void graph_free(graph *g)
 /* parents(t) = inputs of t's parent operation (Appendix C.2 "Data dependencies");
  * children(t) = tensors whose parent operation reads t (the dependents, deps^T);
  * a tensor whose last external reference goes away after op o is released
- * after o (reference counting, Appendix A.2) unless it is a constant or a
- * required output. */
+ * after o (reference counting, Appendix A.2) unless it is a required output;
+ * a constant is released after its last reader (one that nothing reads is
+ * never released). */
 static int graph_build(graph *g, const oracle_trace *tr)
 {
     int32_t n = tr->n_tensors, F = tr->n_ops;
@@ -169,7 +176,7 @@ static int graph_build(graph *g, const oracle_trace *tr)
         }
     /* release lists: ascending id within an op */
     for (int32_t t = 0; t < n; t++) {
-        if (tr->tensor_flags[t] & (O_FLAG_CONSTANT | O_FLAG_REQUIRED)) continue;
+        if (tr->tensor_flags[t] & O_FLAG_REQUIRED) continue;
         if (last[t] >= 0) g->rel_off[last[t] + 1]++;
     }
     for (int32_t o = 0; o < F; o++) g->rel_off[o + 1] += g->rel_off[o];
@@ -177,7 +184,7 @@ static int graph_build(graph *g, const oracle_trace *tr)
     if (!rfill) { free(last); free(fill); graph_free(g); return -1; }
     for (int32_t o = 0; o < F; o++) rfill[o] = g->rel_off[o];
     for (int32_t t = 0; t < n; t++) {   /* ascending t gives ascending ids per list */
-        if (tr->tensor_flags[t] & (O_FLAG_CONSTANT | O_FLAG_REQUIRED)) continue;
+        if (tr->tensor_flags[t] & O_FLAG_REQUIRED) continue;
         if (last[t] >= 0) g->rel[rfill[last[t]]++] = t;
     }
     free(rfill); free(last); free(fill);
@@ -190,11 +197,14 @@ typedef struct {
     const graph *g;
     const oracle_trace *tr;
     int heuristic;
+    int policy;
     int64_t budget;
     uint64_t seed;
 
     uint8_t *state;
     int32_t *locks;
+    uint8_t *pinned;              /* children of banished tensors: never evictable */
+    uint8_t *pending;             /* released, banishing deferred */
     int64_t *last_access;
     int64_t clock, memory, peak;
     int64_t r[R_NFIELDS];
@@ -261,13 +271,50 @@ static int32_t uf_union(sim *s, int32_t a, int32_t b)
     return a;
 }
 
-static void lock(sim *s, int32_t t) { s->locks[t]++; }
+static void evict(sim *s, int32_t v, int eager);
+
+/* a banished tensor is never read again (its children are pinned), so a lock
+ * on one means the policy's invariant broke */
+static void lock(sim *s, int32_t t)
+{
+    if (s->state[t] == ST_BANISHED) abort();
+    s->locks[t]++;
+}
 static void unlock(sim *s, int32_t t) { s->locks[t]--; }
 
 static int is_evictable(const sim *s, int32_t t)
 {
-    return s->state[t] == ST_RESIDENT && s->locks[t] == 0 &&
+    return s->state[t] == ST_RESIDENT && s->locks[t] == 0 && !s->pinned[t] &&
            !(s->tr->tensor_flags[t] & O_FLAG_CONSTANT);
+}
+
+/* Banish t if none of its children is evicted and no operation in progress
+ * holds it (Appendix C.4): its memory is reclaimed if resident, it leaves the
+ * graph for good, and every resident child is pinned.  Otherwise t stays
+ * pending and is retried when one of its children is rematerialized. */
+static void try_banish(sim *s, int32_t t)
+{
+    const graph *g = s->g;
+    int blocked = s->locks[t] > 0;
+    for (int64_t e = g->ch_off[t]; e < g->ch_off[t + 1] && !blocked; e++)
+        if (s->state[g->ch[e]] == ST_EVICTED) blocked = 1;
+    if (blocked) { s->pending[t] = 1; return; }
+    s->pending[t] = 0;
+    if (s->state[t] == ST_RESIDENT) s->memory -= s->tr->tensor_size[t];
+    s->state[t] = ST_BANISHED;
+    s->r[R_EAGER]++;              /* deallocation-driven removals */
+    for (int64_t e = g->ch_off[t]; e < g->ch_off[t + 1]; e++)
+        if (s->state[g->ch[e]] == ST_RESIDENT) s->pinned[g->ch[e]] = 1;
+}
+
+/* deallocation of t after its last reader (Section 2, Appendix C.5) */
+static void release(sim *s, int32_t t)
+{
+    if (s->policy == OP_EAGER) {
+        if (is_evictable(s, t)) evict(s, t, 1);
+    } else if (s->policy == OP_BANISH) {
+        try_banish(s, t);
+    }
 }
 
 /* e_R(x) (Section 4.1): evicted tensors reachable from x through evicted
@@ -590,6 +637,10 @@ static void remat(sim *s, int32_t u)
     if (s->stopped) return;
     for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
         unlock(s, tr->op_inputs[e]);
+    /* u is a dependent of each of its parents: retry their deferred banishing */
+    if (s->policy == OP_BANISH)
+        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
+            if (s->pending[tr->op_inputs[e]]) try_banish(s, tr->op_inputs[e]);
 }
 
 static void sim_run(sim *s)
@@ -626,10 +677,7 @@ static void sim_run(sim *s)
         if (s->stopped) goto done;
         for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++)
             unlock(s, tr->op_inputs[e]);
-        for (int64_t e = g->rel_off[o]; e < g->rel_off[o + 1]; e++) {
-            int32_t r = g->rel[e];
-            if (is_evictable(s, r)) evict(s, r, 1);
-        }
+        for (int64_t e = g->rel_off[o]; e < g->rel_off[o + 1]; e++) release(s, g->rel[e]);
         if (s->probe && s->probe->stop_after_op == o) {
             dump_state(s);
             s->stopped = OS_STOPPED;
@@ -663,24 +711,29 @@ static int run_one(const oracle_trace *tr, const graph *g, const oracle_spec *sp
     s.g = g;
     s.tr = tr;
     s.heuristic = sp->heuristic;
+    s.policy = sp->policy;
     s.budget = sp->budget;
     s.seed = sp->seed;
     s.probe = probe;
     size_t nn = (size_t)(n > 0 ? n : 1);
     s.state = calloc(nn, 1);
+    s.pinned = calloc(nn, 1);
+    s.pending = calloc(nn, 1);
     s.locks = calloc(nn, sizeof(int32_t));
     s.last_access = calloc(nn, sizeof(int64_t));
     s.node_of = malloc(sizeof(int32_t) * nn);
     s.queue = malloc(sizeof(int32_t) * nn);
     s.mark = calloc(nn, sizeof(int64_t));
     int rc = 0;
-    if (!s.state || !s.locks || !s.last_access || !s.node_of || !s.queue || !s.mark) rc = -1;
+    if (!s.state || !s.pinned || !s.pending || !s.locks || !s.last_access || !s.node_of || !s.queue || !s.mark)
+        rc = -1;
     else {
         for (int32_t t = 0; t < n; t++) s.node_of[t] = -1;
         sim_run(&s);
         for (int i = 0; i < R_NFIELDS; i++) result[i] = s.r[i];
     }
-    free(s.state); free(s.locks); free(s.last_access); free(s.node_of); free(s.queue); free(s.mark);
+    free(s.state); free(s.pinned); free(s.pending); free(s.locks); free(s.last_access); free(s.node_of);
+    free(s.queue); free(s.mark);
     free(s.uf_parent); free(s.uf_cost); free(s.uf_mark);
     return rc;
 }
@@ -731,7 +784,9 @@ int oracle_run(const oracle_trace *traces, int32_t n_traces, const oracle_spec *
     if (n_traces < 0 || n_sims < 0 || (probe && n_sims != 1)) return -2;
     for (int32_t i = 0; i < n_sims; i++)
         if (specs[i].trace < 0 || specs[i].trace >= n_traces ||
-            !((specs[i].heuristic >= 0 && specs[i].heuristic <= OH_MSPS) || family(specs[i].heuristic)))
+            !((specs[i].heuristic >= 0 && specs[i].heuristic <= OH_MSPS) || family(specs[i].heuristic)) ||
+            specs[i].policy < OP_EAGER || specs[i].policy > OP_BANISH ||
+            (specs[i].policy == OP_BANISH && uses_uf(specs[i].heuristic)))
             return -2;
     graph *graphs = calloc((size_t)(n_traces > 0 ? n_traces : 1), sizeof(graph));
     if (!graphs) return -1;

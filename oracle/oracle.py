@@ -24,7 +24,7 @@ RESULT_FIELDS = ["total_cost", "base_cost", "remat_cost", "peak_memory", "final_
 RESULT_DTYPE = np.dtype([(f, "<i8") for f in RESULT_FIELDS])
 
 STATUS_OK, STATUS_OOM, STATUS_CLOCK_OVERFLOW, STATUS_STOPPED = 0, 1, 2, 100
-UNCOMPUTED, RESIDENT, EVICTED = 0, 1, 2
+UNCOMPUTED, RESIDENT, EVICTED, BANISHED = 0, 1, 2, 3
 
 
 def build(force: bool = False) -> str:

@@ -170,13 +170,13 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
     // release lists, ascending id
     d.rel_off.assign(F + 1, 0);
     for (int32_t t = 0; t < n; t++)
-        if (!(d.flags[t] & (DTR_FLAG_CONSTANT | DTR_FLAG_REQUIRED)) && last[t] >= 0) d.rel_off[last[t] + 1]++;
+        if (!(d.flags[t] & DTR_FLAG_REQUIRED) && last[t] >= 0) d.rel_off[last[t] + 1]++;
     for (int32_t o = 0; o < F; o++) d.rel_off[o + 1] += d.rel_off[o];
     d.rel.resize(d.rel_off[F]);
     {
         std::vector<int32_t> fill(d.rel_off.begin(), d.rel_off.end() - 1);
         for (int32_t t = 0; t < n; t++)
-            if (!(d.flags[t] & (DTR_FLAG_CONSTANT | DTR_FLAG_REQUIRED)) && last[t] >= 0) d.rel[fill[last[t]]++] = t;
+            if (!(d.flags[t] & DTR_FLAG_REQUIRED) && last[t] >= 0) d.rel[fill[last[t]]++] = t;
     }
     d.rec.resize(n);
     for (int32_t t = 0; t < n; t++) {
@@ -246,7 +246,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
         int rc = validate_and_derive(traces[i], i, p.traces[i]);
         if (rc) return rc;
     }
-    bool need_uf = false, need_walk = false;
+    bool need_uf = false, need_walk = false, need_banish = false;
     int32_t n_max = 1;
     for (int32_t i = 0; i < n_sims; i++) {
         const dtr_sim_spec &s = sims[i];
@@ -255,6 +255,12 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
         if (!heuristic_known(s.heuristic))
             return fail(DTR_ETRACE, "sim %d: unknown heuristic %d", i, s.heuristic);
         if (s.budget < 0) return fail(DTR_ETRACE, "sim %d: negative budget", i);
+        if (s.policy < DTR_POLICY_EAGER || s.policy > DTR_POLICY_BANISH)
+            return fail(DTR_ETRACE, "sim %d: unknown deallocation policy %d", i, s.policy);
+        if (s.policy == DTR_POLICY_BANISH && heuristic_class(s.heuristic) == 0)
+            return fail(DTR_ETRACE, "sim %d: banishing is not defined for union-find heuristics", i);
+        if (s.reserved != 0) return fail(DTR_ETRACE, "sim %d: reserved word must be 0", i);
+        need_banish |= s.policy == DTR_POLICY_BANISH;
         need_uf |= heuristic_class(s.heuristic) == 0;
         need_walk |= heuristic_class(s.heuristic) == 1;
         n_max = std::max(n_max, p.traces[s.trace].n);
@@ -275,6 +281,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     take(L.stack, sizeof(dtr::StackFrame) * (size_t)(n + 1));
     take(L.stamp, need_walk ? 4 * n * dtr::WAVE : 0);
     take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);
+    take(L.pending, need_banish ? n : 0);
     L.bytes = (int64_t)o;
 
     int32_t cus = 0;
@@ -413,7 +420,7 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec
     }
     std::memcpy(H + p.desc_off, descs.data(), sizeof(dtr::TraceDev) * n_traces);
     for (int32_t i = 0; i < n_sims; i++) {
-        dtr::SpecDev s{sims[i].trace, sims[i].heuristic, sims[i].budget, sims[i].seed};
+        dtr::SpecDev s{sims[i].trace, sims[i].heuristic, sims[i].budget, sims[i].seed, sims[i].policy, 0};
         std::memcpy(H + p.spec_off + i * sizeof(dtr::SpecDev), &s, sizeof(s));
     }
     if (n_sims) std::memcpy(H + p.order_off, p.order.data(), sizeof(int32_t) * n_sims);

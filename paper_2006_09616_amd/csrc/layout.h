@@ -61,7 +61,9 @@ struct SpecDev {
     int32_t trace, heuristic;
     int64_t budget;
     uint64_t seed;
+    int32_t policy, reserved;
 };
+static_assert(sizeof(SpecDev) == 32, "spec layout");
 
 struct ResultDev {
     int64_t total_cost, base_cost, remat_cost, peak_memory, final_memory;
@@ -84,6 +86,7 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 //   nodes     union-find nodes {running cost, parent, size}
 //   stack     rematerialization frames (tensor, next input, the tensor's record)
 //   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
+//   pending   one byte per tensor: released, banishing deferred (banishing policy)
 constexpr int NB_CACHE = 8;
 // union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
 // the rest in the slot's global node array
@@ -99,6 +102,7 @@ struct SlotLayout {
     int64_t nodes, uf_remap;
     int64_t stack;
     int64_t stamp, queue;
+    int64_t pending;
     int64_t pcap, ucap, n_max;
 };
 

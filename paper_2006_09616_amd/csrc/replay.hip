@@ -51,9 +51,12 @@ enum { CM_ESTAR = 0, CM_EQCLASS = 1, CM_LOCAL = 2, CM_NONE = 3, CM_ANCESTORS = 4
 enum { ST_OK = 0, ST_OOM = 1, ST_CLOCK = 2, ST_CAPACITY = 3 };
 
 // state word values (low 32 bits of a tensor's state); >= 0: evicted (node)
+constexpr int32_t S_BANISHED = -5;    // freed for good (banishing policy)
+constexpr int32_t S_PINNED = -4;      // resident, never evictable: a banished tensor's child
 constexpr int32_t S_CONST = -3;
 constexpr int32_t S_UNCOMPUTED = -2;
 constexpr int32_t S_RESIDENT = -1;
+enum { POLICY_EAGER = 0, POLICY_IGNORE = 1, POLICY_BANISH = 2 };
 constexpr uint32_t MAX_LOCKS = 255;
 constexpr uint8_t FLAG_CONST = 1;
 constexpr int K = NB_CACHE;
@@ -159,6 +162,7 @@ struct Slot {
     GAS i32x4 *stack;             // StackFrame records, three quads each
     GAS uint32_t *stamp;
     GAS int32_t *queue;
+    GAS uint8_t *pending;         // released, banishing deferred (banishing policy)
     int32_t pcap, ucap, n_max;
     __device__ __forceinline__ PoolSlot &pool(int32_t i) const
     {
@@ -181,6 +185,7 @@ __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
     S.stack = (GAS i32x4 *)(b + a.L.stack);
     S.stamp = (GAS uint32_t *)(b + a.L.stamp);
     S.queue = (GAS int32_t *)(b + a.L.queue);
+    S.pending = (GAS uint8_t *)(b + a.L.pending);
     S.pcap = (int32_t)a.L.pcap;
     S.ucap = (int32_t)a.L.ucap;
     S.n_max = (int32_t)a.L.n_max;
@@ -193,6 +198,7 @@ struct Sim {
     Slot S;
     int32_t h;
     int32_t cmode, use_s, use_m;  // the heuristic as (cost measure, staleness used, size used)
+    int32_t policy;               // what a release does
     int32_t lane;
     int64_t budget;
     uint64_t seed;
@@ -1244,6 +1250,72 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
     return s.status == ST_OK;
 }
 
+// Banish t (Appendix C.4) unless one of its children is evicted or an
+// operation in progress holds it, in which case it stays pending: its memory
+// is reclaimed if resident (constants included), it is gone for good, and its
+// resident children are pinned (never evictable).  Counted with the eager
+// evictions.
+__device__ __forceinline__ void try_banish(Sim &s, int32_t t)
+{
+    const uint64_t w = (uint64_t)uni64((int64_t)s.S.tst[t]);
+    const int32_t b = uni(cld(s.t.ch_off + t)), e = uni(cld(s.t.ch_off + t + 1));
+    bool blocked = ts_locks(w) > 0;
+    for (int32_t k0 = b; k0 < e && !blocked; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        const bool ev = k < e && ts_sw(s.S.tst[gld(s.t.ch + k)]) >= 0;
+        blocked = __ballot(ev) != 0;
+    }
+    if (blocked) {
+        if (s.lane == 0) s.S.pending[t] = 1;
+        return;
+    }
+    if (s.lane == 0) s.S.pending[t] = 0;
+    const int32_t sw = ts_sw(w);
+    if (sw == S_RESIDENT || sw == S_PINNED || sw == S_CONST) s.mem -= rec_u(s, t).size;
+    if (ts_in_pool(w)) {
+        if (s.lane == 0) s.S.pool((int32_t)ts_pos(w)).id = -1;
+        s.pool_live--;
+    }
+    s.S.tst[t] = ts_make(S_BANISHED, 0, 0);
+    s.eager++;
+    for (int32_t k0 = b; k0 < e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        bool killed = false;
+        if (k < e) {
+            const int32_t c = gld(s.t.ch + k);
+            const uint64_t wc = s.S.tst[c];
+            if (ts_sw(wc) == S_RESIDENT) {
+                killed = ts_in_pool(wc);
+                if (killed) s.S.pool((int32_t)ts_pos(wc)).id = -1;
+                s.S.tst[c] = ts_make(S_PINNED, ts_pos(wc), ts_locks(wc));
+            }
+        }
+        s.pool_live -= __popcll(__ballot(killed));
+    }
+}
+
+// after a rematerialization by the operation with inputs [b, e): the new
+// tensor is a child of each input, so pending inputs retry banishing (in
+// listed order)
+__device__ __forceinline__ void retry_banish(Sim &s, int32_t b, int32_t e)
+{
+    for (int32_t k0 = b; k0 < e; k0 += WAVE) {
+        const int32_t k = k0 + s.lane;
+        int32_t p = -1;
+        bool pend = false;
+        if (k < e) {
+            p = gld(s.t.in + k);
+            pend = s.S.pending[p] != 0;
+        }
+        uint64_t m = __ballot(pend);
+        while (m) {
+            const int32_t j = __ffsll((long long)m) - 1;
+            m &= m - 1;
+            try_banish(s, __builtin_amdgcn_readlane(p, j));
+        }
+    }
+}
+
 __device__ __forceinline__ void stack_push(const Sim &s, int32_t sp, int32_t t, int32_t next, const TRec &r)
 {
     GAS i32x4 *F = s.S.stack + 3 * (size_t)sp;
@@ -1329,6 +1401,7 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         PROF_T0(tu);
         unlock_inputs<HC>(s, b, e, start, f);
         PROF_ADD(PH_UNLOCK, tu);
+        if (HC != HC_EQ && remat && s.policy == POLICY_BANISH) retry_banish(s, b, e);
         if (!remat) {
             // a trace operation's output is unlocked: it joins the pool at once
             PROF_T0(to);
@@ -1350,11 +1423,17 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
     }
 }
 
-// eager eviction of the tensors released after op o (ascending id)
+// what happens to the tensors released after op o (ascending id): eager
+// eviction, nothing, or banishing
 template <int HC>
 __device__ __forceinline__ bool release(Sim &s, int32_t o)
 {
     const int32_t b = uni(cld(s.t.rel_off + o)), e = uni(cld(s.t.rel_off + o + 1));
+    if (s.policy == POLICY_IGNORE) return true;
+    if (HC != HC_EQ && s.policy == POLICY_BANISH) {    // never a union-find heuristic
+        for (int32_t k = b; k < e; k++) try_banish(s, uni(cld(s.t.rel + k)));
+        return true;
+    }
     for (int32_t k0 = b; k0 < e; k0 += WAVE) {
         const int32_t k = k0 + s.lane;
         int32_t r = -1, pos = 0;
@@ -1383,6 +1462,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.t = a.traces[sp.trace];
     s.S = S;
     s.h = sp.heuristic;
+    s.policy = sp.policy;
     if (s.h >= H_FAMILY) {             // h'(s, m, c) = 16 + 4c + 2s + m
         s.cmode = (s.h - H_FAMILY) >> 2;
         s.use_s = (s.h >> 1) & 1;
@@ -1422,6 +1502,8 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     const int32_t n = s.t.n;
     for (int32_t x = lane; x < n; x += WAVE)
         s.S.tst[x] = ts_make((gld(s.t.flags + x) & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
+    if (HC != HC_EQ && s.policy == POLICY_BANISH)
+        for (int32_t x = lane; x < n; x += WAVE) s.S.pending[x] = 0;
     if (HC == HC_WALK) clear_stamps(s);
     if (HC == HC_EQ && lane == 0) {
         UfNode z;

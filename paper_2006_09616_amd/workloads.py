@@ -52,8 +52,20 @@ ALL_FAMILY = [h_family(c, s, m) for c in range(4) for s in (0, 1) for m in (0, 1
 
 BUDGET_UNLIMITED = (1 << 63) - 1
 
+# deallocation policies (what a release does): evict eagerly, nothing, banish
+POLICY_EAGER, POLICY_IGNORE, POLICY_BANISH = range(3)
+
 SPEC_DTYPE = np.dtype([("trace", "<i4"), ("heuristic", "<i4"),
-                       ("budget", "<i8"), ("seed", "<u8")])
+                       ("budget", "<i8"), ("seed", "<u8"),
+                       ("policy", "<i4"), ("reserved", "<i4")])
+
+
+def make_specs(rows) -> np.ndarray:
+    """Simulation specs from rows (trace, heuristic, budget, seed[, policy])."""
+    a = np.zeros(len(rows), dtype=SPEC_DTYPE)
+    for i, r in enumerate(rows):
+        a[i] = (r[0], r[1], r[2], r[3], r[4] if len(r) > 4 else POLICY_EAGER, 0)
+    return a
 
 
 @dataclass
@@ -228,10 +240,7 @@ def splitmix64(x: int) -> int:
 
 
 def _specs(rows):
-    a = np.zeros(len(rows), dtype=SPEC_DTYPE)
-    for i, (t, h, b, s) in enumerate(rows):
-        a[i] = (t, h, b, s)
-    return a
+    return make_specs(rows)
 
 
 # ----------------------------------------------------------------------------

@@ -4,8 +4,9 @@ Python rendering of the same state machine.
 The machine follows the operator call of Section 2 and Appendix C.4: lock the
 inputs, rematerialize evicted inputs (recursively, in listed order), allocate
 the output (evicting while memory is insufficient), run the operator, unlock,
-then release tensors whose last reader has run (eager eviction, Appendix C.5),
-and at the end rematerialize and lock the required outputs (Appendix C.6).
+then release tensors whose last reader has run (eager eviction, ignoring the
+release, or banishing, Appendix C.4/C.5), and at the end rematerialize and
+lock the required outputs (Appendix C.6).
 It is written as an explicit-stack machine so that a state at an eviction
 decision is a hashable value; the only nondeterminism is *which* evictable
 tensor is evicted.
@@ -25,7 +26,8 @@ from __future__ import annotations
 import sys
 from fractions import Fraction
 
-UNCOMPUTED, RESIDENT, EVICTED = 0, 1, 2
+UNCOMPUTED, RESIDENT, EVICTED, BANISHED = 0, 1, 2, 3
+EAGER, IGNORE, BANISH = 0, 1, 2
 FLAG_CONSTANT, FLAG_REQUIRED = 1, 2
 CLOCK_LIMIT = 1 << 40
 MASK64 = (1 << 64) - 1
@@ -58,7 +60,7 @@ class Program:
                 last[u] = max(last[u], o)
         self.release = [[] for _ in range(self.F)]
         for t in range(self.n):
-            if self.flags[t] & (FLAG_CONSTANT | FLAG_REQUIRED) or last[t] < 0:
+            if self.flags[t] & FLAG_REQUIRED or last[t] < 0:
                 continue
             self.release[last[t]].append(t)
         self.required = [t for t in range(self.n) if self.flags[t] & FLAG_REQUIRED]
@@ -70,11 +72,14 @@ class Machine:
 
     __slots__ = ("p", "budget", "frames", "state", "locks", "mem", "peak", "cost", "remat_cost",
                  "clock", "last", "done", "oom", "overflow", "n_evict", "n_eager", "n_remat",
-                 "n_exec", "n_scores", "uf", "evict_no")
+                 "n_exec", "n_scores", "uf", "evict_no", "policy", "pinned", "pending")
 
-    def __init__(self, prog: Program, budget: int, track_uf: bool = False):
+    def __init__(self, prog: Program, budget: int, track_uf: bool = False, policy: int = EAGER):
         self.p = prog
         self.budget = budget
+        self.policy = policy
+        self.pinned = [False] * prog.n
+        self.pending = [False] * prog.n
         self.state = [UNCOMPUTED] * prog.n
         self.locks = [0] * prog.n
         self.last = [0] * prog.n
@@ -105,12 +110,13 @@ class Machine:
         return m
 
     def key(self):
-        return (tuple(tuple(f) for f in self.frames), tuple(self.state), tuple(self.locks))
+        return (tuple(tuple(f) for f in self.frames), tuple(self.state), tuple(self.locks),
+                tuple(self.pinned), tuple(self.pending))
 
     def candidates(self):
         p = self.p
         return [x for x in range(p.n) if self.state[x] == RESIDENT and self.locks[x] == 0
-                and not p.flags[x] & FLAG_CONSTANT]
+                and not p.flags[x] & FLAG_CONSTANT and not self.pinned[x]]
 
     def evict(self, x, eager=False):
         self.state[x] = EVICTED
@@ -122,6 +128,22 @@ class Machine:
             self.evict_no += 1
         if self.uf is not None:
             self.uf.on_evict(x, self)
+
+    def banish(self, t):
+        """Permanent removal once no child is evicted and nothing holds t;
+        resident children become pinned.  Else t waits for a child's remat."""
+        p = self.p
+        if self.locks[t] > 0 or any(self.state[c] == EVICTED for c in p.children[t]):
+            self.pending[t] = True
+            return
+        self.pending[t] = False
+        if self.state[t] == RESIDENT:
+            self.mem -= p.size[t]
+        self.state[t] = BANISHED
+        self.n_eager += 1
+        for c in p.children[t]:
+            if self.state[c] == RESIDENT:
+                self.pinned[c] = True
 
     def _frame_op(self, f):
         return f[1] if f[0] == "op" else self.p.producer[f[1]]
@@ -150,6 +172,7 @@ class Machine:
             ins = p.ins[o]
             if f[2] == -1:
                 for u in ins:
+                    assert self.state[u] != BANISHED
                     self.locks[u] += 1
                 f[2] = 0
             if f[2] < len(ins):
@@ -186,10 +209,18 @@ class Machine:
             for u in ins:
                 self.locks[u] -= 1
             self.frames.pop()
+            if f[0] == "remat" and self.policy == BANISH:
+                for u in ins:
+                    if self.pending[u]:
+                        self.banish(u)
             if f[0] == "op":
                 for r in p.release[o]:
-                    if self.state[r] == RESIDENT and self.locks[r] == 0 and not p.flags[r] & FLAG_CONSTANT:
-                        self.evict(r, eager=True)
+                    if self.policy == EAGER:
+                        if self.state[r] == RESIDENT and self.locks[r] == 0 and not p.flags[r] & FLAG_CONSTANT \
+                                and not self.pinned[r]:
+                            self.evict(r, eager=True)
+                    elif self.policy == BANISH:
+                        self.banish(r)
                 self.frames.append(["op", o + 1, -1] if o + 1 < p.F else ["out", 0])
         return None
 
@@ -326,12 +357,12 @@ def _mix64(z):
     return z ^ (z >> 31)
 
 
-def simulate(trace, budget: int, heuristic: int, seed: int = 0) -> dict:
-    """Heuristic-driven run of the same machine (h ids as in the C-ABI)."""
+def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EAGER) -> dict:
+    """Heuristic-driven run of the same machine (h ids and policies as in the C-ABI)."""
     prog = Program(trace)
     fam = heuristic >= 16
     fc, fs, fm = ((heuristic - 16) >> 2, ((heuristic - 16) >> 1) & 1, (heuristic - 16) & 1) if fam else (-1, 0, 0)
-    m = Machine(prog, budget, track_uf=(heuristic == 1 or fc == 1))
+    m = Machine(prog, budget, track_uf=(heuristic == 1 or fc == 1), policy=policy)
     c = None if m.oom else m.run()
     while c is not None:
         best, bkey = None, None

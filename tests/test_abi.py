@@ -18,16 +18,23 @@ def test_library_exports_every_declared_function():
         assert hasattr(lib, n), n
 
 
+def test_spec_layout_matches_header():
+    """Field offsets of the Python spec record against the C struct in the
+    header (parsed, not restated)."""
+    text = open(D.HEADER).read()
+    body = text[text.index("typedef struct {", text.index("DTR_POLICY_BANISH")):text.index("} dtr_sim_spec;")]
+    fields = [l.split()[-1].rstrip(";") for l in body.splitlines() if l.strip().endswith(";")]
+    assert fields == list(W.SPEC_DTYPE.names)
+
+
 def test_struct_sizes_match_header():
     assert C.sizeof(D._Trace) == 8 + 6 * 8
-    assert W.SPEC_DTYPE.itemsize == 24
+    assert W.SPEC_DTYPE.itemsize == 32
     assert D.RESULT_DTYPE.itemsize == 104
 
 
 def _spec(h=W.H_LRU, b=10, trace=0):
-    s = np.zeros(1, W.SPEC_DTYPE)
-    s[0] = (trace, h, b, 0)
-    return s
+    return W.make_specs([(trace, h, b, 0)])
 
 
 def _expect(code, traces, specs, match):
@@ -68,6 +75,14 @@ def test_validation_rejects_malformed_traces():
     _expect(D.DTR_ETRACE, [good], _spec(h=9), "unknown heuristic 9")
     for h in (8, 15, 32, -1):
         _expect(D.DTR_ETRACE, [good], _spec(h=h), f"unknown heuristic {h}")
+    _expect(D.DTR_ETRACE, [good], W.make_specs([(0, W.H_LRU, 4, 0, 3)]), "unknown deallocation policy 3")
+    _expect(D.DTR_ETRACE, [good], W.make_specs([(0, W.H_EQ, 4, 0, W.POLICY_BANISH)]),
+            "banishing is not defined for union-find heuristics")
+    _expect(D.DTR_ETRACE, [good], W.make_specs([(0, W.h_family(W.C_EQCLASS, 0, 1), 4, 0, W.POLICY_BANISH)]),
+            "banishing is not defined for union-find heuristics")
+    bad = W.make_specs([(0, W.H_LRU, 4, 0)])
+    bad["reserved"] = 1
+    _expect(D.DTR_ETRACE, [good], bad, "reserved word must be 0")
     _expect(D.DTR_ETRACE, [good], _spec(trace=1), "trace index 1 out of range")
     _expect(D.DTR_ETRACE, [good], _spec(b=-1), "negative budget")
 
@@ -112,6 +127,6 @@ def test_family_and_msps_ids_accepted():
     good = W.chain_trace(4)
     for h in [W.H_MSPS] + W.ALL_FAMILY:
         try:
-            assert D.dtr_sim_workspace_bytes([good], np.array([(0, h, 4, 0)], dtype=W.SPEC_DTYPE)) > 0
+            assert D.dtr_sim_workspace_bytes([good], W.make_specs([(0, h, 4, 0)])) > 0
         except D.DtrError as e:
             assert e.code == D.DTR_EHIP and "heuristic" not in str(e), (h, str(e))

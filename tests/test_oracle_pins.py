@@ -21,10 +21,8 @@ from paper_2006_09616_amd import workloads as W
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def spec(h, b, seed=0, trace=0):
-    s = np.zeros(1, W.SPEC_DTYPE)
-    s[0] = (trace, h, b, seed)
-    return s[0]
+def spec(h, b, seed=0, trace=0, policy=W.POLICY_EAGER):
+    return W.make_specs([(trace, h, b, seed, policy)])[0]
 
 
 def run1(O, tr, h, b, seed=0):
@@ -576,7 +574,7 @@ def test_family_reproduces_named_heuristics(oracle_lib):
             for b in (peak // 3, peak // 2, (3 * peak) // 4):
                 specs.append((0, named, b, seed))
                 specs.append((0, fam, b, seed))
-        arr = np.array(specs, dtype=W.SPEC_DTYPE)
+        arr = W.make_specs(specs)
         res = O.run([tr], arr)
         for i in range(0, len(arr), 2):
             for f in O.RESULT_FIELDS:
@@ -595,3 +593,132 @@ def test_msps_and_family_match_independent_python_machine(oracle_lib):
                 s = brute.simulate(tr, b, h, seed)
                 for k, v in s.items():
                     assert int(r[k]) == v, (seed, h, b, k)
+
+
+# ------------------------------------------------ deallocation policies (f1) --
+
+UF_HEURISTICS = {W.H_EQ, W.h_family(W.C_EQCLASS, 0, 0), W.h_family(W.C_EQCLASS, 0, 1),
+                 W.h_family(W.C_EQCLASS, 1, 0), W.h_family(W.C_EQCLASS, 1, 1)}
+
+
+def _liveness_peak(tr, free_constants):
+    """Memory of the program with every tensor freed after its last use (and
+    never otherwise): the unlimited-budget peak of banishing."""
+    n = tr.n_tensors
+    last = np.full(n, -1)
+    for o in range(tr.n_ops):
+        last[tr.op_output[o]] = max(last[tr.op_output[o]], o)
+        for u in tr.inputs(o):
+            last[u] = max(last[u], o)
+    const = (tr.tensor_flags & W.FLAG_CONSTANT) != 0
+    req = (tr.tensor_flags & W.FLAG_REQUIRED) != 0
+    mem = int(tr.tensor_size[const].sum())
+    peak = mem
+    for o in range(tr.n_ops):
+        mem += int(tr.tensor_size[tr.op_output[o]])
+        peak = max(peak, mem)
+        for t in range(n):
+            if last[t] == o and not req[t] and (free_constants or not const[t]):
+                mem -= int(tr.tensor_size[t])
+    return peak, mem
+
+
+def test_ignore_policy_unlimited_keeps_everything(oracle_lib):
+    O = oracle_lib
+    for seed in range(20):
+        tr = W.random_program(seed, n_ops=30, n_const=3, backward=seed % 2 == 0)
+        for h in (W.H_DTR, W.H_EQ, W.H_LRU):
+            r = O.run([tr], W.make_specs([(0, h, W.BUDGET_UNLIMITED, 0, W.POLICY_IGNORE)]))[0]
+            total = int(tr.tensor_size.sum())
+            assert r["status"] == 0 and r["n_eager_evictions"] == 0 and r["n_evictions"] == 0
+            assert r["peak_memory"] == total and r["final_memory"] == total
+
+
+def test_banish_policy_unlimited_frees_at_last_use(oracle_lib):
+    O = oracle_lib
+    for seed in range(20):
+        tr = W.random_program(seed, n_ops=30, n_const=3, backward=seed % 2 == 0)
+        peak, final = _liveness_peak(tr, free_constants=True)
+        for h in (W.H_DTR, W.H_LRU, W.H_MSPS):
+            r = O.run([tr], W.make_specs([(0, h, W.BUDGET_UNLIMITED, 0, W.POLICY_BANISH)]))[0]
+            assert r["status"] == 0 and r["n_evictions"] == 0 and r["n_remats"] == 0
+            assert r["peak_memory"] == peak and r["final_memory"] == final
+        # eager eviction keeps constants: its unlimited peak is the usual one
+        r = O.run([tr], W.make_specs([(0, W.H_DTR, W.BUDGET_UNLIMITED, 0, W.POLICY_EAGER)]))[0]
+        assert r["peak_memory"] == _liveness_peak(tr, free_constants=False)[0] == W.natural_peak(tr)
+
+
+def test_banishing_frees_constants(oracle_lib):
+    """A constant of size 8 read only by the first op of a unit-size chain:
+    budget 9 runs out under eager eviction (the constant can never be evicted
+    and the chain needs two units beside it) but fits once banishing frees it."""
+    O = oracle_lib
+    n = 7
+    size = np.ones(n, np.int64)
+    size[0] = 8
+    flags = np.zeros(n, np.uint8)
+    flags[0] = W.FLAG_CONSTANT
+    flags[n - 1] = W.FLAG_REQUIRED
+    out = np.arange(1, n, dtype=np.int32)
+    off = np.arange(0, n, dtype=np.int64)
+    ins = np.arange(0, n - 1, dtype=np.int32)
+    tr = W.Trace("const-chain", size, flags, out, np.ones(n - 1, np.int64), off, ins)
+    eager = O.run([tr], W.make_specs([(0, W.H_DTR, 9, 0, W.POLICY_EAGER)]))[0]
+    banish = O.run([tr], W.make_specs([(0, W.H_DTR, 9, 0, W.POLICY_BANISH)]))[0]
+    assert eager["status"] == 1
+    assert banish["status"] == 0 and banish["n_remats"] == 0 and banish["peak_memory"] == 9
+
+
+def test_theorem31_with_banishing(oracle_lib):
+    """Theorem 3.1's own setting (h_{e*} with banishing, Appendix A): at
+    B = 2*ceil(sqrt(N)) the operation count grows linearly in N."""
+    O = oracle_lib
+
+    def ops_per_n(N):
+        tr = W.chain_trace(N)
+        r = O.run([tr], W.make_specs([(0, W.H_ESTAR, 2 * math.ceil(math.sqrt(N)), 0, W.POLICY_BANISH)]))[0]
+        assert r["status"] == 0
+        return r["n_executed_ops"] / N
+
+    assert ops_per_n(4096) / ops_per_n(256) <= 1.5
+
+
+def test_policies_match_independent_python_machine(oracle_lib):
+    O = oracle_lib
+    hs = [W.H_DTR, W.H_EQ, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_RAND, W.H_ESTAR, W.H_MSPS]
+    for seed in range(60):
+        tr = W.random_program(seed, n_ops=6 + seed % 12, n_const=seed % 3, backward=seed % 2 == 0, max_size=6)
+        peak = W.natural_peak(tr)
+        for policy in (W.POLICY_IGNORE, W.POLICY_BANISH):
+            for h in hs:
+                if policy == W.POLICY_BANISH and h in UF_HEURISTICS:
+                    continue
+                for b in sorted({max(1, peak // 3), max(1, peak // 2), max(1, 2 * peak // 3), peak}):
+                    r = O.run([tr], W.make_specs([(0, h, b, seed, policy)]))[0]
+                    s = brute.simulate(tr, b, h, seed, policy)
+                    for k, v in s.items():
+                        assert int(r[k]) == v, (seed, policy, h, b, k)
+
+
+def test_policy_invariants(oracle_lib):
+    O = oracle_lib
+    for seed in range(40):
+        tr = W.random_program(seed, n_ops=25 + seed % 30, n_const=seed % 4, backward=seed % 2 == 0,
+                              max_size=10, max_cost=7)
+        peak = W.natural_peak(tr)
+        for policy in (W.POLICY_IGNORE, W.POLICY_BANISH):
+            for h in (W.H_DTR, W.H_LRU, W.H_MSPS, W.H_RAND):
+                for b in (peak // 3, peak // 2, peak):
+                    p = O.run_probe(tr, spec(h, b, seed, policy=policy))
+                    r = p["result"]
+                    assert r["total_cost"] == r["base_cost"] + r["remat_cost"]
+                    if policy == W.POLICY_IGNORE:
+                        assert r["n_eager_evictions"] == 0
+                    if r["status"] == 0:
+                        assert r["base_cost"] == int(tr.op_cost.sum()) and r["peak_memory"] <= b
+                        res = p["state"] == O.RESIDENT
+                        assert r["final_memory"] == int(tr.tensor_size[res].sum())
+                        req = (tr.tensor_flags & W.FLAG_REQUIRED) != 0
+                        assert np.all(p["state"][req] == O.RESIDENT)
+                        if policy == W.POLICY_IGNORE:
+                            assert not np.any(p["state"] == O.BANISHED)

@@ -35,10 +35,7 @@ def compare(gpu_res, ref, specs, label):
 
 
 def specs_of(rows):
-    s = np.zeros(len(rows), W.SPEC_DTYPE)
-    for i, r in enumerate(rows):
-        s[i] = r
-    return s
+    return W.make_specs(rows)
 
 
 def test_chain_all_heuristics(gpu, oracle_lib):
@@ -88,6 +85,34 @@ def test_msps_and_ablation_family(gpu, oracle_lib):
     specs = specs_of(rows)
     print(f"family batch: {len(traces)} traces, {len(specs)} sims", flush=True)
     compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "family")
+
+
+def test_deallocation_policies(gpu, oracle_lib):
+    """Ignoring releases and banishing, every heuristic the policy allows."""
+    uf = {W.H_EQ} | {W.h_family(W.C_EQCLASS, s, m) for s in (0, 1) for m in (0, 1)}
+    traces = []
+    rows = []
+    hs = [W.H_DTR, W.H_EQ, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_RAND, W.H_ESTAR, W.H_MSPS,
+          W.h_family(W.C_ESTAR, 1, 0), W.h_family(W.C_NONE, 0, 0)]
+    for s in range(40):
+        tr = W.random_program(900 + s, n_ops=10 + (s * 11) % 100, n_const=1 + s % 4, backward=s % 2 == 0,
+                              max_in=1 + s % 4, max_size=1 + s % 20, max_cost=1 + s % 7)
+        traces.append(tr)
+        peak = W.natural_peak(tr)
+        for policy in (W.POLICY_IGNORE, W.POLICY_BANISH):
+            for h in hs:
+                if policy == W.POLICY_BANISH and h in uf:
+                    continue
+                for frac in (0.3, 0.6, 1.0):
+                    rows.append((len(traces) - 1, h, max(1, int(peak * frac)), s * 31 + h, policy))
+    n_chain = len(traces)
+    traces.append(W.chain_trace(200))
+    for B in (2 * 15, 40, 80):
+        rows.append((n_chain, W.H_ESTAR, B, 0, W.POLICY_BANISH))
+        rows.append((n_chain, W.H_DTR, B, 0, W.POLICY_BANISH))
+    specs = specs_of(rows)
+    print(f"policy batch: {len(traces)} traces, {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "policies")
 
 
 def test_empty_and_degenerate(gpu, oracle_lib):
