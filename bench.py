@@ -100,6 +100,49 @@ def copy_probe(mib: int):
     print(json.dumps({"copy_probe_bytes": n, "copies": 3}))
 
 
+def search_study(wl, steps: int):
+    """The prototype's search approximations (ignore small candidates, sample
+    sqrt(n) of the pool; Appendix E) against exact search on the same batch:
+    OOM rate, total cost relative to exact search where both finish, scores
+    searched, and launch time."""
+    import torch
+    from paper_2006_09616_amd import dtr as D
+    variants = {"exact": 0, "ignore_small": W.SEARCH_IGNORE_SMALL, "sample": W.SEARCH_SAMPLE,
+                "ignore_small+sample": W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE}
+    out, base = {}, None
+    for name, flags in variants.items():
+        specs = wl.specs.copy()
+        specs["search"] = flags
+        sim = D.Simulator(wl.traces, specs, device="cuda:0")
+        sim.run()
+        torch.cuda.synchronize()
+        ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+        for i in range(steps):
+            ev0[i].record(sim.stream)
+            sim.run()
+            ev1[i].record(sim.stream)
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in zip(ev0, ev1)) / steps
+        res = sim.results()
+        sim.close()
+        ok = res["status"] == 0
+        row = {"launch_ms": ms, "oom_rate": float(np.mean(res["status"] == 1)),
+               "scores": int(res["n_scores"].sum()), "ops": int(res["n_executed_ops"].sum())}
+        if base is None:
+            base = (res, ms)
+        else:
+            both = ok & (base[0]["status"] == 0)
+            ratio = res["total_cost"][both] / base[0]["total_cost"][both]
+            row.update(speedup=base[1] / ms, cost_ratio_mean=float(ratio.mean()) if both.any() else None,
+                       cost_ratio_max=float(ratio.max()) if both.any() else None,
+                       scores_vs_exact=row["scores"] / max(1, int(base[0]["n_scores"].sum())),
+                       newly_oom=int(((res["status"] == 1) & (base[0]["status"] == 0)).sum()))
+        out[name] = row
+        print(f"[bench] search study {name}: {ms:.1f} ms, oom {row['oom_rate']:.4f}", file=sys.stderr, flush=True)
+    return out
+
+
 WORKLOADS = {
     "treelstm4096": lambda: W.make_config("treelstm4096"),
     "resnet50blk": lambda: W.make_config("resnet50blk"),
@@ -135,6 +178,8 @@ def main():
     ap.add_argument("--slots", type=int, default=0)
     ap.add_argument("--cpu-sample", type=int, default=32, help="oracle on every k-th simulation (0: skip)")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--search-study", action="store_true",
+                    help="only compare the search approximations with exact search on the workload")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (counter calibration)")
     args = ap.parse_args()
@@ -156,6 +201,11 @@ def main():
     gen_s = time.perf_counter() - t0
     print(f"[bench] workload {wl.name}: {len(wl.traces)} traces, {wl.n_sims} sims, generated in {gen_s:.1f}s",
           file=sys.stderr, flush=True)
+    if args.search_study:
+        torch.cuda.set_device(0)
+        print(json.dumps({"search_study": search_study(wl, args.steps), "workload": wl.name,
+                          "n_sims": wl.n_sims, "n_gpus": 1}))
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     sim = D.Simulator(wl.traces, wl.specs, device="cuda:0", slots=args.slots)

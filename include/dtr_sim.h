@@ -117,17 +117,28 @@ typedef struct {
                                 heuristics (DTR_H_EQ, DTR_C_EQCLASS): rejected.
                                 Banishments are counted in n_eager_evictions. */
 
+/* ---- search approximations of the prototype (Appendix E), bit flags ------ */
+#define DTR_SEARCH_IGNORE_SMALL 1u  /* skip candidates with size below 1% of the
+                                       pool's mean size (100 size n < sum)      */
+#define DTR_SEARCH_SAMPLE       2u  /* search a random sample: each candidate kept
+                                       with probability ceil(sqrt(n))/n, n = pool
+                                       size, by a SplitMix64 draw per (seed ^
+                                       0xD6E8FEB86659FD93, eviction number, id);
+                                       if no candidate is left, every candidate
+                                       that is not small is searched.  n_scores
+                                       counts the candidates scored.            */
+
 /* One simulation (32 bytes): trace index, DTR_H_* heuristic, memory budget
  * (same unit as tensor_size; DTR_BUDGET_UNLIMITED for none), seed (used by
- * DTR_H_RAND), DTR_POLICY_* deallocation policy, and a reserved word that
- * must be 0. */
+ * DTR_H_RAND and DTR_SEARCH_SAMPLE), DTR_POLICY_* deallocation policy, and
+ * DTR_SEARCH_* flags (0: exact search). */
 typedef struct {
     int32_t trace;
     int32_t heuristic;
     int64_t budget;
     uint64_t seed;
     int32_t policy;
-    int32_t reserved;
+    int32_t search;
 } dtr_sim_spec;
 
 /* Result of one simulation (104 bytes). */

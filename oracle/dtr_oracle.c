@@ -32,7 +32,12 @@
  *     s and size m each used or not, and c the full e* cost, the
  *     equivalence-class cost, the local cost or none (c = 1);
  *   - output condition: tensors the program still holds at the end are
- *     rematerialized and locked (Appendix C.6 log semantics).
+ *     rematerialized and locked (Appendix C.6 log semantics);
+ *   - the prototype's search approximations (Appendix E): candidates smaller
+ *     than 1% of the pool's mean size are ignored, and/or only a random
+ *     sample of the pool is searched (each candidate kept with probability
+ *     ceil(sqrt(n))/n); when nothing is left the search falls back to every
+ *     candidate that is not small.
  *
  * No caching, no incremental data structure beyond the paper's own
  * union-find: every eviction rescans every tensor and every h_DTR score
@@ -86,7 +91,8 @@ typedef struct {
     const int32_t *op_inputs;
 } oracle_trace;
 
-typedef struct { int32_t trace, heuristic; int64_t budget; uint64_t seed; int32_t policy, reserved; } oracle_spec;
+typedef struct { int32_t trace, heuristic; int64_t budget; uint64_t seed; int32_t policy, search; } oracle_spec;
+enum { OSR_IGNORE_SMALL = 1, OSR_SAMPLE = 2 };   /* search approximation flags */
 
 /* result fields (int64 each) */
 enum {
@@ -198,6 +204,7 @@ typedef struct {
     const oracle_trace *tr;
     int heuristic;
     int policy;
+    int search;                   /* OSR_* flags */
     int64_t budget;
     uint64_t seed;
 
@@ -550,30 +557,63 @@ static void dump_state(sim *s)
     }
 }
 
-/* while memory is insufficient, evict the lowest-scored evictable tensor */
+/* smallest r with r * r >= n */
+static uint64_t ceil_sqrt(uint64_t n)
+{
+    uint64_t r = 0;
+    while (r * r < n) r++;
+    return r;
+}
+
+/* the sampling draw of candidate x at an eviction decision: SplitMix64 on a
+ * stream of its own (the seed offset by a fixed odd constant) */
+static uint64_t sample_key(uint64_t seed, int64_t eviction_no, int32_t x)
+{
+    uint64_t key = ((uint64_t)eviction_no << 32) + (uint64_t)(uint32_t)x;
+    return splitmix64_mix((seed ^ 0xD6E8FEB86659FD93ull) + 0x9E3779B97F4A7C15ull * key);
+}
+
+/* while memory is insufficient, evict the lowest-scored evictable tensor
+ * (of the searched candidates, under the search approximations) */
 static void allocate(sim *s, int64_t size)
 {
     int32_t n = s->tr->n_tensors;
     while (s->memory + size > s->budget) {
         oracle_probe *p = s->probe;
         int dumping = p && p->stop_at_eviction >= 0 && s->eviction_no == p->stop_at_eviction;
+        /* pool statistics for the approximations: count and total size */
+        int64_t n0 = 0, size_sum = 0;
+        for (int32_t x = 0; x < n; x++)
+            if (is_evictable(s, x)) { n0++; size_sum += s->tr->tensor_size[x]; }
+        /* sampling: keep each candidate with probability k/n0, k = ceil(sqrt(n0)) */
+        uint64_t k = ceil_sqrt((uint64_t)n0);
+        int sample_all = k >= (uint64_t)n0;
+        uint64_t tau = sample_all ? 0 : (uint64_t)((((u128)k) << 64) / (u128)(uint64_t)n0);
         int32_t best = -1;
         uint64_t bn = 0;
         u128 bd = 0;
         int64_t count = 0;
-        for (int32_t x = 0; x < n; x++) {
-            if (!is_evictable(s, x)) continue;
-            uint64_t N;
-            u128 D;
-            score(s, x, &N, &D);
-            count++;
-            if (dumping) {
-                if (p->score_n_out) p->score_n_out[x] = N;
-                if (p->score_d_lo_out) p->score_d_lo_out[x] = (uint64_t)D;
-                if (p->score_d_hi_out) p->score_d_hi_out[x] = (uint64_t)(D >> 64);
-                if (p->candidate_out) p->candidate_out[x] = 1;
+        for (int pass = 0; pass < 2 && best < 0; pass++) {
+            int sampling = pass == 0 && (s->search & OSR_SAMPLE) && !sample_all;
+            if (pass == 1 && !(s->search & OSR_SAMPLE)) break;
+            for (int32_t x = 0; x < n; x++) {
+                if (!is_evictable(s, x)) continue;
+                if ((s->search & OSR_IGNORE_SMALL) &&
+                    (u128)100 * (u128)(uint64_t)s->tr->tensor_size[x] * (u128)(uint64_t)n0 < (u128)(uint64_t)size_sum)
+                    continue;     /* smaller than 1% of the mean size */
+                if (sampling && sample_key(s->seed, s->eviction_no, x) >= tau) continue;
+                uint64_t N;
+                u128 D;
+                score(s, x, &N, &D);
+                count++;
+                if (dumping) {
+                    if (p->score_n_out) p->score_n_out[x] = N;
+                    if (p->score_d_lo_out) p->score_d_lo_out[x] = (uint64_t)D;
+                    if (p->score_d_hi_out) p->score_d_hi_out[x] = (uint64_t)(D >> 64);
+                    if (p->candidate_out) p->candidate_out[x] = 1;
+                }
+                if (best < 0 || better(N, D, x, bn, bd, best)) { best = x; bn = N; bd = D; }
             }
-            if (best < 0 || better(N, D, x, bn, bd, best)) { best = x; bn = N; bd = D; }
         }
         if (dumping) { dump_state(s); s->stopped = OS_STOPPED; s->r[R_STATUS] = OS_STOPPED; return; }
         if (best < 0) { s->r[R_STATUS] = OS_OOM; s->stopped = OS_OOM; return; }
@@ -712,6 +752,7 @@ static int run_one(const oracle_trace *tr, const graph *g, const oracle_spec *sp
     s.tr = tr;
     s.heuristic = sp->heuristic;
     s.policy = sp->policy;
+    s.search = sp->search;
     s.budget = sp->budget;
     s.seed = sp->seed;
     s.probe = probe;
@@ -786,6 +827,7 @@ int oracle_run(const oracle_trace *traces, int32_t n_traces, const oracle_spec *
         if (specs[i].trace < 0 || specs[i].trace >= n_traces ||
             !((specs[i].heuristic >= 0 && specs[i].heuristic <= OH_MSPS) || family(specs[i].heuristic)) ||
             specs[i].policy < OP_EAGER || specs[i].policy > OP_BANISH ||
+            specs[i].search < 0 || specs[i].search > (OSR_IGNORE_SMALL | OSR_SAMPLE) ||
             (specs[i].policy == OP_BANISH && uses_uf(specs[i].heuristic)))
             return -2;
     graph *graphs = calloc((size_t)(n_traces > 0 ? n_traces : 1), sizeof(graph));
@@ -851,6 +893,11 @@ int64_t oracle_estar(const oracle_trace *tr, const uint8_t *state, int32_t x, in
 }
 
 /* Test hook: the SplitMix64 draw used by h_rand for (seed, eviction number, id). */
+uint64_t oracle_sample_key(uint64_t seed, int64_t eviction_no, int32_t x)
+{
+    return sample_key(seed, eviction_no, x);
+}
+
 uint64_t oracle_rand_key(uint64_t seed, int64_t eviction_no, int32_t x)
 {
     uint64_t key = ((uint64_t)eviction_no << 32) + (uint64_t)(uint32_t)x;

@@ -70,6 +70,8 @@ def lib():
         _lib.oracle_estar.restype = C.c_int64
         _lib.oracle_rand_key.argtypes = [C.c_uint64, C.c_int64, C.c_int32]
         _lib.oracle_rand_key.restype = C.c_uint64
+        _lib.oracle_sample_key.argtypes = [C.c_uint64, C.c_int64, C.c_int32]
+        _lib.oracle_sample_key.restype = C.c_uint64
         assert _lib.oracle_result_fields() == len(RESULT_FIELDS)
     return _lib
 
@@ -160,3 +162,7 @@ def estar(trace, state, x: int, ancestors_only: bool = False):
 
 def rand_key(seed: int, eviction_no: int, x: int) -> int:
     return int(lib().oracle_rand_key(seed, eviction_no, x))
+
+
+def sample_key(seed: int, eviction_no: int, x: int) -> int:
+    return int(lib().oracle_sample_key(seed, eviction_no, x))

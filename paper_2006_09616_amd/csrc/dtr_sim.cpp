@@ -210,7 +210,7 @@ struct Plan {
     dtr::SlotLayout L{};
     int32_t n_slots = 0;
     std::vector<int32_t> order;
-    int32_t class_count[3] = {0, 0, 0};
+    int32_t class_count[dtr::N_GROUPS] = {0, 0, 0, 0, 0, 0};
 };
 
 template <class T>
@@ -259,7 +259,8 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
             return fail(DTR_ETRACE, "sim %d: unknown deallocation policy %d", i, s.policy);
         if (s.policy == DTR_POLICY_BANISH && heuristic_class(s.heuristic) == 0)
             return fail(DTR_ETRACE, "sim %d: banishing is not defined for union-find heuristics", i);
-        if (s.reserved != 0) return fail(DTR_ETRACE, "sim %d: reserved word must be 0", i);
+        if (s.search & ~(int32_t)(DTR_SEARCH_IGNORE_SMALL | DTR_SEARCH_SAMPLE))
+            return fail(DTR_ETRACE, "sim %d: unknown search flags %d", i, s.search);
         need_banish |= s.policy == DTR_POLICY_BANISH;
         need_uf |= heuristic_class(s.heuristic) == 0;
         need_walk |= heuristic_class(s.heuristic) == 1;
@@ -295,7 +296,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
 
     // grouped by heuristic class (one kernel specialisation each), then
     // longest first: ops of the trace, then lower budget first
-    auto cls = [&](int32_t i) { return heuristic_class(sims[i].heuristic); };
+    auto cls = [&](int32_t i) { return heuristic_class(sims[i].heuristic) + (sims[i].search ? 3 : 0); };
     p.order.resize(n_sims);
     std::iota(p.order.begin(), p.order.end(), 0);
     std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {
@@ -304,7 +305,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
         if (fa != fb) return fa > fb;
         return sims[a].budget < sims[b].budget;
     });
-    for (int c = 0; c < 3; c++) p.class_count[c] = 0;
+    for (int c = 0; c < dtr::N_GROUPS; c++) p.class_count[c] = 0;
     for (int32_t i = 0; i < n_sims; i++) p.class_count[cls(i)]++;
 
     size_t w = align_up(64);   // header: work counter
@@ -420,7 +421,8 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec
     }
     std::memcpy(H + p.desc_off, descs.data(), sizeof(dtr::TraceDev) * n_traces);
     for (int32_t i = 0; i < n_sims; i++) {
-        dtr::SpecDev s{sims[i].trace, sims[i].heuristic, sims[i].budget, sims[i].seed, sims[i].policy, 0};
+        dtr::SpecDev s{sims[i].trace, sims[i].heuristic, sims[i].budget, sims[i].seed, sims[i].policy,
+                       sims[i].search};
         std::memcpy(H + p.spec_off + i * sizeof(dtr::SpecDev), &s, sizeof(s));
     }
     if (n_sims) std::memcpy(H + p.order_off, p.order.data(), sizeof(int32_t) * n_sims);
@@ -441,9 +443,9 @@ int dtr_sim_run(dtr_sim *h, void *stream)
     if (!h) return fail(DTR_EINVAL, "null handle");
     const Plan &p = h->plan;
     if (h->n_sims == 0) { h->ran = true; h->last_stream = (hipStream_t)stream; return DTR_OK; }
-    dtr::KernelArgs a[3];
+    dtr::KernelArgs a[dtr::N_GROUPS];
     int32_t first = 0;
-    for (int c = 0; c < 3; c++) {
+    for (int c = 0; c < dtr::N_GROUPS; c++) {
         a[c].traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
         a[c].specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
         a[c].order = (const int32_t *)(h->ws + p.order_off) + first;

@@ -61,7 +61,7 @@ struct SpecDev {
     int32_t trace, heuristic;
     int64_t budget;
     uint64_t seed;
-    int32_t policy, reserved;
+    int32_t policy, search;
 };
 static_assert(sizeof(SpecDev) == 32, "spec layout");
 
@@ -128,6 +128,11 @@ struct __attribute__((aligned(16))) UfNode {
     int32_t parent;
     int32_t size;
 };
+
+// simulation groups, one kernel specialisation each: heuristic class
+// (union-find neighbourhood, neighbourhood walk, none), plus 3 with the
+// search approximations on
+constexpr int N_GROUPS = 6;
 
 struct KernelArgs {
     const TraceDev *traces;

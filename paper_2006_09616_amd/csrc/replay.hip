@@ -57,6 +57,7 @@ constexpr int32_t S_CONST = -3;
 constexpr int32_t S_UNCOMPUTED = -2;
 constexpr int32_t S_RESIDENT = -1;
 enum { POLICY_EAGER = 0, POLICY_IGNORE = 1, POLICY_BANISH = 2 };
+enum { SEARCH_IGNORE_SMALL = 1, SEARCH_SAMPLE = 2 };
 constexpr uint32_t MAX_LOCKS = 255;
 constexpr uint8_t FLAG_CONST = 1;
 constexpr int K = NB_CACHE;
@@ -64,14 +65,17 @@ constexpr int KQ = K / 4;        // 16-byte quads of cached nodes per pool slot
 constexpr int PQ = (int)(sizeof(PoolSlot) / 16);   // quads per pool slot
 static_assert(K % 4 == 0 && PQ == 2 + KQ, "pool slot: two header quads, then the cache");
 constexpr int LB = 8;            // neighbour reads issued together when building a cache
-// kernel specialisations by heuristic class (register budgets differ widely)
-enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2 };
+// kernel specialisations by heuristic class (register budgets differ widely),
+// each with exact search or with the search approximations (HC | HC_APPROX)
+enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2, HC_APPROX = 4 };
+__host__ __device__ constexpr int cls(int hc) { return hc & 3; }
+__host__ __device__ constexpr bool approx(int hc) { return (hc & HC_APPROX) != 0; }
 // candidates per lane per scan round (their reads are issued together); the
 // h_DTR^eq round is instruction-issue bound, so a second candidate per lane
 // only doubles the round
 template <int HC>
 struct Round {
-    static constexpr int value = HC == HC_EQ ? 1 : 2;
+    static constexpr int value = cls(HC) == HC_EQ ? 1 : 2;
     static_assert(POOL_LDS % (WAVE * value) == 0, "a scan round lies wholly in LDS or wholly in global memory");
 };
 
@@ -199,6 +203,7 @@ struct Sim {
     int32_t h;
     int32_t cmode, use_s, use_m;  // the heuristic as (cost measure, staleness used, size used)
     int32_t policy;               // what a release does
+    int32_t search;               // search approximation flags
     int32_t lane;
     int64_t budget;
     uint64_t seed;
@@ -375,7 +380,7 @@ __device__ __forceinline__ void pool_compact(Sim &s)
         const i32x4 q0 = P[0], q1 = P[1];
         i32x4 qc[KQ];
 #pragma unroll
-        for (int k = 0; k < KQ; k++) qc[k] = HC == HC_EQ ? P[2 + k] : 0;
+        for (int k = 0; k < KQ; k++) qc[k] = cls(HC) == HC_EQ ? P[2 + k] : 0;
         const int32_t x = i < s.pool_end ? q0.x : -1;
         const bool keep = x >= 0;
         const uint64_t m = __ballot(keep);
@@ -385,7 +390,7 @@ __device__ __forceinline__ void pool_compact(Sim &s)
             i32x4 *Q = (i32x4 *)&s.S.pool(j);
             Q[0] = q0;
             Q[1] = q1;
-            if (HC == HC_EQ)
+            if (cls(HC) == HC_EQ)
 #pragma unroll
                 for (int k = 0; k < KQ; k++) Q[2 + k] = qc[k];
             s.S.tst[x] = ts_make(S_RESIDENT, (uint32_t)j, 0);
@@ -414,7 +419,7 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
         const TRec r = rec_v(s, x);
         int32_t deg = (r.adj_e - r.adj_b) << 8;
         NbCache nb;
-        if (HC == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg);
+        if (cls(HC) == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg);
         i32x4 q0, q1;
         q0.x = x;
         q0.y = deg;
@@ -427,7 +432,7 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
         i32x4 *Q = (i32x4 *)&s.S.pool(i);
         Q[0] = q0;
         Q[1] = q1;
-        if (HC == HC_EQ) cache_store(s.S.pool(i), nb);
+        if (cls(HC) == HC_EQ) cache_store(s.S.pool(i), nb);
     }
     s.pool_end += cnt;
     s.pool_live += cnt;
@@ -665,7 +670,7 @@ __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eage
     s.mem -= rv.size;
     if (eager) s.eager++;
     else s.evictions++;
-    if (HC != HC_EQ) {
+    if (cls(HC) != HC_EQ) {
         s.S.tst[v] = ts_make(0, 0, 0);
         return true;
     }
@@ -872,9 +877,64 @@ __device__ __forceinline__ void take(Best &b, bool valid, float sc, uint64_t N, 
     b.have = t ? 1 : b.have;
 }
 
-// Score every pool entry; return the victim (uniform) and its slot, or -1.
+// Which candidates an eviction decision searches (the prototype's search
+// approximations, Appendix E): those of size >= min_size (size at least 1% of
+// the pool's mean: 100 size n0 >= sum of sizes, i.e. size >= ceil(sum / (100
+// n0)); 0 without the flag) and, with `sample`, whose sampling draw is below
+// tau (probability ceil(sqrt(n0))/n0).
+struct Filter {
+    bool sample;
+    uint64_t min_size, tau;
+};
+
+__device__ __forceinline__ uint64_t sample_draw(const Sim &s, int32_t x)
+{
+    const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)x;
+    return mix64((s.seed ^ 0xD6E8FEB86659FD93ull) + 0x9E3779B97F4A7C15ull * key);
+}
+
+// filter of the first search pass; `sample` stays off when it would keep
+// every candidate (ceil(sqrt(n0)) >= n0)
 template <int HC>
-__device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
+__device__ __forceinline__ Filter make_filter(Sim &s)
+{
+    Filter F;
+    const uint32_t n0 = (uint32_t)s.pool_live;
+    F.min_size = 0;
+    if (s.search & SEARCH_IGNORE_SMALL) {
+        uint64_t sum = 0;
+        for (int32_t i = s.lane; i < s.pool_end; i += WAVE) {
+            const i32x4 *P = (const i32x4 *)&s.S.pool(i);
+            const i32x4 q0 = P[0], q1 = P[1];
+            if (q0.x >= 0) sum += ((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x;
+        }
+        for (int off = WAVE / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, WAVE);
+        sum = (uint64_t)uni64((int64_t)sum);
+        const uint64_t d = 100 * (uint64_t)n0;
+        F.min_size = (sum + d - 1) / d;
+    }
+    F.sample = false;
+    F.tau = 0;
+    if (s.search & SEARCH_SAMPLE) {
+        uint32_t k = (uint32_t)sqrtf((float)n0);          // then corrected to ceil(sqrt(n0))
+        while (k * k < n0) k++;
+        while (k > 0 && (k - 1) * (k - 1) >= n0) k--;
+        if (k < n0) {
+            // tau = floor(k 2^64 / n0) by long division in two 32-bit digits
+            const uint64_t a = (uint64_t)k << 32;
+            const uint64_t q1 = a / n0, r1 = a % n0;
+            const uint64_t q2 = (r1 << 32) / n0;
+            F.tau = (q1 << 32) + q2;
+            F.sample = true;
+        }
+    }
+    return F;
+}
+
+// Score every searched pool entry; return the victim (uniform) and its slot,
+// or -1; `scored` receives the number of candidates scored.
+template <int HC>
+__device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filter &F, int64_t &scored)
 {
     const int32_t end = s.pool_end;
     const int32_t lane = s.lane;
@@ -890,7 +950,7 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
     best.slot = -1;
     best.have = 0;
     constexpr int U = Round<HC>::value;
-    if (HC == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
+    if (cls(HC) == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
         clear_stamps(s);
     for (int32_t base = 0; base < end; base += WAVE * U) {
         int32_t id[U], pd[U];
@@ -913,7 +973,7 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 Q0[u] = L4[PQ * slot[u]];
                 Q1[u] = L4[PQ * slot[u] + 1];
 #pragma unroll
-                for (int k = 0; k < KQ; k++) QC[u][k] = HC == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
+                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
             }
         } else {
 #pragma unroll
@@ -921,7 +981,7 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 Q0[u] = G4[PQ * slot[u]];
                 Q1[u] = G4[PQ * slot[u] + 1];
 #pragma unroll
-                for (int k = 0; k < KQ; k++) QC[u][k] = HC == HC_EQ ? G4[PQ * slot[u] + 2 + k] : 0;
+                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? G4[PQ * slot[u] + 2 + k] : 0;
             }
         }
 #pragma unroll
@@ -942,9 +1002,13 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 nb[u][4 * k + 3] = QC[u][k].w;
             }
             ok[u] = id[u] >= 0;
+            if (approx(HC)) {
+                ok[u] = ok[u] && (uint64_t)size[u] >= F.min_size;
+                if (F.sample) ok[u] = ok[u] && sample_draw(s, id[u]) < F.tau;
+            }
         }
         uint64_t N[U], DA[U], DB[U];
-        if (HC == HC_EQ) {
+        if (cls(HC) == HC_EQ) {
             const bool lds_nodes = s.uf_n <= UF_LDS;
             // level 2: every cached node (unused entries hold node 0, the null
             // node); level 3: its parent, so nodes one merge away resolve too
@@ -1028,7 +1092,7 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
                 s.nbr += ok[u] ? ev[u] : 0;
                 s.adj += ok[u] ? (pd[u] >> 8) : 0;
             }
-        } else if (HC == HC_WALK) {
+        } else if (cls(HC) == HC_WALK) {
 #pragma unroll
             for (int u = 0; u < U; u++) {
                 N[u] = 0;
@@ -1058,8 +1122,10 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot)
             }
         }
 #pragma unroll
-        for (int u = 0; u < U; u++)
+        for (int u = 0; u < U; u++) {
             take(best, ok[u], score_est(N[u], DA[u], DB[u]), N[u], DA[u], DB[u], id[u], (int32_t)slot[u]);
+            if (approx(HC)) scored += __popcll(__ballot(ok[u]));
+        }
     }
     if (__ballot(bad)) { set_status(s, ST_CAPACITY); return -1; }
     // cross-lane minimum: the smallest estimate bounds the winner; only the
@@ -1105,12 +1171,22 @@ __device__ __forceinline__ bool allocate(Sim &s, int64_t sz)
         s.prof_rounds += (s.pool_end + WAVE * Round<HC>::value - 1) / (WAVE * Round<HC>::value);
 #endif
         int32_t slot = -1;
-        const int32_t v = scan<HC>(s, slot);
+        int64_t scored = 0;
+        Filter F;
+        F.sample = false;
+        F.min_size = F.tau = 0;
+        if (approx(HC)) F = make_filter<HC>(s);
+        int32_t v;
+        for (;;) {
+            v = scan<HC>(s, slot, F, scored);
+            if (v >= 0 || !F.sample || s.status != ST_OK) break;
+            F.sample = false;      // the sample missed every candidate that is not small: search those
+        }
 #ifdef DTR_PROFILE
         s.prof_scan_cycles += (int64_t)__builtin_readcyclecounter() - c0_;
 #endif
         if (v < 0) { set_status(s, ST_CAPACITY); return false; }
-        s.scores += s.pool_live;
+        s.scores += approx(HC) ? scored : s.pool_live;
         PROF_T0(te);
         const bool evicted = evict<HC>(s, v, slot, false);
         PROF_ADD(PH_EVICT, te);
@@ -1221,7 +1297,7 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
     else s.base += c;
     s.mem += rt.size;
     if (s.mem > s.peak) s.peak = s.mem;
-    if (HC == HC_EQ && remat) {
+    if (cls(HC) == HC_EQ && remat) {
         // split approximation: the set loses c0(t); t leaves it (its node stays as a phantom)
         const int32_t old = uni(ts_sw(s.S.tst[t]));
         if (s.uf_n <= UF_LDS) {
@@ -1401,7 +1477,7 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         PROF_T0(tu);
         unlock_inputs<HC>(s, b, e, start, f);
         PROF_ADD(PH_UNLOCK, tu);
-        if (HC != HC_EQ && remat && s.policy == POLICY_BANISH) retry_banish(s, b, e);
+        if (cls(HC) != HC_EQ && remat && s.policy == POLICY_BANISH) retry_banish(s, b, e);
         if (!remat) {
             // a trace operation's output is unlocked: it joins the pool at once
             PROF_T0(to);
@@ -1430,7 +1506,7 @@ __device__ __forceinline__ bool release(Sim &s, int32_t o)
 {
     const int32_t b = uni(cld(s.t.rel_off + o)), e = uni(cld(s.t.rel_off + o + 1));
     if (s.policy == POLICY_IGNORE) return true;
-    if (HC != HC_EQ && s.policy == POLICY_BANISH) {    // never a union-find heuristic
+    if (cls(HC) != HC_EQ && s.policy == POLICY_BANISH) {    // never a union-find heuristic
         for (int32_t k = b; k < e; k++) try_banish(s, uni(cld(s.t.rel + k)));
         return true;
     }
@@ -1463,6 +1539,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.S = S;
     s.h = sp.heuristic;
     s.policy = sp.policy;
+    s.search = sp.search;
     if (s.h >= H_FAMILY) {             // h'(s, m, c) = 16 + 4c + 2s + m
         s.cmode = (s.h - H_FAMILY) >> 2;
         s.use_s = (s.h >> 1) & 1;
@@ -1502,10 +1579,10 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     const int32_t n = s.t.n;
     for (int32_t x = lane; x < n; x += WAVE)
         s.S.tst[x] = ts_make((gld(s.t.flags + x) & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
-    if (HC != HC_EQ && s.policy == POLICY_BANISH)
+    if (cls(HC) != HC_EQ && s.policy == POLICY_BANISH)
         for (int32_t x = lane; x < n; x += WAVE) s.S.pending[x] = 0;
-    if (HC == HC_WALK) clear_stamps(s);
-    if (HC == HC_EQ && lane == 0) {
+    if (cls(HC) == HC_WALK) clear_stamps(s);
+    if (cls(HC) == HC_EQ && lane == 0) {
         UfNode z;
         z.cost = 0;
         z.parent = 0;
@@ -1585,7 +1662,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
 template <int HC>
 __global__ void __launch_bounds__(WAVE) replay_kernel(KernelArgs a)
 {
-    __shared__ UfNode lds_nodes[HC == HC_EQ ? UF_LDS : 1];
+    __shared__ UfNode lds_nodes[cls(HC) == HC_EQ ? UF_LDS : 1];
     __shared__ PoolSlot lds_pool[POOL_LDS];
     const int32_t lane = threadIdx.x;
     Slot S = slot_at(a, blockIdx.x);
@@ -1609,17 +1686,23 @@ __global__ void reset_kernel(uint32_t *queue, int32_t n)
 
 }  // namespace dtr
 
-// Launch entry used by the host library (same shared object): args[c] holds
-// the simulations of heuristic class c (h_DTR^eq; h_DTR and h_{e*}; the
-// rest), each with its own work counter; empty classes are skipped.
+// Launch entry used by the host library (same shared object): args[g] holds
+// the simulations of group g = heuristic class (union-find; neighbourhood
+// walk; none) + 3 if the search approximations are on, each with its own
+// work counter; empty groups are skipped.
 extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream)
 {
-    hipLaunchKernelGGL(dtr::reset_kernel, dim3(1), dim3(dtr::WAVE), 0, stream, args[0].queue, 3);
-    if (args[0].n_sims > 0)
-        hipLaunchKernelGGL(dtr::replay_kernel<dtr::HC_EQ>, dim3(args[0].n_slots), dim3(dtr::WAVE), 0, stream, args[0]);
-    if (args[1].n_sims > 0)
-        hipLaunchKernelGGL(dtr::replay_kernel<dtr::HC_WALK>, dim3(args[1].n_slots), dim3(dtr::WAVE), 0, stream, args[1]);
-    if (args[2].n_sims > 0)
-        hipLaunchKernelGGL(dtr::replay_kernel<dtr::HC_SIMPLE>, dim3(args[2].n_slots), dim3(dtr::WAVE), 0, stream, args[2]);
+    using namespace dtr;
+    hipLaunchKernelGGL(reset_kernel, dim3(1), dim3(WAVE), 0, stream, args[0].queue, N_GROUPS);
+    const dim3 blk(WAVE);
+    if (args[0].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_EQ>, dim3(args[0].n_slots), blk, 0, stream, args[0]);
+    if (args[1].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_WALK>, dim3(args[1].n_slots), blk, 0, stream, args[1]);
+    if (args[2].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_SIMPLE>, dim3(args[2].n_slots), blk, 0, stream, args[2]);
+    if (args[3].n_sims > 0)
+        hipLaunchKernelGGL(replay_kernel<HC_EQ | HC_APPROX>, dim3(args[3].n_slots), blk, 0, stream, args[3]);
+    if (args[4].n_sims > 0)
+        hipLaunchKernelGGL(replay_kernel<HC_WALK | HC_APPROX>, dim3(args[4].n_slots), blk, 0, stream, args[4]);
+    if (args[5].n_sims > 0)
+        hipLaunchKernelGGL(replay_kernel<HC_SIMPLE | HC_APPROX>, dim3(args[5].n_slots), blk, 0, stream, args[5]);
     return hipGetLastError();
 }

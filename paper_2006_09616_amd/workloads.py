@@ -54,17 +54,19 @@ BUDGET_UNLIMITED = (1 << 63) - 1
 
 # deallocation policies (what a release does): evict eagerly, nothing, banish
 POLICY_EAGER, POLICY_IGNORE, POLICY_BANISH = range(3)
+# search approximation flags: ignore small candidates, search a random sample
+SEARCH_IGNORE_SMALL, SEARCH_SAMPLE = 1, 2
 
 SPEC_DTYPE = np.dtype([("trace", "<i4"), ("heuristic", "<i4"),
                        ("budget", "<i8"), ("seed", "<u8"),
-                       ("policy", "<i4"), ("reserved", "<i4")])
+                       ("policy", "<i4"), ("search", "<i4")])
 
 
 def make_specs(rows) -> np.ndarray:
-    """Simulation specs from rows (trace, heuristic, budget, seed[, policy])."""
+    """Simulation specs from rows (trace, heuristic, budget, seed[, policy[, search]])."""
     a = np.zeros(len(rows), dtype=SPEC_DTYPE)
     for i, r in enumerate(rows):
-        a[i] = (r[0], r[1], r[2], r[3], r[4] if len(r) > 4 else POLICY_EAGER, 0)
+        a[i] = (r[0], r[1], r[2], r[3], r[4] if len(r) > 4 else POLICY_EAGER, r[5] if len(r) > 5 else 0)
     return a
 
 

@@ -357,8 +357,33 @@ def _mix64(z):
     return z ^ (z >> 31)
 
 
-def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EAGER) -> dict:
-    """Heuristic-driven run of the same machine (h ids and policies as in the C-ABI)."""
+IGNORE_SMALL, SAMPLE = 1, 2
+
+
+def _searched(prog, m, cands, search, seed):
+    """Candidates the search approximations leave (Appendix E): drop those
+    below 1% of the pool's mean size; keep each with probability
+    ceil(sqrt(n))/n by a SplitMix64 draw on its own stream; fall back to the
+    non-small ones when nothing is left."""
+    n = len(cands)
+    total = sum(prog.size[x] for x in cands)
+    big = [x for x in cands if not (search & IGNORE_SMALL) or 100 * prog.size[x] * n >= total]
+    if not (search & SAMPLE):
+        return big
+    k = 0
+    while k * k < n:
+        k += 1
+    if k >= n:
+        return big
+    tau = (k << 64) // n
+    keep = [x for x in big
+            if _mix64(((seed ^ 0xD6E8FEB86659FD93) + 0x9E3779B97F4A7C15 * ((m.evict_no << 32) + x)) & MASK64) < tau]
+    return keep if keep else big
+
+
+def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EAGER, search: int = 0) -> dict:
+    """Heuristic-driven run of the same machine (h ids, policies and search
+    flags as in the C-ABI)."""
     prog = Program(trace)
     fam = heuristic >= 16
     fc, fs, fm = ((heuristic - 16) >> 2, ((heuristic - 16) >> 1) & 1, (heuristic - 16) & 1) if fam else (-1, 0, 0)
@@ -366,6 +391,8 @@ def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EA
     c = None if m.oom else m.run()
     while c is not None:
         best, bkey = None, None
+        if search:
+            c = _searched(prog, m, c, search, seed)
         for x in c:
             s = m.clock - m.last[x]
             sz = prog.size[x]

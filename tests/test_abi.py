@@ -80,9 +80,7 @@ def test_validation_rejects_malformed_traces():
             "banishing is not defined for union-find heuristics")
     _expect(D.DTR_ETRACE, [good], W.make_specs([(0, W.h_family(W.C_EQCLASS, 0, 1), 4, 0, W.POLICY_BANISH)]),
             "banishing is not defined for union-find heuristics")
-    bad = W.make_specs([(0, W.H_LRU, 4, 0)])
-    bad["reserved"] = 1
-    _expect(D.DTR_ETRACE, [good], bad, "reserved word must be 0")
+    _expect(D.DTR_ETRACE, [good], W.make_specs([(0, W.H_LRU, 4, 0, 0, 4)]), "unknown search flags 4")
     _expect(D.DTR_ETRACE, [good], _spec(trace=1), "trace index 1 out of range")
     _expect(D.DTR_ETRACE, [good], _spec(b=-1), "negative budget")
 

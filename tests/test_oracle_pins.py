@@ -722,3 +722,80 @@ def test_policy_invariants(oracle_lib):
                         assert np.all(p["state"][req] == O.RESIDENT)
                         if policy == W.POLICY_IGNORE:
                             assert not np.any(p["state"] == O.BANISHED)
+
+
+# ------------------------------------------------- search approximations (f4) --
+
+def test_sample_stream_is_splitmix64(oracle_lib):
+    """The sampling draw is SplitMix64 on the seed xor 0xD6E8FEB86659FD93: with
+    that seed it is the golden sequence from state 0."""
+    O = oracle_lib
+    g = json.load(open(os.path.join(GOLDEN, "splitmix64_state0.json")))
+    for k, v in enumerate(g["outputs_from_state0"], start=1):
+        assert O.sample_key(0xD6E8FEB86659FD93, 0, k) == int(v, 16)
+
+
+def test_ignore_small_searches_exactly_the_large(oracle_lib):
+    """At each probed decision the searched candidates are the evictable
+    tensors with size >= 1% of the evictable mean (exact integer test)."""
+    O = oracle_lib
+    checked = 0
+    for seed in range(6):
+        tr = W.random_program(seed, n_ops=60, n_const=2, backward=True, max_size=400)
+        tr.tensor_size[::3] = 1            # plenty of tiny tensors
+        peak = W.natural_peak(tr)
+        for k in (0, 3, 9):
+            p = O.run_probe(tr, W.make_specs([(0, W.H_DTR, peak // 3, seed, W.POLICY_EAGER,
+                                              W.SEARCH_IGNORE_SMALL)])[0], stop_at_eviction=k)
+            if p["result"]["status"] != O.STATUS_STOPPED:
+                continue
+            const = (tr.tensor_flags & W.FLAG_CONSTANT) != 0
+            pool = (p["state"] == O.RESIDENT) & (p["locks"] == 0) & ~const
+            n0 = int(pool.sum())
+            total = int(tr.tensor_size[pool].sum())
+            big = pool & (100 * tr.tensor_size.astype(object) * n0 >= total)
+            assert np.array_equal(p["candidate"], big.astype(bool))
+            checked += 1
+    assert checked >= 8
+
+
+def test_sampling_keeps_about_sqrt_n(oracle_lib):
+    """Over many decisions the searched fraction is ceil(sqrt(n))/n (binomial
+    bounds, 6 sigma)."""
+    O = oracle_lib
+    tr = W.resnet_trace(seed=3, blocks=20)
+    peak = W.natural_peak(tr)
+    kept = expect = var = 0.0
+    for k in range(0, 150, 5):
+        p = O.run_probe(tr, W.make_specs([(0, W.H_LRU, peak // 4, 11, W.POLICY_EAGER, W.SEARCH_SAMPLE)])[0],
+                        stop_at_eviction=k)
+        if p["result"]["status"] != O.STATUS_STOPPED:
+            continue
+        const = (tr.tensor_flags & W.FLAG_CONSTANT) != 0
+        pool = (p["state"] == O.RESIDENT) & (p["locks"] == 0) & ~const
+        n = int(pool.sum())
+        s = math.isqrt(n - 1) + 1 if n > 0 else 0
+        if s >= n or not p["candidate"].any():
+            continue
+        assert not np.any(p["candidate"] & ~pool)
+        kept += int(p["candidate"].sum())
+        expect += s
+        var += n * (s / n) * (1 - s / n)
+    assert expect > 50
+    assert abs(kept - expect) <= 6 * math.sqrt(var)
+
+
+def test_search_approximations_match_independent_python_machine(oracle_lib):
+    O = oracle_lib
+    hs = [W.H_DTR, W.H_EQ, W.H_LRU, W.H_RAND, W.H_MSPS]
+    for seed in range(50):
+        tr = W.random_program(seed, n_ops=8 + seed % 14, n_const=seed % 3, backward=seed % 2 == 0,
+                              max_size=1 + (seed * 7) % 60)
+        peak = W.natural_peak(tr)
+        for search in (W.SEARCH_IGNORE_SMALL, W.SEARCH_SAMPLE, W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE):
+            for h in hs:
+                for b in sorted({max(1, peak // 3), max(1, 2 * peak // 3)}):
+                    r = O.run([tr], W.make_specs([(0, h, b, seed, W.POLICY_EAGER, search)]))[0]
+                    s = brute.simulate(tr, b, h, seed, search=search)
+                    for k, v in s.items():
+                        assert int(r[k]) == v, (seed, search, h, b, k)

@@ -115,6 +115,33 @@ def test_deallocation_policies(gpu, oracle_lib):
     compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "policies")
 
 
+def test_search_approximations(gpu, oracle_lib):
+    """Ignoring small candidates and sampling the pool, with every heuristic
+    class, on random programs and on the ResNet trace."""
+    traces = []
+    rows = []
+    hs = [W.H_DTR, W.H_EQ, W.H_LOCAL, W.H_LRU, W.H_RAND, W.H_MSPS]
+    flags = (W.SEARCH_IGNORE_SMALL, W.SEARCH_SAMPLE, W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE)
+    for s in range(30):
+        tr = W.random_program(1300 + s, n_ops=20 + (s * 17) % 120, n_const=s % 4, backward=s % 2 == 0,
+                              max_in=1 + s % 4, max_size=1 + (s * 13) % 200, max_cost=1 + s % 7)
+        traces.append(tr)
+        peak = W.natural_peak(tr)
+        for search in flags:
+            for h in hs:
+                for frac in (0.3, 0.6):
+                    rows.append((len(traces) - 1, h, max(1, int(peak * frac)), s * 53 + h, W.POLICY_EAGER, search))
+    rn = W.make_config("resnet50blk")
+    traces.append(rn.traces[0])
+    for search in flags:
+        for h in (W.H_DTR, W.H_EQ, W.H_LRU):
+            for k in range(0, 256, 32):
+                rows.append((len(traces) - 1, h, int(rn.specs["budget"][k]), 7 + k, W.POLICY_EAGER, search))
+    specs = specs_of(rows)
+    print(f"search batch: {len(traces)} traces, {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs), specs, "search")
+
+
 def test_empty_and_degenerate(gpu, oracle_lib):
     empty = W.Trace("empty", np.zeros(0, np.int64), np.zeros(0, np.uint8), np.zeros(0, np.int32),
                     np.zeros(0, np.int64), np.zeros(1, np.int64), np.zeros(0, np.int32))
