@@ -226,6 +226,11 @@ typedef struct {
     int64_t *uf_mark;             /* epoch stamps per UF node (root dedup) */
     int64_t uf_n, uf_cap;
 
+    /* log replay: residency generation per storage, generation at which each
+     * tensor's operator last ran (NULL for plain traces) */
+    int64_t *sgen, *gen;
+    const void *logp;             /* the lowered log (log replay only) */
+
     /* scratch for neighbourhood walks */
     int64_t *mark;                /* epoch stamps */
     int64_t epoch;
@@ -295,12 +300,15 @@ static int is_evictable(const sim *s, int32_t t)
            !(s->tr->tensor_flags[t] & O_FLAG_CONSTANT);
 }
 
+static void log_try_banish(sim *s, int32_t st);
+
 /* Banish t if none of its children is evicted and no operation in progress
  * holds it (Appendix C.4): its memory is reclaimed if resident, it leaves the
  * graph for good, and every resident child is pinned.  Otherwise t stays
  * pending and is retried when one of its children is rematerialized. */
 static void try_banish(sim *s, int32_t t)
 {
+    if (s->logp) { log_try_banish(s, t); return; }
     const graph *g = s->g;
     int blocked = s->locks[t] > 0;
     for (int64_t e = g->ch_off[t]; e < g->ch_off[t + 1] && !blocked; e++)
@@ -902,4 +910,605 @@ uint64_t oracle_rand_key(uint64_t seed, int64_t eviction_no, int32_t x)
 {
     uint64_t key = ((uint64_t)eviction_no << 32) + (uint64_t)(uint32_t)x;
     return splitmix64_mix(seed + 0x9E3779B97F4A7C15ull * key);
+}
+
+/* ============================================================ log replay ==
+ *
+ * Operator logs (Appendix C.6) lowered to storages, simulator tensors and
+ * operators (Appendix C.1), and the eviction loop over storages:
+ *   - CALL: an operator whose outputs are new tensors; an output described by
+ *     ALIAS to nothing owns a new storage of its MEMORY size, one aliased to a
+ *     name is a view (size 0) of that name's storage;
+ *   - MUTATE: a pure operator whose outputs are clones (new storages of the
+ *     same size) of the mutated inputs; the mutated names are rebound to the
+ *     clones (Appendix C.6 "Supporting mutation");
+ *   - CONSTANT: a nullary operator of cost 0 whose storage is pinned;
+ *   - COPY, COPYFROM, RELEASE: external reference counts; a storage whose
+ *     count drops to zero is released after the last operator issued;
+ *   - tensors still referenced at the end are the required outputs.
+ * A tensor is defined when its storage is resident and its operator ran after
+ * the storage last became resident.  An operator call locks its inputs'
+ * storages, defines undefined inputs in listed order (rematerialization),
+ * allocates all its non-view outputs, runs, frees the new copies of outputs
+ * that were already defined (Appendix C.4), and unlocks.  A storage's cost
+ * sums the operators computing any tensor that views it (each once) and its
+ * dependencies are the storages those operators read (Appendix C.2, over the
+ * views of the whole log); its staleness uses the latest reference to any of
+ * its tensors.  Banishing a released storage needs every tensor computed from
+ * it (outside it) defined or gone, and pins their resident storages.
+ * Scoring, eviction, union-find, deallocation policies and search
+ * approximations are the trace simulator's, run over storages.
+ */
+
+typedef struct {
+    int32_t n_instrs, n_names;
+    const int32_t *kind, *a, *b, *n_in;
+    const int64_t *value, *list_offsets;
+    const int32_t *ids;
+} oracle_log;
+
+enum { LG_MEMORY = 0, LG_ALIAS, LG_CALL, LG_MUTATE, LG_CONSTANT, LG_COPY, LG_COPYFROM, LG_RELEASE };
+
+typedef struct { int64_t n, cap; int64_t *v; } vec64;
+typedef struct { int64_t n, cap; int32_t *v; } vec32;
+
+static int v64_push(vec64 *x, int64_t e)
+{
+    if (x->n == x->cap) {
+        int64_t c = x->cap ? 2 * x->cap : 64;
+        int64_t *p = realloc(x->v, sizeof(int64_t) * (size_t)c);
+        if (!p) return -1;
+        x->v = p;
+        x->cap = c;
+    }
+    x->v[x->n++] = e;
+    return 0;
+}
+
+static int v32_push(vec32 *x, int32_t e)
+{
+    if (x->n == x->cap) {
+        int64_t c = x->cap ? 2 * x->cap : 64;
+        int32_t *p = realloc(x->v, sizeof(int32_t) * (size_t)c);
+        if (!p) return -1;
+        x->v = p;
+        x->cap = c;
+    }
+    x->v[x->n++] = e;
+    return 0;
+}
+
+typedef struct {
+    vec64 s_size, t_storage, t_op, t_alias, s_root, s_const, s_eref, t_eref;
+    vec64 op_cost, in_off, out_off, rel_off;
+    vec32 ins, outs, rel, req;
+    int64_t F;
+    /* storage-level metadata program: operator s produces storage s from its
+     * parent storages, at the cost of the root's operator */
+    oracle_trace meta;
+    int64_t *m_size, *m_cost, *m_in_off;
+    uint8_t *m_flags;
+    int32_t *m_out, *m_in;
+    int64_t *dt_off;              /* tensors computed from each storage (outside it) */
+    int32_t *dt;
+    graph g;
+    int built;
+} log_prog;
+
+static void log_prog_free(log_prog *L)
+{
+    vec64 *v64s[] = {&L->s_size, &L->t_storage, &L->t_op, &L->t_alias, &L->s_root, &L->s_const, &L->s_eref,
+                     &L->t_eref, &L->op_cost, &L->in_off, &L->out_off, &L->rel_off};
+    for (size_t i = 0; i < sizeof(v64s) / sizeof(v64s[0]); i++) free(v64s[i]->v);
+    free(L->ins.v); free(L->outs.v); free(L->rel.v); free(L->req.v);
+    free(L->m_size); free(L->m_cost); free(L->m_in_off); free(L->m_flags); free(L->m_out); free(L->m_in);
+    free(L->dt_off); free(L->dt);
+    if (L->built) graph_free(&L->g);
+    memset(L, 0, sizeof(*L));
+}
+
+/* external references: the storage released when its count reaches zero */
+static int lg_ref(log_prog *L, int64_t t, int d)
+{
+    int64_t st = L->t_storage.v[t];
+    L->t_eref.v[t] += d;
+    L->s_eref.v[st] += d;
+    if (L->t_eref.v[t] < 0 || L->s_eref.v[st] < 0) return -1;
+    if (d < 0 && L->s_eref.v[st] == 0) {
+        if (L->F == 0) return -1;
+        if (v32_push(&L->rel, (int32_t)st)) return -1;
+        L->rel_off.v[L->F]++;          /* counts per op, prefix-summed later */
+    }
+    return 0;
+}
+
+static int64_t lg_new_storage(log_prog *L, int64_t size, int constant, int64_t root)
+{
+    if (v64_push(&L->s_size, size) || v64_push(&L->s_const, constant) || v64_push(&L->s_root, root) ||
+        v64_push(&L->s_eref, 0))
+        return -1;
+    return L->s_size.n - 1;
+}
+
+static int64_t lg_new_tensor(log_prog *L, int64_t storage, int64_t op, int alias)
+{
+    if (v64_push(&L->t_storage, storage) || v64_push(&L->t_op, op) || v64_push(&L->t_alias, alias) ||
+        v64_push(&L->t_eref, 0))
+        return -1;
+    return L->t_storage.n - 1;
+}
+
+static int64_t lg_new_op(log_prog *L, int64_t cost)
+{
+    if (v64_push(&L->op_cost, cost) || v64_push(&L->rel_off, 0)) return -1;
+    L->F++;
+    return L->F - 1;
+}
+
+/* Lower a log; returns 0 or -2 on a malformed log. */
+static int log_lower(log_prog *L, const oracle_log *lg)
+{
+    memset(L, 0, sizeof(*L));
+    int32_t nn = lg->n_names > 0 ? lg->n_names : 1;
+    int64_t *name = malloc(sizeof(int64_t) * (size_t)nn);     /* name -> tensor, -1 unbound */
+    int64_t *local = malloc(sizeof(int64_t) * (size_t)nn);    /* names of one call's own storages */
+    if (!name || !local) { free(name); free(local); return -1; }
+    for (int32_t i = 0; i < nn; i++) name[i] = local[i] = -1;
+    int rc = 0;
+    if (v64_push(&L->rel_off, 0) || v64_push(&L->in_off, 0) || v64_push(&L->out_off, 0)) rc = -1;
+#define BAD_NAME(x) ((x) < 0 || (x) >= lg->n_names)
+    for (int32_t i = 0; i < lg->n_instrs && rc == 0;) {
+        int32_t k = lg->kind[i];
+        if (k == LG_CONSTANT) {
+            int32_t nm = lg->a[i];
+            if (i + 1 >= lg->n_instrs || lg->kind[i + 1] != LG_MEMORY || lg->a[i + 1] != nm || BAD_NAME(nm) ||
+                name[nm] >= 0 || lg->value[i + 1] < 1) { rc = -2; break; }
+            int64_t o = lg_new_op(L, 0);
+            int64_t t = lg_new_tensor(L, -1, o, 0);
+            int64_t st = lg_new_storage(L, lg->value[i + 1], 1, t);
+            if (o < 0 || t < 0 || st < 0 || v32_push(&L->outs, (int32_t)t)) { rc = -1; break; }
+            L->t_storage.v[t] = st;
+            if (v64_push(&L->in_off, L->ins.n) || v64_push(&L->out_off, L->outs.n)) { rc = -1; break; }
+            name[nm] = t;
+            if (lg_ref(L, t, +1)) { rc = -2; break; }
+            i += 2;
+        } else if (k == LG_CALL || k == LG_MUTATE) {
+            int64_t lo = lg->list_offsets[i], hi = lg->list_offsets[i + 1];
+            int32_t nin = lg->n_in[i];
+            int64_t nout = hi - lo - nin;
+            if (nin < 0 || nout < 0 || lg->value[i] < 1 || (k == LG_CALL && nout < 1)) { rc = -2; break; }
+            for (int64_t e = lo; e < lo + nin && rc == 0; e++) {
+                int32_t nm = lg->ids[e];
+                if (BAD_NAME(nm) || name[nm] < 0) rc = -2;
+            }
+            if (rc) break;
+            int64_t o = lg_new_op(L, lg->value[i]);
+            if (o < 0) { rc = -1; break; }
+            for (int64_t e = lo; e < lo + nin; e++)
+                if (v32_push(&L->ins, (int32_t)name[lg->ids[e]])) { rc = -1; break; }
+            if (rc) break;
+            if (k == LG_CALL) {
+                if (i + 2 * nout >= lg->n_instrs) { rc = -2; break; }
+                for (int64_t j = 0; j < nout && rc == 0; j++) {
+                    int32_t nm = lg->ids[lo + nin + j];
+                    int32_t mi = i + 1 + 2 * (int32_t)j, ai = mi + 1;
+                    if (BAD_NAME(nm) || name[nm] >= 0 || local[nm] >= 0 || lg->kind[mi] != LG_MEMORY ||
+                        lg->kind[ai] != LG_ALIAS || lg->a[mi] != nm || lg->a[ai] != nm) { rc = -2; break; }
+                    int32_t src = lg->b[ai];
+                    int64_t t;
+                    if (src < 0) {
+                        if (lg->value[mi] < 1) { rc = -2; break; }
+                        t = lg_new_tensor(L, -1, o, 0);
+                        int64_t st = lg_new_storage(L, lg->value[mi], 0, t);
+                        if (t < 0 || st < 0) { rc = -1; break; }
+                        L->t_storage.v[t] = st;
+                        local[nm] = t;
+                    } else {
+                        /* a view of an input's storage or of one of this call's own new storages */
+                        int64_t of = -1;
+                        if (!BAD_NAME(src) && local[src] >= 0) of = local[src];
+                        else if (!BAD_NAME(src) && name[src] >= 0) {
+                            for (int64_t e = lo; e < lo + nin; e++)
+                                if (lg->ids[e] == src) of = name[src];
+                        }
+                        if (of < 0) { rc = -2; break; }
+                        t = lg_new_tensor(L, L->t_storage.v[of], o, 1);
+                        if (t < 0) { rc = -1; break; }
+                    }
+                    if (v32_push(&L->outs, (int32_t)t)) { rc = -1; break; }
+                }
+                if (rc) break;
+                for (int64_t j = 0; j < nout; j++) {
+                    int32_t nm = lg->ids[lo + nin + j];
+                    local[nm] = -1;
+                    name[nm] = L->outs.v[L->outs.n - nout + j];
+                    if (lg_ref(L, name[nm], +1)) { rc = -2; break; }
+                }
+                i += 1 + 2 * (int32_t)nout;
+            } else {
+                /* MUTATE: the mutated inputs (a subset of the inputs) become clones */
+                int64_t first = L->outs.n;
+                for (int64_t j = 0; j < nout && rc == 0; j++) {
+                    int32_t nm = lg->ids[lo + nin + j];
+                    int found = 0;
+                    for (int64_t e = lo; e < lo + nin; e++) found |= lg->ids[e] == nm;
+                    for (int64_t q = lo + nin; q < lo + nin + j; q++) found &= lg->ids[q] != nm;
+                    if (!found) { rc = -2; break; }
+                    int64_t old = name[nm];
+                    int64_t t = lg_new_tensor(L, -1, o, 0);
+                    int64_t st = lg_new_storage(L, L->s_size.v[L->t_storage.v[old]], 0, t);
+                    if (t < 0 || st < 0 || v32_push(&L->outs, (int32_t)t)) { rc = -1; break; }
+                    L->t_storage.v[t] = st;
+                }
+                if (rc) break;
+                for (int64_t j = 0; j < nout && rc == 0; j++) {
+                    int32_t nm = lg->ids[lo + nin + j];
+                    int64_t old = name[nm];
+                    name[nm] = L->outs.v[first + j];
+                    if (lg_ref(L, name[nm], +1) || lg_ref(L, old, -1)) rc = -2;
+                }
+                i += 1;
+            }
+            if (rc == 0 && (v64_push(&L->in_off, L->ins.n) || v64_push(&L->out_off, L->outs.n))) rc = -1;
+        } else if (k == LG_COPY) {
+            int32_t to = lg->a[i], ti = lg->b[i];
+            if (BAD_NAME(to) || BAD_NAME(ti) || name[to] >= 0 || name[ti] < 0) { rc = -2; break; }
+            name[to] = name[ti];
+            if (lg_ref(L, name[ti], +1)) rc = -2;
+            i += 1;
+        } else if (k == LG_COPYFROM) {
+            int32_t to = lg->a[i], ti = lg->b[i];
+            if (BAD_NAME(to) || BAD_NAME(ti) || name[to] < 0 || name[ti] < 0) { rc = -2; break; }
+            int64_t old = name[to];
+            name[to] = name[ti];
+            if (lg_ref(L, name[ti], +1) || lg_ref(L, old, -1)) rc = -2;
+            i += 1;
+        } else if (k == LG_RELEASE) {
+            int32_t nm = lg->a[i];
+            if (BAD_NAME(nm) || name[nm] < 0) { rc = -2; break; }
+            int64_t old = name[nm];
+            name[nm] = -1;
+            if (lg_ref(L, old, -1)) rc = -2;
+            i += 1;
+        } else {
+            rc = -2;
+        }
+    }
+#undef BAD_NAME
+    free(name);
+    free(local);
+    if (rc) { log_prog_free(L); return rc; }
+    /* release lists: counts per op -> offsets (events stay in log order) */
+    for (int64_t o = 0; o < L->F; o++) L->rel_off.v[o + 1] += L->rel_off.v[o];
+    for (int64_t t = 0; t < L->t_storage.n; t++)
+        if (L->t_eref.v[t] > 0 && v32_push(&L->req, (int32_t)t)) { log_prog_free(L); return -1; }
+    /* storage metadata program: tensors grouped by storage, then per storage
+     * the distinct operators of its tensors, their cost and input storages */
+    int64_t S = L->s_size.n, T = L->t_storage.n, F = L->F;
+    size_t sn = (size_t)(S > 0 ? S : 1);
+    int64_t *tb_off = calloc(sn + 1, sizeof(int64_t));
+    int32_t *tb = malloc(sizeof(int32_t) * (size_t)(T > 0 ? T : 1));
+    int64_t *seen_op = malloc(sizeof(int64_t) * (size_t)(F > 0 ? F : 1));
+    int64_t *seen_st = malloc(sizeof(int64_t) * sn);
+    L->m_size = malloc(sizeof(int64_t) * sn);
+    L->m_cost = malloc(sizeof(int64_t) * sn);
+    L->m_flags = calloc(sn, 1);
+    L->m_out = malloc(sizeof(int32_t) * sn);
+    L->m_in_off = calloc(sn + 1, sizeof(int64_t));
+    L->dt_off = calloc(sn + 1, sizeof(int64_t));
+    /* a storage's parents come from the operators of its tensors: at most
+     * inputs x outputs over all operators */
+    int64_t pbound = 1;
+    for (int64_t o = 0; o < F; o++)
+        pbound += (L->in_off.v[o + 1] - L->in_off.v[o]) * (L->out_off.v[o + 1] - L->out_off.v[o]);
+    L->m_in = malloc(sizeof(int32_t) * (size_t)pbound);
+    L->dt = malloc(sizeof(int32_t) * (size_t)pbound);
+    if (!tb_off || !tb || !seen_op || !seen_st || !L->m_size || !L->m_cost || !L->m_flags || !L->m_out ||
+        !L->m_in_off || !L->dt_off || !L->m_in || !L->dt) {
+        free(tb_off); free(tb); free(seen_op); free(seen_st);
+        log_prog_free(L);
+        return -1;
+    }
+    for (int64_t t = 0; t < T; t++) tb_off[L->t_storage.v[t] + 1]++;
+    for (int64_t st = 0; st < S; st++) tb_off[st + 1] += tb_off[st];
+    {
+        int64_t *fill = malloc(sizeof(int64_t) * sn);
+        if (!fill) { free(tb_off); free(tb); free(seen_op); free(seen_st); log_prog_free(L); return -1; }
+        for (int64_t st = 0; st < S; st++) fill[st] = tb_off[st];
+        for (int64_t t = 0; t < T; t++) tb[fill[L->t_storage.v[t]]++] = (int32_t)t;
+        free(fill);
+    }
+    for (int64_t o = 0; o < F; o++) seen_op[o] = -1;
+    for (int64_t st = 0; st < S; st++) seen_st[st] = -1;
+    int64_t w = 0;
+    for (int64_t st = 0; st < S; st++) {
+        L->m_size[st] = L->s_size.v[st];
+        L->m_flags[st] = L->s_const.v[st] ? O_FLAG_CONSTANT : 0;
+        L->m_out[st] = (int32_t)st;
+        int64_t cost = 0;
+        seen_st[st] = st;                       /* never its own parent */
+        for (int64_t q = tb_off[st]; q < tb_off[st + 1]; q++) {
+            int64_t o = L->t_op.v[tb[q]];
+            if (seen_op[o] == st) continue;
+            seen_op[o] = st;
+            cost += L->op_cost.v[o];
+            for (int64_t e = L->in_off.v[o]; e < L->in_off.v[o + 1]; e++) {
+                int64_t p = L->t_storage.v[L->ins.v[e]];
+                if (seen_st[p] == st) continue;
+                seen_st[p] = st;
+                L->m_in[w++] = (int32_t)p;
+            }
+        }
+        L->m_cost[st] = L->s_const.v[st] ? 1 : cost;
+        L->m_in_off[st + 1] = w;
+    }
+    free(tb_off); free(tb); free(seen_op); free(seen_st);
+    /* tensors computed from each storage: outputs (of another storage) of
+     * operators reading it; a pair repeats only within one operator, so the
+     * operator's input storages are deduplicated first */
+    {
+        int64_t n_dt = 0;
+        int64_t *cnt = calloc(sn + 1, sizeof(int64_t));
+        int64_t *ps = malloc(sizeof(int64_t) * (size_t)pbound);
+        int32_t *pt = malloc(sizeof(int32_t) * (size_t)pbound);
+        int64_t *uniq = malloc(sizeof(int64_t) * (size_t)(L->ins.n > 0 ? L->ins.n : 1));
+        if (!cnt || !ps || !pt || !uniq) { free(cnt); free(ps); free(pt); free(uniq); log_prog_free(L); return -1; }
+        for (int64_t o = 0; o < F; o++) {
+            int64_t nu = 0;
+            for (int64_t e = L->in_off.v[o]; e < L->in_off.v[o + 1]; e++) {
+                int64_t p = L->t_storage.v[L->ins.v[e]];
+                int dup = 0;
+                for (int64_t z = 0; z < nu && !dup; z++) dup = uniq[z] == p;
+                if (!dup) uniq[nu++] = p;
+            }
+            for (int64_t z = 0; z < nu; z++)
+                for (int64_t q = L->out_off.v[o]; q < L->out_off.v[o + 1]; q++) {
+                    int32_t v = L->outs.v[q];
+                    if (L->t_storage.v[v] == uniq[z]) continue;
+                    ps[n_dt] = uniq[z];
+                    pt[n_dt++] = v;
+                    cnt[uniq[z] + 1]++;
+                }
+        }
+        for (int64_t st = 0; st < S; st++) cnt[st + 1] += cnt[st];
+        for (int64_t st = 0; st <= S; st++) L->dt_off[st] = cnt[st];
+        for (int64_t z = 0; z < n_dt; z++) L->dt[cnt[ps[z]]++] = pt[z];
+        free(cnt); free(ps); free(pt); free(uniq);
+    }
+    L->meta.n_tensors = (int32_t)S;
+    L->meta.n_ops = (int32_t)S;
+    L->meta.tensor_size = L->m_size;
+    L->meta.tensor_flags = L->m_flags;
+    L->meta.op_output = L->m_out;
+    L->meta.op_cost = L->m_cost;
+    L->meta.op_input_offsets = L->m_in_off;
+    L->meta.op_inputs = L->m_in;
+    if (graph_build(&L->g, &L->meta)) { log_prog_free(L); return -1; }
+    L->built = 1;
+    /* a constant storage has no parent operation and costs nothing */
+    for (int64_t st = 0; st < S; st++)
+        if (L->s_const.v[st]) { L->g.producer[st] = -1; L->g.c0[st] = 0; }
+    return 0;
+}
+
+static int log_defined(const sim *s, const log_prog *L, int64_t t)
+{
+    int64_t st = L->t_storage.v[t];
+    return s->state[st] == ST_RESIDENT && s->gen[t] == s->sgen[st];
+}
+
+/* Banishing over storages: st must be unheld, and every tensor computed from
+ * it (outside it) defined or gone; the resident storages of those tensors are
+ * pinned.  Otherwise st stays pending. */
+static void log_try_banish(sim *s, int32_t st)
+{
+    const log_prog *L = s->logp;
+    int blocked = s->locks[st] > 0;
+    for (int64_t e = L->dt_off[st]; e < L->dt_off[st + 1] && !blocked; e++) {
+        int32_t v = L->dt[e];
+        blocked = !log_defined(s, L, v) && s->state[L->t_storage.v[v]] != ST_BANISHED;
+    }
+    if (blocked) { s->pending[st] = 1; return; }
+    s->pending[st] = 0;
+    if (s->state[st] == ST_RESIDENT) s->memory -= L->s_size.v[st];
+    s->state[st] = ST_BANISHED;
+    s->r[R_EAGER]++;
+    for (int64_t e = L->dt_off[st]; e < L->dt_off[st + 1]; e++) {
+        int64_t d = L->t_storage.v[L->dt[e]];
+        if (s->state[d] == ST_RESIDENT) s->pinned[d] = 1;
+    }
+}
+
+/* run operator o (a rematerialization if remat), defining its outputs */
+static void log_call(sim *s, const log_prog *L, int64_t o, int remat)
+{
+    const int64_t ib = L->in_off.v[o], ie = L->in_off.v[o + 1];
+    const int64_t ob = L->out_off.v[o], oe = L->out_off.v[o + 1];
+    for (int64_t e = ib; e < ie; e++) lock(s, (int32_t)L->t_storage.v[L->ins.v[e]]);
+    for (int64_t e = ib; e < ie; e++) {
+        int32_t u = L->ins.v[e];
+        if (!log_defined(s, L, u)) {
+            log_call(s, L, L->t_op.v[u], 1);
+            if (s->stopped) return;
+        }
+    }
+    int64_t need = 0;
+    for (int64_t e = ob; e < oe; e++)
+        if (!L->t_alias.v[L->outs.v[e]]) need += L->s_size.v[L->t_storage.v[L->outs.v[e]]];
+    allocate(s, need);
+    if (s->stopped) return;
+    for (int64_t e = ib; e < ie; e++) s->last_access[L->t_storage.v[L->ins.v[e]]] = s->clock;
+    for (int64_t e = ob; e < oe; e++) s->last_access[L->t_storage.v[L->outs.v[e]]] = s->clock;
+    int64_t c = L->op_cost.v[o];
+    s->clock += c;
+    s->r[R_TOTAL_COST] += c;
+    s->r[R_EXECUTED]++;
+    if (remat) { s->r[R_REMATS]++; s->r[R_REMAT_COST] += c; }
+    else s->r[R_BASE_COST] += c;
+    s->memory += need;
+    if (s->memory > s->peak) s->peak = s->memory;
+    for (int64_t e = ob; e < oe; e++) {
+        int32_t v = L->outs.v[e];
+        if (L->t_alias.v[v]) continue;
+        int32_t st = (int32_t)L->t_storage.v[v];
+        if (s->state[st] == ST_RESIDENT) { s->memory -= L->s_size.v[st]; continue; }   /* copy of a defined output */
+        int was_evicted = s->state[st] == ST_EVICTED;
+        s->state[st] = ST_RESIDENT;
+        s->gen[v] = ++s->sgen[st];
+        if (uses_uf(s->heuristic)) {
+            if (was_evicted) {
+                int32_t r = uf_find(s, s->node_of[st]);
+                s->uf_cost[r] -= s->g->c0[st];
+            }
+            int32_t nd = uf_new(s);
+            if (nd < 0) abort();
+            s->node_of[st] = nd;
+        }
+    }
+    for (int64_t e = ob; e < oe; e++) {
+        int32_t v = L->outs.v[e];
+        if (L->t_alias.v[v]) s->gen[v] = s->sgen[L->t_storage.v[v]];
+    }
+    if (s->clock >= CLOCK_LIMIT) { s->r[R_STATUS] = OS_CLOCK_OVERFLOW; s->stopped = OS_CLOCK_OVERFLOW; return; }
+    for (int64_t e = ib; e < ie; e++) unlock(s, (int32_t)L->t_storage.v[L->ins.v[e]]);
+    if (remat && s->policy == OP_BANISH)
+        for (int64_t e = ib; e < ie; e++) {
+            int32_t st = (int32_t)L->t_storage.v[L->ins.v[e]];
+            if (s->pending[st]) try_banish(s, st);
+        }
+}
+
+static void log_run(sim *s, const log_prog *L)
+{
+    s->r[R_FAILED_OP] = -1;
+    for (int64_t o = 0; o < L->F; o++) {
+        s->cur_op = o;
+        log_call(s, L, o, 0);
+        if (s->stopped) goto done;
+        for (int64_t e = L->rel_off.v[o]; e < L->rel_off.v[o + 1]; e++) release(s, L->rel.v[e]);
+    }
+    s->cur_op = L->F;
+    for (int64_t k = 0; k < L->req.n; k++) {
+        int32_t t = L->req.v[k];
+        lock(s, (int32_t)L->t_storage.v[t]);
+        if (!log_defined(s, L, t)) {
+            log_call(s, L, L->t_op.v[t], 1);
+            if (s->stopped) goto done;
+        }
+    }
+done:
+    if (s->stopped == OS_OOM || s->stopped == OS_CLOCK_OVERFLOW) s->r[R_FAILED_OP] = s->cur_op;
+    s->r[R_PEAK] = s->peak;
+    s->r[R_FINAL_MEM] = s->memory;
+}
+
+static int run_one_log(const log_prog *L, const oracle_spec *sp, int64_t *result)
+{
+    int64_t S = L->s_size.n, T = L->t_storage.n;
+    sim s;
+    memset(&s, 0, sizeof(s));
+    s.g = &L->g;
+    s.tr = &L->meta;
+    s.logp = L;
+    s.heuristic = sp->heuristic;
+    s.policy = sp->policy;
+    s.search = sp->search;
+    s.budget = sp->budget;
+    s.seed = sp->seed;
+    size_t sn = (size_t)(S > 0 ? S : 1), tn = (size_t)(T > 0 ? T : 1);
+    s.state = calloc(sn, 1);
+    s.pinned = calloc(sn, 1);
+    s.pending = calloc(sn, 1);
+    s.locks = calloc(sn, sizeof(int32_t));
+    s.last_access = calloc(sn, sizeof(int64_t));
+    s.node_of = malloc(sizeof(int32_t) * sn);
+    s.queue = malloc(sizeof(int32_t) * sn);
+    s.mark = calloc(sn, sizeof(int64_t));
+    s.sgen = calloc(sn, sizeof(int64_t));
+    s.gen = malloc(sizeof(int64_t) * tn);
+    int rc = 0;
+    if (!s.state || !s.pinned || !s.pending || !s.locks || !s.last_access || !s.node_of || !s.queue || !s.mark ||
+        !s.sgen || !s.gen)
+        rc = -1;
+    else {
+        for (int64_t i = 0; i < S; i++) s.node_of[i] = -1;
+        for (int64_t i = 0; i < T; i++) s.gen[i] = -1;
+        for (int64_t i = 0; i < S; i++) s.pinned[i] = (uint8_t)L->s_const.v[i];
+        log_run(&s, L);
+        for (int i = 0; i < R_NFIELDS; i++) result[i] = s.r[i];
+    }
+    free(s.state); free(s.pinned); free(s.pending); free(s.locks); free(s.last_access); free(s.node_of);
+    free(s.queue); free(s.mark); free(s.sgen); free(s.gen);
+    free(s.uf_parent); free(s.uf_cost); free(s.uf_mark);
+    return rc;
+}
+
+typedef struct {
+    const log_prog *progs;
+    const oracle_spec *specs;
+    int64_t *results;
+    int32_t n_sims, next;
+    pthread_mutex_t mu;
+    int rc;
+} log_batch;
+
+static void *log_worker(void *arg)
+{
+    log_batch *b = arg;
+    for (;;) {
+        pthread_mutex_lock(&b->mu);
+        int32_t i = b->next++;
+        pthread_mutex_unlock(&b->mu);
+        if (i >= b->n_sims) break;
+        int rc = run_one_log(&b->progs[b->specs[i].trace], &b->specs[i], b->results + (int64_t)i * R_NFIELDS);
+        if (rc) { pthread_mutex_lock(&b->mu); b->rc = rc; pthread_mutex_unlock(&b->mu); }
+    }
+    return NULL;
+}
+
+/* Replay n_sims simulations over n_logs operator logs on n_threads threads.
+ * Returns 0, -1 on allocation failure, -2 on a bad argument or a malformed
+ * log. */
+int oracle_run_log(const oracle_log *logs, int32_t n_logs, const oracle_spec *specs, int32_t n_sims,
+                   int64_t *results, int32_t n_threads)
+{
+    if (n_logs < 0 || n_sims < 0) return -2;
+    for (int32_t i = 0; i < n_sims; i++)
+        if (specs[i].trace < 0 || specs[i].trace >= n_logs ||
+            !((specs[i].heuristic >= 0 && specs[i].heuristic <= OH_MSPS) || family(specs[i].heuristic)) ||
+            specs[i].policy < OP_EAGER || specs[i].policy > OP_BANISH ||
+            specs[i].search < 0 || specs[i].search > (OSR_IGNORE_SMALL | OSR_SAMPLE) ||
+            (specs[i].policy == OP_BANISH && uses_uf(specs[i].heuristic)))
+            return -2;
+    log_prog *progs = calloc((size_t)(n_logs > 0 ? n_logs : 1), sizeof(log_prog));
+    if (!progs) return -1;
+    int rc = 0;
+    int32_t built = 0;
+    for (; built < n_logs; built++)
+        if ((rc = log_lower(&progs[built], &logs[built])) != 0) break;
+    if (rc == 0) {
+        log_batch b;
+        memset(&b, 0, sizeof(b));
+        b.progs = progs; b.specs = specs; b.results = results; b.n_sims = n_sims;
+        pthread_mutex_init(&b.mu, NULL);
+        if (n_threads < 1) n_threads = 1;
+        if (n_threads > n_sims) n_threads = n_sims > 0 ? n_sims : 1;
+        pthread_t *th = calloc((size_t)n_threads, sizeof(pthread_t));
+        pthread_attr_t attr;
+        pthread_attr_init(&attr);
+        pthread_attr_setstacksize(&attr, WORKER_STACK);
+        int started = 0;
+        if (th)
+            for (; started < n_threads; started++)
+                if (pthread_create(&th[started], &attr, log_worker, &b)) break;
+        if (started == 0) log_worker(&b);
+        for (int k = 0; k < started; k++) pthread_join(th[k], NULL);
+        pthread_attr_destroy(&attr);
+        free(th);
+        pthread_mutex_destroy(&b.mu);
+        rc = b.rc;
+    }
+    for (int32_t i = 0; i < built; i++) log_prog_free(&progs[i]);
+    free(progs);
+    return rc;
 }

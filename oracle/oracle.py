@@ -107,6 +107,37 @@ def run(traces, specs, threads: int | None = None) -> np.ndarray:
     return out
 
 
+class _Log(C.Structure):
+    _fields_ = [("n_instrs", C.c_int32), ("n_names", C.c_int32), ("kind", C.c_void_p), ("a", C.c_void_p),
+                ("b", C.c_void_p), ("n_in", C.c_void_p), ("value", C.c_void_p), ("list_offsets", C.c_void_p),
+                ("ids", C.c_void_p)]
+
+
+def run_log(logs, specs, threads: int | None = None) -> np.ndarray:
+    """Replay operator logs (the spec's trace field indexes ``logs``); one
+    RESULT_DTYPE row per simulation."""
+    specs = np.ascontiguousarray(specs)
+    arr = (_Log * max(1, len(logs)))()
+    keep = []
+    for i, g in enumerate(logs):
+        cols = [np.ascontiguousarray(g.kind, np.int32), np.ascontiguousarray(g.a, np.int32),
+                np.ascontiguousarray(g.b, np.int32), np.ascontiguousarray(g.n_in, np.int32),
+                np.ascontiguousarray(g.value, np.int64), np.ascontiguousarray(g.list_offsets, np.int64),
+                np.ascontiguousarray(g.ids, np.int32)]
+        keep.extend(cols)
+        arr[i] = _Log(g.n_instrs, g.n_names, *[c.ctypes.data for c in cols])
+    out = np.zeros(len(specs), dtype=RESULT_DTYPE)
+    threads = threads or os.cpu_count() or 1
+    L = lib()
+    L.oracle_run_log.argtypes = [C.c_void_p, C.c_int32, C.c_void_p, C.c_int32, C.c_void_p, C.c_int32]
+    L.oracle_run_log.restype = C.c_int
+    rc = L.oracle_run_log(C.addressof(arr), len(logs), _ptr(specs), len(specs), _ptr(out), int(threads))
+    del keep
+    if rc != 0:
+        raise RuntimeError(f"oracle_run_log failed with {rc}")
+    return out
+
+
 def run_probe(trace, spec, stop_after_op: int = -1, stop_at_eviction: int = -1,
               log_cap: int = 1 << 20) -> dict:
     """One simulation with the test probes: state at a stop point, every

@@ -541,3 +541,182 @@ CONFIGS = {
 
 def make_config(name: str, **kw) -> Workload:
     return CONFIGS[name](**kw)
+
+
+# ----------------------------------------------------------------------------
+# operator logs (Appendix C.6 log format): storages, views, multi-output and
+# in-place operators, explicit reference counting
+# ----------------------------------------------------------------------------
+
+LOG_MEMORY, LOG_ALIAS, LOG_CALL, LOG_MUTATE, LOG_CONSTANT, LOG_COPY, LOG_COPYFROM, LOG_RELEASE = range(8)
+LOG_KIND_NAMES = ["MEMORY", "ALIAS", "CALL", "MUTATE", "CONSTANT", "COPY", "COPYFROM", "RELEASE"]
+
+
+@dataclass
+class Log:
+    """A log as parallel arrays, one row per instruction.  Names are integers.
+      MEMORY   a = name, value = size          ALIAS    a = name, b = viewed name or -1
+      CALL     ids = inputs then outputs (n_in inputs), value = cost; each output
+               is then described by MEMORY and ALIAS, in output order
+      MUTATE   ids = inputs then mutated inputs (n_in inputs), value = cost
+      CONSTANT a = name (then MEMORY)           COPY     a = new name, b = name
+      COPYFROM a = name, b = name               RELEASE  a = name"""
+    name: str
+    kind: np.ndarray              # int32 [n]
+    a: np.ndarray                 # int32 [n]
+    b: np.ndarray                 # int32 [n]
+    n_in: np.ndarray              # int32 [n]
+    value: np.ndarray             # int64 [n]
+    list_offsets: np.ndarray      # int64 [n + 1]
+    ids: np.ndarray               # int32 [list_offsets[n]]
+    n_names: int = 0
+    meta: dict = field(default_factory=dict)
+
+    @property
+    def n_instrs(self) -> int:
+        return int(self.kind.shape[0])
+
+    def lists(self, i: int):
+        lo, hi = int(self.list_offsets[i]), int(self.list_offsets[i + 1])
+        k = int(self.n_in[i])
+        return self.ids[lo:lo + k], self.ids[lo + k:hi]
+
+    def digest(self) -> str:
+        h = hashlib.sha256()
+        for arr in (self.kind, self.a, self.b, self.n_in, self.value, self.list_offsets, self.ids):
+            h.update(np.ascontiguousarray(arr).tobytes())
+        return h.hexdigest()
+
+
+class LogBuilder:
+    def __init__(self, name: str):
+        self.name = name
+        self.rows = []            # (kind, a, b, n_in, value, ids)
+        self.next_name = 0
+
+    def fresh(self) -> int:
+        self.next_name += 1
+        return self.next_name - 1
+
+    def _row(self, kind, a=-1, b=-1, value=0, ins=(), outs=()):
+        self.rows.append((kind, a, b, len(ins), value, list(ins) + list(outs)))
+
+    def constant(self, t, size):
+        self._row(LOG_CONSTANT, a=t)
+        self._row(LOG_MEMORY, a=t, value=size)
+
+    def call(self, ins, outs, cost, sizes, aliases):
+        """outs[k] has MEMORY sizes[k] and ALIAS aliases[k] (a name or -1)."""
+        self._row(LOG_CALL, value=cost, ins=ins, outs=outs)
+        for o, sz, al in zip(outs, sizes, aliases):
+            self._row(LOG_MEMORY, a=o, value=sz)
+            self._row(LOG_ALIAS, a=o, b=al)
+
+    def mutate(self, ins, muts, cost):
+        self._row(LOG_MUTATE, value=cost, ins=ins, outs=muts)
+
+    def copy(self, to, ti):
+        self._row(LOG_COPY, a=to, b=ti)
+
+    def copyfrom(self, to, ti):
+        self._row(LOG_COPYFROM, a=to, b=ti)
+
+    def release(self, t):
+        self._row(LOG_RELEASE, a=t)
+
+    def build(self, **meta) -> Log:
+        n = len(self.rows)
+        lens = [len(r[5]) for r in self.rows]
+        off = np.zeros(n + 1, np.int64)
+        off[1:] = np.cumsum(lens)
+        ids = np.array([v for r in self.rows for v in r[5]], np.int32)
+        return Log(self.name, np.array([r[0] for r in self.rows], np.int32),
+                   np.array([r[1] for r in self.rows], np.int32), np.array([r[2] for r in self.rows], np.int32),
+                   np.array([r[3] for r in self.rows], np.int32), np.array([r[4] for r in self.rows], np.int64),
+                   off, ids, self.next_name, dict(meta))
+
+
+def log_from_trace(tr: Trace) -> Log:
+    """The trace as a log: constants first (CONSTANT, MEMORY), then one CALL per
+    operation creating a fresh storage, and a RELEASE after the last reader of
+    every tensor that is not a required output (after its producer if nothing
+    reads it; constants that nothing reads are never released).  Names are the
+    trace's tensor ids."""
+    n, F = tr.n_tensors, tr.n_ops
+    b = LogBuilder(tr.name + "-log")
+    b.next_name = n
+    last = np.full(n, -1, np.int64)
+    prod = np.full(n, -1, np.int64)
+    prod[tr.op_output] = np.arange(F)
+    for o in range(F):
+        for u in tr.inputs(o):
+            last[u] = max(last[u], o)
+    last = np.maximum(last, prod)
+    rel = [[] for _ in range(F)]
+    for t in range(n):
+        if not (tr.tensor_flags[t] & FLAG_REQUIRED) and last[t] >= 0:
+            rel[last[t]].append(t)
+    for t in range(n):
+        if tr.tensor_flags[t] & FLAG_CONSTANT:
+            b.constant(t, int(tr.tensor_size[t]))
+    for o in range(F):
+        t = int(tr.op_output[o])
+        b.call([int(u) for u in tr.inputs(o)], [t], int(tr.op_cost[o]), [int(tr.tensor_size[t])], [-1])
+        for r in rel[o]:
+            b.release(r)
+    return b.build()
+
+
+def random_log(seed: int, n_steps: int, n_const: int = 3, max_size: int = 8, max_cost: int = 5,
+               max_in: int = 3, keep: int = 2) -> Log:
+    """A PyTorch-like random log: constants; operator calls whose outputs are
+    fresh storages or views of an input (or of an earlier output of the same
+    call), with 1-3 outputs; in-place operators; variable copies and
+    rebindings; releases of dead variables.  At the end every name but `keep`
+    of them is released, so those stay live (the output condition)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    b = LogBuilder(f"randlog{seed}")
+    live = []
+    for _ in range(n_const):
+        t = b.fresh()
+        b.constant(t, int(rng.integers(1, max_size + 1)))
+        live.append(t)
+    for _ in range(n_steps):
+        r = rng.random()
+        if not live or r < 0.5:
+            k = int(rng.integers(0, min(max_in, len(live)) + 1))
+            ins = [live[int(i)] for i in rng.choice(len(live), size=k, replace=False)] if k else []
+            n_out = 1 if rng.random() < 0.75 else int(rng.integers(2, 4))
+            outs, sizes, aliases, roots = [], [], [], []
+            for j in range(n_out):
+                o = b.fresh()
+                view = (ins or roots) and rng.random() < 0.3
+                if view:
+                    pool = ins + roots
+                    aliases.append(pool[int(rng.integers(0, len(pool)))])
+                else:
+                    aliases.append(-1)
+                    roots.append(o)
+                outs.append(o)
+                sizes.append(int(rng.integers(1, max_size + 1)))
+            cost = 1 if all(a >= 0 for a in aliases) else int(rng.integers(1, max_cost + 1))
+            b.call(ins, outs, cost, sizes, aliases)
+            live += outs
+        elif r < 0.62:
+            k = int(rng.integers(1, min(max_in, len(live)) + 1))
+            ins = [live[int(i)] for i in rng.choice(len(live), size=k, replace=False)]
+            b.mutate(ins, [ins[0]], int(rng.integers(1, max_cost + 1)))
+        elif r < 0.68:
+            to = b.fresh()
+            b.copy(to, live[int(rng.integers(0, len(live)))])
+            live.append(to)
+        elif r < 0.72 and len(live) >= 2:
+            i, j = rng.choice(len(live), size=2, replace=False)
+            b.copyfrom(live[int(i)], live[int(j)])
+        else:
+            i = int(rng.integers(0, len(live)))
+            b.release(live.pop(i))
+    order = rng.permutation(len(live))
+    for i in order[keep:]:
+        b.release(live[int(i)])
+    return b.build(seed=seed)

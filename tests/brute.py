@@ -394,35 +394,7 @@ def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EA
         if search:
             c = _searched(prog, m, c, search, seed)
         for x in c:
-            s = m.clock - m.last[x]
-            sz = prog.size[x]
-            if heuristic in (0, 6):
-                num = prog.c0[x] + sum(prog.c0[u] for u in evicted_closure(prog, m.state, x))
-                key = Fraction(num, sz * s) if heuristic == 0 else Fraction(num, sz)
-            elif heuristic == 1:
-                key = Fraction(prog.c0[x] + m.uf.neighbourhood_cost(x, m), sz * s)
-            elif heuristic == 2:
-                key = Fraction(prog.c0[x], sz * s)
-            elif heuristic == 3:
-                key = Fraction(1, s)
-            elif heuristic == 4:
-                key = Fraction(1, sz)
-            elif heuristic == 5:
-                key = _mix64((seed + 0x9E3779B97F4A7C15 * ((m.evict_no << 32) + x)) & MASK64)
-            elif heuristic == 7:
-                key = Fraction(prog.c0[x] + sum(prog.c0[u] for u in evicted_ancestors(prog, m.state, x)), sz)
-            elif fam:
-                if fc == 0:
-                    num = prog.c0[x] + sum(prog.c0[u] for u in evicted_closure(prog, m.state, x))
-                elif fc == 1:
-                    num = prog.c0[x] + m.uf.neighbourhood_cost(x, m)
-                elif fc == 2:
-                    num = prog.c0[x]
-                else:
-                    num = 1
-                key = Fraction(num, (sz if fm else 1) * (s if fs else 1))
-            else:
-                raise ValueError(heuristic)
+            key = score_key(prog, m, x, heuristic, seed, m.clock - m.last[x])
             if bkey is None or key < bkey or (key == bkey and x < best):
                 best, bkey = x, key
         m.n_scores += len(c)
@@ -433,3 +405,37 @@ def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EA
                 peak_memory=m.peak, final_memory=m.mem, n_executed_ops=m.n_exec,
                 n_remats=m.n_remat, n_evictions=m.n_evict, n_eager_evictions=m.n_eager,
                 n_scores=m.n_scores, status=status)
+
+
+def score_key(prog, m, x, heuristic, seed, s):
+    """Exact score of candidate x (a Fraction, or an int for h_rand) given its
+    staleness s; prog supplies size, c0, parents and children, m the state,
+    the union-find and the eviction number."""
+    sz = prog.size[x]
+    if heuristic in (0, 6):
+        num = prog.c0[x] + sum(prog.c0[u] for u in evicted_closure(prog, m.state, x))
+        return Fraction(num, sz * s) if heuristic == 0 else Fraction(num, sz)
+    if heuristic == 1:
+        return Fraction(prog.c0[x] + m.uf.neighbourhood_cost(x, m), sz * s)
+    if heuristic == 2:
+        return Fraction(prog.c0[x], sz * s)
+    if heuristic == 3:
+        return Fraction(1, s)
+    if heuristic == 4:
+        return Fraction(1, sz)
+    if heuristic == 5:
+        return _mix64((seed + 0x9E3779B97F4A7C15 * ((m.evict_no << 32) + x)) & MASK64)
+    if heuristic == 7:
+        return Fraction(prog.c0[x] + sum(prog.c0[u] for u in evicted_ancestors(prog, m.state, x)), sz)
+    if heuristic < 16:
+        raise ValueError(heuristic)
+    fc, fs, fm = (heuristic - 16) >> 2, ((heuristic - 16) >> 1) & 1, (heuristic - 16) & 1
+    if fc == 0:
+        num = prog.c0[x] + sum(prog.c0[u] for u in evicted_closure(prog, m.state, x))
+    elif fc == 1:
+        num = prog.c0[x] + m.uf.neighbourhood_cost(x, m)
+    elif fc == 2:
+        num = prog.c0[x]
+    else:
+        num = 1
+    return Fraction(num, (sz if fm else 1) * (s if fs else 1))
