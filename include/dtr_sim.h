@@ -193,6 +193,74 @@ int dtr_sim_run(dtr_sim *sim, void *stream);
  * the stream of the last run.  DTR_ESTATE if no run was enqueued. */
 int dtr_sim_results(dtr_sim *sim, dtr_sim_result *host_out, int32_t n_sims);
 
+/* ---- operator logs (Appendix C.6) ------------------------------------------
+ * A log is a sequence of instructions over integer names 0..n_names-1, as
+ * parallel arrays (one entry per instruction):
+ *   DTR_LOG_MEMORY    a = name, value = size in bytes (ignored for a view)
+ *   DTR_LOG_ALIAS     a = name, b = the name it views, or -1 for a new storage
+ *   DTR_LOG_CALL      ids[list_offsets[i] ..] = n_in input names, then the
+ *                     output names (fresh); value = cost (1..2^28); each
+ *                     output is then described by MEMORY and ALIAS, in output
+ *                     order; a view must view an input or an earlier output of
+ *                     the same call that owns a new storage
+ *   DTR_LOG_MUTATE    ids = n_in input names, then the mutated ones (distinct,
+ *                     among the inputs); value = cost.  Replayed as a pure
+ *                     operator whose outputs are clones (new storages of the
+ *                     same size); the mutated names are rebound to the clones
+ *   DTR_LOG_CONSTANT  a = fresh name, then MEMORY: a nullary operator of cost 0
+ *                     whose storage is pinned (never evicted)
+ *   DTR_LOG_COPY      a = fresh name, b = name: one more reference to b's tensor
+ *   DTR_LOG_COPYFROM  a = name rebound to b's tensor
+ *   DTR_LOG_RELEASE   a = name dropped
+ * Storages are the unit of eviction.  A storage whose references drop to zero
+ * is released after the last operator issued (the deallocation policy then
+ * applies); tensors still referenced at the end are required outputs.  A
+ * tensor is defined when its storage is resident and its operator ran after
+ * the storage last became resident; an operator call locks its inputs'
+ * storages, defines undefined inputs in listed order, allocates every
+ * non-view output, runs, frees the new copies of outputs that were already
+ * defined, and unlocks (Appendix C.4).  A storage's cost sums the operators
+ * computing any tensor that views it (each once), its dependencies are the
+ * storages they read, its staleness counts from the latest reference to any
+ * of its tensors (Appendix C.2).  Banishing a storage needs every tensor
+ * computed from it (outside it) defined or gone, and pins their storages.
+ * Results: operators count once per execution (views and constants
+ * included); failed_op indexes operators in log order. */
+#define DTR_LOG_MEMORY   0
+#define DTR_LOG_ALIAS    1
+#define DTR_LOG_CALL     2
+#define DTR_LOG_MUTATE   3
+#define DTR_LOG_CONSTANT 4
+#define DTR_LOG_COPY     5
+#define DTR_LOG_COPYFROM 6
+#define DTR_LOG_RELEASE  7
+
+typedef struct {
+    int32_t n_instrs;
+    int32_t n_names;
+    const int32_t *kind;          /* [n_instrs] DTR_LOG_*                         */
+    const int32_t *a;             /* [n_instrs] name operand                      */
+    const int32_t *b;             /* [n_instrs] second name operand, or -1        */
+    const int32_t *n_in;          /* [n_instrs] inputs in the list (CALL, MUTATE) */
+    const int64_t *value;         /* [n_instrs] size (MEMORY) or cost             */
+    const int64_t *list_offsets;  /* [n_instrs + 1] into ids                      */
+    const int32_t *ids;           /* [list_offsets[n_instrs]]                     */
+} dtr_log;
+
+/* As dtr_sim_workspace_bytes / dtr_sim_create, for operator logs: the spec's
+ * trace field indexes `logs`.  Logs are validated and lowered on the host
+ * (DTR_ETRACE names the log, instruction and reason).  The handle is run,
+ * read and destroyed with the dtr_sim_* calls below.  Every heuristic, policy
+ * and search flag is accepted under the same rules as traces. */
+int dtr_log_workspace_bytes(const dtr_log *logs, int32_t n_logs,
+                            const dtr_sim_spec *sims, int32_t n_sims,
+                            const dtr_sim_options *options, size_t *bytes);
+int dtr_log_create(const dtr_log *logs, int32_t n_logs,
+                   const dtr_sim_spec *sims, int32_t n_sims,
+                   const dtr_sim_options *options,
+                   void *device_workspace, size_t workspace_bytes,
+                   void *stream, dtr_sim **out);
+
 /* Release the handle (not the caller's workspace).  NULL is ignored. */
 void dtr_sim_destroy(dtr_sim *sim);
 

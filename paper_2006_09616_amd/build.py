@@ -8,7 +8,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
-SOURCES = [os.path.join(CSRC, "dtr_sim.cpp"), os.path.join(CSRC, "replay.hip")]
+SOURCES = [os.path.join(CSRC, f) for f in ("dtr_sim.cpp", "dtr_log.cpp", "replay.hip", "replay_log.hip")]
 OUT = os.path.join(HERE, "libdtrsim.so")
 ARCH = "gfx950"
 

@@ -19,11 +19,12 @@
 #include <vector>
 
 #include "../../include/dtr_sim.h"
+#include "host.h"
 #include "layout.h"
 
 extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream);
 
-namespace {
+namespace dtrhost {
 
 thread_local std::string g_err;
 
@@ -43,8 +44,6 @@ bool heuristic_known(int32_t h)
     return (h >= DTR_H_DTR && h <= DTR_H_MSPS) || (h >= DTR_H_FAMILY(0, 0, 0) && h <= DTR_H_FAMILY(3, 1, 1));
 }
 
-// kernel specialisation: 0 union-find neighbourhood, 1 neighbourhood walk
-// (e* or e_R), 2 no neighbourhood
 int32_t heuristic_class(int32_t h)
 {
     if (h >= DTR_H_FAMILY(0, 0, 0)) {
@@ -54,14 +53,38 @@ int32_t heuristic_class(int32_t h)
     return h == DTR_H_EQ ? 0 : (h == DTR_H_DTR || h == DTR_H_ESTAR || h == DTR_H_MSPS) ? 1 : 2;
 }
 
-constexpr int64_t MAX_SIZE = int64_t(1) << 36;
-constexpr int64_t MAX_COST = int64_t(1) << 28;
-constexpr int64_t MAX_TOTAL_COST = int64_t(1) << 50;
-constexpr size_t ALIGN = 256;
+int check_spec(const dtr_sim_spec &s, int32_t i)
+{
+    if (!heuristic_known(s.heuristic)) return fail(DTR_ETRACE, "sim %d: unknown heuristic %d", i, s.heuristic);
+    if (s.budget < 0) return fail(DTR_ETRACE, "sim %d: negative budget", i);
+    if (s.policy < DTR_POLICY_EAGER || s.policy > DTR_POLICY_BANISH)
+        return fail(DTR_ETRACE, "sim %d: unknown deallocation policy %d", i, s.policy);
+    if (s.policy == DTR_POLICY_BANISH && heuristic_class(s.heuristic) == 0)
+        return fail(DTR_ETRACE, "sim %d: banishing is not defined for union-find heuristics", i);
+    if (s.search & ~(int32_t)(DTR_SEARCH_IGNORE_SMALL | DTR_SEARCH_SAMPLE))
+        return fail(DTR_ETRACE, "sim %d: unknown search flags %d", i, s.search);
+    return DTR_OK;
+}
+
+int device_cus(int32_t *cus)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return fail(DTR_EHIP, "hipGetDevice failed");
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+        return fail(DTR_EHIP, "hipDeviceGetAttribute(multiProcessorCount) failed");
+    *cus = v;
+    return DTR_OK;
+}
+
+}  // namespace dtrhost
+
+namespace {
+
+using namespace dtrhost;
+
 constexpr int32_t MAX_TENSORS = 8000000;       // pool positions are packed in 24 bits
 constexpr int32_t MAX_DEGREE = (1 << 23) - 1;  // degrees are packed in 23 bits
-
-size_t align_up(size_t x) { return (x + ALIGN - 1) / ALIGN * ALIGN; }
 
 struct Derived {
     int32_t n = 0, F = 0;
@@ -224,17 +247,6 @@ size_t trace_bytes(const Derived &d)
            bytes_of(d.consts) + bytes_of(d.rec) + 8 * ALIGN;
 }
 
-int device_cus(int32_t *cus)
-{
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess) return fail(DTR_EHIP, "hipGetDevice failed");
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-        return fail(DTR_EHIP, "hipDeviceGetAttribute(multiProcessorCount) failed");
-    *cus = v;
-    return DTR_OK;
-}
-
 int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sims, int32_t n_sims,
               const dtr_sim_options *opt, Plan &p)
 {
@@ -252,15 +264,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
         const dtr_sim_spec &s = sims[i];
         if (s.trace < 0 || s.trace >= n_traces)
             return fail(DTR_ETRACE, "sim %d: trace index %d out of range", i, s.trace);
-        if (!heuristic_known(s.heuristic))
-            return fail(DTR_ETRACE, "sim %d: unknown heuristic %d", i, s.heuristic);
-        if (s.budget < 0) return fail(DTR_ETRACE, "sim %d: negative budget", i);
-        if (s.policy < DTR_POLICY_EAGER || s.policy > DTR_POLICY_BANISH)
-            return fail(DTR_ETRACE, "sim %d: unknown deallocation policy %d", i, s.policy);
-        if (s.policy == DTR_POLICY_BANISH && heuristic_class(s.heuristic) == 0)
-            return fail(DTR_ETRACE, "sim %d: banishing is not defined for union-find heuristics", i);
-        if (s.search & ~(int32_t)(DTR_SEARCH_IGNORE_SMALL | DTR_SEARCH_SAMPLE))
-            return fail(DTR_ETRACE, "sim %d: unknown search flags %d", i, s.search);
+        if (int rc = check_spec(s, i)) return rc;
         need_banish |= s.policy == DTR_POLICY_BANISH;
         need_uf |= heuristic_class(s.heuristic) == 0;
         need_walk |= heuristic_class(s.heuristic) == 1;
@@ -337,12 +341,14 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
 
 struct dtr_sim {
     Plan plan;
+    dtrhost::LogPlan *log = nullptr;    // set for operator logs
     uint8_t *ws = nullptr;
     size_t ws_bytes = 0;
     std::vector<uint8_t> staging;
     hipStream_t last_stream = nullptr;
     bool ran = false;
     int32_t n_sims = 0;
+    ~dtr_sim() { dtrhost::log_plan_free(log); }
 };
 
 extern "C" {
@@ -443,6 +449,12 @@ int dtr_sim_run(dtr_sim *h, void *stream)
     if (!h) return fail(DTR_EINVAL, "null handle");
     const Plan &p = h->plan;
     if (h->n_sims == 0) { h->ran = true; h->last_stream = (hipStream_t)stream; return DTR_OK; }
+    if (h->log) {
+        if (int rc = dtrhost::log_plan_launch(h->log, h->ws, (hipStream_t)stream)) return rc;
+        h->ran = true;
+        h->last_stream = (hipStream_t)stream;
+        return DTR_OK;
+    }
     dtr::KernelArgs a[dtr::N_GROUPS];
     int32_t first = 0;
     for (int c = 0; c < dtr::N_GROUPS; c++) {
@@ -476,7 +488,8 @@ int dtr_sim_results(dtr_sim *h, dtr_sim_result *host_out, int32_t n_sims)
     if (!h->ran) return fail(DTR_ESTATE, "no run enqueued");
     if (n_sims == 0) return DTR_OK;
     static_assert(sizeof(dtr_sim_result) == sizeof(dtr::ResultDev), "result layout");
-    if (hipMemcpyAsync(host_out, h->ws + h->plan.result_off, sizeof(dtr_sim_result) * n_sims,
+    const size_t result_off = h->log ? dtrhost::log_plan_result_off(h->log) : h->plan.result_off;
+    if (hipMemcpyAsync(host_out, h->ws + result_off, sizeof(dtr_sim_result) * n_sims,
                        hipMemcpyDeviceToHost, h->last_stream) != hipSuccess ||
         hipStreamSynchronize(h->last_stream) != hipSuccess)
         return fail(DTR_EHIP, "result copy failed");
@@ -485,12 +498,51 @@ int dtr_sim_results(dtr_sim *h, dtr_sim_result *host_out, int32_t n_sims)
 
 void dtr_sim_destroy(dtr_sim *h) { delete h; }
 
+int dtr_log_workspace_bytes(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims, int32_t n_sims,
+                            const dtr_sim_options *options, size_t *bytes)
+{
+    g_err.clear();
+    if (!bytes) return fail(DTR_EINVAL, "null bytes");
+    dtrhost::LogPlan *p = nullptr;
+    if (int rc = dtrhost::log_plan_make(logs, n_logs, sims, n_sims, options, &p)) return rc;
+    *bytes = dtrhost::log_plan_total(p);
+    dtrhost::log_plan_free(p);
+    return DTR_OK;
+}
+
+int dtr_log_create(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims, int32_t n_sims,
+                   const dtr_sim_options *options, void *device_workspace, size_t workspace_bytes, void *stream,
+                   dtr_sim **out)
+{
+    g_err.clear();
+    if (!out) return fail(DTR_EINVAL, "null out");
+    *out = nullptr;
+    if (!device_workspace) return fail(DTR_EINVAL, "null device workspace");
+    if ((uintptr_t)device_workspace % ALIGN) return fail(DTR_EINVAL, "workspace must be 256-byte aligned");
+    dtr_sim *h = new dtr_sim();
+    int rc = dtrhost::log_plan_make(logs, n_logs, sims, n_sims, options, &h->log);
+    if (rc) { delete h; return rc; }
+    const size_t need = dtrhost::log_plan_total(h->log);
+    if (workspace_bytes < need) {
+        rc = fail(DTR_EINVAL, "workspace too small: %zu bytes given, %zu needed", workspace_bytes, need);
+        delete h;
+        return rc;
+    }
+    h->ws = (uint8_t *)device_workspace;
+    h->ws_bytes = workspace_bytes;
+    h->n_sims = n_sims;
+    rc = dtrhost::log_plan_upload(h->log, h->ws, (hipStream_t)stream);
+    if (rc) { delete h; return rc; }
+    *out = h;
+    return DTR_OK;
+}
+
 #ifdef DTR_PROFILE
 // Phase timers of the last run (DTR_PROFILE builds only; not part of the
 // public header): PROF_FIELDS int64 per simulation.
 int dtr_sim_profile(dtr_sim *h, int64_t *host_out, int32_t n_sims)
 {
-    if (!h || n_sims != h->n_sims || !h->ran) return fail(DTR_EINVAL, "bad profile request");
+    if (!h || h->log || n_sims != h->n_sims || !h->ran) return fail(DTR_EINVAL, "bad profile request");
     if (hipMemcpyAsync(host_out, h->ws + h->plan.prof_off, sizeof(int64_t) * dtr::PROF_FIELDS * n_sims,
                        hipMemcpyDeviceToHost, h->last_stream) != hipSuccess ||
         hipStreamSynchronize(h->last_stream) != hipSuccess)

@@ -1,0 +1,84 @@
+// layout_log.h -- device-side tables of the operator-log replay, shared by the
+// host lowering (dtr_log.cpp) and its kernel (replay_log.hip).  Everything
+// lives in the caller's workspace.
+#pragma once
+#include <stdint.h>
+
+#include "layout.h"
+
+namespace dtr {
+
+// A lowered operator log (read-only during a run).  Storages are the unit of
+// eviction; tensors are a storage's root or views of it; operators may have
+// several outputs.  CSR offsets are int32 (validated sizes).
+struct LogProgDev {
+    int32_t S, T, F, n_req;
+    // storages
+    const int64_t *s_size;        // [S]
+    const int64_t *s_c0;          // [S] summed cost of the operators computing its tensors
+    const uint8_t *s_const;       // [S] constant (pinned from creation)
+    const int32_t *par_off, *par; // storage graph: parents (distinct input storages of those operators)
+    const int32_t *ch_off, *ch;   //   and children
+    const int32_t *dt_off, *dt;   // tensors computed from the storage outside it (banishing)
+    // tensors
+    const int32_t *t_storage;     // [T]
+    const int32_t *t_op;          // [T]
+    const uint8_t *t_alias;       // [T] a view of another tensor's storage
+    // operators, in log order
+    const int64_t *op_cost;       // [F]
+    const int64_t *op_need;       // [F] summed size of its non-view outputs
+    const int32_t *in_off, *in;   // input tensors, listed order
+    const int32_t *ls_off, *ls;   // distinct input storages (locking)
+    const int32_t *out_off, *out; // output tensors
+    const int32_t *rel_off, *rel; // storages released after each operator, in log order
+    const int32_t *req;           // [n_req] tensors still referenced at the end, ascending
+};
+
+// Per-slot working memory of the log replay, sized for the largest log of
+// the batch.  Byte offsets from the slot base, 256-byte aligned.
+//   state/pinned/pending   u8  [S_max]  storage state, never-evictable flag,
+//                                       banishing deferred
+//   locks, node            i32 [S_max]  holds by operators in progress; the
+//                                       union-find node of an evicted storage
+//   sgen, last             i64 [S_max]  residency generation; last access
+//   gen                    i64 [T_max]  generation at which each tensor's
+//                                       operator last ran
+//   uf_*                   [ucap]       union-find nodes (parent, set size,
+//                                       running cost), the compaction map and
+//                                       a cost staging array
+//   mark                   u32 [mcap * WAVE]  lane-private epoch stamps:
+//                                       storages (neighbourhood walks) or
+//                                       union-find roots (h_DTR^eq)
+//   queue                  i32 [S_max * WAVE] lane-private walk queues
+//   stack                  LogFrame [F_max + 2] operator calls in progress
+struct LogSlotLayout {
+    int64_t bytes;
+    int64_t state, pinned, pending;
+    int64_t locks, node;
+    int64_t sgen, last;
+    int64_t gen;
+    int64_t uf_parent, uf_size, uf_remap, uf_cost, uf_tmp;
+    int64_t mark, queue;
+    int64_t stack;
+    int64_t S_max, T_max, F_max, ucap, mcap;
+};
+
+// one operator call in progress: the operator, the next input to check, and
+// whether it is a rematerialization
+struct LogFrame {
+    int32_t op, next, remat, pad;
+};
+static_assert(sizeof(LogFrame) == 16, "frame layout");
+
+struct LogKernelArgs {
+    const LogProgDev *progs;
+    const SpecDev *specs;
+    const int32_t *order;
+    ResultDev *results;
+    uint32_t *queue;
+    uint8_t *slots;
+    LogSlotLayout L;
+    int32_t n_sims, n_slots;
+};
+
+}  // namespace dtr

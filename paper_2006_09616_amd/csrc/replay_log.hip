@@ -1,0 +1,662 @@
+// replay_log.hip -- gfx950 kernel of operator-log replay: DTR's eviction loop
+// over storages (Appendix C.1, C.4, C.6), one wavefront per simulation.
+//
+// Control is wave-uniform: every lane computes the same clock, memory,
+// counters and stack frame, and a state update is stored by every lane with
+// the same value, so each lane later reads its own write.  Lanes work apart
+// where the work is wide:
+//   * the eviction search scores one storage per lane per round and reduces
+//     the exact (score, id) minimum across the wave (scores N/D compared by
+//     128-bit cross-multiplication, ties to the smaller storage id);
+//   * h_DTR / h_{e*} / h_MSPS walk each candidate's evicted neighbourhood
+//     (e* or the evicted ancestors e_R, Appendix C.2; Section 4.1) with a
+//     lane-private queue and lane-private epoch stamps;
+//   * h_DTR^eq keeps union-find sets of evicted storages with their running
+//     cost (Appendix C.2): a node is created when a storage is evicted and
+//     merged with its evicted neighbours' sets; rematerialization subtracts
+//     c0 and detaches the storage (split approximation); when the node pool
+//     is full it is compacted to one node per live set;
+//   * an operator's inputs are checked for definedness 64 at a time, and a
+//     banishing test checks a storage's dependents 64 at a time.
+// Operator calls (lock inputs, define undefined inputs in listed order by
+// rematerialization, allocate, run, free duplicate outputs, unlock) run on an
+// explicit stack of frames in the slot; a rematerialization always calls an
+// earlier operator, so the depth is bounded by the operator count.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "layout_log.h"
+
+namespace dtr {
+namespace logk {
+
+typedef unsigned __int128 u128;
+
+enum { ST_UNCOMPUTED = 0, ST_RESIDENT = 1, ST_EVICTED = 2, ST_BANISHED = 3 };
+enum { STATUS_OK = 0, STATUS_OOM = 1, STATUS_CLOCK = 2, STATUS_CAPACITY = 3 };
+enum { POLICY_EAGER = 0, POLICY_IGNORE = 1, POLICY_BANISH = 2 };
+enum { SEARCH_IGNORE_SMALL = 1, SEARCH_SAMPLE = 2 };
+// cost measure of a score N / (m^use_m * s^use_s)
+enum { CM_ESTAR = 0, CM_EQCLASS = 1, CM_LOCAL = 2, CM_NONE = 3, CM_ANCESTORS = 4, CM_RAND = 5 };
+constexpr uint64_t GOLDEN = 0x9E3779B97F4A7C15ull;
+constexpr uint64_t SAMPLE_STREAM = 0xD6E8FEB86659FD93ull;
+
+__device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+__device__ __forceinline__ int64_t uni64(int64_t v)
+{
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)v >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+
+// SplitMix64 output function (Steele, Lea and Flood, OOPSLA 2014)
+__device__ __forceinline__ uint64_t mix64(uint64_t z)
+{
+    z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+    z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+    return z ^ (z >> 31);
+}
+
+__device__ __forceinline__ uint64_t shfl64(uint64_t v, int lane_mask)
+{
+    const uint32_t lo = (uint32_t)__shfl_xor((int)(uint32_t)v, lane_mask, WAVE);
+    const uint32_t hi = (uint32_t)__shfl_xor((int)(uint32_t)(v >> 32), lane_mask, WAVE);
+    return ((uint64_t)hi << 32) | lo;
+}
+
+__device__ __forceinline__ int64_t wave_sum(int64_t v)
+{
+    for (int m = WAVE / 2; m >= 1; m >>= 1) v += (int64_t)shfl64((uint64_t)v, m);
+    return uni64(v);
+}
+
+// a strictly better (lower score) than b; id -1 is no candidate
+__device__ __forceinline__ bool better(uint64_t na, u128 da, int32_t ia, uint64_t nb, u128 db, int32_t ib)
+{
+    if (ia < 0) return false;
+    if (ib < 0) return true;
+    const u128 l = (u128)na * db, r = (u128)nb * da;
+    if (l != r) return l < r;
+    return ia < ib;
+}
+
+struct Sim {
+    LogProgDev P;
+    // slot memory
+    uint8_t *state, *pinned, *pending;
+    int32_t *locks, *node;
+    int64_t *sgen, *last, *gen;
+    int32_t *ufp, *ufs, *remap;
+    int64_t *ufc, *uft;
+    uint32_t *mark;            // this lane's stamps
+    int32_t *queue;            // this lane's queue
+    LogFrame *stack;
+    int32_t ucap;
+    // spec
+    int64_t budget;
+    uint64_t seed;
+    int32_t policy, search, cmode;
+    bool use_s, use_m, uf, walk;
+    // run state (uniform)
+    int64_t clock, memory, peak;
+    int64_t total, base, remat_cost, executed, remats, evictions, eager;
+    int64_t eviction_no, cur_op;
+    int32_t status, uf_n, sp;
+    // per-lane
+    int32_t lane;
+    uint32_t epoch;
+    int64_t scores_l, nbr_l, adj_l;
+};
+
+__device__ __forceinline__ bool defined(const Sim &s, int32_t t)
+{
+    const int32_t st = s.P.t_storage[t];
+    return s.state[st] == ST_RESIDENT && s.gen[t] == s.sgen[st];
+}
+
+__device__ __forceinline__ bool evictable(const Sim &s, int32_t st)
+{
+    return s.state[st] == ST_RESIDENT && s.locks[st] == 0 && !s.pinned[st] && !s.P.s_const[st];
+}
+
+// ----------------------------------------------------------- union-find --
+
+// root of v, compressing the path (uniform: every lane stores the same links)
+__device__ int32_t uf_find(Sim &s, int32_t v)
+{
+    int32_t r = v;
+    for (int32_t it = 0; s.ufp[r] != r; it++) {
+        if (it > s.uf_n) { s.status = STATUS_CAPACITY; return r; }
+        r = s.ufp[r];
+    }
+    while (s.ufp[v] != r) {
+        const int32_t nx = s.ufp[v];
+        s.ufp[v] = r;
+        v = nx;
+    }
+    return r;
+}
+
+// root of v without writes (lane-parallel reads)
+__device__ __forceinline__ int32_t uf_root(const Sim &s, int32_t v)
+{
+    for (int32_t it = 0; it <= s.uf_n; it++) {
+        const int32_t p = s.ufp[v];
+        if (p == v) return v;
+        v = p;
+    }
+    return v;
+}
+
+__device__ int32_t uf_unite(Sim &s, int32_t a, int32_t b)
+{
+    a = uf_find(s, a);
+    b = uf_find(s, b);
+    if (a == b) return a;
+    if (s.ufs[a] < s.ufs[b]) { const int32_t t = a; a = b; b = t; }
+    s.ufp[b] = a;
+    s.ufs[a] += s.ufs[b];
+    s.ufc[a] += s.ufc[b];
+    return a;
+}
+
+// one node per live set: the sets reachable from evicted storages keep their
+// cost; every evicted storage points at its set's new node
+__device__ void uf_compact(Sim &s)
+{
+    const int32_t S = s.P.S, n = s.uf_n;
+    for (int32_t i = s.lane; i < n; i += WAVE) s.remap[i] = 0;
+    __syncthreads();
+    for (int32_t st = s.lane; st < S; st += WAVE)
+        if (s.state[st] == ST_EVICTED) {
+            const int32_t r = uf_root(s, s.node[st]);
+            s.node[st] = r;
+            s.remap[r] = 1;
+        }
+    __syncthreads();
+    int32_t kept = 0;
+    for (int32_t b = 0; b < n; b += WAVE) {
+        const int32_t i = b + s.lane;
+        const bool keep = i < n && s.remap[i] != 0;
+        const uint64_t m = __ballot(keep);
+        if (keep) {
+            const int32_t k = kept + (int32_t)__builtin_amdgcn_mbcnt_hi(
+                                         (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
+            s.remap[i] = k;
+            s.uft[k] = s.ufc[i];
+        }
+        kept += __popcll(m);
+    }
+    __syncthreads();
+    for (int32_t k = s.lane; k < kept; k += WAVE) {
+        s.ufc[k] = s.uft[k];
+        s.ufp[k] = k;
+        s.ufs[k] = 1;
+    }
+    for (int32_t st = s.lane; st < S; st += WAVE)
+        if (s.state[st] == ST_EVICTED) s.node[st] = s.remap[s.node[st]];
+    __syncthreads();
+    s.uf_n = uni(kept);
+}
+
+// --------------------------------------------------------------- scores --
+
+__device__ __forceinline__ uint32_t next_epoch(Sim &s, int32_t used)
+{
+    if (++s.epoch == 0) {        // wrapped: clear this lane's stamps
+        for (int32_t i = 0; i < used; i++) s.mark[i] = 0;
+        s.epoch = 1;
+    }
+    return s.epoch;
+}
+
+// summed c0 over the evicted ancestors of x (and its evicted descendants when
+// both), each storage once; the set size goes to cnt
+__device__ int64_t walk_cost(Sim &s, int32_t x, bool both, int64_t &cnt)
+{
+    const uint32_t ep = next_epoch(s, s.P.S);
+    int64_t sum = 0;
+    cnt = 0;
+    for (int side = 0; side < (both ? 2 : 1); side++) {
+        const int32_t *off = side == 0 ? s.P.par_off : s.P.ch_off;
+        const int32_t *adj = side == 0 ? s.P.par : s.P.ch;
+        int32_t head = 0, tail = 0;
+        s.queue[tail++] = x;
+        while (head < tail) {
+            const int32_t u = s.queue[head++];
+            for (int32_t e = off[u]; e < off[u + 1]; e++) {
+                const int32_t v = adj[e];
+                if (s.state[v] != ST_EVICTED || s.mark[v] == ep) continue;
+                s.mark[v] = ep;
+                sum += s.P.s_c0[v];
+                cnt++;
+                s.queue[tail++] = v;
+            }
+        }
+    }
+    return sum;
+}
+
+// union of the sets of x's evicted parents and children, each set once
+__device__ int64_t eq_cost(Sim &s, int32_t x, int64_t &cnt)
+{
+    const uint32_t ep = next_epoch(s, s.ucap);
+    int64_t sum = 0;
+    cnt = 0;
+    for (int side = 0; side < 2; side++) {
+        const int32_t *off = side == 0 ? s.P.par_off : s.P.ch_off;
+        const int32_t *adj = side == 0 ? s.P.par : s.P.ch;
+        for (int32_t e = off[x]; e < off[x + 1]; e++) {
+            const int32_t v = adj[e];
+            if (s.state[v] != ST_EVICTED) continue;
+            cnt++;
+            const int32_t r = uf_root(s, s.node[v]);
+            if (s.mark[r] == ep) continue;
+            s.mark[r] = ep;
+            sum += s.ufc[r];
+        }
+    }
+    return sum;
+}
+
+__device__ __forceinline__ void score(Sim &s, int32_t x, uint64_t &N, u128 &D)
+{
+    const int64_t m = s.P.s_size[x];
+    const int64_t stale = s.clock - s.last[x];
+    const int64_t c0 = s.P.s_c0[x];
+    const int64_t deg = (s.P.par_off[x + 1] - s.P.par_off[x]) + (s.P.ch_off[x + 1] - s.P.ch_off[x]);
+    int64_t cnt = 0;
+    switch (s.cmode) {
+    case CM_ESTAR: N = (uint64_t)(c0 + walk_cost(s, x, true, cnt)); break;
+    case CM_ANCESTORS: N = (uint64_t)(c0 + walk_cost(s, x, false, cnt)); break;
+    case CM_EQCLASS: N = (uint64_t)(c0 + eq_cost(s, x, cnt)); break;
+    case CM_LOCAL: N = (uint64_t)c0; break;
+    case CM_NONE: N = 1; break;
+    default: {
+        const uint64_t key = ((uint64_t)s.eviction_no << 32) + (uint64_t)(uint32_t)x;
+        N = mix64(s.seed + GOLDEN * key);
+        D = 1;
+        return;
+    }
+    }
+    if (s.cmode == CM_ESTAR || s.cmode == CM_ANCESTORS || s.cmode == CM_EQCLASS) {
+        s.nbr_l += cnt;
+        s.adj_l += deg;
+    }
+    D = (u128)(uint64_t)(s.use_m ? m : 1) * (u128)(uint64_t)(s.use_s ? stale : 1);
+}
+
+// ----------------------------------------------------------- eviction --
+
+__device__ void evict(Sim &s, int32_t st, bool eager)
+{
+    if (s.uf && s.uf_n >= s.ucap) {
+        uf_compact(s);
+        if (s.uf_n >= s.ucap) { s.status = STATUS_CAPACITY; return; }
+    }
+    s.state[st] = ST_EVICTED;
+    s.memory -= s.P.s_size[st];
+    if (eager) s.eager++;
+    else s.evictions++;
+    if (!s.uf) return;
+    const int32_t nd = s.uf_n++;
+    s.ufp[nd] = nd;
+    s.ufs[nd] = 1;
+    s.ufc[nd] = s.P.s_c0[st];
+    s.node[st] = nd;
+    int32_t r = nd;
+    for (int side = 0; side < 2; side++) {
+        const int32_t *off = side == 0 ? s.P.par_off : s.P.ch_off;
+        const int32_t *adj = side == 0 ? s.P.par : s.P.ch;
+        for (int32_t e = off[st]; e < off[st + 1]; e++) {
+            const int32_t v = adj[e];
+            if (s.state[v] == ST_EVICTED) r = uf_unite(s, r, s.node[v]);
+        }
+    }
+}
+
+// smallest r with r * r >= n
+__device__ __forceinline__ uint64_t ceil_sqrt(uint64_t n)
+{
+    uint64_t k = (uint64_t)sqrtf((float)n);
+    while (k * k < n) k++;
+    while (k > 0 && (k - 1) * (k - 1) >= n) k--;
+    return k;
+}
+
+// evict while memory is insufficient (Appendix C.4), under the search
+// approximations when asked (Appendix E)
+__device__ void allocate(Sim &s, int64_t need)
+{
+    const int32_t S = s.P.S;
+    while (s.memory + need > s.budget) {
+        uint64_t min_size = 0, tau = 0;
+        bool sample = false;
+        if (s.search) {
+            int64_t n0 = 0, sum = 0;
+            for (int32_t x = s.lane; x < S; x += WAVE)
+                if (evictable(s, x)) { n0++; sum += s.P.s_size[x]; }
+            n0 = wave_sum(n0);
+            sum = wave_sum(sum);
+            if (n0 > 0 && (s.search & SEARCH_IGNORE_SMALL)) {
+                const uint64_t d = 100 * (uint64_t)n0;
+                min_size = ((uint64_t)sum + d - 1) / d;
+            }
+            if (n0 > 0 && (s.search & SEARCH_SAMPLE)) {
+                const uint64_t k = ceil_sqrt((uint64_t)n0);
+                if (k < (uint64_t)n0) {
+                    // tau = floor(k 2^64 / n0) in two 32-bit digits
+                    const uint64_t a = k << 32, q1 = a / (uint64_t)n0, r1 = a % (uint64_t)n0;
+                    tau = (q1 << 32) + (r1 << 32) / (uint64_t)n0;
+                    sample = true;
+                }
+            }
+        }
+        uint64_t bn = 0;
+        u128 bd = 0;
+        int32_t bi = -1;
+        for (int pass = 0; pass < 2; pass++) {
+            if (pass == 1 && !(s.search & SEARCH_SAMPLE)) break;
+            const bool sampling = pass == 0 && sample;
+            for (int32_t x = s.lane; x < S; x += WAVE) {
+                if (!evictable(s, x)) continue;
+                if ((uint64_t)s.P.s_size[x] < min_size) continue;
+                if (sampling) {
+                    const uint64_t key = ((uint64_t)s.eviction_no << 32) + (uint64_t)(uint32_t)x;
+                    if (mix64((s.seed ^ SAMPLE_STREAM) + GOLDEN * key) >= tau) continue;
+                }
+                uint64_t N;
+                u128 D;
+                score(s, x, N, D);
+                s.scores_l++;
+                if (better(N, D, x, bn, bd, bi)) { bn = N; bd = D; bi = x; }
+            }
+            // exact minimum across the wave
+            for (int m = WAVE / 2; m >= 1; m >>= 1) {
+                const uint64_t on = shfl64(bn, m);
+                const uint64_t dlo = shfl64((uint64_t)bd, m), dhi = shfl64((uint64_t)(bd >> 64), m);
+                const int32_t oi = __shfl_xor(bi, m, WAVE);
+                const u128 od = ((u128)dhi << 64) | dlo;
+                if (better(on, od, oi, bn, bd, bi)) { bn = on; bd = od; bi = oi; }
+            }
+            bi = uni(bi);
+            if (bi >= 0) break;
+        }
+        if (bi < 0) { s.status = STATUS_OOM; return; }
+        evict(s, bi, false);
+        if (s.status) return;
+        s.eviction_no++;
+    }
+}
+
+// ----------------------------------------------------------- policies --
+
+// Banish st if no operator holds it and every tensor computed from it
+// (outside it) is defined or gone; pin those tensors' resident storages.
+// Otherwise st stays pending (Appendix C.4, C.5).
+__device__ void try_banish(Sim &s, int32_t st)
+{
+    const int32_t b = s.P.dt_off[st], e = s.P.dt_off[st + 1];
+    bool blocked = s.locks[st] > 0;
+    for (int32_t q = b; q < e && !blocked; q += WAVE) {
+        bool bad = false;
+        if (q + s.lane < e) {
+            const int32_t v = s.P.dt[q + s.lane];
+            bad = !defined(s, v) && s.state[s.P.t_storage[v]] != ST_BANISHED;
+        }
+        blocked = __ballot(bad) != 0;
+    }
+    if (blocked) { s.pending[st] = 1; return; }
+    s.pending[st] = 0;
+    if (s.state[st] == ST_RESIDENT) s.memory -= s.P.s_size[st];
+    s.state[st] = ST_BANISHED;
+    s.eager++;
+    for (int32_t q = b + s.lane; q < e; q += WAVE) {
+        const int32_t d = s.P.t_storage[s.P.dt[q]];
+        if (s.state[d] == ST_RESIDENT) s.pinned[d] = 1;
+    }
+    __syncthreads();
+}
+
+__device__ void release(Sim &s, int32_t st)
+{
+    if (s.policy == POLICY_EAGER) {
+        if (evictable(s, st)) evict(s, st, true);
+    } else if (s.policy == POLICY_BANISH) {
+        try_banish(s, st);
+    }
+}
+
+// ---------------------------------------------------------- operators --
+
+__device__ void push(Sim &s, int32_t o, int32_t remat)
+{
+    if (s.sp >= s.P.F + 2) { s.status = STATUS_CAPACITY; return; }
+    for (int32_t e = s.P.ls_off[o]; e < s.P.ls_off[o + 1]; e++) s.locks[s.P.ls[e]] += 1;
+    LogFrame f;
+    f.op = o;
+    f.next = s.P.in_off[o];
+    f.remat = remat;
+    f.pad = 0;
+    s.stack[s.sp] = f;
+    s.sp++;
+}
+
+// run operator o once its inputs are defined: allocate its new storages, run,
+// free the copies of outputs already defined, unlock (Appendix C.4)
+__device__ void execute(Sim &s, int32_t o, bool remat)
+{
+    const int64_t need = s.P.op_need[o];
+    allocate(s, need);
+    if (s.status) return;
+    const int32_t ib = s.P.in_off[o], ie = s.P.in_off[o + 1];
+    const int32_t ob = s.P.out_off[o], oe = s.P.out_off[o + 1];
+    for (int32_t e = s.P.ls_off[o]; e < s.P.ls_off[o + 1]; e++) s.last[s.P.ls[e]] = s.clock;
+    for (int32_t q = ob; q < oe; q++) s.last[s.P.t_storage[s.P.out[q]]] = s.clock;
+    const int64_t c = s.P.op_cost[o];
+    s.clock += c;
+    s.total += c;
+    s.executed++;
+    if (remat) { s.remats++; s.remat_cost += c; }
+    else s.base += c;
+    s.memory += need;
+    if (s.memory > s.peak) s.peak = s.memory;
+    for (int32_t q = ob; q < oe; q++) {
+        const int32_t v = s.P.out[q];
+        if (s.P.t_alias[v]) continue;
+        const int32_t st = s.P.t_storage[v];
+        const uint8_t was = s.state[st];
+        if (was == ST_RESIDENT) { s.memory -= s.P.s_size[st]; continue; }
+        s.state[st] = ST_RESIDENT;
+        const int64_t g = s.sgen[st] + 1;
+        s.sgen[st] = g;
+        s.gen[v] = g;
+        if (s.uf && was == ST_EVICTED) {
+            const int32_t r = uf_find(s, s.node[st]);
+            s.ufc[r] -= s.P.s_c0[st];
+            s.node[st] = -1;
+        }
+    }
+    for (int32_t q = ob; q < oe; q++) {
+        const int32_t v = s.P.out[q];
+        if (s.P.t_alias[v]) s.gen[v] = s.sgen[s.P.t_storage[v]];
+    }
+    if (s.clock >= CLOCK_LIMIT) { s.status = STATUS_CLOCK; return; }
+    for (int32_t e = s.P.ls_off[o]; e < s.P.ls_off[o + 1]; e++) s.locks[s.P.ls[e]] -= 1;
+    if (remat && s.policy == POLICY_BANISH)
+        for (int32_t e = ib; e < ie; e++) {
+            const int32_t st = s.P.t_storage[s.P.in[e]];
+            if (s.pending[st]) try_banish(s, st);
+        }
+}
+
+// call operator o (a rematerialization if remat), defining undefined inputs
+// first, in listed order, by calling their operators
+__device__ void call(Sim &s, int32_t o, int32_t remat)
+{
+    const int32_t floor = s.sp;
+    push(s, o, remat);
+    while (s.sp > floor && !s.status) {
+        const LogFrame f = s.stack[s.sp - 1];
+        const int32_t end = s.P.in_off[f.op + 1];
+        int32_t found = -1;
+        for (int32_t e = f.next; e < end; e += WAVE) {
+            const int32_t i = e + s.lane;
+            const bool undef = i < end && !defined(s, s.P.in[i]);
+            const uint64_t m = __ballot(undef);
+            if (m) { found = e + (int32_t)__builtin_ctzll(m); break; }
+        }
+        found = uni(found);
+        if (found >= 0) {
+            s.stack[s.sp - 1].next = found + 1;
+            push(s, s.P.t_op[s.P.in[found]], 1);
+            continue;
+        }
+        execute(s, f.op, f.remat != 0);
+        if (s.status) return;
+        s.sp--;
+    }
+}
+
+__device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int32_t lane)
+{
+    Sim s;
+    const SpecDev sp = a.specs[sim];
+    s.P = a.progs[sp.trace];
+    const LogSlotLayout &L = a.L;
+    s.state = base + L.state;
+    s.pinned = base + L.pinned;
+    s.pending = base + L.pending;
+    s.locks = (int32_t *)(base + L.locks);
+    s.node = (int32_t *)(base + L.node);
+    s.sgen = (int64_t *)(base + L.sgen);
+    s.last = (int64_t *)(base + L.last);
+    s.gen = (int64_t *)(base + L.gen);
+    s.ufp = (int32_t *)(base + L.uf_parent);
+    s.ufs = (int32_t *)(base + L.uf_size);
+    s.remap = (int32_t *)(base + L.uf_remap);
+    s.ufc = (int64_t *)(base + L.uf_cost);
+    s.uft = (int64_t *)(base + L.uf_tmp);
+    s.mark = (uint32_t *)(base + L.mark) + (size_t)lane * (size_t)L.mcap;
+    s.queue = (int32_t *)(base + L.queue) + (size_t)lane * (size_t)L.S_max;
+    s.stack = (LogFrame *)(base + L.stack);
+    s.ucap = (int32_t)L.ucap;
+    s.budget = sp.budget;
+    s.seed = sp.seed;
+    s.policy = sp.policy;
+    s.search = sp.search;
+    const int32_t h = sp.heuristic;
+    if (h >= 16) {
+        const int32_t f = h - 16;
+        s.cmode = f >> 2;
+        s.use_s = (f & 2) != 0;
+        s.use_m = (f & 1) != 0;
+    } else {
+        // h_DTR, h_DTR^eq, h_DTR^local, h_LRU, h_size, h_rand, h_{e*}, h_MSPS:
+        // cost measure (a nibble each), staleness used, size used
+        constexpr uint32_t CM = (CM_ESTAR << 0) | (CM_EQCLASS << 4) | (CM_LOCAL << 8) | (CM_NONE << 12) |
+                                (CM_NONE << 16) | (CM_RAND << 20) | (CM_ESTAR << 24) | ((uint32_t)CM_ANCESTORS << 28);
+        constexpr uint32_t US = 0x0F, UM = 0xD7;
+        const int32_t i = h & 7;
+        s.cmode = (int32_t)((CM >> (4 * i)) & 0xF);
+        s.use_s = ((US >> i) & 1) != 0;
+        s.use_m = ((UM >> i) & 1) != 0;
+    }
+    s.uf = s.cmode == CM_EQCLASS;
+    s.walk = s.cmode == CM_ESTAR || s.cmode == CM_ANCESTORS;
+    s.lane = lane;
+    s.epoch = 0;
+    s.scores_l = s.nbr_l = s.adj_l = 0;
+    s.clock = s.memory = s.peak = 0;
+    s.total = s.base = s.remat_cost = s.executed = s.remats = s.evictions = s.eager = 0;
+    s.eviction_no = s.cur_op = 0;
+    s.status = STATUS_OK;
+    s.uf_n = 0;
+    s.sp = 0;
+
+    const int32_t S = s.P.S, T = s.P.T, F = s.P.F;
+    for (int32_t i = lane; i < S; i += WAVE) {
+        s.state[i] = ST_UNCOMPUTED;
+        s.pinned[i] = s.P.s_const[i];
+        s.pending[i] = 0;
+        s.locks[i] = 0;
+        s.node[i] = -1;
+        s.sgen[i] = 0;
+        s.last[i] = 0;
+    }
+    for (int32_t i = lane; i < T; i += WAVE) s.gen[i] = -1;
+    if (s.walk || s.uf) {
+        const int32_t used = s.walk ? S : s.ucap;
+        uint32_t *M = (uint32_t *)(base + L.mark);
+        for (int32_t l = 0; l < WAVE; l++)
+            for (int32_t i = lane; i < used; i += WAVE) M[(size_t)l * (size_t)L.mcap + i] = 0;
+    }
+    __syncthreads();
+
+    for (int32_t o = 0; o < F && !s.status; o++) {
+        s.cur_op = o;
+        call(s, o, 0);
+        if (s.status) break;
+        for (int32_t e = s.P.rel_off[o]; e < s.P.rel_off[o + 1] && !s.status; e++) release(s, s.P.rel[e]);
+    }
+    if (!s.status) {
+        // output condition: every tensor still referenced is defined and held
+        s.cur_op = F;
+        for (int32_t k = 0; k < s.P.n_req && !s.status; k++) {
+            const int32_t t = s.P.req[k];
+            s.locks[s.P.t_storage[t]] += 1;
+            if (!defined(s, t)) call(s, s.P.t_op[t], 1);
+        }
+    }
+    const int64_t scores = wave_sum(s.scores_l), nbr = wave_sum(s.nbr_l), adj = wave_sum(s.adj_l);
+    if (lane == 0) {
+        ResultDev r;
+        r.total_cost = s.total;
+        r.base_cost = s.base;
+        r.remat_cost = s.remat_cost;
+        r.peak_memory = s.peak;
+        r.final_memory = s.memory;
+        r.n_executed_ops = s.executed;
+        r.n_remats = s.remats;
+        r.n_evictions = s.evictions;
+        r.n_eager_evictions = s.eager;
+        r.n_scores = scores;
+        r.n_nbr_visits = nbr;
+        r.n_adj_visits = adj;
+        r.status = s.status;
+        r.failed_op = s.status == STATUS_OK ? -1 : (int32_t)s.cur_op;
+        a.results[sim] = r;
+    }
+    __syncthreads();
+}
+
+__global__ void __launch_bounds__(WAVE) log_kernel(LogKernelArgs a)
+{
+    const int32_t lane = threadIdx.x;
+    uint8_t *base = a.slots + (size_t)blockIdx.x * (size_t)a.L.bytes;
+    for (;;) {
+        uint32_t k = 0;
+        if (lane == 0) k = atomicAdd(a.queue, 1u);
+        k = (uint32_t)uni((int32_t)k);
+        if (k >= (uint32_t)a.n_sims) break;
+        run_sim(a, a.order[k], base, lane);
+    }
+}
+
+__global__ void log_reset_kernel(uint32_t *queue)
+{
+    if (threadIdx.x == 0) queue[0] = 0;
+}
+
+}  // namespace logk
+}  // namespace dtr
+
+// Launch entry used by the host library (same shared object).
+extern "C" hipError_t dtr_launch_log(const dtr::LogKernelArgs *args, hipStream_t stream)
+{
+    using namespace dtr;
+    hipLaunchKernelGGL(logk::log_reset_kernel, dim3(1), dim3(WAVE), 0, stream, args->queue);
+    if (args->n_sims > 0)
+        hipLaunchKernelGGL(logk::log_kernel, dim3(args->n_slots), dim3(WAVE), 0, stream, *args);
+    return hipGetLastError();
+}

@@ -64,7 +64,10 @@ def lib():
         L.dtr_sim_destroy.argtypes = [vp]
         L.dtr_sim_destroy.restype = None
         L.dtr_sim_last_error.restype = C.c_char_p
-        for f in ("dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run", "dtr_sim_results"):
+        L.dtr_log_workspace_bytes.argtypes = [vp, i32, vp, i32, vp, C.POINTER(sz)]
+        L.dtr_log_create.argtypes = [vp, i32, vp, i32, vp, vp, sz, vp, C.POINTER(vp)]
+        for f in ("dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run", "dtr_sim_results",
+                  "dtr_log_workspace_bytes", "dtr_log_create"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -106,6 +109,46 @@ class _Packed:
                 C.addressof(self.opt) if self.opt is not None else None)
 
 
+class _Log(C.Structure):
+    _fields_ = [("n_instrs", C.c_int32), ("n_names", C.c_int32), ("kind", C.c_void_p), ("a", C.c_void_p),
+                ("b", C.c_void_p), ("n_in", C.c_void_p), ("value", C.c_void_p), ("list_offsets", C.c_void_p),
+                ("ids", C.c_void_p)]
+
+
+class _PackedLogs(_Packed):
+    """Operator logs (``workloads.Log``) packed into ``dtr_log`` structs."""
+
+    def __init__(self, logs, specs, options):
+        self.cols = []
+        self.arr = (_Log * max(1, len(logs)))()
+        for i, g in enumerate(logs):
+            cols = [np.ascontiguousarray(g.kind, np.int32), np.ascontiguousarray(g.a, np.int32),
+                    np.ascontiguousarray(g.b, np.int32), np.ascontiguousarray(g.n_in, np.int32),
+                    np.ascontiguousarray(g.value, np.int64), np.ascontiguousarray(g.list_offsets, np.int64),
+                    np.ascontiguousarray(g.ids, np.int32)]
+            self.cols.extend(cols)
+            self.arr[i] = _Log(int(g.n_instrs), int(g.n_names), *[c.ctypes.data for c in cols])
+        self.n_traces = len(logs)
+        self.specs = np.ascontiguousarray(specs, dtype=SPEC_DTYPE)
+        self.opt = _Options(int(options.get("slots", 0)), int(options.get("flags", 0))) if options else None
+
+
+def dtr_log_workspace_bytes(logs, specs, options: dict | None = None) -> int:
+    p = _PackedLogs(logs, specs, options)
+    out = C.c_size_t(0)
+    _check(lib().dtr_log_workspace_bytes(*p.args(), C.byref(out)))
+    return int(out.value)
+
+
+def dtr_log_create(logs, specs, workspace_ptr: int, workspace_bytes: int, stream_ptr: int,
+                   options: dict | None = None) -> int:
+    p = _PackedLogs(logs, specs, options)
+    h = C.c_void_p()
+    _check(lib().dtr_log_create(*p.args(), C.c_void_p(workspace_ptr), C.c_size_t(workspace_bytes),
+                                C.c_void_p(stream_ptr), C.byref(h)))
+    return int(h.value)
+
+
 def dtr_sim_workspace_bytes(traces, specs, options: dict | None = None) -> int:
     p = _Packed(traces, specs, options)
     out = C.c_size_t(0)
@@ -142,7 +185,9 @@ class Simulator:
     enqueued on a torch stream.  ``run()`` is asynchronous; ``results()``
     synchronizes."""
 
-    def __init__(self, traces, specs, device: str = "cuda", slots: int = 0, stream=None):
+    def __init__(self, traces, specs, device: str = "cuda", slots: int = 0, stream=None, logs=None):
+        """Simulate ``traces`` (dtr_trace), or operator ``logs`` (dtr_log)
+        when given; the specs' trace field indexes whichever is given."""
         import torch
         lib()                                   # fail loudly before touching the GPU
         self.torch = torch
@@ -151,10 +196,16 @@ class Simulator:
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
         opts = {"slots": slots} if slots else None
         with torch.cuda.device(self.device):
-            self.bytes = dtr_sim_workspace_bytes(traces, specs, opts)
-            self.workspace = torch.empty(self.bytes, dtype=torch.uint8, device=self.device)
-            self.handle = dtr_sim_create(traces, specs, self.workspace.data_ptr(), self.bytes,
-                                         self.stream.cuda_stream, opts)
+            if logs is not None:
+                self.bytes = dtr_log_workspace_bytes(logs, specs, opts)
+                self.workspace = torch.empty(self.bytes, dtype=torch.uint8, device=self.device)
+                self.handle = dtr_log_create(logs, specs, self.workspace.data_ptr(), self.bytes,
+                                             self.stream.cuda_stream, opts)
+            else:
+                self.bytes = dtr_sim_workspace_bytes(traces, specs, opts)
+                self.workspace = torch.empty(self.bytes, dtype=torch.uint8, device=self.device)
+                self.handle = dtr_sim_create(traces, specs, self.workspace.data_ptr(), self.bytes,
+                                             self.stream.cuda_stream, opts)
 
     def run(self):
         with self.torch.cuda.device(self.device):
@@ -179,6 +230,17 @@ class Simulator:
 def run(traces, specs, device: str = "cuda", slots: int = 0) -> np.ndarray:
     """Simulate every spec on the GPU and return the results (numpy)."""
     sim = Simulator(traces, specs, device=device, slots=slots)
+    try:
+        sim.run()
+        return sim.results()
+    finally:
+        sim.close()
+
+
+def run_log(logs, specs, device: str = "cuda", slots: int = 0) -> np.ndarray:
+    """Replay operator logs on the GPU (the specs' trace field indexes
+    ``logs``) and return the results (numpy)."""
+    sim = Simulator(None, specs, device=device, slots=slots, logs=logs)
     try:
         sim.run()
         return sim.results()

@@ -1,6 +1,7 @@
 """C-ABI library: loads, exports what include/dtr_sim.h declares, and
 validates traces on the host (no GPU needed for any of these)."""
 import ctypes as C
+import re
 
 import numpy as np
 import pytest
@@ -128,3 +129,77 @@ def test_family_and_msps_ids_accepted():
             assert D.dtr_sim_workspace_bytes([good], W.make_specs([(0, h, 4, 0)])) > 0
         except D.DtrError as e:
             assert e.code == D.DTR_EHIP and "heuristic" not in str(e), (h, str(e))
+
+
+def test_log_struct_matches_header():
+    text = open(D.HEADER).read()
+    body = text[text.index("typedef struct {", text.index("DTR_LOG_RELEASE")):text.index("} dtr_log;")]
+    fields = [l.split(";")[0].split()[-1].lstrip("*") for l in body.splitlines() if ";" in l]
+    assert fields == [f for f, _ in D._Log._fields_]
+    kinds = {k: int(v) for k, v in re.findall(r"#define DTR_LOG_(\w+)\s+(\d+)", text)}
+    assert kinds == {n: getattr(W, "LOG_" + n) for n in kinds}
+
+
+def _log_expect(logs, specs, match, code=None):
+    with pytest.raises(D.DtrError) as e:
+        D.dtr_log_workspace_bytes(logs, specs)
+    assert e.value.code == (D.DTR_ETRACE if code is None else code), str(e.value)
+    assert match in str(e.value), str(e.value)
+
+
+def _rows(kind_rows):
+    """A log from (kind, a, b, value, ins, outs) rows."""
+    b = W.LogBuilder("m")
+    for k, a_, b_, v, ins, outs in kind_rows:
+        b._row(k, a_, b_, v, ins, outs)
+    b.next_name = 1 + max([r[1] for r in kind_rows] + [x for r in kind_rows for x in r[4] + r[5]] + [0])
+    return b.build()
+
+
+def test_log_validation_rejects_malformed_logs():
+    M, A, CALL, MUT, CONST, COPY, CF, REL = (W.LOG_MEMORY, W.LOG_ALIAS, W.LOG_CALL, W.LOG_MUTATE,
+                                              W.LOG_CONSTANT, W.LOG_COPY, W.LOG_COPYFROM, W.LOG_RELEASE)
+    sp = W.make_specs([(0, W.H_LRU, 10, 0)])
+    good = [(CALL, -1, -1, 3, [], [0]), (M, 0, -1, 4, [], []), (A, 0, -1, 0, [], [])]
+    cases = [
+        ([(CALL, -1, -1, 3, [5], [0]), (M, 0, -1, 4, [], []), (A, 0, -1, 0, [], [])], "input name 5 is not bound"),
+        (good + [(CALL, -1, -1, 3, [0], [0]), (M, 0, -1, 4, [], []), (A, 0, -1, 0, [], [])], "output name 0 is not fresh"),
+        ([(CALL, -1, -1, 0, [], [0]), (M, 0, -1, 4, [], []), (A, 0, -1, 0, [], [])], "cost 0 outside"),
+        ([(CALL, -1, -1, 3, [], [0]), (M, 0, -1, 0, [], []), (A, 0, -1, 0, [], [])], "size 0 outside"),
+        ([(CALL, -1, -1, 3, [], [0]), (M, 0, -1, 4, [], [])], "outputs are not all described"),
+        ([(CALL, -1, -1, 3, [], [0]), (A, 0, -1, 0, [], []), (M, 0, -1, 4, [], [])], "MEMORY then ALIAS"),
+        ([(CALL, -1, -1, 3, [], [0]), (M, 0, -1, 4, [], []), (A, 0, 7, 0, [], [])], "neither an input"),
+        ([(CALL, -1, -1, 3, [], []), ], "a call has no output"),
+        (good + [(MUT, -1, -1, 2, [0], [3])], "mutated name 3 is not a distinct input"),
+        (good + [(MUT, -1, -1, 2, [0], [0, 0])], "mutated name 0 is not a distinct input"),
+        (good + [(REL, 0, -1, 0, [], []), (REL, 0, -1, 0, [], [])], "release of unbound name 0"),
+        (good + [(COPY, 0, 0, 0, [], [])], "copy 0 <- 0"),
+        (good + [(CF, 4, 0, 0, [], [])], "copyfrom 4 <- 0"),
+        ([(CONST, 0, -1, 0, [], []), (M, 1, -1, 3, [], [])], "not followed by its MEMORY"),
+        ([(M, 0, -1, 3, [], [])], "unexpected instruction kind 0"),
+        ([(9, 0, -1, 3, [], [])], "unexpected instruction kind 9"),
+    ]
+    for rows, match in cases:
+        _log_expect([_rows(rows)], sp, match)
+    # two outputs of one call: the second views the first's new storage (accepted)
+    ok = _rows([(CALL, -1, -1, 3, [], [0, 1]), (M, 0, -1, 4, [], []), (A, 0, -1, 0, [], []),
+                (M, 1, -1, 4, [], []), (A, 1, 0, 0, [], [])])
+    try:
+        D.dtr_log_workspace_bytes([ok], sp)
+    except D.DtrError as e:
+        assert e.code == D.DTR_EHIP, str(e)
+    _log_expect([ok], W.make_specs([(1, W.H_LRU, 10, 0)]), "log index 1 out of range")
+    _log_expect([ok], W.make_specs([(0, W.H_EQ, 10, 0, W.POLICY_BANISH)]),
+                "banishing is not defined for union-find heuristics")
+    _log_expect([ok], W.make_specs([(0, 12, 10, 0)]), "unknown heuristic 12")
+
+
+def test_generated_logs_pass_validation():
+    """Every generator's logs are accepted (without a GPU the call then stops
+    at the device query, after lowering)."""
+    logs = [W.random_log(s, n_steps=80) for s in range(10)] + [W.log_from_trace(W.chain_trace(20))]
+    specs = W.make_specs([(i, h, 50, 0) for i in range(len(logs)) for h in (W.H_DTR, W.H_EQ, W.H_MSPS)])
+    try:
+        assert D.dtr_log_workspace_bytes(logs, specs) > 0
+    except D.DtrError as e:
+        assert e.code == D.DTR_EHIP, str(e)

@@ -1,0 +1,155 @@
+"""GPU parity of operator-log replay (Appendix C.6): the HIP path, called
+through the C ABI (dtr_log_create), against the CPU oracle's log replay,
+field by field and bit-exact."""
+import numpy as np
+import pytest
+
+import brute_log
+
+from paper_2006_09616_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+FIELDS = ["total_cost", "base_cost", "remat_cost", "peak_memory", "final_memory", "n_executed_ops",
+          "n_remats", "n_evictions", "n_eager_evictions", "n_scores", "n_nbr_visits", "n_adj_visits",
+          "status", "failed_op"]
+UF = {W.H_EQ} | {W.h_family(W.C_EQCLASS, s, m) for s in (0, 1) for m in (0, 1)}
+HS = [W.H_DTR, W.H_EQ, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_RAND, W.H_ESTAR, W.H_MSPS,
+      W.h_family(W.C_ESTAR, 1, 0), W.h_family(W.C_EQCLASS, 0, 1), W.h_family(W.C_LOCAL, 1, 1),
+      W.h_family(W.C_NONE, 0, 0)]
+
+
+@pytest.fixture(scope="module")
+def gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2006_09616_amd import dtr as D
+    D.lib()
+    return D
+
+
+def compare(got, ref, specs, label):
+    bad = []
+    for k in range(len(specs)):
+        for f in FIELDS:
+            if int(got[f][k]) != int(ref[f][k]):
+                bad.append((k, f, int(got[f][k]), int(ref[f][k]), tuple(specs[k])))
+                break
+    assert not bad, f"{label}: {len(bad)}/{len(specs)} differ; first: {bad[:4]}"
+
+
+def unlimited_peaks(O, logs):
+    specs = W.make_specs([(i, W.H_LRU, W.BUDGET_UNLIMITED, 0) for i in range(len(logs))])
+    return [int(v) for v in O.run_log(logs, specs)["peak_memory"]]
+
+
+def rows_for(i, peak, seed, hs, policies=(W.POLICY_EAGER,), searches=(0,), fracs=(0.3, 0.6, 1.0)):
+    rows = []
+    for policy in policies:
+        for search in searches:
+            for h in hs:
+                if policy == W.POLICY_BANISH and h in UF:
+                    continue
+                for frac in fracs:
+                    rows.append((i, h, max(1, int(peak * frac)), seed * 97 + h, policy, search))
+    return rows
+
+
+def test_random_logs_all_heuristics_and_policies(gpu, oracle_lib):
+    logs = [W.random_log(s, n_steps=10 + (s * 13) % 140, n_const=s % 4, max_size=1 + s % 12,
+                         max_cost=1 + s % 6, max_in=1 + s % 4, keep=s % 4) for s in range(48)]
+    peaks = unlimited_peaks(oracle_lib, logs)
+    rows = []
+    for i, pk in enumerate(peaks):
+        rows += rows_for(i, pk, i, HS, policies=(W.POLICY_EAGER, W.POLICY_IGNORE, W.POLICY_BANISH))
+    specs = W.make_specs(rows)
+    print(f"random logs: {len(logs)} logs, {len(specs)} sims", flush=True)
+    compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "random logs")
+
+
+def test_random_logs_search_approximations(gpu, oracle_lib):
+    logs = [W.random_log(700 + s, n_steps=60 + (s * 29) % 200, n_const=s % 3, max_size=1 + (s * 7) % 60,
+                         max_cost=1 + s % 5, max_in=1 + s % 4) for s in range(24)]
+    peaks = unlimited_peaks(oracle_lib, logs)
+    rows = []
+    flags = (W.SEARCH_IGNORE_SMALL, W.SEARCH_SAMPLE, W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE)
+    for i, pk in enumerate(peaks):
+        rows += rows_for(i, pk, i, [W.H_DTR, W.H_EQ, W.H_LRU, W.H_RAND, W.H_MSPS], searches=flags,
+                         fracs=(0.3, 0.6))
+    specs = W.make_specs(rows)
+    print(f"search logs: {len(specs)} sims", flush=True)
+    compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "search logs")
+
+
+def test_plain_programs_as_logs(gpu, oracle_lib):
+    """Traces written as logs (one storage per tensor), constants included."""
+    logs = []
+    rows = []
+    for s in range(24):
+        tr = W.random_program(300 + s, n_ops=15 + (s * 11) % 90, n_const=s % 3, backward=s % 2 == 0,
+                              max_in=1 + s % 4, max_size=1 + s % 15, max_cost=1 + s % 6)
+        logs.append(W.log_from_trace(tr))
+        rows += rows_for(len(logs) - 1, W.natural_peak(tr), s, HS, policies=(W.POLICY_EAGER, W.POLICY_BANISH),
+                         fracs=(0.25, 0.5, 1.0))
+    specs = W.make_specs(rows)
+    print(f"plain logs: {len(specs)} sims", flush=True)
+    compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "plain logs")
+
+
+def test_long_logs_compaction_and_ragged_tiles(gpu, oracle_lib):
+    """Logs of a few thousand operators (storage scans over many 64-wide
+    rounds with a ragged tail; thousands of evictions against a union-find
+    pool of 2S + 64 nodes, so it is compacted repeatedly)."""
+    logs = [W.random_log(5000 + s, n_steps=1500 + 700 * s, n_const=3, max_size=20, max_cost=7, max_in=3, keep=3)
+            for s in range(3)]
+    peaks = unlimited_peaks(oracle_lib, logs)
+    rows = []
+    for i, pk in enumerate(peaks):
+        rows += rows_for(i, pk, i, [W.H_DTR, W.H_EQ, W.H_LRU, W.H_MSPS, W.h_family(W.C_EQCLASS, 1, 0)],
+                         policies=(W.POLICY_EAGER, W.POLICY_IGNORE), fracs=(0.1, 0.15, 0.3))
+    specs = W.make_specs(rows)
+    s_max = max(len(brute_log.StorageProgram(L).size) for L in logs)
+    print(f"long logs: {s_max} storages at most, {len(specs)} sims", flush=True)
+    got = gpu.run_log(logs, specs)
+    ref = oracle_lib.run_log(logs, specs)
+    compare(got, ref, specs, "long logs")
+    # union-find nodes are created per eviction from a pool of 2 S_max + 64
+    eq = [k for k in range(len(specs)) if specs["heuristic"][k] in UF]
+    assert max(int(ref["n_evictions"][k] + ref["n_eager_evictions"][k]) for k in eq) > 3 * (2 * s_max + 64)
+
+
+def test_empty_and_degenerate_logs(gpu, oracle_lib):
+    b = W.LogBuilder("consts")
+    c = [b.fresh() for _ in range(3)]
+    for k, t in enumerate(c):
+        b.constant(t, 3 + k)
+    b.release(c[1])
+    consts = b.build()
+    empty = W.LogBuilder("empty").build()
+    b = W.LogBuilder("one")
+    x = b.fresh()
+    b.call([], [x], 4, [5], [-1])
+    one = b.build()
+    logs = [empty, consts, one, W.random_log(9, n_steps=3, n_const=0)]
+    rows = []
+    for i in range(len(logs)):
+        for h in HS:
+            for policy in (W.POLICY_EAGER, W.POLICY_IGNORE, W.POLICY_BANISH):
+                if policy == W.POLICY_BANISH and h in UF:
+                    continue
+                for bud in (0, 1, 4, 7, 12, W.BUDGET_UNLIMITED):
+                    rows.append((i, h, bud, 5, policy))
+    specs = W.make_specs(rows)
+    compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "degenerate logs")
+    assert len(gpu.run_log(logs, specs[:0])) == 0
+
+
+def test_log_determinism_across_slot_counts(gpu):
+    logs = [W.random_log(40 + s, n_steps=200) for s in range(6)]
+    rows = [(i, h, 20 + 7 * i, 3, W.POLICY_EAGER) for i in range(6) for h in HS]
+    specs = W.make_specs(rows)
+    a = gpu.run_log(logs, specs, slots=3)
+    b = gpu.run_log(logs, specs, slots=500)
+    c = gpu.run_log(logs, specs)
+    assert a.tobytes() == b.tobytes() == c.tobytes()
