@@ -148,7 +148,13 @@ WORKLOADS = {
     "resnet50blk": lambda: W.make_config("resnet50blk"),
     "transformer12": lambda: W.make_config("transformer12"),
     "chain32": lambda: W.make_config("chain32"),
+    "resnet50log": lambda: W.make_config("resnet50log"),
 }
+
+
+def is_log(wl) -> bool:
+    """Operator-log workloads replay through dtr_log_create (Appendix C.6)."""
+    return isinstance(wl.traces[0], W.Log)
 
 
 def cpu_baseline(wl, gpu_res, sample_every: int, threads: int):
@@ -157,7 +163,7 @@ def cpu_baseline(wl, gpu_res, sample_every: int, threads: int):
     idx = np.arange(0, wl.n_sims, sample_every)
     specs = wl.specs[idx]
     t0 = time.perf_counter()
-    ref = O.run(wl.traces, specs, threads=threads)
+    ref = (O.run_log if is_log(wl) else O.run)(wl.traces, specs, threads=threads)
     dt = time.perf_counter() - t0
     ops = int(ref["n_executed_ops"].sum())
     scores = int(ref["n_scores"].sum())
@@ -201,6 +207,8 @@ def main():
     gen_s = time.perf_counter() - t0
     print(f"[bench] workload {wl.name}: {len(wl.traces)} traces, {wl.n_sims} sims, generated in {gen_s:.1f}s",
           file=sys.stderr, flush=True)
+    if args.search_study and is_log(wl):
+        sys.exit("--search-study runs on trace workloads")
     if args.search_study:
         torch.cuda.set_device(0)
         print(json.dumps({"search_study": search_study(wl, args.steps), "workload": wl.name,
@@ -208,7 +216,9 @@ def main():
         return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    sim = D.Simulator(wl.traces, wl.specs, device="cuda:0", slots=args.slots)
+    log = is_log(wl)
+    sim = D.Simulator(None if log else wl.traces, wl.specs, device="cuda:0", slots=args.slots,
+                      logs=wl.traces if log else None)
     stream = sim.stream
     for i in range(args.warmup):
         sim.run()
@@ -262,7 +272,7 @@ def main():
         "eviction_scores_per_s": scores / avg_s,
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(wl.name),
-                     "kernel": "replay_kernel", "algorithmic_bytes_per_launch": nbytes,
+                     "kernel": "log_kernel" if log else "replay_kernel", "algorithmic_bytes_per_launch": nbytes,
                      "avg_launch_ms": avg_s * 1e3},
         "cpu_baseline": cpu,
     }

@@ -164,8 +164,14 @@ typedef struct {
 /* Launch options (NULL = defaults). */
 typedef struct {
     int32_t slots;   /* simulations resident on the GPU at once (0 = 16 per CU) */
-    int32_t flags;   /* reserved, must be 0                                     */
+    int32_t flags;   /* 0, or DTR_OPT_* bits (operator logs only)               */
 } dtr_sim_options;
+
+/* Operator-log replay keeps every per-simulation array in device memory even
+ * when the storage states, visited sets and storage graph of the batch's
+ * largest log fit in LDS (results are identical; a testing aid).  Rejected
+ * for traces. */
+#define DTR_OPT_LOG_NO_LDS 1
 
 typedef struct dtr_sim dtr_sim;
 

@@ -40,6 +40,7 @@ namespace {
 
 constexpr int64_t MAX_ITEMS = int64_t(1) << 26;    // storages, tensors, operators, list entries
 constexpr int64_t MAX_C0_SUM = int64_t(1) << 50;    // keeps every score numerator below 2^51
+constexpr size_t LDS_LIMIT = 160 * 1024;            // dynamic LDS of the log kernel (and the device's)
 
 struct Lowered {
     int32_t S = 0, T = 0, F = 0;
@@ -414,6 +415,8 @@ struct LogPlan {
     std::vector<int32_t> order;
     dtr::LogSlotLayout L{};
     int32_t n_slots = 1;
+    int32_t lds_bytes = 0, lds_state = 0, lds_wm = 0, lds_po = 0, lds_co = 0, lds_pa = 0, lds_ca = 0, wm_words = 0;
+    int32_t lds_c0 = 0, lds_cand = 0, lds_stk = 0, lds_ctr = 0, lds_sz = 0, lds_last = 0;
     std::vector<size_t> log_off;
     size_t desc_off = 0, spec_off = 0, order_off = 0, tables_bytes = 0, result_off = 0, slot_off = 0, total = 0;
 };
@@ -424,7 +427,7 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
     *out = nullptr;
     if (n_logs < 0 || n_sims < 0) return fail(DTR_EINVAL, "negative n_logs or n_sims");
     if ((n_logs > 0 && !logs) || (n_sims > 0 && !sims)) return fail(DTR_EINVAL, "null logs or sims");
-    if (opt && (opt->slots < 0 || opt->flags != 0)) return fail(DTR_EINVAL, "bad options");
+    if (opt && (opt->slots < 0 || (opt->flags & ~DTR_OPT_LOG_NO_LDS))) return fail(DTR_EINVAL, "bad options");
     LogPlan *p = new LogPlan();
     auto give_up = [&](int rc) { delete p; return rc; };
     p->logs.resize(n_logs);
@@ -433,7 +436,7 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
         if (int rc = lw.run()) return give_up(rc);
     }
     bool need_uf = false, need_walk = false;
-    int64_t S_max = 1, T_max = 1, F_max = 1;
+    int64_t S_max = 1, T_max = 1, F_max = 1, E_max = 0;
     for (int32_t i = 0; i < n_sims; i++) {
         const dtr_sim_spec &s = sims[i];
         if (s.trace < 0 || s.trace >= n_logs) return give_up(fail(DTR_ETRACE, "sim %d: log index %d out of range", i, s.trace));
@@ -444,6 +447,7 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
         S_max = std::max<int64_t>(S_max, d.S);
         T_max = std::max<int64_t>(T_max, d.T);
         F_max = std::max<int64_t>(F_max, d.F);
+        E_max = std::max<int64_t>(E_max, (int64_t)d.par.size());
     }
     p->sims.assign(sims, sims + n_sims);
     // slot layout
@@ -454,7 +458,8 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
     L.T_max = T_max;
     L.F_max = F_max;
     L.ucap = need_uf ? 2 * S_max + 64 : 0;
-    L.mcap = std::max<int64_t>(need_walk ? S_max : 0, L.ucap);
+    L.mcap = L.ucap;
+    const int64_t W = (S_max + 127) / 128 * 4;     // 32-bit words, whole 16-byte quads
     const size_t S = (size_t)S_max, U = (size_t)L.ucap;
     take(L.state, S);
     take(L.pinned, S);
@@ -470,9 +475,37 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
     take(L.uf_cost, 8 * U);
     take(L.uf_tmp, 8 * U);
     take(L.mark, 4 * (size_t)L.mcap * dtr::WAVE);
-    take(L.queue, need_walk ? 4 * S * dtr::WAVE : 0);
+    take(L.wmark, need_walk ? 4 * (size_t)W * dtr::WAVE : 0);
+    take(L.queue, need_walk ? 4 * (S + 2) * dtr::WAVE : 0);
     take(L.stack, sizeof(dtr::LogFrame) * (size_t)(F_max + 2));
     L.bytes = (int64_t)o;
+
+    // walk state in LDS when the largest log fits: storage states, 64 visited
+    // bitsets, storage graph with 16-bit neighbour ids
+    {
+        size_t q = 0;
+        auto at = [&](int32_t &field, size_t bytes) { field = (int32_t)q; q += (bytes + 15) / 16 * 16; };
+        at(p->lds_state, (size_t)S_max);
+        at(p->lds_wm, 4 * (size_t)W * dtr::WAVE);
+        at(p->lds_po, 4 * (size_t)(S_max + 1));
+        at(p->lds_co, 4 * (size_t)(S_max + 1));
+        at(p->lds_pa, 2 * (size_t)E_max);
+        at(p->lds_ca, 2 * (size_t)E_max);
+        at(p->lds_c0, 8 * (size_t)S_max);
+        at(p->lds_cand, 2 * (size_t)S_max);
+        at(p->lds_stk, 2 * (size_t)dtr::LOG_LDS_STACK * dtr::WAVE);
+        at(p->lds_ctr, 4);
+        at(p->lds_sz, 8 * (size_t)S_max);
+        at(p->lds_last, 8 * (size_t)S_max);
+        int dev = 0, lds_max = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+            return give_up(fail(DTR_EHIP, "hipDeviceGetAttribute(maxSharedMemoryPerBlock) failed"));
+        const size_t limit = std::min<size_t>(LDS_LIMIT, (size_t)lds_max);
+        const bool fits = S_max <= 65535 && q <= limit && !(opt && (opt->flags & DTR_OPT_LOG_NO_LDS));
+        p->lds_bytes = fits ? (int32_t)q : 0;
+        p->wm_words = (int32_t)W;
+    }
 
     int32_t cus = 0;
     if (int rc = device_cus(&cus)) return give_up(rc);
@@ -587,6 +620,20 @@ int log_plan_launch(const LogPlan *p, uint8_t *ws, hipStream_t st)
     a.L = p->L;
     a.n_sims = (int32_t)p->sims.size();
     a.n_slots = p->n_slots;
+    a.lds_bytes = p->lds_bytes;
+    a.lds_state = p->lds_state;
+    a.lds_wm = p->lds_wm;
+    a.lds_po = p->lds_po;
+    a.lds_co = p->lds_co;
+    a.lds_pa = p->lds_pa;
+    a.lds_ca = p->lds_ca;
+    a.wm_words = p->wm_words;
+    a.lds_c0 = p->lds_c0;
+    a.lds_cand = p->lds_cand;
+    a.lds_stk = p->lds_stk;
+    a.lds_ctr = p->lds_ctr;
+    a.lds_sz = p->lds_sz;
+    a.lds_last = p->lds_last;
     hipError_t e = dtr_launch_log(&a, st);
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return DTR_OK;

@@ -46,10 +46,11 @@ struct LogProgDev {
 //   uf_*                   [ucap]       union-find nodes (parent, set size,
 //                                       running cost), the compaction map and
 //                                       a cost staging array
-//   mark                   u32 [mcap * WAVE]  lane-private epoch stamps:
-//                                       storages (neighbourhood walks) or
+//   mark                   u32 [ucap * WAVE]  lane-private epoch stamps of
 //                                       union-find roots (h_DTR^eq)
-//   queue                  i32 [S_max * WAVE] lane-private walk queues
+//   wmark                  u32 [wm_words * WAVE] lane-private visited bitsets
+//                                       of the walks, when not in LDS
+//   queue                  i32 [(S_max + 2) * WAVE] lane-private walk queues
 //   stack                  LogFrame [F_max + 2] operator calls in progress
 struct LogSlotLayout {
     int64_t bytes;
@@ -58,7 +59,7 @@ struct LogSlotLayout {
     int64_t sgen, last;
     int64_t gen;
     int64_t uf_parent, uf_size, uf_remap, uf_cost, uf_tmp;
-    int64_t mark, queue;
+    int64_t mark, wmark, queue;
     int64_t stack;
     int64_t S_max, T_max, F_max, ucap, mcap;
 };
@@ -79,6 +80,16 @@ struct LogKernelArgs {
     uint8_t *slots;
     LogSlotLayout L;
     int32_t n_sims, n_slots;
+    // walk state in LDS when lds_bytes > 0: byte offsets of the storage
+    // states, the 64 visited bitsets and the storage graph (16-bit ids)
+    int32_t lds_bytes, lds_state, lds_wm, lds_po, lds_co, lds_pa, lds_ca;
+    // and for the walk scan: storage costs c0, the candidate list, 64
+    // pending-storage stacks of LOG_LDS_STACK entries, the candidate counter
+    int32_t lds_c0, lds_cand, lds_stk, lds_ctr;
+    int32_t lds_sz, lds_last;  // storage sizes and last-access times
+    int32_t wm_words;         // 32-bit words per visited bitset (a multiple of 4)
 };
+
+constexpr int LOG_LDS_STACK = 32;
 
 }  // namespace dtr

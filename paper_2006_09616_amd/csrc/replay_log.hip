@@ -10,7 +10,10 @@
 //     128-bit cross-multiplication, ties to the smaller storage id);
 //   * h_DTR / h_{e*} / h_MSPS walk each candidate's evicted neighbourhood
 //     (e* or the evicted ancestors e_R, Appendix C.2; Section 4.1) with a
-//     lane-private queue and lane-private epoch stamps;
+//     lane-private queue and a lane-private visited bitset, cleared after
+//     each walk from the queue; when the batch's largest log fits, the
+//     storage states, the bitsets and the storage graph live in LDS
+//     (kernel variant L), so a walk step costs LDS round trips only;
 //   * h_DTR^eq keeps union-find sets of evicted storages with their running
 //     cost (Appendix C.2): a node is created when a storage is evicted and
 //     merged with its evicted neighbours' sets; rematerialization subtracts
@@ -24,6 +27,8 @@
 // earlier operator, so the depth is bounded by the operator count.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include <type_traits>
 
 #include "layout_log.h"
 
@@ -80,17 +85,93 @@ __device__ __forceinline__ bool better(uint64_t na, u128 da, int32_t ia, uint64_
     return ia < ib;
 }
 
+#define GAS __attribute__((address_space(1)))
+#define LAS __attribute__((address_space(3)))
+// per-simulation arrays of the walks: in LDS (L) or in the slot's device memory
+template <bool L, class T>
+struct Ptr {
+    typedef GAS T *type;
+};
+template <class T>
+struct Ptr<true, T> {
+    typedef LAS T *type;
+};
+template <bool L, class T>
+using Mem = typename Ptr<L, T>::type;
+// neighbour ids: 16 bits in LDS
+template <bool L>
+using Adj = typename std::conditional<L, uint16_t, int32_t>::type;
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// the lowered program's tables, read with global (never flat) loads
+struct ProgG {
+    int32_t S, T, F, n_req;
+    const GAS int64_t *s_size, *s_c0;
+    const GAS uint8_t *s_const;
+    const GAS int32_t *par_off, *par, *ch_off, *ch, *dt_off, *dt;
+    const GAS int32_t *t_storage, *t_op;
+    const GAS uint8_t *t_alias;
+    const GAS int64_t *op_cost, *op_need;
+    const GAS int32_t *in_off, *in, *ls_off, *ls, *out_off, *out, *rel_off, *rel, *req;
+};
+
+__device__ __forceinline__ ProgG prog_global(const LogProgDev &d)
+{
+    ProgG g;
+    g.S = d.S;
+    g.T = d.T;
+    g.F = d.F;
+    g.n_req = d.n_req;
+    g.s_size = (const GAS int64_t *)d.s_size;
+    g.s_c0 = (const GAS int64_t *)d.s_c0;
+    g.s_const = (const GAS uint8_t *)d.s_const;
+    g.par_off = (const GAS int32_t *)d.par_off;
+    g.par = (const GAS int32_t *)d.par;
+    g.ch_off = (const GAS int32_t *)d.ch_off;
+    g.ch = (const GAS int32_t *)d.ch;
+    g.dt_off = (const GAS int32_t *)d.dt_off;
+    g.dt = (const GAS int32_t *)d.dt;
+    g.t_storage = (const GAS int32_t *)d.t_storage;
+    g.t_op = (const GAS int32_t *)d.t_op;
+    g.t_alias = (const GAS uint8_t *)d.t_alias;
+    g.op_cost = (const GAS int64_t *)d.op_cost;
+    g.op_need = (const GAS int64_t *)d.op_need;
+    g.in_off = (const GAS int32_t *)d.in_off;
+    g.in = (const GAS int32_t *)d.in;
+    g.ls_off = (const GAS int32_t *)d.ls_off;
+    g.ls = (const GAS int32_t *)d.ls;
+    g.out_off = (const GAS int32_t *)d.out_off;
+    g.out = (const GAS int32_t *)d.out;
+    g.rel_off = (const GAS int32_t *)d.rel_off;
+    g.rel = (const GAS int32_t *)d.rel;
+    g.req = (const GAS int32_t *)d.req;
+    return g;
+}
+
+template <bool L>
 struct Sim {
-    LogProgDev P;
+    ProgG P;
+    Mem<L, uint8_t> state;       // storage states
+    Mem<L, uint32_t> wm;         // this lane's visited bitset (walks)
+    Mem<L, const int32_t> po, co;          // storage graph: parents, children
+    Mem<L, const Adj<L>> pa, ca;
+    // walk scan in LDS (L only): storage costs, candidate list, this lane's
+    // pending stack, the candidate counter
+    LAS int64_t *c0l;
+    LAS uint16_t *cand, *stk;
+    LAS uint32_t *ctr;
+    int32_t wmw;               // words per visited bitset
     // slot memory
-    uint8_t *state, *pinned, *pending;
-    int32_t *locks, *node;
-    int64_t *sgen, *last, *gen;
-    int32_t *ufp, *ufs, *remap;
-    int64_t *ufc, *uft;
-    uint32_t *mark;            // this lane's stamps
-    int32_t *queue;            // this lane's queue
-    LogFrame *stack;
+    GAS uint8_t *pinned, *pending;
+    GAS int32_t *locks, *node;
+    GAS int64_t *sgen, *gen;
+    GAS int32_t *ufp, *ufs, *remap;
+    GAS int64_t *ufc, *uft;
+    GAS uint32_t *mark;        // this lane's union-find root stamps (h_DTR^eq)
+    GAS int32_t *queue;        // this lane's queue
+    GAS LogFrame *stack;
+    Mem<L, int64_t> last;      // last access per storage
+    Mem<L, const int64_t> sz;  // storage sizes
     int32_t ucap;
     // spec
     int64_t budget;
@@ -108,13 +189,15 @@ struct Sim {
     int64_t scores_l, nbr_l, adj_l;
 };
 
-__device__ __forceinline__ bool defined(const Sim &s, int32_t t)
+template <bool L>
+__device__ __forceinline__ bool defined(const Sim<L> &s, int32_t t)
 {
     const int32_t st = s.P.t_storage[t];
     return s.state[st] == ST_RESIDENT && s.gen[t] == s.sgen[st];
 }
 
-__device__ __forceinline__ bool evictable(const Sim &s, int32_t st)
+template <bool L>
+__device__ __forceinline__ bool evictable(const Sim<L> &s, int32_t st)
 {
     return s.state[st] == ST_RESIDENT && s.locks[st] == 0 && !s.pinned[st] && !s.P.s_const[st];
 }
@@ -122,7 +205,8 @@ __device__ __forceinline__ bool evictable(const Sim &s, int32_t st)
 // ----------------------------------------------------------- union-find --
 
 // root of v, compressing the path (uniform: every lane stores the same links)
-__device__ int32_t uf_find(Sim &s, int32_t v)
+template <bool L>
+__device__ int32_t uf_find(Sim<L> &s, int32_t v)
 {
     int32_t r = v;
     for (int32_t it = 0; s.ufp[r] != r; it++) {
@@ -138,7 +222,8 @@ __device__ int32_t uf_find(Sim &s, int32_t v)
 }
 
 // root of v without writes (lane-parallel reads)
-__device__ __forceinline__ int32_t uf_root(const Sim &s, int32_t v)
+template <bool L>
+__device__ __forceinline__ int32_t uf_root(const Sim<L> &s, int32_t v)
 {
     for (int32_t it = 0; it <= s.uf_n; it++) {
         const int32_t p = s.ufp[v];
@@ -148,7 +233,8 @@ __device__ __forceinline__ int32_t uf_root(const Sim &s, int32_t v)
     return v;
 }
 
-__device__ int32_t uf_unite(Sim &s, int32_t a, int32_t b)
+template <bool L>
+__device__ int32_t uf_unite(Sim<L> &s, int32_t a, int32_t b)
 {
     a = uf_find(s, a);
     b = uf_find(s, b);
@@ -162,7 +248,8 @@ __device__ int32_t uf_unite(Sim &s, int32_t a, int32_t b)
 
 // one node per live set: the sets reachable from evicted storages keep their
 // cost; every evicted storage points at its set's new node
-__device__ void uf_compact(Sim &s)
+template <bool L>
+__device__ void uf_compact(Sim<L> &s)
 {
     const int32_t S = s.P.S, n = s.uf_n;
     for (int32_t i = s.lane; i < n; i += WAVE) s.remap[i] = 0;
@@ -201,7 +288,8 @@ __device__ void uf_compact(Sim &s)
 
 // --------------------------------------------------------------- scores --
 
-__device__ __forceinline__ uint32_t next_epoch(Sim &s, int32_t used)
+template <bool L>
+__device__ __forceinline__ uint32_t next_epoch(Sim<L> &s, int32_t used)
 {
     if (++s.epoch == 0) {        // wrapped: clear this lane's stamps
         for (int32_t i = 0; i < used; i++) s.mark[i] = 0;
@@ -211,41 +299,50 @@ __device__ __forceinline__ uint32_t next_epoch(Sim &s, int32_t used)
 }
 
 // summed c0 over the evicted ancestors of x (and its evicted descendants when
-// both), each storage once; the set size goes to cnt
-__device__ int64_t walk_cost(Sim &s, int32_t x, bool both, int64_t &cnt)
+// both), each storage once; the set size goes to cnt.  The visited bitset is
+// clear before and after: the queue lists every storage marked.
+template <bool L>
+__device__ int64_t walk_cost(Sim<L> &s, int32_t x, bool both, int64_t &cnt)
 {
-    const uint32_t ep = next_epoch(s, s.P.S);
     int64_t sum = 0;
+    int32_t tail = 0;
     cnt = 0;
     for (int side = 0; side < (both ? 2 : 1); side++) {
-        const int32_t *off = side == 0 ? s.P.par_off : s.P.ch_off;
-        const int32_t *adj = side == 0 ? s.P.par : s.P.ch;
-        int32_t head = 0, tail = 0;
+        const auto off = side == 0 ? s.po : s.co;
+        const auto adj = side == 0 ? s.pa : s.ca;
+        int32_t head = tail;
         s.queue[tail++] = x;
         while (head < tail) {
             const int32_t u = s.queue[head++];
-            for (int32_t e = off[u]; e < off[u + 1]; e++) {
+            for (int32_t e = off[u], end = off[u + 1]; e < end; e++) {
                 const int32_t v = adj[e];
-                if (s.state[v] != ST_EVICTED || s.mark[v] == ep) continue;
-                s.mark[v] = ep;
+                if (s.state[v] != ST_EVICTED) continue;
+                const uint32_t bit = 1u << (v & 31), w = s.wm[v >> 5];
+                if (w & bit) continue;
+                s.wm[v >> 5] = w | bit;
                 sum += s.P.s_c0[v];
                 cnt++;
                 s.queue[tail++] = v;
             }
         }
     }
+    for (int32_t i = 0; i < tail; i++) {
+        const int32_t v = s.queue[i];
+        s.wm[v >> 5] &= ~(1u << (v & 31));
+    }
     return sum;
 }
 
 // union of the sets of x's evicted parents and children, each set once
-__device__ int64_t eq_cost(Sim &s, int32_t x, int64_t &cnt)
+template <bool L>
+__device__ int64_t eq_cost(Sim<L> &s, int32_t x, int64_t &cnt)
 {
     const uint32_t ep = next_epoch(s, s.ucap);
     int64_t sum = 0;
     cnt = 0;
     for (int side = 0; side < 2; side++) {
-        const int32_t *off = side == 0 ? s.P.par_off : s.P.ch_off;
-        const int32_t *adj = side == 0 ? s.P.par : s.P.ch;
+        const auto off = side == 0 ? s.po : s.co;
+        const auto adj = side == 0 ? s.pa : s.ca;
         for (int32_t e = off[x]; e < off[x + 1]; e++) {
             const int32_t v = adj[e];
             if (s.state[v] != ST_EVICTED) continue;
@@ -259,12 +356,13 @@ __device__ int64_t eq_cost(Sim &s, int32_t x, int64_t &cnt)
     return sum;
 }
 
-__device__ __forceinline__ void score(Sim &s, int32_t x, uint64_t &N, u128 &D)
+template <bool L>
+__device__ __forceinline__ void score(Sim<L> &s, int32_t x, uint64_t &N, u128 &D)
 {
-    const int64_t m = s.P.s_size[x];
+    const int64_t m = s.sz[x];
     const int64_t stale = s.clock - s.last[x];
     const int64_t c0 = s.P.s_c0[x];
-    const int64_t deg = (s.P.par_off[x + 1] - s.P.par_off[x]) + (s.P.ch_off[x + 1] - s.P.ch_off[x]);
+    const int64_t deg = (s.po[x + 1] - s.po[x]) + (s.co[x + 1] - s.co[x]);
     int64_t cnt = 0;
     switch (s.cmode) {
     case CM_ESTAR: N = (uint64_t)(c0 + walk_cost(s, x, true, cnt)); break;
@@ -288,14 +386,15 @@ __device__ __forceinline__ void score(Sim &s, int32_t x, uint64_t &N, u128 &D)
 
 // ----------------------------------------------------------- eviction --
 
-__device__ void evict(Sim &s, int32_t st, bool eager)
+template <bool L>
+__device__ void evict(Sim<L> &s, int32_t st, bool eager)
 {
     if (s.uf && s.uf_n >= s.ucap) {
         uf_compact(s);
         if (s.uf_n >= s.ucap) { s.status = STATUS_CAPACITY; return; }
     }
     s.state[st] = ST_EVICTED;
-    s.memory -= s.P.s_size[st];
+    s.memory -= s.sz[st];
     if (eager) s.eager++;
     else s.evictions++;
     if (!s.uf) return;
@@ -306,13 +405,112 @@ __device__ void evict(Sim &s, int32_t st, bool eager)
     s.node[st] = nd;
     int32_t r = nd;
     for (int side = 0; side < 2; side++) {
-        const int32_t *off = side == 0 ? s.P.par_off : s.P.ch_off;
-        const int32_t *adj = side == 0 ? s.P.par : s.P.ch;
+        const auto off = side == 0 ? s.po : s.co;
+        const auto adj = side == 0 ? s.pa : s.ca;
         for (int32_t e = off[st]; e < off[st + 1]; e++) {
             const int32_t v = adj[e];
             if (s.state[v] == ST_EVICTED) r = uf_unite(s, r, s.node[v]);
         }
     }
+}
+
+// The walk scan with all its data in LDS: the searched candidates are listed
+// first; each lane then takes the next candidate from a shared counter as
+// soon as its previous walk (and the clearing of its visited bitset) is done,
+// and every iteration advances each lane's own walk by one edge, so lanes do
+// not wait for the longest walk of a round.  Pending storages go on a small
+// LDS stack per lane, spilling to the lane's queue in device memory; any
+// order visits the same set.
+template <bool L>
+__device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint64_t tau, uint64_t &bn,
+                              u128 &bd, int32_t &bi)
+{
+    const int32_t S = s.P.S;
+    int32_t n = 0;
+    for (int32_t b = 0; b < S; b += WAVE) {
+        const int32_t x = b + s.lane;
+        bool ok = false;
+        if (x < S) {
+            // every read issued before the first test
+            const uint8_t st = s.state[x], pin = s.pinned[x], cst = s.P.s_const[x];
+            const int32_t lk = s.locks[x];
+            const uint64_t sz = (uint64_t)s.sz[x];
+            ok = (st == ST_RESIDENT) & (lk == 0) & (pin == 0) & (cst == 0) & (sz >= min_size);
+        }
+        if (ok && sampling) {
+            const uint64_t key = ((uint64_t)s.eviction_no << 32) + (uint64_t)(uint32_t)x;
+            ok = mix64((s.seed ^ SAMPLE_STREAM) + GOLDEN * key) < tau;
+        }
+        const uint64_t m = __ballot(ok);
+        if (ok)
+            s.cand[n + (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0))] = (uint16_t)x;
+        n += __popcll(m);
+    }
+    *s.ctr = 0;
+    __syncthreads();
+    const bool both = s.cmode == CM_ESTAR;
+    const int32_t W = s.wmw;
+    int32_t x = -1, e = 0, end = 0, side = 0, spl = 0, spg = 0, clr = -1;
+    int64_t sum = 0, cnt = 0, xm = 0, xlast = 0;
+    auto fetch = [&]() {
+        const uint32_t k = atomicAdd((uint32_t *)s.ctr, 1u);
+        x = k < (uint32_t)n ? (int32_t)s.cand[k] : -1;
+        if (x >= 0) {
+            xm = s.sz[x];          // used when the walk ends: read now
+            xlast = s.last[x];
+            side = 0;
+            e = s.po[x];
+            end = s.po[x + 1];
+            sum = cnt = 0;
+        }
+    };
+    fetch();
+    while (__ballot(x >= 0) != 0) {
+        if (x < 0) continue;
+        if (clr >= 0) {                      // clear the visited bitset, a quad per step
+            *(LAS u32x4 *)&s.wm[clr] = u32x4{0, 0, 0, 0};
+            clr += 4;
+            if (clr >= W) {
+                clr = -1;
+                fetch();
+            }
+            continue;
+        }
+        if (e < end) {
+            const int32_t v = side == 0 ? s.pa[e] : s.ca[e];
+            e++;
+            if (s.state[v] == ST_EVICTED) {
+                const uint32_t bit = 1u << (v & 31), w = s.wm[v >> 5];
+                if (!(w & bit)) {
+                    s.wm[v >> 5] = w | bit;
+                    sum += s.c0l[v];
+                    cnt++;
+                    if (spl < LOG_LDS_STACK) s.stk[spl++] = (uint16_t)v;
+                    else s.queue[spg++] = v;
+                }
+            }
+        } else if (spl > 0 || spg > 0) {
+            const int32_t u = spl > 0 ? (int32_t)s.stk[--spl] : s.queue[--spg];
+            e = side == 0 ? s.po[u] : s.co[u];
+            end = side == 0 ? s.po[u + 1] : s.co[u + 1];
+        } else if (side == 0 && both) {
+            side = 1;
+            e = s.co[x];
+            end = s.co[x + 1];
+        } else {
+            const int64_t m = xm;
+            const int64_t stale = s.clock - xlast;
+            const uint64_t N = (uint64_t)(s.c0l[x] + sum);
+            const u128 D = (u128)(uint64_t)(s.use_m ? m : 1) * (u128)(uint64_t)(s.use_s ? stale : 1);
+            if (better(N, D, x, bn, bd, bi)) { bn = N; bd = D; bi = x; }
+            s.scores_l++;
+            s.nbr_l += cnt;
+            s.adj_l += (s.po[x + 1] - s.po[x]) + (s.co[x + 1] - s.co[x]);
+            clr = 0;
+        }
+    }
+    __syncthreads();
 }
 
 // smallest r with r * r >= n
@@ -326,7 +524,8 @@ __device__ __forceinline__ uint64_t ceil_sqrt(uint64_t n)
 
 // evict while memory is insufficient (Appendix C.4), under the search
 // approximations when asked (Appendix E)
-__device__ void allocate(Sim &s, int64_t need)
+template <bool L>
+__device__ void allocate(Sim<L> &s, int64_t need)
 {
     const int32_t S = s.P.S;
     while (s.memory + need > s.budget) {
@@ -335,7 +534,7 @@ __device__ void allocate(Sim &s, int64_t need)
         if (s.search) {
             int64_t n0 = 0, sum = 0;
             for (int32_t x = s.lane; x < S; x += WAVE)
-                if (evictable(s, x)) { n0++; sum += s.P.s_size[x]; }
+                if (evictable(s, x)) { n0++; sum += s.sz[x]; }
             n0 = wave_sum(n0);
             sum = wave_sum(sum);
             if (n0 > 0 && (s.search & SEARCH_IGNORE_SMALL)) {
@@ -358,9 +557,15 @@ __device__ void allocate(Sim &s, int64_t need)
         for (int pass = 0; pass < 2; pass++) {
             if (pass == 1 && !(s.search & SEARCH_SAMPLE)) break;
             const bool sampling = pass == 0 && sample;
+            if constexpr (L) {
+                if (s.walk) {
+                    scan_walk_lds(s, min_size, sampling, tau, bn, bd, bi);
+                    goto reduce;
+                }
+            }
             for (int32_t x = s.lane; x < S; x += WAVE) {
                 if (!evictable(s, x)) continue;
-                if ((uint64_t)s.P.s_size[x] < min_size) continue;
+                if ((uint64_t)s.sz[x] < min_size) continue;
                 if (sampling) {
                     const uint64_t key = ((uint64_t)s.eviction_no << 32) + (uint64_t)(uint32_t)x;
                     if (mix64((s.seed ^ SAMPLE_STREAM) + GOLDEN * key) >= tau) continue;
@@ -371,6 +576,7 @@ __device__ void allocate(Sim &s, int64_t need)
                 s.scores_l++;
                 if (better(N, D, x, bn, bd, bi)) { bn = N; bd = D; bi = x; }
             }
+        reduce:
             // exact minimum across the wave
             for (int m = WAVE / 2; m >= 1; m >>= 1) {
                 const uint64_t on = shfl64(bn, m);
@@ -394,7 +600,8 @@ __device__ void allocate(Sim &s, int64_t need)
 // Banish st if no operator holds it and every tensor computed from it
 // (outside it) is defined or gone; pin those tensors' resident storages.
 // Otherwise st stays pending (Appendix C.4, C.5).
-__device__ void try_banish(Sim &s, int32_t st)
+template <bool L>
+__device__ void try_banish(Sim<L> &s, int32_t st)
 {
     const int32_t b = s.P.dt_off[st], e = s.P.dt_off[st + 1];
     bool blocked = s.locks[st] > 0;
@@ -408,7 +615,7 @@ __device__ void try_banish(Sim &s, int32_t st)
     }
     if (blocked) { s.pending[st] = 1; return; }
     s.pending[st] = 0;
-    if (s.state[st] == ST_RESIDENT) s.memory -= s.P.s_size[st];
+    if (s.state[st] == ST_RESIDENT) s.memory -= s.sz[st];
     s.state[st] = ST_BANISHED;
     s.eager++;
     for (int32_t q = b + s.lane; q < e; q += WAVE) {
@@ -418,7 +625,8 @@ __device__ void try_banish(Sim &s, int32_t st)
     __syncthreads();
 }
 
-__device__ void release(Sim &s, int32_t st)
+template <bool L>
+__device__ void release(Sim<L> &s, int32_t st)
 {
     if (s.policy == POLICY_EAGER) {
         if (evictable(s, st)) evict(s, st, true);
@@ -429,22 +637,23 @@ __device__ void release(Sim &s, int32_t st)
 
 // ---------------------------------------------------------- operators --
 
-__device__ void push(Sim &s, int32_t o, int32_t remat)
+template <bool L>
+__device__ void push(Sim<L> &s, int32_t o, int32_t remat)
 {
     if (s.sp >= s.P.F + 2) { s.status = STATUS_CAPACITY; return; }
     for (int32_t e = s.P.ls_off[o]; e < s.P.ls_off[o + 1]; e++) s.locks[s.P.ls[e]] += 1;
-    LogFrame f;
-    f.op = o;
-    f.next = s.P.in_off[o];
-    f.remat = remat;
-    f.pad = 0;
-    s.stack[s.sp] = f;
+    GAS LogFrame *f = &s.stack[s.sp];
+    f->op = o;
+    f->next = s.P.in_off[o];
+    f->remat = remat;
+    f->pad = 0;
     s.sp++;
 }
 
 // run operator o once its inputs are defined: allocate its new storages, run,
 // free the copies of outputs already defined, unlock (Appendix C.4)
-__device__ void execute(Sim &s, int32_t o, bool remat)
+template <bool L>
+__device__ void execute(Sim<L> &s, int32_t o, bool remat)
 {
     const int64_t need = s.P.op_need[o];
     allocate(s, need);
@@ -466,7 +675,7 @@ __device__ void execute(Sim &s, int32_t o, bool remat)
         if (s.P.t_alias[v]) continue;
         const int32_t st = s.P.t_storage[v];
         const uint8_t was = s.state[st];
-        if (was == ST_RESIDENT) { s.memory -= s.P.s_size[st]; continue; }
+        if (was == ST_RESIDENT) { s.memory -= s.sz[st]; continue; }
         s.state[st] = ST_RESIDENT;
         const int64_t g = s.sgen[st] + 1;
         s.sgen[st] = g;
@@ -492,15 +701,17 @@ __device__ void execute(Sim &s, int32_t o, bool remat)
 
 // call operator o (a rematerialization if remat), defining undefined inputs
 // first, in listed order, by calling their operators
-__device__ void call(Sim &s, int32_t o, int32_t remat)
+template <bool L>
+__device__ void call(Sim<L> &s, int32_t o, int32_t remat)
 {
     const int32_t floor = s.sp;
     push(s, o, remat);
     while (s.sp > floor && !s.status) {
-        const LogFrame f = s.stack[s.sp - 1];
-        const int32_t end = s.P.in_off[f.op + 1];
+        const GAS LogFrame *top = &s.stack[s.sp - 1];
+        const int32_t f_op = top->op, f_next = top->next, f_remat = top->remat;
+        const int32_t end = s.P.in_off[f_op + 1];
         int32_t found = -1;
-        for (int32_t e = f.next; e < end; e += WAVE) {
+        for (int32_t e = f_next; e < end; e += WAVE) {
             const int32_t i = e + s.lane;
             const bool undef = i < end && !defined(s, s.P.in[i]);
             const uint64_t m = __ballot(undef);
@@ -512,35 +723,60 @@ __device__ void call(Sim &s, int32_t o, int32_t remat)
             push(s, s.P.t_op[s.P.in[found]], 1);
             continue;
         }
-        execute(s, f.op, f.remat != 0);
+        execute(s, f_op, f_remat != 0);
         if (s.status) return;
         s.sp--;
     }
 }
 
-__device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int32_t lane)
+template <bool L>
+__device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int32_t lane, uint8_t *lds)
 {
-    Sim s;
+    Sim<L> s;
     const SpecDev sp = a.specs[sim];
-    s.P = a.progs[sp.trace];
-    const LogSlotLayout &L = a.L;
-    s.state = base + L.state;
-    s.pinned = base + L.pinned;
-    s.pending = base + L.pending;
-    s.locks = (int32_t *)(base + L.locks);
-    s.node = (int32_t *)(base + L.node);
-    s.sgen = (int64_t *)(base + L.sgen);
-    s.last = (int64_t *)(base + L.last);
-    s.gen = (int64_t *)(base + L.gen);
-    s.ufp = (int32_t *)(base + L.uf_parent);
-    s.ufs = (int32_t *)(base + L.uf_size);
-    s.remap = (int32_t *)(base + L.uf_remap);
-    s.ufc = (int64_t *)(base + L.uf_cost);
-    s.uft = (int64_t *)(base + L.uf_tmp);
-    s.mark = (uint32_t *)(base + L.mark) + (size_t)lane * (size_t)L.mcap;
-    s.queue = (int32_t *)(base + L.queue) + (size_t)lane * (size_t)L.S_max;
-    s.stack = (LogFrame *)(base + L.stack);
-    s.ucap = (int32_t)L.ucap;
+    s.P = prog_global(a.progs[sp.trace]);
+    const LogSlotLayout &Y = a.L;
+    GAS uint8_t *gb = (GAS uint8_t *)base;
+    s.pinned = gb + Y.pinned;
+    s.pending = gb + Y.pending;
+    s.locks = (GAS int32_t *)(gb + Y.locks);
+    s.node = (GAS int32_t *)(gb + Y.node);
+    s.sgen = (GAS int64_t *)(gb + Y.sgen);
+    s.gen = (GAS int64_t *)(gb + Y.gen);
+    s.ufp = (GAS int32_t *)(gb + Y.uf_parent);
+    s.ufs = (GAS int32_t *)(gb + Y.uf_size);
+    s.remap = (GAS int32_t *)(gb + Y.uf_remap);
+    s.ufc = (GAS int64_t *)(gb + Y.uf_cost);
+    s.uft = (GAS int64_t *)(gb + Y.uf_tmp);
+    s.mark = (GAS uint32_t *)(gb + Y.mark) + (size_t)lane * (size_t)Y.mcap;
+    s.queue = (GAS int32_t *)(gb + Y.queue) + (size_t)lane * (size_t)(Y.S_max + 2);
+    s.stack = (GAS LogFrame *)(gb + Y.stack);
+    s.ucap = (int32_t)Y.ucap;
+    const int32_t W = a.wm_words;
+    s.wmw = W;
+    if constexpr (L) {
+        s.state = (Mem<L, uint8_t>)(lds + a.lds_state);
+        s.wm = (Mem<L, uint32_t>)(lds + a.lds_wm) + lane * W;
+        s.po = (Mem<L, const int32_t>)(lds + a.lds_po);
+        s.co = (Mem<L, const int32_t>)(lds + a.lds_co);
+        s.pa = (Mem<L, const Adj<L>>)(lds + a.lds_pa);
+        s.ca = (Mem<L, const Adj<L>>)(lds + a.lds_ca);
+        s.c0l = (LAS int64_t *)(lds + a.lds_c0);
+        s.cand = (LAS uint16_t *)(lds + a.lds_cand);
+        s.stk = (LAS uint16_t *)(lds + a.lds_stk) + lane * LOG_LDS_STACK;
+        s.ctr = (LAS uint32_t *)(lds + a.lds_ctr);
+        s.last = (Mem<L, int64_t>)(lds + a.lds_last);
+        s.sz = (Mem<L, const int64_t>)(lds + a.lds_sz);
+    } else {
+        s.state = (Mem<L, uint8_t>)(base + Y.state);
+        s.wm = (Mem<L, uint32_t>)(base + Y.wmark) + lane * W;
+        s.po = (Mem<L, const int32_t>)s.P.par_off;
+        s.co = (Mem<L, const int32_t>)s.P.ch_off;
+        s.pa = (Mem<L, const Adj<L>>)s.P.par;
+        s.ca = (Mem<L, const Adj<L>>)s.P.ch;
+        s.last = (Mem<L, int64_t>)(gb + Y.last);
+        s.sz = s.P.s_size;
+    }
     s.budget = sp.budget;
     s.seed = sp.seed;
     s.policy = sp.policy;
@@ -585,11 +821,33 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         s.last[i] = 0;
     }
     for (int32_t i = lane; i < T; i += WAVE) s.gen[i] = -1;
-    if (s.walk || s.uf) {
-        const int32_t used = s.walk ? S : s.ucap;
-        uint32_t *M = (uint32_t *)(base + L.mark);
+    if (s.uf) {
+        GAS uint32_t *M = (GAS uint32_t *)(gb + Y.mark);
         for (int32_t l = 0; l < WAVE; l++)
-            for (int32_t i = lane; i < used; i += WAVE) M[(size_t)l * (size_t)L.mcap + i] = 0;
+            for (int32_t i = lane; i < s.ucap; i += WAVE) M[(size_t)l * (size_t)Y.mcap + i] = 0;
+    }
+    if (s.walk) {
+        Mem<L, uint32_t> M = s.wm - lane * W;
+        for (int32_t i = lane; i < WAVE * W; i += WAVE) M[i] = 0;
+    }
+    if constexpr (L) {
+        // the storage graph of this log, 16-bit neighbour ids
+        Mem<L, int32_t> po = (Mem<L, int32_t>)s.po, co = (Mem<L, int32_t>)s.co;
+        Mem<L, Adj<L>> pa = (Mem<L, Adj<L>>)s.pa, ca = (Mem<L, Adj<L>>)s.ca;
+        for (int32_t i = lane; i <= S; i += WAVE) {
+            po[i] = s.P.par_off[i];
+            co[i] = s.P.ch_off[i];
+        }
+        const int32_t E = s.P.par_off[S];
+        for (int32_t e = lane; e < E; e += WAVE) {
+            pa[e] = (Adj<L>)s.P.par[e];
+            ca[e] = (Adj<L>)s.P.ch[e];
+        }
+        Mem<L, int64_t> szl = (Mem<L, int64_t>)s.sz;
+        for (int32_t i = lane; i < S; i += WAVE) {
+            s.c0l[i] = s.P.s_c0[i];
+            szl[i] = s.P.s_size[i];
+        }
     }
     __syncthreads();
 
@@ -630,8 +888,10 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
     __syncthreads();
 }
 
+template <bool L>
 __global__ void __launch_bounds__(WAVE) log_kernel(LogKernelArgs a)
 {
+    extern __shared__ uint8_t lds_dyn[];
     const int32_t lane = threadIdx.x;
     uint8_t *base = a.slots + (size_t)blockIdx.x * (size_t)a.L.bytes;
     for (;;) {
@@ -639,7 +899,7 @@ __global__ void __launch_bounds__(WAVE) log_kernel(LogKernelArgs a)
         if (lane == 0) k = atomicAdd(a.queue, 1u);
         k = (uint32_t)uni((int32_t)k);
         if (k >= (uint32_t)a.n_sims) break;
-        run_sim(a, a.order[k], base, lane);
+        run_sim<L>(a, a.order[k], base, lane, lds_dyn);
     }
 }
 
@@ -656,7 +916,17 @@ extern "C" hipError_t dtr_launch_log(const dtr::LogKernelArgs *args, hipStream_t
 {
     using namespace dtr;
     hipLaunchKernelGGL(logk::log_reset_kernel, dim3(1), dim3(WAVE), 0, stream, args->queue);
-    if (args->n_sims > 0)
-        hipLaunchKernelGGL(logk::log_kernel, dim3(args->n_slots), dim3(WAVE), 0, stream, *args);
+    if (args->n_sims > 0) {
+        if (args->lds_bytes > 0) {
+            if (args->lds_bytes > 64 * 1024) {
+                hipError_t e = hipFuncSetAttribute((const void *)logk::log_kernel<true>,
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, args->lds_bytes);
+                if (e != hipSuccess) return e;
+            }
+            hipLaunchKernelGGL(logk::log_kernel<true>, dim3(args->n_slots), dim3(WAVE), args->lds_bytes, stream, *args);
+        }
+        else
+            hipLaunchKernelGGL(logk::log_kernel<false>, dim3(args->n_slots), dim3(WAVE), 0, stream, *args);
+    }
     return hipGetLastError();
 }

@@ -21,6 +21,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "dtr_sim.h")
 
 DTR_OK, DTR_EINVAL, DTR_ETRACE, DTR_EHIP, DTR_ESTATE = 0, -1, -2, -3, -4
 STATUS_OK, STATUS_OOM, STATUS_CLOCK_OVERFLOW, STATUS_CAPACITY = 0, 1, 2, 3
+OPT_LOG_NO_LDS = 1
 
 RESULT_FIELDS = ["total_cost", "base_cost", "remat_cost", "peak_memory", "final_memory",
                  "n_executed_ops", "n_remats", "n_evictions", "n_eager_evictions", "n_scores",
@@ -185,7 +186,7 @@ class Simulator:
     enqueued on a torch stream.  ``run()`` is asynchronous; ``results()``
     synchronizes."""
 
-    def __init__(self, traces, specs, device: str = "cuda", slots: int = 0, stream=None, logs=None):
+    def __init__(self, traces, specs, device: str = "cuda", slots: int = 0, stream=None, logs=None, flags: int = 0):
         """Simulate ``traces`` (dtr_trace), or operator ``logs`` (dtr_log)
         when given; the specs' trace field indexes whichever is given."""
         import torch
@@ -194,7 +195,7 @@ class Simulator:
         self.device = torch.device(device)
         self.n_sims = len(specs)
         self.stream = stream if stream is not None else torch.cuda.current_stream(self.device)
-        opts = {"slots": slots} if slots else None
+        opts = {"slots": slots, "flags": flags} if (slots or flags) else None
         with torch.cuda.device(self.device):
             if logs is not None:
                 self.bytes = dtr_log_workspace_bytes(logs, specs, opts)
@@ -237,10 +238,10 @@ def run(traces, specs, device: str = "cuda", slots: int = 0) -> np.ndarray:
         sim.close()
 
 
-def run_log(logs, specs, device: str = "cuda", slots: int = 0) -> np.ndarray:
+def run_log(logs, specs, device: str = "cuda", slots: int = 0, flags: int = 0) -> np.ndarray:
     """Replay operator logs on the GPU (the specs' trace field indexes
     ``logs``) and return the results (numpy)."""
-    sim = Simulator(None, specs, device=device, slots=slots, logs=logs)
+    sim = Simulator(None, specs, device=device, slots=slots, logs=logs, flags=flags)
     try:
         sim.run()
         return sim.results()

@@ -667,6 +667,224 @@ def log_from_trace(tr: Trace) -> Log:
     return b.build()
 
 
+def log_peak(log: Log) -> int:
+    """Peak memory of a log replayed with no eviction: each operator adds its
+    new storages, and a storage whose last reference goes is freed after the
+    operator it follows (constants stay).  The log's own memory profile, used
+    to space budgets."""
+    name = {}                      # name -> storage
+    size, const, refs = [], [], []
+    mem = peak = 0
+    pending = []                   # storages released since the last operator
+
+    def drop(st):
+        refs[st] -= 1
+        if refs[st] == 0:
+            pending.append(st)
+
+    def flush():
+        nonlocal mem
+        for st in pending:
+            if not const[st]:
+                mem -= size[st]
+        pending.clear()
+
+    def new(sz, c):
+        size.append(sz)
+        const.append(c)
+        refs.append(0)
+        return len(size) - 1
+
+    i, n = 0, log.n_instrs
+    while i < n:
+        k = int(log.kind[i])
+        if k == LOG_CONSTANT:
+            flush()
+            st = new(int(log.value[i + 1]), True)
+            mem += size[st]
+            peak = max(peak, mem)
+            name[int(log.a[i])] = st
+            refs[st] += 1
+            i += 2
+        elif k == LOG_CALL:
+            flush()
+            ins, outs = log.lists(i)
+            need, bound = 0, []
+            own = {}
+            for j, o in enumerate(outs):
+                al = int(log.b[i + 2 + 2 * j])
+                if al < 0:
+                    st = new(int(log.value[i + 1 + 2 * j]), False)
+                    need += size[st]
+                    own[int(o)] = st
+                else:
+                    st = own[al] if al in own else name[al]
+                bound.append((int(o), st))
+            mem += need
+            peak = max(peak, mem)
+            for o, st in bound:
+                name[o] = st
+                refs[st] += 1
+            i += 1 + 2 * len(outs)
+        elif k == LOG_MUTATE:
+            flush()
+            _, muts = log.lists(i)
+            clones = [new(size[name[int(m)]], False) for m in muts]
+            mem += sum(size[c] for c in clones)
+            peak = max(peak, mem)
+            for m, c in zip(muts, clones):
+                old = name[int(m)]
+                name[int(m)] = c
+                refs[c] += 1
+                drop(old)
+            i += 1
+        elif k == LOG_COPY:
+            name[int(log.a[i])] = name[int(log.b[i])]
+            refs[name[int(log.b[i])]] += 1
+            i += 1
+        elif k == LOG_COPYFROM:
+            old = name[int(log.a[i])]
+            name[int(log.a[i])] = name[int(log.b[i])]
+            refs[name[int(log.b[i])]] += 1
+            drop(old)
+            i += 1
+        elif k == LOG_RELEASE:
+            drop(name.pop(int(log.a[i])))
+            i += 1
+        else:
+            raise ValueError(f"instruction {i}: unexpected kind {k}")
+    return int(peak)
+
+
+def resnet_log(seed: int = 2, blocks: int = 50) -> Log:
+    """A PyTorch-style log of one training step of a ResNet-like network, as
+    the DTR prototype records it: weights are constants; batch norm is one
+    call with three outputs (result, saved mean, saved inverse std); ReLU is
+    in place (MUTATE); autograd keeps saved tensors as extra references (COPY)
+    dropped when their backward operator has run (RELEASE); the head flattens
+    through a view; the backward pass computes input and weight gradients in
+    one call, passes the residual gradient by reference and accumulates it,
+    and keeps every weight gradient and the loss to the end.  Activation sizes
+    are log-normal (median 4 MiB, sigma 1), weights log-normal (median 1 MiB,
+    sigma 0.5); every cost is max(1, bytes // 4096) x U{1..4}."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    b = LogBuilder(f"resnet{blocks}-log")
+    size = {}
+
+    def act():
+        return max(1, int(round(rng.lognormal(math.log(4 * MiB), 1.0))))
+
+    def cost(nbytes):
+        return max(1, nbytes // 4096) * int(rng.integers(1, 5))
+
+    def const(nbytes):
+        t = b.fresh()
+        b.constant(t, nbytes)
+        size[t] = nbytes
+        return t
+
+    def call(ins, sizes, aliases=None):
+        outs = [b.fresh() for _ in sizes]
+        aliases = aliases if aliases is not None else [-1] * len(sizes)
+        own = sum(sz for sz, al in zip(sizes, aliases) if al < 0)
+        b.call(ins, outs, cost(max(own, 1)) if own else 1, sizes, aliases)
+        for o, sz, al in zip(outs, sizes, aliases):
+            size[o] = size[al] if al >= 0 else sz
+        return outs
+
+    def relu_(t):
+        b.mutate([t], [t], cost(size[t]))
+
+    def save(t):
+        c = b.fresh()
+        b.copy(c, t)
+        size[c] = size[t]
+        return c
+
+    def drop(*ts):
+        for t in ts:
+            b.release(t)
+
+    STAT = 4096
+    keep = []
+    x, = call([], [act()])                          # the input batch
+    tape = []
+    for _ in range(blocks):
+        w1, w2 = (const(max(1, int(round(rng.lognormal(math.log(MiB), 0.5))))) for _ in range(2))
+        g1, g2 = const(STAT), const(STAT)
+        sv = dict(w1=w1, w2=w2, g1=g1, g2=g2, x=save(x))
+        y1, = call([x, w1], [act()])
+        z1, m1, v1 = call([y1, g1], [size[y1], STAT, STAT])
+        sv.update(y1=save(y1), m1=save(m1), v1=save(v1))
+        drop(y1, m1, v1)
+        relu_(z1)
+        sv["z1"] = save(z1)
+        y2, = call([z1, w2], [act()])
+        drop(z1)
+        z2, m2, v2 = call([y2, g2], [size[y2], STAT, STAT])
+        sv.update(y2=save(y2), m2=save(m2), v2=save(v2))
+        drop(y2, m2, v2)
+        s, = call([z2, x], [size[z2]])
+        drop(z2, x)
+        relu_(s)
+        sv["s"] = save(s)
+        tape.append(sv)
+        x = s
+    wfc = const(4 * 2048 * 1000)
+    f, = call([x], [size[x]], [x])                  # flatten: a view
+    drop(x)
+    logits, = call([f, wfc], [4 * 64 * 1000])
+    sf, sl = save(f), save(logits)
+    drop(f)
+    loss, = call([logits], [4])
+    drop(logits)
+    keep.append(loss)
+    # backward
+    gl, = call([loss], [4])
+    glog, = call([gl, sl], [size[sl]])
+    drop(gl, sl)
+    gf, gwfc = call([glog, sf, wfc], [size[sf], size[wfc]])
+    drop(glog, sf)
+    keep.append(gwfc)
+    g, = call([gf], [size[gf]], [gf])               # unflatten the gradient: a view
+    drop(gf)
+    for sv in reversed(tape):
+        ga, = call([g, sv["s"]], [size[sv["s"]]])    # ReLU backward from its output
+        drop(g, sv["s"])
+        gskip = save(ga)                            # the residual branch shares the gradient
+        gy2, gg2 = call([ga, sv["y2"], sv["g2"], sv["m2"], sv["v2"]], [size[sv["y2"]], STAT])
+        drop(ga, sv["y2"], sv["m2"], sv["v2"])
+        gz1, gw2 = call([gy2, sv["z1"], sv["w2"]], [size[sv["z1"]], size[sv["w2"]]])
+        drop(gy2)
+        gz1r, = call([gz1, sv["z1"]], [size[sv["z1"]]])
+        drop(gz1, sv["z1"])
+        gy1, gg1 = call([gz1r, sv["y1"], sv["g1"], sv["m1"], sv["v1"]], [size[sv["y1"]], STAT])
+        drop(gz1r, sv["y1"], sv["m1"], sv["v1"])
+        gx1, gw1 = call([gy1, sv["x"], sv["w1"]], [size[sv["x"]], size[sv["w1"]]])
+        drop(gy1, sv["x"])
+        g, = call([gx1, gskip], [size[gx1]])        # gradient accumulation at the block input
+        drop(gx1, gskip)
+        keep += [gg2, gw2, gg1, gw1]
+    keep.append(g)
+    return b.build(seed=seed, blocks=blocks, kept=len(keep))
+
+
+def config_resnet_log(blocks: int = 50) -> Workload:
+    """The ResNet log at 256 budgets from 10% to 100% of its no-eviction peak
+    x {h_DTR, h_DTR^eq, h_DTR^local, h_LRU, h_size, h_rand}: 1536 replays."""
+    lg = resnet_log(blocks=blocks)
+    peak = log_peak(lg)
+    rows = []
+    for h in (H_DTR, H_EQ, H_LOCAL, H_LRU, H_SIZE, H_RAND):
+        for bud in linear_budgets(peak, 10, 100, 256):
+            rows.append((0, h, bud, 2 * (1 << 32) + len(rows)))
+    return Workload(f"resnet{blocks}log", [lg], _specs(rows), [peak],
+                    f"PyTorch-style ResNet log, {blocks} blocks, 256 budgets x 6 heuristics")
+
+
+CONFIGS["resnet50log"] = config_resnet_log
+
+
 def random_log(seed: int, n_steps: int, n_const: int = 3, max_size: int = 8, max_cost: int = 5,
                max_in: int = 3, keep: int = 2) -> Log:
     """A PyTorch-like random log: constants; operator calls whose outputs are

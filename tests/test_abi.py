@@ -203,3 +203,23 @@ def test_generated_logs_pass_validation():
         assert D.dtr_log_workspace_bytes(logs, specs) > 0
     except D.DtrError as e:
         assert e.code == D.DTR_EHIP, str(e)
+
+
+def test_log_options():
+    """DTR_OPT_LOG_NO_LDS is accepted for logs only; other bits are rejected."""
+    lib = D.lib()
+    ok = W.log_from_trace(W.chain_trace(4))
+    sp = W.make_specs([(0, W.H_DTR, 4, 0)])
+    for flags, want in ((D.OPT_LOG_NO_LDS, None), (2, D.DTR_EINVAL)):
+        try:
+            D.dtr_log_workspace_bytes([ok], sp, {"slots": 0, "flags": flags})
+            got = None
+        except D.DtrError as e:
+            got = e.code
+        if want is None:
+            assert got in (None, D.DTR_EHIP)
+        else:
+            assert got == want
+    with pytest.raises(D.DtrError) as e:
+        D.dtr_sim_workspace_bytes([W.chain_trace(4)], sp, {"slots": 0, "flags": D.OPT_LOG_NO_LDS})
+    assert e.value.code == D.DTR_EINVAL

@@ -56,7 +56,9 @@ def rows_for(i, peak, seed, hs, policies=(W.POLICY_EAGER,), searches=(0,), fracs
     return rows
 
 
-def test_random_logs_all_heuristics_and_policies(gpu, oracle_lib):
+@pytest.mark.parametrize("flags", [0, 1], ids=["lds", "device-memory"])
+def test_random_logs_all_heuristics_and_policies(gpu, oracle_lib, flags):
+    """Both kernel variants: walk state in LDS, and all in device memory."""
     logs = [W.random_log(s, n_steps=10 + (s * 13) % 140, n_const=s % 4, max_size=1 + s % 12,
                          max_cost=1 + s % 6, max_in=1 + s % 4, keep=s % 4) for s in range(48)]
     peaks = unlimited_peaks(oracle_lib, logs)
@@ -64,8 +66,8 @@ def test_random_logs_all_heuristics_and_policies(gpu, oracle_lib):
     for i, pk in enumerate(peaks):
         rows += rows_for(i, pk, i, HS, policies=(W.POLICY_EAGER, W.POLICY_IGNORE, W.POLICY_BANISH))
     specs = W.make_specs(rows)
-    print(f"random logs: {len(logs)} logs, {len(specs)} sims", flush=True)
-    compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "random logs")
+    print(f"random logs: {len(logs)} logs, {len(specs)} sims, flags {flags}", flush=True)
+    compare(gpu.run_log(logs, specs, flags=flags), oracle_lib.run_log(logs, specs), specs, "random logs")
 
 
 def test_random_logs_search_approximations(gpu, oracle_lib):
@@ -111,9 +113,9 @@ def test_long_logs_compaction_and_ragged_tiles(gpu, oracle_lib):
     specs = W.make_specs(rows)
     s_max = max(len(brute_log.StorageProgram(L).size) for L in logs)
     print(f"long logs: {s_max} storages at most, {len(specs)} sims", flush=True)
-    got = gpu.run_log(logs, specs)
     ref = oracle_lib.run_log(logs, specs)
-    compare(got, ref, specs, "long logs")
+    compare(gpu.run_log(logs, specs), ref, specs, "long logs")
+    compare(gpu.run_log(logs, specs, flags=gpu.OPT_LOG_NO_LDS), ref, specs, "long logs, device memory")
     # union-find nodes are created per eviction from a pool of 2 S_max + 64
     eq = [k for k in range(len(specs)) if specs["heuristic"][k] in UF]
     assert max(int(ref["n_evictions"][k] + ref["n_eager_evictions"][k]) for k in eq) > 3 * (2 * s_max + 64)
@@ -153,3 +155,12 @@ def test_log_determinism_across_slot_counts(gpu):
     b = gpu.run_log(logs, specs, slots=500)
     c = gpu.run_log(logs, specs)
     assert a.tobytes() == b.tobytes() == c.tobytes()
+
+
+def test_resnet_log_config_sampled(gpu, oracle_lib):
+    """The PyTorch-style ResNet log (every instruction kind but COPYFROM, at
+    its benchmark size): every 8th replay of the 1536 against the oracle."""
+    wl = W.make_config("resnet50log")
+    specs = wl.specs[::8]
+    print(f"resnet log: {len(specs)} sims", flush=True)
+    compare(gpu.run_log(wl.traces, specs), oracle_lib.run_log(wl.traces, specs), specs, "resnet50log")
