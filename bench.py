@@ -149,6 +149,7 @@ WORKLOADS = {
     "transformer12": lambda: W.make_config("transformer12"),
     "chain32": lambda: W.make_config("chain32"),
     "resnet50log": lambda: W.make_config("resnet50log"),
+    "randdag100k": lambda: W.make_config("randdag100k"),
 }
 
 

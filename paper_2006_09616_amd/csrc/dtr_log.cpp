@@ -416,7 +416,7 @@ struct LogPlan {
     dtr::LogSlotLayout L{};
     int32_t n_slots = 1;
     int32_t lds_bytes = 0, lds_state = 0, lds_wm = 0, lds_po = 0, lds_co = 0, lds_pa = 0, lds_ca = 0, wm_words = 0;
-    int32_t lds_c0 = 0, lds_cand = 0, lds_stk = 0, lds_ctr = 0, lds_sz = 0, lds_last = 0;
+    int32_t lds_c0 = 0, lds_cand = 0, lds_stk = 0, lds_ctr = 0, lds_sz = 0, lds_last = 0, lds_rsum = 0, lds_rcnt = 0;
     std::vector<size_t> log_off;
     size_t desc_off = 0, spec_off = 0, order_off = 0, tables_bytes = 0, result_off = 0, slot_off = 0, total = 0;
 };
@@ -497,6 +497,8 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
         at(p->lds_ctr, 4);
         at(p->lds_sz, 8 * (size_t)S_max);
         at(p->lds_last, 8 * (size_t)S_max);
+        at(p->lds_rsum, 8 * (size_t)S_max);
+        at(p->lds_rcnt, 4 * (size_t)S_max);
         int dev = 0, lds_max = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
@@ -634,6 +636,8 @@ int log_plan_launch(const LogPlan *p, uint8_t *ws, hipStream_t st)
     a.lds_ctr = p->lds_ctr;
     a.lds_sz = p->lds_sz;
     a.lds_last = p->lds_last;
+    a.lds_rsum = p->lds_rsum;
+    a.lds_rcnt = p->lds_rcnt;
     hipError_t e = dtr_launch_log(&a, st);
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return DTR_OK;

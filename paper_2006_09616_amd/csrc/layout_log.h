@@ -87,6 +87,7 @@ struct LogKernelArgs {
     // pending-storage stacks of LOG_LDS_STACK entries, the candidate counter
     int32_t lds_c0, lds_cand, lds_stk, lds_ctr;
     int32_t lds_sz, lds_last;  // storage sizes and last-access times
+    int32_t lds_rsum, lds_rcnt;  // per listed candidate: walked cost, count
     int32_t wm_words;         // 32-bit words per visited bitset (a multiple of 4)
 };
 

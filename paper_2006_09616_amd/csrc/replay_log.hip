@@ -160,6 +160,8 @@ struct Sim {
     LAS int64_t *c0l;
     LAS uint16_t *cand, *stk;
     LAS uint32_t *ctr;
+    LAS int64_t *rsum;         // per listed candidate: walked cost and count
+    LAS int32_t *rcnt;
     int32_t wmw;               // words per visited bitset
     // slot memory
     GAS uint8_t *pinned, *pending;
@@ -451,24 +453,27 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
     __syncthreads();
     const bool both = s.cmode == CM_ESTAR;
     const int32_t W = s.wmw;
-    int32_t x = -1, e = 0, end = 0, side = 0, spl = 0, spg = 0, clr = -1;
-    int64_t sum = 0, cnt = 0, xm = 0, xlast = 0;
+    int32_t x = -1, k = 0, e = 0, end = 0, side = 0, spl = 0, spg = 0, clr = -1;
+    int64_t sum = 0;
+    int32_t cnt = 0;
     auto fetch = [&]() {
-        const uint32_t k = atomicAdd((uint32_t *)s.ctr, 1u);
-        x = k < (uint32_t)n ? (int32_t)s.cand[k] : -1;
+        k = (int32_t)atomicAdd((uint32_t *)s.ctr, 1u);
+        x = k < n ? (int32_t)s.cand[k] : -1;
         if (x >= 0) {
-            xm = s.sz[x];          // used when the walk ends: read now
-            xlast = s.last[x];
             side = 0;
             e = s.po[x];
             end = s.po[x + 1];
-            sum = cnt = 0;
+            sum = 0;
+            cnt = 0;
         }
     };
     fetch();
+    // each iteration: a finished walk clears a quad of its bitset; otherwise
+    // an exhausted adjacency pops the next storage (or turns to the children,
+    // or records the walk), then one edge is examined
     while (__ballot(x >= 0) != 0) {
         if (x < 0) continue;
-        if (clr >= 0) {                      // clear the visited bitset, a quad per step
+        if (clr >= 0) {
             *(LAS u32x4 *)&s.wm[clr] = u32x4{0, 0, 0, 0};
             clr += 4;
             if (clr >= W) {
@@ -477,38 +482,68 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
             }
             continue;
         }
-        if (e < end) {
-            const int32_t v = side == 0 ? s.pa[e] : s.ca[e];
-            e++;
-            if (s.state[v] == ST_EVICTED) {
-                const uint32_t bit = 1u << (v & 31), w = s.wm[v >> 5];
-                if (!(w & bit)) {
-                    s.wm[v >> 5] = w | bit;
-                    sum += s.c0l[v];
-                    cnt++;
-                    if (spl < LOG_LDS_STACK) s.stk[spl++] = (uint16_t)v;
-                    else s.queue[spg++] = v;
-                }
+        if (e >= end) {
+            if (spl > 0 || spg > 0) {
+                const int32_t u = spl > 0 ? (int32_t)s.stk[--spl] : s.queue[--spg];
+                e = side == 0 ? s.po[u] : s.co[u];
+                end = side == 0 ? s.po[u + 1] : s.co[u + 1];
+            } else if (side == 0 && both) {
+                side = 1;
+                e = s.co[x];
+                end = s.co[x + 1];
+            } else {
+                s.rsum[k] = sum;
+                s.rcnt[k] = cnt;
+                clr = 0;
+                continue;
             }
-        } else if (spl > 0 || spg > 0) {
-            const int32_t u = spl > 0 ? (int32_t)s.stk[--spl] : s.queue[--spg];
-            e = side == 0 ? s.po[u] : s.co[u];
-            end = side == 0 ? s.po[u + 1] : s.co[u + 1];
-        } else if (side == 0 && both) {
-            side = 1;
-            e = s.co[x];
-            end = s.co[x + 1];
-        } else {
-            const int64_t m = xm;
-            const int64_t stale = s.clock - xlast;
-            const uint64_t N = (uint64_t)(s.c0l[x] + sum);
-            const u128 D = (u128)(uint64_t)(s.use_m ? m : 1) * (u128)(uint64_t)(s.use_s ? stale : 1);
-            if (better(N, D, x, bn, bd, bi)) { bn = N; bd = D; bi = x; }
-            s.scores_l++;
-            s.nbr_l += cnt;
-            s.adj_l += (s.po[x + 1] - s.po[x]) + (s.co[x + 1] - s.co[x]);
-            clr = 0;
         }
+        if (e < end) {
+            // up to two edges, their reads issued together; the two
+            // neighbours are distinct (adjacency lists are sets) but may share
+            // a bitset word
+            const bool two = e + 1 < end;
+            const auto adj = side == 0 ? s.pa : s.ca;
+            const int32_t v1 = adj[e], v2 = two ? (int32_t)adj[e + 1] : v1;
+            e += two ? 2 : 1;
+            const uint8_t st1 = s.state[v1], st2 = s.state[v2];
+            const int32_t i1 = v1 >> 5, i2 = v2 >> 5;
+            const uint32_t b1 = 1u << (v1 & 31), b2 = 1u << (v2 & 31);
+            const uint32_t w1 = s.wm[i1], w2 = s.wm[i2];
+            const bool n1 = st1 == ST_EVICTED && !(w1 & b1);
+            const bool n2 = two && st2 == ST_EVICTED && !(w2 & b2);
+            if (i1 == i2) {
+                if (n1 | n2) s.wm[i1] = w1 | (n1 ? b1 : 0u) | (n2 ? b2 : 0u);
+            } else {
+                if (n1) s.wm[i1] = w1 | b1;
+                if (n2) s.wm[i2] = w2 | b2;
+            }
+            if (n1) {
+                sum += s.c0l[v1];
+                cnt++;
+                if (spl < LOG_LDS_STACK) s.stk[spl++] = (uint16_t)v1;
+                else s.queue[spg++] = v1;
+            }
+            if (n2) {
+                sum += s.c0l[v2];
+                cnt++;
+                if (spl < LOG_LDS_STACK) s.stk[spl++] = (uint16_t)v2;
+                else s.queue[spg++] = v2;
+            }
+        }
+    }
+    __syncthreads();
+    // score every walked candidate
+    for (int32_t q = s.lane; q < n; q += WAVE) {
+        const int32_t y = s.cand[q];
+        const int64_t m = s.sz[y];
+        const int64_t stale = s.clock - s.last[y];
+        const uint64_t N = (uint64_t)(s.c0l[y] + s.rsum[q]);
+        const u128 D = (u128)(uint64_t)(s.use_m ? m : 1) * (u128)(uint64_t)(s.use_s ? stale : 1);
+        if (better(N, D, y, bn, bd, bi)) { bn = N; bd = D; bi = y; }
+        s.scores_l++;
+        s.nbr_l += s.rcnt[q];
+        s.adj_l += (s.po[y + 1] - s.po[y]) + (s.co[y + 1] - s.co[y]);
     }
     __syncthreads();
 }
@@ -765,6 +800,8 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         s.cand = (LAS uint16_t *)(lds + a.lds_cand);
         s.stk = (LAS uint16_t *)(lds + a.lds_stk) + lane * LOG_LDS_STACK;
         s.ctr = (LAS uint32_t *)(lds + a.lds_ctr);
+        s.rsum = (LAS int64_t *)(lds + a.lds_rsum);
+        s.rcnt = (LAS int32_t *)(lds + a.lds_rcnt);
         s.last = (Mem<L, int64_t>)(lds + a.lds_last);
         s.sz = (Mem<L, const int64_t>)(lds + a.lds_sz);
     } else {
