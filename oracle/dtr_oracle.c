@@ -1092,6 +1092,9 @@ static int log_lower(log_prog *L, const oracle_log *lg)
                 for (int64_t j = 0; j < nout && rc == 0; j++) {
                     int32_t nm = lg->ids[lo + nin + j];
                     int32_t mi = i + 1 + 2 * (int32_t)j, ai = mi + 1;
+                    for (int64_t q = lo + nin; q < lo + nin + j; q++)
+                        if (lg->ids[q] == nm) rc = -2;          /* an output name listed twice */
+                    if (rc) break;
                     if (BAD_NAME(nm) || name[nm] >= 0 || local[nm] >= 0 || lg->kind[mi] != LG_MEMORY ||
                         lg->kind[ai] != LG_ALIAS || lg->a[mi] != nm || lg->a[ai] != nm) { rc = -2; break; }
                     int32_t src = lg->b[ai];

@@ -161,6 +161,7 @@ def test_malformed_logs_are_rejected(oracle_lib):
         lambda b: (b.call([], [0], 1, [1], [-1]), b.release(0), b.release(0)),      # double release
         lambda b: (b.call([], [0], 1, [1], [-1]), b.call([], [1], 1, [1], [0])),    # view of a non-input
         lambda b: (b.call([], [0], 1, [1], [-1]), b.mutate([0], [3], 1)),           # mutates a non-input
+        lambda b: (b.call([], [0], 1, [1], [-1]), b.call([0], [1, 1], 1, [1, 1], [0, 0])),  # output listed twice
     ]
     for build in bad:
         with pytest.raises(RuntimeError):
