@@ -225,10 +225,10 @@ int dtr_sim_results(dtr_sim *sim, dtr_sim_result *host_out, int32_t n_sims);
  * the storage last became resident; an operator call locks its inputs'
  * storages, defines undefined inputs in listed order, allocates every
  * non-view output, runs, frees the new copies of outputs that were already
- * defined, and unlocks (Appendix C.4).  A storage's cost sums the operators
- * computing any tensor that views it (each once), its dependencies are the
- * storages they read, its staleness counts from the latest reference to any
- * of its tensors (Appendix C.2).  Banishing a storage needs every tensor
+ * defined, and unlocks (Appendix C.4).  A storage's cost sums the operator
+ * cost of every tensor that views it, its dependencies are the storages those
+ * operators read, its staleness counts from the latest reference to any of
+ * its tensors (Appendix C.2).  Banishing a storage needs every tensor
  * computed from it (outside it) defined or gone, and pins their storages.
  * Results: operators count once per execution (views and constants
  * included); failed_op indexes operators in log order. */

@@ -931,10 +931,10 @@ uint64_t oracle_rand_key(uint64_t seed, int64_t eviction_no, int32_t x)
  * storages, defines undefined inputs in listed order (rematerialization),
  * allocates all its non-view outputs, runs, frees the new copies of outputs
  * that were already defined (Appendix C.4), and unlocks.  A storage's cost
- * sums the operators computing any tensor that views it (each once) and its
- * dependencies are the storages those operators read (Appendix C.2, over the
- * views of the whole log); its staleness uses the latest reference to any of
- * its tensors.  Banishing a released storage needs every tensor computed from
+ * sums, over every tensor that views it, the cost of that tensor's operator,
+ * and its dependencies are the storages those operators read (Appendix C.2,
+ * over the views of the whole log); its staleness uses the latest reference
+ * to any of its tensors.  Banishing a released storage needs every tensor computed from
  * it (outside it) defined or gone, and pins their resident storages.
  * Scoring, eviction, union-find, deallocation policies and search
  * approximations are the trace simulator's, run over storages.
@@ -1232,9 +1232,9 @@ static int log_lower(log_prog *L, const oracle_log *lg)
         seen_st[st] = st;                       /* never its own parent */
         for (int64_t q = tb_off[st]; q < tb_off[st + 1]; q++) {
             int64_t o = L->t_op.v[tb[q]];
+            cost += L->op_cost.v[o];           /* one term per tensor viewing the storage */
             if (seen_op[o] == st) continue;
             seen_op[o] = st;
-            cost += L->op_cost.v[o];
             for (int64_t e = L->in_off.v[o]; e < L->in_off.v[o + 1]; e++) {
                 int64_t p = L->t_storage.v[L->ins.v[e]];
                 if (seen_st[p] == st) continue;

@@ -14,8 +14,8 @@
 //     RELEASE drops one; a storage whose last reference goes is released
 //     after the latest operator (release events keep log order); tensors
 //     still referenced at the end are required;
-//   * a storage's cost c0 sums the distinct operators that compute any of its
-//     tensors, its parents are the storages those operators read (never
+//   * a storage's cost c0 sums the cost of the operator of every tensor
+//     viewing it, its parents are the storages those operators read (never
 //     itself), its children are the reverse; a storage's dependents for
 //     banishing are the tensors (outside it) computed by operators reading it.
 //     Constant storages cost 0.
@@ -353,9 +353,9 @@ private:
             int64_t c0 = 0;
             for (int32_t q = tof_off[s]; q < tof_off[s + 1]; q++) {
                 const int32_t o = L.t_op[tof[q]];
+                c0 += L.op_cost[o];                 // a term per tensor of the storage
                 if (op_seen[o] == s) continue;
                 op_seen[o] = s;
-                c0 += L.op_cost[o];
                 for (int32_t e = L.ls_off[o]; e < L.ls_off[o + 1]; e++) {
                     const int32_t p = L.ls[e];
                     if (seen[p] == s) continue;

@@ -16,8 +16,8 @@ it) and operators, and the eviction loop runs over storages.
   * rematerialization (Appendix C.4): lock the input storages, define the
     undefined inputs in listed order, allocate every non-view output, run,
     free the new copies of outputs that were already defined, unlock.
-  * metadata (Appendix C.2): the cost of a storage sums the operators that
-    compute any tensor viewing it (each operator once); its dependencies are
+  * metadata (Appendix C.2): the cost of a storage sums, over the tensors
+    viewing it, the cost of each tensor's operator; its dependencies are
     the storages those operators read (views of the whole log); staleness uses
     the latest reference to any tensor of the storage.
   * banishing: a released storage is banished when no operation holds it and
@@ -146,7 +146,11 @@ class StorageProgram:
         for t, st in enumerate(self.t_storage):
             if self.t_op[t] not in ops_of[st]:
                 ops_of[st].append(self.t_op[t])
-        self.c0 = [0 if self.const[s] else sum(self.op_cost[o] for o in ops_of[s]) for s in range(S)]
+        # cost(S): the operator cost of every tensor viewing S, one term per tensor
+        self.c0 = [0] * S
+        for t, st in enumerate(self.t_storage):
+            if not self.const[st]:
+                self.c0[st] += self.op_cost[self.t_op[t]]
         self.parents = [[] for _ in range(S)]
         for s in range(S):
             for o in ops_of[s]:

@@ -166,3 +166,28 @@ def test_malformed_logs_are_rejected(oracle_lib):
     for build in bad:
         with pytest.raises(RuntimeError):
             run_log(O, _log(build), W.H_DTR, 10)
+
+
+def test_storage_cost_sums_over_its_tensors(oracle_lib):
+    """Appendix C.2 'Cost': cost(S) sums cost(op(t)) over every tensor t
+    viewing S, so an operator returning a storage and a view of it counts
+    twice.  A call returns a (4 units) and a view of a, at cost 3; a second
+    call returns b (4 units) at cost 5; a third call needs 8 units under a
+    budget of 12.  With c = c0 and staleness ablated (score c0/m), a's storage
+    scores 6/4 and b's 5/4, so b is evicted (counting the call once would give
+    3/4 and evict a).  c is released at once; the output condition then
+    rematerializes b: total cost 3 + 5 + 1 + 5 = 14."""
+    b = W.LogBuilder("shared-op")
+    a, av, bb, c = b.fresh(), b.fresh(), b.fresh(), b.fresh()
+    b.call([], [a, av], 3, [4, 4], [-1, a])
+    b.call([], [bb], 5, [4], [-1])
+    b.call([], [c], 1, [8], [-1])
+    b.release(c)
+    L = b.build()
+    h = W.h_family(W.C_LOCAL, 0, 1)
+    r = run_log(oracle_lib, L, h, 12)
+    assert int(r["status"]) == 0
+    assert (int(r["n_evictions"]), int(r["n_eager_evictions"]), int(r["n_remats"])) == (1, 1, 1)
+    assert (int(r["remat_cost"]), int(r["total_cost"])) == (5, 14)
+    assert int(r["peak_memory"]) == 12
+    assert brute_log.simulate(L, 12, h, 0)["total_cost"] == 14
