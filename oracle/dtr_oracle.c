@@ -230,6 +230,11 @@ typedef struct {
      * tensor's operator last ran (NULL for plain traces) */
     int64_t *sgen, *gen;
     const void *logp;             /* the lowered log (log replay only) */
+    /* log replay: the storage graph as of now (Appendix C.2: indexed by time),
+     * grown when an operator first creates its tensors */
+    int64_t *dc0;                 /* cost of each storage's tensors created so far */
+    int32_t **dpar, **dch;        /* parents and children created so far */
+    int64_t *npar, *nch, *cpar, *cch;   /* their counts and capacities */
 
     /* scratch for neighbourhood walks */
     int64_t *mark;                /* epoch stamps */
@@ -332,26 +337,48 @@ static void release(sim *s, int32_t t)
     }
 }
 
+/* Neighbours and local cost of node u.  A trace's graph is static: parents
+ * are the inputs of u's parent operation, children the outputs of the
+ * operations reading u.  A log's storage graph is the one that exists now. */
+static int64_t n_par(const sim *s, int32_t u)
+{
+    if (s->logp) return s->npar[u];
+    int32_t o = s->g->producer[u];
+    return o < 0 ? 0 : s->tr->op_input_offsets[o + 1] - s->tr->op_input_offsets[o];
+}
+static int32_t par_at(const sim *s, int32_t u, int64_t k)
+{
+    if (s->logp) return s->dpar[u][k];
+    return s->tr->op_inputs[s->tr->op_input_offsets[s->g->producer[u]] + k];
+}
+static int64_t n_ch(const sim *s, int32_t u)
+{
+    if (s->logp) return s->nch[u];
+    return s->g->ch_off[u + 1] - s->g->ch_off[u];
+}
+static int32_t ch_at(const sim *s, int32_t u, int64_t k)
+{
+    if (s->logp) return s->dch[u][k];
+    return s->g->ch[s->g->ch_off[u] + k];
+}
+static int64_t c0_of(const sim *s, int32_t u) { return s->logp ? s->dc0[u] : s->g->c0[u]; }
+
 /* e_R(x) (Section 4.1): evicted tensors reachable from x through evicted
  * parents only, i.e. those that rematerializing x would rematerialize.
  * Returns the sum of their local costs; the set size goes to *count. */
 static int64_t ancestors_cost(sim *s, int32_t x, int64_t *count)
 {
-    const graph *g = s->g;
-    const oracle_trace *tr = s->tr;
     int64_t sum = 0, cnt = 0;
     s->epoch++;
     int64_t head = 0, tail = 0;
     s->queue[tail++] = x;
     while (head < tail) {
         int32_t u = s->queue[head++];
-        int32_t o = g->producer[u];
-        if (o < 0) continue;
-        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
-            int32_t p = tr->op_inputs[e];
+        for (int64_t k = 0; k < n_par(s, u); k++) {
+            int32_t p = par_at(s, u, k);
             if (s->state[p] != ST_EVICTED || s->mark[p] == s->epoch) continue;
             s->mark[p] = s->epoch;
-            sum += g->c0[p];
+            sum += c0_of(s, p);
             cnt++;
             s->queue[tail++] = p;
         }
@@ -367,7 +394,6 @@ static int64_t ancestors_cost(sim *s, int32_t x, int64_t *count)
  * *count. */
 static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
 {
-    const graph *g = s->g;
     int64_t cnt = 0;
     int64_t sum = ancestors_cost(s, x, &cnt);
     /* descendants (same epoch: a tensor is never on both sides) */
@@ -375,11 +401,11 @@ static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
     s->queue[tail++] = x;
     while (head < tail) {
         int32_t u = s->queue[head++];
-        for (int64_t e = g->ch_off[u]; e < g->ch_off[u + 1]; e++) {
-            int32_t c = g->ch[e];
+        for (int64_t k = 0; k < n_ch(s, u); k++) {
+            int32_t c = ch_at(s, u, k);
             if (s->state[c] != ST_EVICTED || s->mark[c] == s->epoch) continue;
             s->mark[c] = s->epoch;
-            sum += g->c0[c];
+            sum += c0_of(s, c);
             cnt++;
             s->queue[tail++] = c;
         }
@@ -393,23 +419,19 @@ static int64_t estar_cost(sim *s, int32_t x, int64_t *count)
  * merged only for the query (no union is performed). */
 static int64_t eq_cost(sim *s, int32_t x, int64_t *count)
 {
-    const graph *g = s->g;
-    const oracle_trace *tr = s->tr;
     int64_t sum = 0, cnt = 0;
     s->epoch++;
-    int32_t o = g->producer[x];
-    if (o >= 0)
-        for (int64_t e = tr->op_input_offsets[o]; e < tr->op_input_offsets[o + 1]; e++) {
-            int32_t p = tr->op_inputs[e];
-            if (s->state[p] != ST_EVICTED) continue;
-            cnt++;
-            int32_t r = uf_find(s, s->node_of[p]);
-            if (s->uf_mark[r] == s->epoch) continue;
-            s->uf_mark[r] = s->epoch;
-            sum += s->uf_cost[r];
-        }
-    for (int64_t e = g->ch_off[x]; e < g->ch_off[x + 1]; e++) {
-        int32_t c = g->ch[e];
+    for (int64_t k = 0; k < n_par(s, x); k++) {
+        int32_t p = par_at(s, x, k);
+        if (s->state[p] != ST_EVICTED) continue;
+        cnt++;
+        int32_t r = uf_find(s, s->node_of[p]);
+        if (s->uf_mark[r] == s->epoch) continue;
+        s->uf_mark[r] = s->epoch;
+        sum += s->uf_cost[r];
+    }
+    for (int64_t k = 0; k < n_ch(s, x); k++) {
+        int32_t c = ch_at(s, x, k);
         if (s->state[c] != ST_EVICTED) continue;
         cnt++;
         int32_t r = uf_find(s, s->node_of[c]);
@@ -421,13 +443,7 @@ static int64_t eq_cost(sim *s, int32_t x, int64_t *count)
     return sum;
 }
 
-static int64_t degree(const sim *s, int32_t x)
-{
-    int32_t o = s->g->producer[x];
-    int64_t d = s->g->ch_off[x + 1] - s->g->ch_off[x];
-    if (o >= 0) d += s->tr->op_input_offsets[o + 1] - s->tr->op_input_offsets[o];
-    return d;
-}
+static int64_t degree(const sim *s, int32_t x) { return n_par(s, x) + n_ch(s, x); }
 
 /* SplitMix64 (Steele, Lea and Flood, OOPSLA 2014): state advanced by the
  * golden-ratio gamma, then the variant-13 output mix. */
@@ -443,7 +459,7 @@ static void score(sim *s, int32_t x, uint64_t *N, u128 *D)
 {
     int64_t stale = s->clock - s->last_access[x];   /* >= 1 by construction */
     int64_t m = s->tr->tensor_size[x];
-    int64_t c0 = s->g->c0[x];
+    int64_t c0 = c0_of(s, x);
     int64_t cnt = 0;
     if (stale < 1) abort();
     switch (s->heuristic) {
@@ -534,15 +550,13 @@ static void evict(sim *s, int32_t v, int eager)
     if (uses_uf(s->heuristic)) {
         /* add c0(v) to its component, then union with every evicted neighbour */
         int32_t r = uf_find(s, s->node_of[v]);
-        s->uf_cost[r] += s->g->c0[v];
-        int32_t o = s->g->producer[v];
-        if (o >= 0)
-            for (int64_t e = s->tr->op_input_offsets[o]; e < s->tr->op_input_offsets[o + 1]; e++) {
-                int32_t p = s->tr->op_inputs[e];
-                if (s->state[p] == ST_EVICTED) r = uf_union(s, r, s->node_of[p]);
-            }
-        for (int64_t e = s->g->ch_off[v]; e < s->g->ch_off[v + 1]; e++) {
-            int32_t c = s->g->ch[e];
+        s->uf_cost[r] += c0_of(s, v);
+        for (int64_t k = 0; k < n_par(s, v); k++) {
+            int32_t p = par_at(s, v, k);
+            if (s->state[p] == ST_EVICTED) r = uf_union(s, r, s->node_of[p]);
+        }
+        for (int64_t k = 0; k < n_ch(s, v); k++) {
+            int32_t c = ch_at(s, v, k);
             if (s->state[c] == ST_EVICTED) r = uf_union(s, r, s->node_of[c]);
         }
     }
@@ -932,9 +946,11 @@ uint64_t oracle_rand_key(uint64_t seed, int64_t eviction_no, int32_t x)
  * allocates all its non-view outputs, runs, frees the new copies of outputs
  * that were already defined (Appendix C.4), and unlocks.  A storage's cost
  * sums, over every tensor that views it, the cost of that tensor's operator,
- * and its dependencies are the storages those operators read (Appendix C.2,
- * over the views of the whole log); its staleness uses the latest reference
- * to any of its tensors.  Banishing a released storage needs every tensor computed from
+ * and its dependencies are the storages those operators read (Appendix C.2);
+ * both cover the tensors that exist, so they grow when the first run of an
+ * operator creates its tensors (the graph is indexed by time, and the cost
+ * changes when a view is made); its staleness uses the latest reference to
+ * any of its tensors.  Banishing a released storage needs every tensor computed from
  * it (outside it) defined or gone, and pins their resident storages.
  * Scoring, eviction, union-find, deallocation policies and search
  * approximations are the trace simulator's, run over storages.
@@ -1322,6 +1338,40 @@ static void log_try_banish(sim *s, int32_t st)
     }
 }
 
+static int push32(int32_t **v, int64_t *n, int64_t *cap, int32_t e)
+{
+    if (*n == *cap) {
+        int64_t c = *cap ? 2 * *cap : 4;
+        int32_t *q = realloc(*v, sizeof(int32_t) * (size_t)c);
+        if (!q) return -1;
+        *v = q;
+        *cap = c;
+    }
+    (*v)[(*n)++] = e;
+    return 0;
+}
+
+/* The first run of operator o creates its tensors: each adds the operator's
+ * cost to its storage's cost and makes the storages o reads (other than its
+ * own) parents of it (Appendix C.2, over the tensors that exist). */
+static void log_create(sim *s, const log_prog *L, int64_t o)
+{
+    for (int64_t q = L->out_off.v[o]; q < L->out_off.v[o + 1]; q++) {
+        int32_t st = (int32_t)L->t_storage.v[L->outs.v[q]];
+        if (!L->s_const.v[st]) s->dc0[st] += L->op_cost.v[o];
+        for (int64_t e = L->in_off.v[o]; e < L->in_off.v[o + 1]; e++) {
+            int32_t p = (int32_t)L->t_storage.v[L->ins.v[e]];
+            if (p == st) continue;
+            int known = 0;
+            for (int64_t k = 0; k < s->npar[st] && !known; k++) known = s->dpar[st][k] == p;
+            if (known) continue;
+            if (push32(&s->dpar[st], &s->npar[st], &s->cpar[st], p) ||
+                push32(&s->dch[p], &s->nch[p], &s->cch[p], st))
+                abort();
+        }
+    }
+}
+
 /* run operator o (a rematerialization if remat), defining its outputs */
 static void log_call(sim *s, const log_prog *L, int64_t o, int remat)
 {
@@ -1361,7 +1411,7 @@ static void log_call(sim *s, const log_prog *L, int64_t o, int remat)
         if (uses_uf(s->heuristic)) {
             if (was_evicted) {
                 int32_t r = uf_find(s, s->node_of[st]);
-                s->uf_cost[r] -= s->g->c0[st];
+                s->uf_cost[r] -= c0_of(s, st);
             }
             int32_t nd = uf_new(s);
             if (nd < 0) abort();
@@ -1372,6 +1422,7 @@ static void log_call(sim *s, const log_prog *L, int64_t o, int remat)
         int32_t v = L->outs.v[e];
         if (L->t_alias.v[v]) s->gen[v] = s->sgen[L->t_storage.v[v]];
     }
+    if (!remat) log_create(s, L, o);
     if (s->clock >= CLOCK_LIMIT) { s->r[R_STATUS] = OS_CLOCK_OVERFLOW; s->stopped = OS_CLOCK_OVERFLOW; return; }
     for (int64_t e = ib; e < ie; e++) unlock(s, (int32_t)L->t_storage.v[L->ins.v[e]]);
     if (remat && s->policy == OP_BANISH)
@@ -1429,9 +1480,16 @@ static int run_one_log(const log_prog *L, const oracle_spec *sp, int64_t *result
     s.mark = calloc(sn, sizeof(int64_t));
     s.sgen = calloc(sn, sizeof(int64_t));
     s.gen = malloc(sizeof(int64_t) * tn);
+    s.dc0 = calloc(sn, sizeof(int64_t));
+    s.dpar = calloc(sn, sizeof(int32_t *));
+    s.dch = calloc(sn, sizeof(int32_t *));
+    s.npar = calloc(sn, sizeof(int64_t));
+    s.nch = calloc(sn, sizeof(int64_t));
+    s.cpar = calloc(sn, sizeof(int64_t));
+    s.cch = calloc(sn, sizeof(int64_t));
     int rc = 0;
     if (!s.state || !s.pinned || !s.pending || !s.locks || !s.last_access || !s.node_of || !s.queue || !s.mark ||
-        !s.sgen || !s.gen)
+        !s.sgen || !s.gen || !s.dc0 || !s.dpar || !s.dch || !s.npar || !s.nch || !s.cpar || !s.cch)
         rc = -1;
     else {
         for (int64_t i = 0; i < S; i++) s.node_of[i] = -1;
@@ -1442,6 +1500,8 @@ static int run_one_log(const log_prog *L, const oracle_spec *sp, int64_t *result
     }
     free(s.state); free(s.pinned); free(s.pending); free(s.locks); free(s.last_access); free(s.node_of);
     free(s.queue); free(s.mark); free(s.sgen); free(s.gen);
+    for (int64_t i = 0; i < S && s.dpar && s.dch; i++) { free(s.dpar[i]); free(s.dch[i]); }
+    free(s.dc0); free(s.dpar); free(s.dch); free(s.npar); free(s.nch); free(s.cpar); free(s.cch);
     free(s.uf_parent); free(s.uf_cost); free(s.uf_mark);
     return rc;
 }

@@ -16,9 +16,11 @@
 //     still referenced at the end are required;
 //   * a storage's cost c0 sums the cost of the operator of every tensor
 //     viewing it, its parents are the storages those operators read (never
-//     itself), its children are the reverse; a storage's dependents for
-//     banishing are the tensors (outside it) computed by operators reading it.
-//     Constant storages cost 0.
+//     itself), its children are the reverse, all over the tensors that exist:
+//     the first run of an operator creates its tensors, so the replay grows
+//     costs and edges as it goes (the lists below are ordered for that); a
+//     storage's dependents for banishing are the tensors (outside it)
+//     computed by operators reading it.  Constant storages cost 0.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -27,6 +29,7 @@
 #include <cstdio>
 #include <cstring>
 #include <numeric>
+#include <unordered_set>
 #include <vector>
 
 #include "host.h"
@@ -48,6 +51,7 @@ struct Lowered {
     std::vector<int64_t> s_size, s_c0;
     std::vector<uint8_t> s_const;
     std::vector<int32_t> par_off, par, ch_off, ch, dt_off, dt;
+    std::vector<int32_t> born_off, born;   // per operator: edges its first run creates (parent, storage)
     // tensors
     std::vector<int32_t> t_storage, t_op;
     std::vector<uint8_t> t_alias;
@@ -335,48 +339,45 @@ private:
             }
             L.ls_off[o + 1] = (int32_t)L.ls.size();
         }
-        // per storage: the distinct operators of its tensors (cost), the
-        // storages they read (parents)
-        std::vector<int32_t> tof_off, tof;
-        {
-            std::vector<int32_t> ids(T);
-            std::iota(ids.begin(), ids.end(), 0);
-            csr(S, L.t_storage, ids, tof_off, tof);
-        }
-        std::vector<int32_t> op_seen(std::max(F, 1), -1);
-        std::fill(seen.begin(), seen.end(), -1);
+        // the storage graph in the order its edges appear: an operator's first
+        // run creates its tensors, and each makes the storages the operator
+        // reads parents of its own storage.  Both lists of every storage are
+        // ordered by the operator creating the edge, so the edges that exist
+        // at any time are a prefix; born_* lists each operator's new edges.
+        // The costs of the storages at the end bound every score.
         L.s_c0.assign(S, 0);
-        L.par_off.assign(S + 1, 0);
         int64_t c0_sum = 0;
-        for (int32_t s = 0; s < S; s++) {
-            seen[s] = s;
-            int64_t c0 = 0;
-            for (int32_t q = tof_off[s]; q < tof_off[s + 1]; q++) {
-                const int32_t o = L.t_op[tof[q]];
-                c0 += L.op_cost[o];                 // a term per tensor of the storage
-                if (op_seen[o] == s) continue;
-                op_seen[o] = s;
-                for (int32_t e = L.ls_off[o]; e < L.ls_off[o + 1]; e++) {
-                    const int32_t p = L.ls[e];
-                    if (seen[p] == s) continue;
-                    seen[p] = s;
-                    L.par.push_back(p);
-                    if ((int64_t)L.par.size() >= MAX_ITEMS) return bad(-1, "storage graph exceeds 2^26 edges");
-                }
-            }
-            L.s_c0[s] = L.s_const[s] ? 0 : c0;
-            c0_sum += L.s_c0[s];
+        for (int32_t t = 0; t < T; t++) {
+            const int32_t st = L.t_storage[t];
+            if (L.s_const[st]) continue;
+            L.s_c0[st] += L.op_cost[L.t_op[t]];     // a term per tensor of the storage
+            c0_sum += L.op_cost[L.t_op[t]];
             if (c0_sum >= MAX_C0_SUM) return bad(-1, "storage costs sum to 2^50 or more");
-            L.par_off[s + 1] = (int32_t)L.par.size();
         }
         {
-            std::vector<int32_t> key, val;
-            for (int32_t s = 0; s < S; s++)
-                for (int32_t e = L.par_off[s]; e < L.par_off[s + 1]; e++) {
-                    key.push_back(L.par[e]);
-                    val.push_back(s);
+            std::unordered_set<uint64_t> edges;
+            std::vector<int32_t> pk, pv, ck, cv;    // (storage, neighbour) in creation order
+            L.born_off.assign(F + 1, 0);
+            for (int32_t o = 0; o < F; o++) {
+                for (int32_t q = L.out_off[o]; q < L.out_off[o + 1]; q++) {
+                    const int32_t st = L.t_storage[L.out[q]];
+                    for (int32_t e = L.ls_off[o]; e < L.ls_off[o + 1]; e++) {
+                        const int32_t par = L.ls[e];
+                        if (par == st || !edges.insert(((uint64_t)(uint32_t)par << 32) | (uint32_t)st).second)
+                            continue;
+                        pk.push_back(st);
+                        pv.push_back(par);
+                        ck.push_back(par);
+                        cv.push_back(st);
+                        L.born.push_back(par);
+                        L.born.push_back(st);
+                        if ((int64_t)pk.size() >= MAX_ITEMS) return bad(-1, "storage graph exceeds 2^26 edges");
+                    }
                 }
-            csr(S, key, val, L.ch_off, L.ch);
+                L.born_off[o + 1] = (int32_t)(L.born.size() / 2);
+            }
+            csr(S, pk, pv, L.par_off, L.par);       // a stable fill keeps creation order
+            csr(S, ck, cv, L.ch_off, L.ch);
         }
         // banishing dependents: outputs (outside p) of every operator reading p
         {
@@ -404,7 +405,8 @@ size_t log_bytes(const Lowered &d)
            bytes_of(d.ch_off) + bytes_of(d.ch) + bytes_of(d.dt_off) + bytes_of(d.dt) + bytes_of(d.t_storage) +
            bytes_of(d.t_op) + bytes_of(d.t_alias) + bytes_of(d.op_cost) + bytes_of(d.op_need) +
            bytes_of(d.in_off) + bytes_of(d.in) + bytes_of(d.ls_off) + bytes_of(d.ls) + bytes_of(d.out_off) +
-           bytes_of(d.out) + bytes_of(d.rel_off) + bytes_of(d.rel) + bytes_of(d.req) + 24 * ALIGN;
+           bytes_of(d.out) + bytes_of(d.rel_off) + bytes_of(d.rel) + bytes_of(d.req) + bytes_of(d.born_off) +
+           bytes_of(d.born) + 26 * ALIGN;
 }
 
 }  // namespace
@@ -417,6 +419,7 @@ struct LogPlan {
     int32_t n_slots = 1;
     int32_t lds_bytes = 0, lds_state = 0, lds_wm = 0, lds_po = 0, lds_co = 0, lds_pa = 0, lds_ca = 0, wm_words = 0;
     int32_t lds_c0 = 0, lds_cand = 0, lds_stk = 0, lds_ctr = 0, lds_sz = 0, lds_last = 0, lds_rsum = 0, lds_rcnt = 0;
+    int32_t lds_pcnt = 0, lds_ccnt = 0;
     std::vector<size_t> log_off;
     size_t desc_off = 0, spec_off = 0, order_off = 0, tables_bytes = 0, result_off = 0, slot_off = 0, total = 0;
 };
@@ -469,6 +472,9 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
     take(L.sgen, 8 * S);
     take(L.last, 8 * S);
     take(L.gen, 8 * (size_t)T_max);
+    take(L.c0d, 8 * S);
+    take(L.pcnt, 4 * S);
+    take(L.ccnt, 4 * S);
     take(L.uf_parent, 4 * U);
     take(L.uf_size, 4 * U);
     take(L.uf_remap, 4 * U);
@@ -499,6 +505,8 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
         at(p->lds_last, 8 * (size_t)S_max);
         at(p->lds_rsum, 8 * (size_t)S_max);
         at(p->lds_rcnt, 4 * (size_t)S_max);
+        at(p->lds_pcnt, 4 * (size_t)S_max);
+        at(p->lds_ccnt, 4 * (size_t)S_max);
         int dev = 0, lds_max = 0;
         if (hipGetDevice(&dev) != hipSuccess ||
             hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
@@ -596,6 +604,8 @@ int log_plan_upload(LogPlan *p, uint8_t *ws, hipStream_t st)
         D.rel_off = put(d.rel_off);
         D.rel = put(d.rel);
         D.req = put(d.req);
+        D.born_off = put(d.born_off);
+        D.born = put(d.born);
     }
     std::memcpy(H + p->desc_off, descs.data(), sizeof(dtr::LogProgDev) * n_logs);
     for (int32_t i = 0; i < n_sims; i++) {
@@ -638,6 +648,8 @@ int log_plan_launch(const LogPlan *p, uint8_t *ws, hipStream_t st)
     a.lds_last = p->lds_last;
     a.lds_rsum = p->lds_rsum;
     a.lds_rcnt = p->lds_rcnt;
+    a.lds_pcnt = p->lds_pcnt;
+    a.lds_ccnt = p->lds_ccnt;
     hipError_t e = dtr_launch_log(&a, st);
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return DTR_OK;

@@ -15,10 +15,10 @@ struct LogProgDev {
     int32_t S, T, F, n_req;
     // storages
     const int64_t *s_size;        // [S]
-    const int64_t *s_c0;          // [S] summed cost of the operators computing its tensors
+    const int64_t *s_c0;          // [S] summed cost of the operators computing its tensors (end of log)
     const uint8_t *s_const;       // [S] constant (pinned from creation)
     const int32_t *par_off, *par; // storage graph: parents (distinct input storages of those operators)
-    const int32_t *ch_off, *ch;   //   and children
+    const int32_t *ch_off, *ch;   //   and children; each list in the order its edges are created
     const int32_t *dt_off, *dt;   // tensors computed from the storage outside it (banishing)
     // tensors
     const int32_t *t_storage;     // [T]
@@ -32,6 +32,7 @@ struct LogProgDev {
     const int32_t *out_off, *out; // output tensors
     const int32_t *rel_off, *rel; // storages released after each operator, in log order
     const int32_t *req;           // [n_req] tensors still referenced at the end, ascending
+    const int32_t *born_off, *born; // per operator: (parent, storage) edges its first run creates
 };
 
 // Per-slot working memory of the log replay, sized for the largest log of
@@ -43,6 +44,8 @@ struct LogProgDev {
 //   sgen, last             i64 [S_max]  residency generation; last access
 //   gen                    i64 [T_max]  generation at which each tensor's
 //                                       operator last ran
+//   c0d, pcnt, ccnt        i64/i32/i32 [S_max]  costs and edge counts of the
+//                                       storage graph created so far
 //   uf_*                   [ucap]       union-find nodes (parent, set size,
 //                                       running cost), the compaction map and
 //                                       a cost staging array
@@ -59,6 +62,7 @@ struct LogSlotLayout {
     int64_t sgen, last;
     int64_t gen;
     int64_t uf_parent, uf_size, uf_remap, uf_cost, uf_tmp;
+    int64_t c0d, pcnt, ccnt;          // the graph created so far (device-memory variant)
     int64_t mark, wmark, queue;
     int64_t stack;
     int64_t S_max, T_max, F_max, ucap, mcap;
@@ -88,6 +92,7 @@ struct LogKernelArgs {
     int32_t lds_c0, lds_cand, lds_stk, lds_ctr;
     int32_t lds_sz, lds_last;  // storage sizes and last-access times
     int32_t lds_rsum, lds_rcnt;  // per listed candidate: walked cost, count
+    int32_t lds_pcnt, lds_ccnt;  // edges created so far per storage
     int32_t wm_words;         // 32-bit words per visited bitset (a multiple of 4)
 };
 

@@ -113,6 +113,7 @@ struct ProgG {
     const GAS uint8_t *t_alias;
     const GAS int64_t *op_cost, *op_need;
     const GAS int32_t *in_off, *in, *ls_off, *ls, *out_off, *out, *rel_off, *rel, *req;
+    const GAS int32_t *born_off, *born;
 };
 
 __device__ __forceinline__ ProgG prog_global(const LogProgDev &d)
@@ -145,6 +146,8 @@ __device__ __forceinline__ ProgG prog_global(const LogProgDev &d)
     g.rel_off = (const GAS int32_t *)d.rel_off;
     g.rel = (const GAS int32_t *)d.rel;
     g.req = (const GAS int32_t *)d.req;
+    g.born_off = (const GAS int32_t *)d.born_off;
+    g.born = (const GAS int32_t *)d.born;
     return g;
 }
 
@@ -155,9 +158,12 @@ struct Sim {
     Mem<L, uint32_t> wm;         // this lane's visited bitset (walks)
     Mem<L, const int32_t> po, co;          // storage graph: parents, children
     Mem<L, const Adj<L>> pa, ca;
+    // the graph that exists so far: edges per list (a prefix, lists being in
+    // creation order) and each storage's cost over its tensors created so far
+    Mem<L, int32_t> pcnt, ccnt;
+    Mem<L, int64_t> c0d;
     // walk scan in LDS (L only): storage costs, candidate list, this lane's
     // pending stack, the candidate counter
-    LAS int64_t *c0l;
     LAS uint16_t *cand, *stk;
     LAS uint32_t *ctr;
     LAS int64_t *rsum;         // per listed candidate: walked cost and count
@@ -312,17 +318,18 @@ __device__ int64_t walk_cost(Sim<L> &s, int32_t x, bool both, int64_t &cnt)
     for (int side = 0; side < (both ? 2 : 1); side++) {
         const auto off = side == 0 ? s.po : s.co;
         const auto adj = side == 0 ? s.pa : s.ca;
+        const auto num = side == 0 ? s.pcnt : s.ccnt;
         int32_t head = tail;
         s.queue[tail++] = x;
         while (head < tail) {
             const int32_t u = s.queue[head++];
-            for (int32_t e = off[u], end = off[u + 1]; e < end; e++) {
+            for (int32_t e = off[u], end = off[u] + num[u]; e < end; e++) {
                 const int32_t v = adj[e];
                 if (s.state[v] != ST_EVICTED) continue;
                 const uint32_t bit = 1u << (v & 31), w = s.wm[v >> 5];
                 if (w & bit) continue;
                 s.wm[v >> 5] = w | bit;
-                sum += s.P.s_c0[v];
+                sum += s.c0d[v];
                 cnt++;
                 s.queue[tail++] = v;
             }
@@ -345,7 +352,8 @@ __device__ int64_t eq_cost(Sim<L> &s, int32_t x, int64_t &cnt)
     for (int side = 0; side < 2; side++) {
         const auto off = side == 0 ? s.po : s.co;
         const auto adj = side == 0 ? s.pa : s.ca;
-        for (int32_t e = off[x]; e < off[x + 1]; e++) {
+        const int32_t n = side == 0 ? s.pcnt[x] : s.ccnt[x];
+        for (int32_t e = off[x]; e < off[x] + n; e++) {
             const int32_t v = adj[e];
             if (s.state[v] != ST_EVICTED) continue;
             cnt++;
@@ -363,8 +371,8 @@ __device__ __forceinline__ void score(Sim<L> &s, int32_t x, uint64_t &N, u128 &D
 {
     const int64_t m = s.sz[x];
     const int64_t stale = s.clock - s.last[x];
-    const int64_t c0 = s.P.s_c0[x];
-    const int64_t deg = (s.po[x + 1] - s.po[x]) + (s.co[x + 1] - s.co[x]);
+    const int64_t c0 = s.c0d[x];
+    const int64_t deg = s.pcnt[x] + s.ccnt[x];
     int64_t cnt = 0;
     switch (s.cmode) {
     case CM_ESTAR: N = (uint64_t)(c0 + walk_cost(s, x, true, cnt)); break;
@@ -403,13 +411,14 @@ __device__ void evict(Sim<L> &s, int32_t st, bool eager)
     const int32_t nd = s.uf_n++;
     s.ufp[nd] = nd;
     s.ufs[nd] = 1;
-    s.ufc[nd] = s.P.s_c0[st];
+    s.ufc[nd] = s.c0d[st];
     s.node[st] = nd;
     int32_t r = nd;
     for (int side = 0; side < 2; side++) {
         const auto off = side == 0 ? s.po : s.co;
         const auto adj = side == 0 ? s.pa : s.ca;
-        for (int32_t e = off[st]; e < off[st + 1]; e++) {
+        const int32_t n = side == 0 ? s.pcnt[st] : s.ccnt[st];
+        for (int32_t e = off[st]; e < off[st] + n; e++) {
             const int32_t v = adj[e];
             if (s.state[v] == ST_EVICTED) r = uf_unite(s, r, s.node[v]);
         }
@@ -462,7 +471,7 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
         if (x >= 0) {
             side = 0;
             e = s.po[x];
-            end = s.po[x + 1];
+            end = e + s.pcnt[x];
             sum = 0;
             cnt = 0;
         }
@@ -486,11 +495,11 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
             if (spl > 0 || spg > 0) {
                 const int32_t u = spl > 0 ? (int32_t)s.stk[--spl] : s.queue[--spg];
                 e = side == 0 ? s.po[u] : s.co[u];
-                end = side == 0 ? s.po[u + 1] : s.co[u + 1];
+                end = e + (side == 0 ? s.pcnt[u] : s.ccnt[u]);
             } else if (side == 0 && both) {
                 side = 1;
                 e = s.co[x];
-                end = s.co[x + 1];
+                end = e + s.ccnt[x];
             } else {
                 s.rsum[k] = sum;
                 s.rcnt[k] = cnt;
@@ -519,13 +528,13 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
                 if (n2) s.wm[i2] = w2 | b2;
             }
             if (n1) {
-                sum += s.c0l[v1];
+                sum += s.c0d[v1];
                 cnt++;
                 if (spl < LOG_LDS_STACK) s.stk[spl++] = (uint16_t)v1;
                 else s.queue[spg++] = v1;
             }
             if (n2) {
-                sum += s.c0l[v2];
+                sum += s.c0d[v2];
                 cnt++;
                 if (spl < LOG_LDS_STACK) s.stk[spl++] = (uint16_t)v2;
                 else s.queue[spg++] = v2;
@@ -538,12 +547,12 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
         const int32_t y = s.cand[q];
         const int64_t m = s.sz[y];
         const int64_t stale = s.clock - s.last[y];
-        const uint64_t N = (uint64_t)(s.c0l[y] + s.rsum[q]);
+        const uint64_t N = (uint64_t)(s.c0d[y] + s.rsum[q]);
         const u128 D = (u128)(uint64_t)(s.use_m ? m : 1) * (u128)(uint64_t)(s.use_s ? stale : 1);
         if (better(N, D, y, bn, bd, bi)) { bn = N; bd = D; bi = y; }
         s.scores_l++;
         s.nbr_l += s.rcnt[q];
-        s.adj_l += (s.po[y + 1] - s.po[y]) + (s.co[y + 1] - s.co[y]);
+        s.adj_l += s.pcnt[y] + s.ccnt[y];
     }
     __syncthreads();
 }
@@ -717,13 +726,26 @@ __device__ void execute(Sim<L> &s, int32_t o, bool remat)
         s.gen[v] = g;
         if (s.uf && was == ST_EVICTED) {
             const int32_t r = uf_find(s, s.node[st]);
-            s.ufc[r] -= s.P.s_c0[st];
+            s.ufc[r] -= s.c0d[st];
             s.node[st] = -1;
         }
     }
     for (int32_t q = ob; q < oe; q++) {
         const int32_t v = s.P.out[q];
         if (s.P.t_alias[v]) s.gen[v] = s.sgen[s.P.t_storage[v]];
+    }
+    if (!remat) {
+        // the operator's first run creates its tensors: their costs join
+        // their storages' and their edges join the graph (Appendix C.2)
+        for (int32_t q = ob; q < oe; q++) {
+            const int32_t st = s.P.t_storage[s.P.out[q]];
+            if (!s.P.s_const[st]) s.c0d[st] += c;
+        }
+        for (int32_t b = s.P.born_off[o]; b < s.P.born_off[o + 1]; b++) {
+            const int32_t par = s.P.born[2 * b], st = s.P.born[2 * b + 1];
+            s.pcnt[st] += 1;
+            s.ccnt[par] += 1;
+        }
     }
     if (s.clock >= CLOCK_LIMIT) { s.status = STATUS_CLOCK; return; }
     for (int32_t e = s.P.ls_off[o]; e < s.P.ls_off[o + 1]; e++) s.locks[s.P.ls[e]] -= 1;
@@ -796,7 +818,9 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         s.co = (Mem<L, const int32_t>)(lds + a.lds_co);
         s.pa = (Mem<L, const Adj<L>>)(lds + a.lds_pa);
         s.ca = (Mem<L, const Adj<L>>)(lds + a.lds_ca);
-        s.c0l = (LAS int64_t *)(lds + a.lds_c0);
+        s.c0d = (Mem<L, int64_t>)(lds + a.lds_c0);
+        s.pcnt = (Mem<L, int32_t>)(lds + a.lds_pcnt);
+        s.ccnt = (Mem<L, int32_t>)(lds + a.lds_ccnt);
         s.cand = (LAS uint16_t *)(lds + a.lds_cand);
         s.stk = (LAS uint16_t *)(lds + a.lds_stk) + lane * LOG_LDS_STACK;
         s.ctr = (LAS uint32_t *)(lds + a.lds_ctr);
@@ -813,6 +837,9 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         s.ca = (Mem<L, const Adj<L>>)s.P.ch;
         s.last = (Mem<L, int64_t>)(gb + Y.last);
         s.sz = s.P.s_size;
+        s.c0d = (Mem<L, int64_t>)(gb + Y.c0d);
+        s.pcnt = (Mem<L, int32_t>)(gb + Y.pcnt);
+        s.ccnt = (Mem<L, int32_t>)(gb + Y.ccnt);
     }
     s.budget = sp.budget;
     s.seed = sp.seed;
@@ -856,6 +883,9 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         s.node[i] = -1;
         s.sgen[i] = 0;
         s.last[i] = 0;
+        s.c0d[i] = 0;
+        s.pcnt[i] = 0;
+        s.ccnt[i] = 0;
     }
     for (int32_t i = lane; i < T; i += WAVE) s.gen[i] = -1;
     if (s.uf) {
@@ -881,10 +911,7 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
             ca[e] = (Adj<L>)s.P.ch[e];
         }
         Mem<L, int64_t> szl = (Mem<L, int64_t>)s.sz;
-        for (int32_t i = lane; i < S; i += WAVE) {
-            s.c0l[i] = s.P.s_c0[i];
-            szl[i] = s.P.s_size[i];
-        }
+        for (int32_t i = lane; i < S; i += WAVE) szl[i] = s.P.s_size[i];
     }
     __syncthreads();
 

@@ -16,15 +16,18 @@ it) and operators, and the eviction loop runs over storages.
   * rematerialization (Appendix C.4): lock the input storages, define the
     undefined inputs in listed order, allocate every non-view output, run,
     free the new copies of outputs that were already defined, unlock.
-  * metadata (Appendix C.2): the cost of a storage sums, over the tensors
-    viewing it, the cost of each tensor's operator; its dependencies are
-    the storages those operators read (views of the whole log); staleness uses
-    the latest reference to any tensor of the storage.
+  * metadata (Appendix C.2, indexed by time): a tensor exists once its
+    operator has first run; the cost of a storage sums, over its tensors that
+    exist, the cost of each tensor's operator, and its dependencies are the
+    storages those operators read; staleness uses the latest reference to any
+    tensor of the storage.
   * banishing: a released storage is banished when no operation holds it and
     every tensor computed from it (outside the storage) is defined or gone;
     the resident storages of those tensors are then pinned.
 """
 from __future__ import annotations
+
+import copy
 
 import brute
 from brute import EVICTED, RESIDENT, UNCOMPUTED, BANISHED, EAGER, IGNORE, BANISH, CLOCK_LIMIT
@@ -140,24 +143,7 @@ class StorageProgram:
             else:
                 raise ValueError(f"instruction {i}: unexpected kind {k}")
         self.required = [t for t in range(len(eref_t)) if eref_t[t] > 0]
-        # storage graph over every tensor viewing a storage
         S = len(self.size)
-        ops_of = [[] for _ in range(S)]
-        for t, st in enumerate(self.t_storage):
-            if self.t_op[t] not in ops_of[st]:
-                ops_of[st].append(self.t_op[t])
-        # cost(S): the operator cost of every tensor viewing S, one term per tensor
-        self.c0 = [0] * S
-        for t, st in enumerate(self.t_storage):
-            if not self.const[st]:
-                self.c0[st] += self.op_cost[self.t_op[t]]
-        self.parents = [[] for _ in range(S)]
-        for s in range(S):
-            for o in ops_of[s]:
-                for u in self.op_ins[o]:
-                    p = self.t_storage[u]
-                    if p != s and p not in self.parents[s]:
-                        self.parents[s].append(p)
         # tensors computed from each storage (outside it): what banishing must keep defined
         self.dep_tensors = [[] for _ in range(S)]
         for o in range(len(self.op_ins)):
@@ -166,16 +152,17 @@ class StorageProgram:
                 for v in self.op_outs[o]:
                     if self.t_storage[v] != p and v not in self.dep_tensors[p]:
                         self.dep_tensors[p].append(v)
-        self.children = [[] for _ in range(S)]
-        for s in range(S):
-            for p in self.parents[s]:
-                self.children[p].append(s)
         self.n = S
 
 
 class LogMachine:
     def __init__(self, sp: StorageProgram, budget, heuristic, seed=0, policy=EAGER):
-        self.p = sp
+        # the storage graph that exists so far, grown as operators first run
+        # (its cost c0, parents and children are what the scores read)
+        self.p = copy.copy(sp)
+        self.p.c0 = [0] * sp.n
+        self.p.parents = [[] for _ in range(sp.n)]
+        self.p.children = [[] for _ in range(sp.n)]
         self.budget, self.h, self.seed, self.policy = budget, heuristic, seed, policy
         S = sp.n
         self.state = [UNCOMPUTED] * S
@@ -282,6 +269,17 @@ class LogMachine:
         for v in p.op_outs[o]:
             if p.t_alias[v]:
                 self.gen[v] = self.sgen[p.t_storage[v]]
+        if not remat:
+            # the operator's tensors exist from now on
+            for v in p.op_outs[o]:
+                s = p.t_storage[v]
+                if not p.const[s]:
+                    p.c0[s] += c
+                for u in ins:
+                    q = p.t_storage[u]
+                    if q != s and q not in p.parents[s]:
+                        p.parents[s].append(q)
+                        p.children[q].append(s)
         if self.clock >= CLOCK_LIMIT:
             self.stop = "clock"
             return False

@@ -191,3 +191,26 @@ def test_storage_cost_sums_over_its_tensors(oracle_lib):
     assert (int(r["remat_cost"]), int(r["total_cost"])) == (5, 14)
     assert int(r["peak_memory"]) == 12
     assert brute_log.simulate(L, 12, h, 0)["total_cost"] == 14
+
+
+def test_storage_metadata_grows_with_its_views(oracle_lib):
+    """Appendix C.2: the dependency graph and a storage's cost are those of the
+    tensors that exist at the time (the cost changes when a view is made).
+    a (4 units, cost 3) and b (4 units, cost 5) are made; a call of 8 units
+    under a budget of 12 evicts one of them by c0/m (staleness ablated): a
+    scores 3/4 and is evicted, because the view of a made afterwards (cost 10)
+    does not exist yet (counting it would give a 13/4 and evict b).  The view
+    then rematerializes a (cost 3): total 3 + 5 + 1 + 3 + 10 = 22."""
+    b = W.LogBuilder("later-view")
+    a, bb, c, av = b.fresh(), b.fresh(), b.fresh(), b.fresh()
+    b.call([], [a], 3, [4], [-1])
+    b.call([], [bb], 5, [4], [-1])
+    b.call([], [c], 1, [8], [-1])
+    b.release(c)
+    b.call([a], [av], 10, [4], [a])
+    L = b.build()
+    h = W.h_family(W.C_LOCAL, 0, 1)
+    r = run_log(oracle_lib, L, h, 12)
+    assert int(r["status"]) == 0
+    assert (int(r["n_evictions"]), int(r["n_remats"]), int(r["remat_cost"]), int(r["total_cost"])) == (1, 1, 3, 22)
+    assert brute_log.simulate(L, 12, h, 0)["total_cost"] == 22
