@@ -150,6 +150,8 @@ WORKLOADS = {
     "chain32": lambda: W.make_config("chain32"),
     "resnet50log": lambda: W.make_config("resnet50log"),
     "randdag100k": lambda: W.make_config("randdag100k"),
+    # the random-DAG recipe at 10k forward ops (20k ops), 1024 budgets 5-100%, h_DTR
+    "randdag10k": lambda: W.config_random_dag(n_forward=10_000, n_budgets=1024),
 }
 
 
