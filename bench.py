@@ -193,8 +193,8 @@ def main():
                     help="only run a plain device copy of MIB MiB three times (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU: simulations are independent and this build runs on a "
-              "single MI355X; sharding across GPUs is described in DESIGN.md, not run.", file=sys.stderr)
+        print("bench.py measures one GPU (--gpus 1): simulations are independent and would shard "
+              "across GPUs by simulation with no exchange, which is not run here.", file=sys.stderr)
         sys.exit(2)
 
     if args.copy_probe > 0:
