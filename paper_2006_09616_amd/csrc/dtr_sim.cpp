@@ -93,6 +93,7 @@ struct Derived {
     std::vector<int32_t> producer, out, in_off, in, ch_off, ch, adj_off, adj, rel_off, rel, req, consts;
     std::vector<dtr::TRec> rec;
     int64_t const_mem = 0;
+    int64_t peak = 0;        // memory with no eviction: frees at release points (dispatch order)
 };
 
 int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
@@ -201,6 +202,18 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
         for (int32_t t = 0; t < n; t++)
             if (!(d.flags[t] & DTR_FLAG_REQUIRED) && last[t] >= 0) d.rel[fill[last[t]]++] = t;
     }
+    {
+        int64_t mem = 0;
+        for (int32_t t = 0; t < n; t++)
+            if (d.flags[t] & DTR_FLAG_CONSTANT) mem += d.size[t];
+        d.peak = mem;
+        for (int32_t o = 0; o < F; o++) {
+            mem += d.size[d.out[o]];
+            d.peak = std::max(d.peak, mem);
+            for (int32_t k = d.rel_off[o]; k < d.rel_off[o + 1]; k++)
+                if (!(d.flags[d.rel[k]] & DTR_FLAG_CONSTANT)) mem -= d.size[d.rel[k]];
+        }
+    }
     d.rec.resize(n);
     for (int32_t t = 0; t < n; t++) {
         dtr::TRec &r = d.rec[t];
@@ -298,15 +311,19 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     slots = std::min<int64_t>(slots, std::max<int32_t>(1, n_sims));
     p.n_slots = (int32_t)std::max<int64_t>(1, slots);
 
-    // grouped by heuristic class (one kernel specialisation each), then
-    // longest first: ops of the trace, then lower budget first
+    // grouped by heuristic class (one kernel specialisation each), then the
+    // likely heaviest first: the tightest budget relative to the trace's
+    // no-eviction peak, then the longest trace
     auto cls = [&](int32_t i) { return heuristic_class(sims[i].heuristic) + (sims[i].search ? 3 : 0); };
     p.order.resize(n_sims);
     std::iota(p.order.begin(), p.order.end(), 0);
     std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {
         if (cls(a) != cls(b)) return cls(a) < cls(b);
-        const int32_t fa = p.traces[sims[a].trace].F, fb = p.traces[sims[b].trace].F;
-        if (fa != fb) return fa > fb;
+        const Derived &ta = p.traces[sims[a].trace], &tb = p.traces[sims[b].trace];
+        const unsigned __int128 ra = (unsigned __int128)(uint64_t)sims[a].budget * (uint64_t)std::max<int64_t>(1, tb.peak);
+        const unsigned __int128 rb = (unsigned __int128)(uint64_t)sims[b].budget * (uint64_t)std::max<int64_t>(1, ta.peak);
+        if (ra != rb) return ra < rb;
+        if (ta.F != tb.F) return ta.F > tb.F;
         return sims[a].budget < sims[b].budget;
     });
     for (int c = 0; c < dtr::N_GROUPS; c++) p.class_count[c] = 0;
