@@ -185,7 +185,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="treelstm4096", choices=sorted(WORKLOADS))
     ap.add_argument("--slots", type=int, default=0)
-    ap.add_argument("--cpu-sample", type=int, default=32, help="oracle on every k-th simulation (0: skip)")
+    ap.add_argument("--cpu-sample", type=int, default=64, help="oracle on every k-th simulation (0: skip)")
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--search-study", action="store_true",
                     help="only compare the search approximations with exact search on the workload")
