@@ -79,3 +79,22 @@ def test_random_dag_locality():
 def test_random_programs_valid(seed):
     _valid(W.random_program(seed, n_ops=40, n_const=5, backward=False))
     _valid(W.random_program(seed, n_ops=40, backward=True))
+
+
+def test_log_peak_is_the_unlimited_replay_peak(oracle_lib):
+    """The no-eviction memory profile that spaces log budgets equals the peak
+    the oracle reaches with an unlimited budget (eager eviction of released
+    storages, constants kept)."""
+    logs = [W.random_log(s, n_steps=40 + 7 * s, n_const=s % 4) for s in range(30)] + [W.resnet_log(blocks=3)]
+    specs = W.make_specs([(i, W.H_LRU, W.BUDGET_UNLIMITED, 0) for i in range(len(logs))])
+    res = oracle_lib.run_log(logs, specs)
+    assert [W.log_peak(L) for L in logs] == [int(v) for v in res["peak_memory"]]
+    assert (res["n_evictions"] == 0).all() and (res["n_remats"] == 0).all()
+
+
+def test_resnet_log_uses_the_instruction_kinds():
+    L = W.resnet_log(blocks=4)
+    kinds = set(int(k) for k in L.kind)
+    assert kinds >= {W.LOG_MEMORY, W.LOG_ALIAS, W.LOG_CALL, W.LOG_MUTATE, W.LOG_CONSTANT, W.LOG_COPY,
+                     W.LOG_RELEASE}
+    assert L.digest() == W.resnet_log(blocks=4).digest()
