@@ -952,6 +952,11 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
     constexpr int U = Round<HC>::value;
     if (cls(HC) == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
         clear_stamps(s);
+    // quads of the next round when it lies in global memory, read one round
+    // ahead so that their latency overlaps this round's scoring (scans start
+    // in LDS, so every global round has been read ahead by its predecessor)
+    static_assert(POOL_LDS > 0, "the first round of a scan lies in LDS");
+    i32x4 P0[U], P1[U], PC[U][KQ];
     for (int32_t base = 0; base < end; base += WAVE * U) {
         int32_t id[U], pd[U];
         uint32_t slot[U];
@@ -978,10 +983,10 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
         } else {
 #pragma unroll
             for (int u = 0; u < U; u++) {
-                Q0[u] = G4[PQ * slot[u]];
-                Q1[u] = G4[PQ * slot[u] + 1];
+                Q0[u] = P0[u];
+                Q1[u] = P1[u];
 #pragma unroll
-                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? G4[PQ * slot[u] + 2 + k] : 0;
+                for (int k = 0; k < KQ; k++) QC[u][k] = PC[u][k];
             }
         }
 #pragma unroll
@@ -1005,6 +1010,18 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
             if (approx(HC)) {
                 ok[u] = ok[u] && (uint64_t)size[u] >= F.min_size;
                 if (F.sample) ok[u] = ok[u] && sample_draw(s, id[u]) < F.tau;
+            }
+        }
+        const int32_t nbase = base + WAVE * U;
+        if (nbase < end && nbase >= POOL_LDS) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int32_t i = nbase + u * WAVE + lane;
+                const uint32_t ns = (uint32_t)(i < end ? i : nbase);
+                P0[u] = G4[PQ * ns];
+                P1[u] = G4[PQ * ns + 1];
+#pragma unroll
+                for (int k = 0; k < KQ; k++) PC[u][k] = cls(HC) == HC_EQ ? G4[PQ * ns + 2 + k] : 0;
             }
         }
         uint64_t N[U], DA[U], DB[U];
