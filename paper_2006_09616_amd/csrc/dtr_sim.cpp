@@ -91,7 +91,7 @@ struct Derived {
     std::vector<int64_t> size, c0, cost;
     std::vector<uint8_t> flags;
     std::vector<int32_t> producer, out, in_off, in, ch_off, ch, adj_off, adj, rel_off, rel, req, consts;
-    std::vector<dtr::TRec> rec;
+    std::vector<dtr::TRecX> rec;
     int64_t const_mem = 0;
     int64_t peak = 0;        // memory with no eviction: frees at release points (dispatch order)
 };
@@ -216,7 +216,7 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
     }
     d.rec.resize(n);
     for (int32_t t = 0; t < n; t++) {
-        dtr::TRec &r = d.rec[t];
+        dtr::TRec &r = d.rec[t].r;
         const int32_t o = d.producer[t];
         r.size = d.size[t];
         r.c0 = (int32_t)d.c0[t];
@@ -225,6 +225,8 @@ int validate_and_derive(const dtr_trace &tr, int32_t index, Derived &d)
         r.in_e = o >= 0 ? d.in_off[o + 1] : 0;
         r.adj_b = d.adj_off[t];
         r.adj_e = d.adj_off[t + 1];
+        for (int32_t j = 0; j < dtr::NB_HEAD; j++)
+            d.rec[t].nb[j] = d.adj_off[t] + j < d.adj_off[t + 1] ? d.adj[d.adj_off[t] + j] : 0;
     }
     for (int32_t t = 0; t < n; t++) {
         if (d.flags[t] & DTR_FLAG_REQUIRED) d.req.push_back(t);

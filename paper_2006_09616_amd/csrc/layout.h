@@ -24,6 +24,8 @@ constexpr int WAVE = 64;
 //   req / consts     required outputs and constants, ascending id
 // Per-tensor static record, one scalar load (32 bytes): size, c0, parent
 // operation, its input range in `in`, and the tensor's neighbour range in `adj`.
+constexpr int NB_HEAD = 8;
+
 struct TRec {
     int64_t size;
     int32_t c0;              // cost of the parent operation (<= 2^28), 0 for constants
@@ -32,6 +34,15 @@ struct TRec {
     int32_t adj_b, adj_e;    // parents then children
 };
 static_assert(sizeof(TRec) == 32, "tensor record layout");
+// The record array's element: the record, then the tensor's first NB_HEAD
+// neighbours in `adj` order (its parent operation's inputs first), padded
+// with tensor 0.  The record alone is one 32-byte scalar load; the neighbour
+// ids are addressed by the tensor id alone.
+struct TRecX {
+    TRec r;
+    int32_t nb[NB_HEAD];
+};
+static_assert(sizeof(TRecX) == 64, "tensor record element layout");
 
 struct TraceDev {
     int32_t n;               // tensors
@@ -54,7 +65,7 @@ struct TraceDev {
     const int32_t *rel;      // [<= n]
     const int32_t *req;      // [n_req]
     const int32_t *consts;   // [n_const]
-    const TRec *rec;         // [n]
+    const TRecX *rec;        // [n]
 };
 
 struct SpecDev {

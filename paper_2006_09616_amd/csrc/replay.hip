@@ -242,7 +242,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ TRec rec_u(const Sim &s, int32_t x)
 {
     const __attribute__((address_space(4))) u32x4 *p =
-        (const __attribute__((address_space(4))) u32x4 *)(s.t.rec + x);
+        (const __attribute__((address_space(4))) u32x4 *)&s.t.rec[x].r;
     const u32x4 a = p[0], b = p[1];
     TRec r;
     r.size = (int64_t)((uint64_t)a.x | ((uint64_t)a.y << 32));
@@ -258,7 +258,7 @@ __device__ __forceinline__ TRec rec_u(const Sim &s, int32_t x)
 // per-lane read of a tensor's static record (two 16-byte global loads)
 __device__ __forceinline__ TRec rec_v(const Sim &s, int32_t x)
 {
-    const GAS u32x4 *p = (const GAS u32x4 *)(s.t.rec + x);
+    const GAS u32x4 *p = (const GAS u32x4 *)&s.t.rec[x].r;
     const u32x4 a = p[0], b = p[1];
     TRec r;
     r.size = (int64_t)((uint64_t)a.x | ((uint64_t)a.y << 32));
@@ -403,8 +403,9 @@ __device__ __forceinline__ void pool_compact(Sim &s)
 
 // Every lane with `want` appends tensor x (resident, unlocked) with last
 // access `last`; returns its slot (or -1).  The caller stores x's new state.
+// `known`: x's record when the caller holds it already (uniform x).
 template <int HC>
-__device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int64_t last)
+__device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int64_t last, const TRec *known = nullptr)
 {
     const uint64_t m = __ballot(want);
     if (!m) return -1;
@@ -416,7 +417,7 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
     int32_t i = -1;
     if (want) {
         i = s.pool_end + lane_rank(m);
-        const TRec r = rec_v(s, x);
+        const TRec r = known ? *known : rec_v(s, x);
         int32_t deg = (r.adj_e - r.adj_b) << 8;
         NbCache nb;
         if (cls(HC) == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg);
@@ -575,7 +576,7 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 // (found in parallel, merged under the largest; ties: the earliest), and every
 // neighbour waiting in the pool caches nd.
 template <class NS>
-__device__ __forceinline__ bool evict_merge(Sim &s, const NS &N, int32_t nd, const TRec &rv)
+__device__ __forceinline__ bool evict_merge(Sim &s, const NS &N, int32_t nd, const TRec &rv, int32_t head)
 {
     int32_t R = nd;               // current root of v's set
     int64_t Rcost = rv.c0;
@@ -590,7 +591,7 @@ __device__ __forceinline__ bool evict_merge(Sim &s, const NS &N, int32_t nd, con
         const int32_t k = k0 + s.lane;
         int32_t q = -1, r = -1;
         if (k < rv.adj_e) {
-            const uint64_t w = s.S.tst[gld(s.t.adj + k)];
+            const uint64_t w = s.S.tst[k0 == rv.adj_b && s.lane < NB_HEAD ? head : gld(s.t.adj + k)];
             q = ts_sw(w);
             if (ts_in_pool(w)) list_add(s, (int32_t)ts_pos(w), nd);
             if (q >= 0) {
@@ -655,7 +656,9 @@ template <int HC>
 __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eager)
 {
     // size, c0 and neighbour range come from v's pool slot (LDS for the pool
-    // head), not from the static record
+    // head), not from the static record; the first neighbours from the
+    // fixed-stride table, read at once
+    const int32_t head = cls(HC) == HC_EQ ? gld(s.t.rec[v].nb + (s.lane & (NB_HEAD - 1))) : 0;
     TRec rv;
     {
         const i32x4 *P = (const i32x4 *)&s.S.pool(slot);
@@ -683,11 +686,11 @@ __device__ __forceinline__ bool evict(Sim &s, int32_t v, int32_t slot, bool eage
     if (s.uf_n <= UF_LDS) {
         LdsNodes NL;
         NL.p = s.S.nodes.lds_l;
-        ok = evict_merge(s, NL, nd, rv);
+        ok = evict_merge(s, NL, nd, rv, head);
     } else {
         AnyNodes NA;
         NA.n = s.S.nodes;
-        ok = evict_merge(s, NA, nd, rv);
+        ok = evict_merge(s, NA, nd, rv, head);
     }
     if (!ok) return false;
     s.S.tst[v] = ts_make(nd, 0, 0);
@@ -793,7 +796,7 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
             const size_t sp = (size_t)p * WAVE + lane;
             if (st[sp] == ep) continue;
             st[sp] = ep;
-            sum += gld(&s.t.rec[p].c0);
+            sum += gld(s.t.c0 + p);
             cnt++;
             q[(size_t)tail++ * WAVE + lane] = p;
         }
@@ -808,7 +811,7 @@ __device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t 
             const size_t sc = (size_t)c * WAVE + lane;
             if (st[sc] == ep) continue;
             st[sc] = ep;
-            sum += gld(&s.t.rec[c].c0);
+            sum += gld(s.t.c0 + c);
             cnt++;
             q[(size_t)tail++ * WAVE + lane] = c;
         }
@@ -1223,7 +1226,10 @@ struct Frame {
 
 // lock inputs ids[b..e) (one lane per input); tensors that were evictable
 // leave the pool.  Fills f for single-chunk operations.
-__device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t b, int32_t e, Frame &f)
+// `head`: when >= -1, lanes below NB_HEAD hold the first entries of ids[b..)
+// already (an operation's inputs are the first neighbours of its output)
+__device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t b, int32_t e, Frame &f,
+                                            int32_t head = -2)
 {
     for (int32_t k0 = b; k0 < e; k0 += WAVE) {
         const int32_t k = k0 + s.lane;
@@ -1231,7 +1237,7 @@ __device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t 
         int32_t u = -1;
         uint64_t nw = 0;
         if (k < e) {
-            u = gld(ids + k);
+            u = head >= -1 && k0 == b && s.lane < NB_HEAD ? head : gld(ids + k);
             const uint64_t w = s.S.tst[u];
             const uint32_t l = ts_locks(w);
             nw = ts_make(ts_sw(w), ts_pos(w), l + 1);
@@ -1315,6 +1321,7 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
     s.mem += rt.size;
     if (s.mem > s.peak) s.peak = s.mem;
     if (cls(HC) == HC_EQ && remat) {
+        const int32_t head = gld(s.t.rec[t].nb + (s.lane & (NB_HEAD - 1)));
         // split approximation: the set loses c0(t); t leaves it (its node stays as a phantom)
         const int32_t old = uni(ts_sw(s.S.tst[t]));
         if (s.uf_n <= UF_LDS) {
@@ -1332,7 +1339,7 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
         for (int32_t k0 = rt.adj_b; k0 < rt.adj_e; k0 += WAVE) {
             const int32_t k = k0 + s.lane;
             if (k < rt.adj_e) {
-                const uint64_t wx = s.S.tst[gld(s.t.adj + k)];
+                const uint64_t wx = s.S.tst[k0 == rt.adj_b && s.lane < NB_HEAD ? head : gld(s.t.adj + k)];
                 if (ts_in_pool(wx) && !list_remove(s, (int32_t)ts_pos(wx), old)) lost = true;
             }
         }
@@ -1459,12 +1466,14 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
     f.u = -1;
     f.w = 0;
     TRec rt = rec_u(s, tt);           // record of the current frame's tensor
+    // its first inputs, read alongside the record (their addresses need only tt)
+    int32_t head = gld(s.t.rec[tt].nb + (s.lane & (NB_HEAD - 1)));
     for (;;) {
         PROF_T0(td);
         const int32_t b = rt.in_b, e = rt.in_e;
         if (cur < 0) {
             PROF_T0(tl);
-            lock_inputs(s, s.t.in, b, e, f);
+            lock_inputs(s, s.t.in, b, e, f, head);
             PROF_ADD(PH_LOCK, tl);
             if (s.status != ST_OK) return false;
             cur = 0;
@@ -1483,6 +1492,7 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
             cur = -1;
             remat = true;
             rt = rec_u(s, tt);
+            head = gld(s.t.rec[tt].nb + (s.lane & (NB_HEAD - 1)));
             continue;
         }
         if (!allocate<HC>(s, rt.size)) return false;
@@ -1498,7 +1508,7 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         if (!remat) {
             // a trace operation's output is unlocked: it joins the pool at once
             PROF_T0(to);
-            const int32_t slot = uni(pool_append<HC>(s, s.lane == 0, tt, start));
+            const int32_t slot = uni(pool_append<HC>(s, s.lane == 0, tt, start, &rt));
             s.S.tst[tt] = ts_make(S_RESIDENT, (uint32_t)slot, 0);
             PROF_ADD(PH_OUTPUT, to);
         }
