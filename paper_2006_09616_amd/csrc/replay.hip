@@ -936,6 +936,35 @@ __device__ __forceinline__ Filter make_filter(Sim &s)
 
 // Score every searched pool entry; return the victim (uniform) and its slot,
 // or -1; `scored` receives the number of candidates scored.
+// Sum of the set costs behind the first KK cached nodes of a candidate (nodes
+// in LDS): each node's parent is the set root unless the node is more than one
+// merge away (then `deep` is set and the caller recounts); equal roots count
+// once.
+template <int KK>
+__device__ __forceinline__ int64_t cached_sum(const LAS UfNode *NL, const int32_t (&nb)[K], bool &deep)
+{
+    const LAS i32x4 *NQ = (const LAS i32x4 *)NL;    // {cost lo, cost hi, parent, size}
+    int32_t r[KK];
+    int64_t cost[KK];
+#pragma unroll
+    for (int k = 0; k < KK; k++) r[k] = NL[nb[k]].parent;
+#pragma unroll
+    for (int k = 0; k < KK; k++) {
+        const i32x4 n2 = NQ[r[k]];
+        cost[k] = (int64_t)(((uint64_t)(uint32_t)n2.y << 32) | (uint32_t)n2.x);
+        deep |= n2.z != r[k];
+    }
+    int64_t t = 0;
+#pragma unroll
+    for (int k = 0; k < KK; k++) {
+        bool dup = false;
+#pragma unroll
+        for (int j = 0; j < k; j++) dup |= r[j] == r[k];
+        t += dup ? 0 : cost[k];
+    }
+    return t;
+}
+
 template <int HC>
 __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filter &F, int64_t &scored)
 {
@@ -1040,21 +1069,18 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
                 // roots are their own parent, so the node two hops along (n2)
                 // is the set root whenever the cached node is at most one
                 // merge away from it; its cost is used unconditionally
-                int32_t r[K];
-                int64_t cost[K];
                 bool deep = false;
+                // cache entries at or beyond every lane's count hold the null
+                // node (cost 0, its own root) and are skipped when the whole
+                // wave allows it
                 if (lds_nodes) {
                     const LAS UfNode *NL = s.S.nodes.lds_l;
-                    const LAS i32x4 *NQ = (const LAS i32x4 *)NL;    // {cost lo, cost hi, parent, size}
-#pragma unroll
-                    for (int k = 0; k < K; k++) r[k] = NL[nb[u][k]].parent;
-#pragma unroll
-                    for (int k = 0; k < K; k++) {
-                        const i32x4 n2 = NQ[r[k]];
-                        cost[k] = (int64_t)(((uint64_t)(uint32_t)n2.y << 32) | (uint32_t)n2.x);
-                        deep |= n2.z != r[k];
-                    }
+                    if (!__ballot(c > 2)) sum[u] = cached_sum<2>(NL, nb[u], deep);
+                    else if (!__ballot(c > 4)) sum[u] = cached_sum<4>(NL, nb[u], deep);
+                    else sum[u] = cached_sum<K>(NL, nb[u], deep);
                 } else {
+                    int32_t r[K];
+                    int64_t cost[K];
 #pragma unroll
                     for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
 #pragma unroll
@@ -1063,16 +1089,16 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
                         cost[k] = n2.cost;
                         deep |= n2.parent != r[k];
                     }
-                }
-                int64_t t = 0;
+                    int64_t t = 0;
 #pragma unroll
-                for (int k = 0; k < K; k++) {
-                    bool dup = false;
+                    for (int k = 0; k < K; k++) {
+                        bool dup = false;
 #pragma unroll
-                    for (int j = 0; j < k; j++) dup |= r[j] == r[k];
-                    t += dup ? 0 : cost[k];
+                        for (int j = 0; j < k; j++) dup |= r[j] == r[k];
+                        t += dup ? 0 : cost[k];
+                    }
+                    sum[u] = t;
                 }
-                sum[u] = t;
                 ev[u] = c;
                 slow[u] = ok[u] && (c > K || deep);
             }
