@@ -65,6 +65,7 @@ constexpr int KQ = K / 4;        // 16-byte quads of cached nodes per pool slot
 constexpr int PQ = (int)(sizeof(PoolSlot) / 16);   // quads per pool slot
 static_assert(K % 4 == 0 && PQ == 2 + KQ, "pool slot: two header quads, then the cache");
 constexpr int LB = 8;            // neighbour reads issued together when building a cache
+static_assert(LB == NB_HEAD, "a cache build may take its first chunk from the record element");
 // kernel specialisations by heuristic class (register budgets differ widely),
 // each with exact search or with the search approximations (HC | HC_APPROX)
 enum { HC_EQ = 0, HC_WALK = 1, HC_SIMPLE = 2, HC_APPROX = 4 };
@@ -282,7 +283,8 @@ struct NbCache {
     i32x4 q[KQ];
 };
 
-__device__ __forceinline__ NbCache list_build(const Sim &s, int32_t b, int32_t e, int32_t &deg)
+__device__ __forceinline__ NbCache list_build(const Sim &s, int32_t b, int32_t e, int32_t &deg,
+                                              const i32x4 *head = nullptr)
 {
     int32_t c[K];
 #pragma unroll
@@ -291,8 +293,18 @@ __device__ __forceinline__ NbCache list_build(const Sim &s, int32_t b, int32_t e
     for (int32_t k0 = b; k0 < e; k0 += LB) {
         int32_t w[LB];
         int32_t q[LB];
+        if (head && k0 == b) {
 #pragma unroll
-        for (int j = 0; j < LB; j++) w[j] = gld(s.t.adj + (k0 + j < e ? k0 + j : k0));
+            for (int j = 0; j < LB / 4; j++) {
+                w[4 * j] = head[j].x;
+                w[4 * j + 1] = head[j].y;
+                w[4 * j + 2] = head[j].z;
+                w[4 * j + 3] = head[j].w;
+            }
+        } else {
+#pragma unroll
+            for (int j = 0; j < LB; j++) w[j] = gld(s.t.adj + (k0 + j < e ? k0 + j : k0));
+        }
 #pragma unroll
         for (int j = 0; j < LB; j++) q[j] = ts_sw(s.S.tst[w[j]]);
 #pragma unroll
@@ -417,10 +429,17 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
     int32_t i = -1;
     if (want) {
         i = s.pool_end + lane_rank(m);
+        // the record and the first neighbours are one 64-byte element
+        const GAS i32x4 *px = (const GAS i32x4 *)&s.t.rec[x];
+        i32x4 hd[2];
+        if (cls(HC) == HC_EQ) {
+            hd[0] = px[2];
+            hd[1] = px[3];
+        }
         const TRec r = known ? *known : rec_v(s, x);
         int32_t deg = (r.adj_e - r.adj_b) << 8;
         NbCache nb;
-        if (cls(HC) == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg);
+        if (cls(HC) == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg, hd);
         i32x4 q0, q1;
         q0.x = x;
         q0.y = deg;
