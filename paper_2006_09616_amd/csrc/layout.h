@@ -95,7 +95,8 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 //             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
 //             neighbours (n = NB_CACHE + 1 marks an overflowed cache)
 //   nodes     union-find nodes {running cost, parent, size}
-//   stack     rematerialization frames (tensor, next input, the tensor's record)
+//   stack     rematerialization frames (tensor, next input, the tensor's record,
+//             its first input ids)
 //   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
 //   pending   one byte per tensor: released, banishing deferred (banishing policy)
 constexpr int NB_CACHE = 8;
@@ -131,8 +132,9 @@ static_assert(sizeof(PoolSlot) == 64, "pool slot layout");
 struct __attribute__((aligned(16))) StackFrame {
     int32_t t, next, pad0, pad1;
     TRec rec;
+    int32_t in8[NB_HEAD];    // the frame's first NB_HEAD input ids (-1 past the last)
 };
-static_assert(sizeof(StackFrame) == 48, "stack frame layout");
+static_assert(sizeof(StackFrame) == 80, "stack frame layout");
 
 struct __attribute__((aligned(16))) UfNode {
     int64_t cost;

@@ -1304,11 +1304,12 @@ __device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t 
     }
 }
 
-// reload a frame's inputs after returning from nested rematerializations
-__device__ __forceinline__ void reload_frame(const Sim &s, int32_t b, int32_t e, Frame &f)
+// reload a frame's inputs after returning from nested rematerializations;
+// lanes below NB_HEAD have their input id from the stack frame already (u8)
+__device__ __forceinline__ void reload_frame(const Sim &s, int32_t b, int32_t e, Frame &f, int32_t u8)
 {
     const int32_t k = b + s.lane;
-    f.u = k < e ? gld(s.t.in + k) : -1;
+    f.u = k < e ? (s.lane < NB_HEAD ? u8 : gld(s.t.in + k)) : -1;
     f.w = f.u >= 0 ? s.S.tst[f.u] : 0;
 }
 
@@ -1461,9 +1462,14 @@ __device__ __forceinline__ void retry_banish(Sim &s, int32_t b, int32_t e)
     }
 }
 
-__device__ __forceinline__ void stack_push(const Sim &s, int32_t sp, int32_t t, int32_t next, const TRec &r)
+constexpr int FQ = (int)(sizeof(StackFrame) / 16);    // 16-byte quads per stack frame
+
+// push the current frame (tensor t, next input to check, its record); lane k
+// below NB_HEAD saves its input id u
+__device__ __forceinline__ void stack_push(const Sim &s, int32_t sp, int32_t t, int32_t next, const TRec &r, int32_t u)
 {
-    GAS i32x4 *F = s.S.stack + 3 * (size_t)sp;
+    GAS i32x4 *F = s.S.stack + FQ * (size_t)sp;
+    if (s.lane < NB_HEAD) ((GAS int32_t *)(F + 3))[s.lane] = u;
     i32x4 a, b, c;
     a.x = t;
     a.y = next;
@@ -1481,9 +1487,10 @@ __device__ __forceinline__ void stack_push(const Sim &s, int32_t sp, int32_t t, 
     F[2] = c;
 }
 
-__device__ __forceinline__ void stack_pop(const Sim &s, int32_t sp, int32_t &t, int32_t &next, TRec &r)
+__device__ __forceinline__ void stack_pop(const Sim &s, int32_t sp, int32_t &t, int32_t &next, TRec &r, int32_t &u8)
 {
-    const GAS i32x4 *F = s.S.stack + 3 * (size_t)sp;
+    const GAS i32x4 *F = s.S.stack + FQ * (size_t)sp;
+    u8 = s.lane < NB_HEAD ? ((const GAS int32_t *)(F + 3))[s.lane] : -1;
     const i32x4 a = F[0], b = F[1], c = F[2];
     t = uni(a.x);
     next = uni(a.y);
@@ -1530,7 +1537,7 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
             const int32_t child = j < WAVE ? __builtin_amdgcn_readlane(f.u, j) : uni(cld(s.t.in + b + j));
             const uint32_t clocks = j < WAVE ? ts_locks(readlane64(f.w, j))
                                              : (uint32_t)uni((int32_t)ts_locks(s.S.tst[child]));
-            stack_push(s, sp, tt, j + 1, rt);
+            stack_push(s, sp, tt, j + 1, rt, f.u);
             sp++;
             tt = child;
             tlocks = clocks;
@@ -1561,9 +1568,10 @@ __device__ __forceinline__ bool call(Sim &s, int32_t root, bool root_remat, uint
         if (sp == 0) return true;
         PROF_T0(tr);
         sp--;
-        stack_pop(s, sp, tt, cur, rt);
+        int32_t u8;
+        stack_pop(s, sp, tt, cur, rt, u8);
         remat = sp > 0 ? true : root_remat;
-        reload_frame(s, rt.in_b, rt.in_e, f);
+        reload_frame(s, rt.in_b, rt.in_e, f, u8);
         // locks on the resumed frame's output: none for a trace operation,
         // else whatever its consumers (or the output condition) hold
         tlocks = remat ? (uint32_t)uni((int32_t)ts_locks(s.S.tst[tt])) : 0u;
