@@ -419,7 +419,7 @@ struct LogPlan {
     int32_t n_slots = 1;
     int32_t lds_bytes = 0, lds_state = 0, lds_wm = 0, lds_po = 0, lds_co = 0, lds_pa = 0, lds_ca = 0, wm_words = 0;
     int32_t lds_c0 = 0, lds_cand = 0, lds_stk = 0, lds_ctr = 0, lds_sz = 0, lds_last = 0, lds_rsum = 0, lds_rcnt = 0;
-    int32_t lds_pcnt = 0, lds_ccnt = 0;
+    int32_t lds_pcnt = 0, lds_ccnt = 0, lds_ctl = 0, waves = 1;
     std::vector<size_t> log_off;
     size_t desc_off = 0, spec_off = 0, order_off = 0, tables_bytes = 0, result_off = 0, slot_off = 0, total = 0;
 };
@@ -453,6 +453,49 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
         E_max = std::max<int64_t>(E_max, (int64_t)d.par.size());
     }
     p->sims.assign(sims, sims + n_sims);
+    // walk state in LDS when the largest log fits: storage states, visited
+    // bitsets, storage graph with 16-bit neighbour ids.  With walk heuristics
+    // the workgroup takes up to MAX_LOG_WAVES waves (helpers in the walk
+    // scans), each with its own bitsets and stacks, as many as fit.
+    const int64_t W = (S_max + 127) / 128 * 4;     // 32-bit words, whole 16-byte quads
+    {
+        int dev = 0, lds_max = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+            return give_up(fail(DTR_EHIP, "hipDeviceGetAttribute(maxSharedMemoryPerBlock) failed"));
+        const size_t limit = std::min<size_t>(LDS_LIMIT, (size_t)lds_max);
+        p->lds_bytes = 0;
+        p->waves = 1;
+        for (int32_t nw = need_walk ? dtr::MAX_LOG_WAVES : 1; nw >= 1; nw /= 2) {
+            const size_t lanes = (size_t)dtr::WAVE * (size_t)nw;
+            size_t q = 0;
+            auto at = [&](int32_t &field, size_t bytes) { field = (int32_t)q; q += (bytes + 15) / 16 * 16; };
+            at(p->lds_state, (size_t)S_max);
+            at(p->lds_wm, 4 * (size_t)W * lanes);
+            at(p->lds_po, 4 * (size_t)(S_max + 1));
+            at(p->lds_co, 4 * (size_t)(S_max + 1));
+            at(p->lds_pa, 2 * (size_t)E_max);
+            at(p->lds_ca, 2 * (size_t)E_max);
+            at(p->lds_c0, 8 * (size_t)S_max);
+            at(p->lds_cand, 2 * (size_t)S_max);
+            at(p->lds_stk, 2 * (size_t)dtr::LOG_LDS_STACK * lanes);
+            at(p->lds_ctr, 4);
+            at(p->lds_ctl, 16);
+            at(p->lds_sz, 8 * (size_t)S_max);
+            at(p->lds_last, 8 * (size_t)S_max);
+            at(p->lds_rsum, 8 * (size_t)S_max);
+            at(p->lds_rcnt, 4 * (size_t)S_max);
+            at(p->lds_pcnt, 4 * (size_t)S_max);
+            at(p->lds_ccnt, 4 * (size_t)S_max);
+            const bool fits = S_max <= 65535 && q <= limit && !(opt && (opt->flags & DTR_OPT_LOG_NO_LDS));
+            if (fits) {
+                p->lds_bytes = (int32_t)q;
+                p->waves = nw;
+                break;
+            }
+        }
+        p->wm_words = (int32_t)W;
+    }
     // slot layout
     dtr::LogSlotLayout &L = p->L;
     size_t o = 0;
@@ -462,7 +505,6 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
     L.F_max = F_max;
     L.ucap = need_uf ? 2 * S_max + 64 : 0;
     L.mcap = L.ucap;
-    const int64_t W = (S_max + 127) / 128 * 4;     // 32-bit words, whole 16-byte quads
     const size_t S = (size_t)S_max, U = (size_t)L.ucap;
     take(L.state, S);
     take(L.pinned, S);
@@ -482,40 +524,9 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
     take(L.uf_tmp, 8 * U);
     take(L.mark, 4 * (size_t)L.mcap * dtr::WAVE);
     take(L.wmark, need_walk ? 4 * (size_t)W * dtr::WAVE : 0);
-    take(L.queue, need_walk ? 4 * (S + 2) * dtr::WAVE : 0);
+    take(L.queue, need_walk ? 4 * (S + 2) * dtr::WAVE * (size_t)p->waves : 0);     // per lane of every wave
     take(L.stack, sizeof(dtr::LogFrame) * (size_t)(F_max + 2));
     L.bytes = (int64_t)o;
-
-    // walk state in LDS when the largest log fits: storage states, 64 visited
-    // bitsets, storage graph with 16-bit neighbour ids
-    {
-        size_t q = 0;
-        auto at = [&](int32_t &field, size_t bytes) { field = (int32_t)q; q += (bytes + 15) / 16 * 16; };
-        at(p->lds_state, (size_t)S_max);
-        at(p->lds_wm, 4 * (size_t)W * dtr::WAVE);
-        at(p->lds_po, 4 * (size_t)(S_max + 1));
-        at(p->lds_co, 4 * (size_t)(S_max + 1));
-        at(p->lds_pa, 2 * (size_t)E_max);
-        at(p->lds_ca, 2 * (size_t)E_max);
-        at(p->lds_c0, 8 * (size_t)S_max);
-        at(p->lds_cand, 2 * (size_t)S_max);
-        at(p->lds_stk, 2 * (size_t)dtr::LOG_LDS_STACK * dtr::WAVE);
-        at(p->lds_ctr, 4);
-        at(p->lds_sz, 8 * (size_t)S_max);
-        at(p->lds_last, 8 * (size_t)S_max);
-        at(p->lds_rsum, 8 * (size_t)S_max);
-        at(p->lds_rcnt, 4 * (size_t)S_max);
-        at(p->lds_pcnt, 4 * (size_t)S_max);
-        at(p->lds_ccnt, 4 * (size_t)S_max);
-        int dev = 0, lds_max = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
-            return give_up(fail(DTR_EHIP, "hipDeviceGetAttribute(maxSharedMemoryPerBlock) failed"));
-        const size_t limit = std::min<size_t>(LDS_LIMIT, (size_t)lds_max);
-        const bool fits = S_max <= 65535 && q <= limit && !(opt && (opt->flags & DTR_OPT_LOG_NO_LDS));
-        p->lds_bytes = fits ? (int32_t)q : 0;
-        p->wm_words = (int32_t)W;
-    }
 
     int32_t cus = 0;
     if (int rc = device_cus(&cus)) return give_up(rc);
@@ -650,6 +661,8 @@ int log_plan_launch(const LogPlan *p, uint8_t *ws, hipStream_t st)
     a.lds_rcnt = p->lds_rcnt;
     a.lds_pcnt = p->lds_pcnt;
     a.lds_ccnt = p->lds_ccnt;
+    a.lds_ctl = p->lds_ctl;
+    a.waves = p->waves;
     hipError_t e = dtr_launch_log(&a, st);
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     return DTR_OK;

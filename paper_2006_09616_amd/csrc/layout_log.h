@@ -94,8 +94,12 @@ struct LogKernelArgs {
     int32_t lds_rsum, lds_rcnt;  // per listed candidate: walked cost, count
     int32_t lds_pcnt, lds_ccnt;  // edges created so far per storage
     int32_t wm_words;         // 32-bit words per visited bitset (a multiple of 4)
+    // LDS variant: waves per workgroup (1 .. MAX_LOG_WAVES; the first replays,
+    // the others help with walk scans) and the offset of the control words
+    int32_t waves, lds_ctl;
 };
 
 constexpr int LOG_LDS_STACK = 32;
+constexpr int MAX_LOG_WAVES = 4;
 
 }  // namespace dtr

@@ -47,6 +47,21 @@ constexpr uint64_t GOLDEN = 0x9E3779B97F4A7C15ull;
 constexpr uint64_t SAMPLE_STREAM = 0xD6E8FEB86659FD93ull;
 
 __device__ __forceinline__ int32_t uni(int32_t v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// workgroup control words in LDS (multi-wave workgroups): the replay index,
+// the command for the helper waves, the candidate count and the e* flag of a
+// walk scan
+enum { CTL_K = 0, CTL_CMD = 1, CTL_N = 2, CTL_BOTH = 3 };
+enum { CMD_WALK = 1, CMD_DONE = 2 };
+
+// Order this wave's LDS and global accesses before and after (what a
+// workgroup barrier gives a one-wave workgroup) without synchronizing with the
+// other waves of a multi-wave workgroup.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+}
 __device__ __forceinline__ int64_t uni64(int64_t v)
 {
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)(uint64_t)v);
@@ -168,6 +183,8 @@ struct Sim {
     LAS uint32_t *ctr;
     LAS int64_t *rsum;         // per listed candidate: walked cost and count
     LAS int32_t *rcnt;
+    LAS int32_t *ctl;          // workgroup control words (LogCtl)
+    int32_t nw;                // waves in the workgroup (the others help with walks)
     int32_t wmw;               // words per visited bitset
     // slot memory
     GAS uint8_t *pinned, *pending;
@@ -261,14 +278,14 @@ __device__ void uf_compact(Sim<L> &s)
 {
     const int32_t S = s.P.S, n = s.uf_n;
     for (int32_t i = s.lane; i < n; i += WAVE) s.remap[i] = 0;
-    __syncthreads();
+    wave_sync();
     for (int32_t st = s.lane; st < S; st += WAVE)
         if (s.state[st] == ST_EVICTED) {
             const int32_t r = uf_root(s, s.node[st]);
             s.node[st] = r;
             s.remap[r] = 1;
         }
-    __syncthreads();
+    wave_sync();
     int32_t kept = 0;
     for (int32_t b = 0; b < n; b += WAVE) {
         const int32_t i = b + s.lane;
@@ -282,7 +299,7 @@ __device__ void uf_compact(Sim<L> &s)
         }
         kept += __popcll(m);
     }
-    __syncthreads();
+    wave_sync();
     for (int32_t k = s.lane; k < kept; k += WAVE) {
         s.ufc[k] = s.uft[k];
         s.ufp[k] = k;
@@ -290,7 +307,7 @@ __device__ void uf_compact(Sim<L> &s)
     }
     for (int32_t st = s.lane; st < S; st += WAVE)
         if (s.state[st] == ST_EVICTED) s.node[st] = s.remap[s.node[st]];
-    __syncthreads();
+    wave_sync();
     s.uf_n = uni(kept);
 }
 
@@ -432,35 +449,13 @@ __device__ void evict(Sim<L> &s, int32_t st, bool eager)
 // not wait for the longest walk of a round.  Pending storages go on a small
 // LDS stack per lane, spilling to the lane's queue in device memory; any
 // order visits the same set.
+// Walk the e* (or e_R) sets of the listed candidates cand[0..n): each lane
+// takes the next candidate from the shared counter as soon as its previous
+// walk (and the clearing of its visited bitset) has ended, and records the
+// walked cost and count under the candidate's list index.
 template <bool L>
-__device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint64_t tau, uint64_t &bn,
-                              u128 &bd, int32_t &bi)
+__device__ void walk_candidates(Sim<L> &s, int32_t n, bool both)
 {
-    const int32_t S = s.P.S;
-    int32_t n = 0;
-    for (int32_t b = 0; b < S; b += WAVE) {
-        const int32_t x = b + s.lane;
-        bool ok = false;
-        if (x < S) {
-            // every read issued before the first test
-            const uint8_t st = s.state[x], pin = s.pinned[x], cst = s.P.s_const[x];
-            const int32_t lk = s.locks[x];
-            const uint64_t sz = (uint64_t)s.sz[x];
-            ok = (st == ST_RESIDENT) & (lk == 0) & (pin == 0) & (cst == 0) & (sz >= min_size);
-        }
-        if (ok && sampling) {
-            const uint64_t key = ((uint64_t)s.eviction_no << 32) + (uint64_t)(uint32_t)x;
-            ok = mix64((s.seed ^ SAMPLE_STREAM) + GOLDEN * key) < tau;
-        }
-        const uint64_t m = __ballot(ok);
-        if (ok)
-            s.cand[n + (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0))] = (uint16_t)x;
-        n += __popcll(m);
-    }
-    *s.ctr = 0;
-    __syncthreads();
-    const bool both = s.cmode == CM_ESTAR;
     const int32_t W = s.wmw;
     int32_t x = -1, k = 0, e = 0, end = 0, side = 0, spl = 0, spg = 0, clr = -1;
     int64_t sum = 0;
@@ -541,7 +536,49 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
             }
         }
     }
-    __syncthreads();
+}
+
+template <bool L>
+__device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint64_t tau, uint64_t &bn,
+                              u128 &bd, int32_t &bi)
+{
+    const int32_t S = s.P.S;
+    int32_t n = 0;
+    for (int32_t b = 0; b < S; b += WAVE) {
+        const int32_t x = b + s.lane;
+        bool ok = false;
+        if (x < S) {
+            // every read issued before the first test
+            const uint8_t st = s.state[x], pin = s.pinned[x], cst = s.P.s_const[x];
+            const int32_t lk = s.locks[x];
+            const uint64_t sz = (uint64_t)s.sz[x];
+            ok = (st == ST_RESIDENT) & (lk == 0) & (pin == 0) & (cst == 0) & (sz >= min_size);
+        }
+        if (ok && sampling) {
+            const uint64_t key = ((uint64_t)s.eviction_no << 32) + (uint64_t)(uint32_t)x;
+            ok = mix64((s.seed ^ SAMPLE_STREAM) + GOLDEN * key) < tau;
+        }
+        const uint64_t m = __ballot(ok);
+        if (ok)
+            s.cand[n + (int32_t)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                                           __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0))] = (uint16_t)x;
+        n += __popcll(m);
+    }
+    // the walks: this wave and, in a multi-wave workgroup, the helper waves
+    // take candidates from the shared counter
+    const bool both = s.cmode == CM_ESTAR;
+    *s.ctr = 0;
+    if (s.nw > 1) {
+        s.ctl[CTL_CMD] = CMD_WALK;
+        s.ctl[CTL_N] = n;
+        s.ctl[CTL_BOTH] = both ? 1 : 0;
+        __syncthreads();
+    } else {
+        wave_sync();
+    }
+    walk_candidates(s, n, both);
+    if (s.nw > 1) __syncthreads();
+    else wave_sync();
     // score every walked candidate
     for (int32_t q = s.lane; q < n; q += WAVE) {
         const int32_t y = s.cand[q];
@@ -554,7 +591,7 @@ __device__ void scan_walk_lds(Sim<L> &s, uint64_t min_size, bool sampling, uint6
         s.nbr_l += s.rcnt[q];
         s.adj_l += s.pcnt[y] + s.ccnt[y];
     }
-    __syncthreads();
+    wave_sync();
 }
 
 // smallest r with r * r >= n
@@ -666,7 +703,7 @@ __device__ void try_banish(Sim<L> &s, int32_t st)
         const int32_t d = s.P.t_storage[s.P.dt[q]];
         if (s.state[d] == ST_RESIDENT) s.pinned[d] = 1;
     }
-    __syncthreads();
+    wave_sync();
 }
 
 template <bool L>
@@ -787,7 +824,7 @@ __device__ void call(Sim<L> &s, int32_t o, int32_t remat)
 }
 
 template <bool L>
-__device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int32_t lane, uint8_t *lds)
+__device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int32_t lane, uint8_t *lds, int32_t nw)
 {
     Sim<L> s;
     const SpecDev sp = a.specs[sim];
@@ -811,6 +848,8 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
     s.ucap = (int32_t)Y.ucap;
     const int32_t W = a.wm_words;
     s.wmw = W;
+    s.nw = nw;
+    s.ctl = nullptr;
     if constexpr (L) {
         s.state = (Mem<L, uint8_t>)(lds + a.lds_state);
         s.wm = (Mem<L, uint32_t>)(lds + a.lds_wm) + lane * W;
@@ -826,6 +865,7 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         s.ctr = (LAS uint32_t *)(lds + a.lds_ctr);
         s.rsum = (LAS int64_t *)(lds + a.lds_rsum);
         s.rcnt = (LAS int32_t *)(lds + a.lds_rcnt);
+        s.ctl = (LAS int32_t *)(lds + a.lds_ctl);
         s.last = (Mem<L, int64_t>)(lds + a.lds_last);
         s.sz = (Mem<L, const int64_t>)(lds + a.lds_sz);
     } else {
@@ -913,7 +953,7 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         Mem<L, int64_t> szl = (Mem<L, int64_t>)s.sz;
         for (int32_t i = lane; i < S; i += WAVE) szl[i] = s.P.s_size[i];
     }
-    __syncthreads();
+    wave_sync();
 
     for (int32_t o = 0; o < F && !s.status; o++) {
         s.cur_op = o;
@@ -949,21 +989,86 @@ __device__ void run_sim(const LogKernelArgs &a, int32_t sim, uint8_t *base, int3
         r.failed_op = s.status == STATUS_OK ? -1 : (int32_t)s.cur_op;
         a.results[sim] = r;
     }
-    __syncthreads();
+    if (nw > 1) {
+        // release the helper waves from this replay
+        s.ctl[CTL_CMD] = CMD_DONE;
+        __syncthreads();
+    } else {
+        wave_sync();
+    }
 }
 
+// A helper wave of a multi-wave workgroup: joins the replaying wave's walk
+// scans (one workgroup barrier before, one after each) until it is released.
+// Each of its lanes has its own visited bitset, LDS stack and global queue.
 template <bool L>
-__global__ void __launch_bounds__(WAVE) log_kernel(LogKernelArgs a)
+__device__ void help_walks(const LogKernelArgs &a, uint8_t *base, int32_t lane, int32_t wave, uint8_t *lds)
+{
+    if constexpr (L) {
+        Sim<L> s;
+        const LogSlotLayout &Y = a.L;
+        GAS uint8_t *gb = (GAS uint8_t *)base;
+        const int32_t W = a.wm_words, id = wave * WAVE + lane;
+        s.wmw = W;
+        s.lane = lane;
+        s.state = (Mem<L, uint8_t>)(lds + a.lds_state);
+        s.wm = (Mem<L, uint32_t>)(lds + a.lds_wm) + id * W;
+        s.po = (Mem<L, const int32_t>)(lds + a.lds_po);
+        s.co = (Mem<L, const int32_t>)(lds + a.lds_co);
+        s.pa = (Mem<L, const Adj<L>>)(lds + a.lds_pa);
+        s.ca = (Mem<L, const Adj<L>>)(lds + a.lds_ca);
+        s.c0d = (Mem<L, int64_t>)(lds + a.lds_c0);
+        s.pcnt = (Mem<L, int32_t>)(lds + a.lds_pcnt);
+        s.ccnt = (Mem<L, int32_t>)(lds + a.lds_ccnt);
+        s.cand = (LAS uint16_t *)(lds + a.lds_cand);
+        s.stk = (LAS uint16_t *)(lds + a.lds_stk) + id * LOG_LDS_STACK;
+        s.ctr = (LAS uint32_t *)(lds + a.lds_ctr);
+        s.rsum = (LAS int64_t *)(lds + a.lds_rsum);
+        s.rcnt = (LAS int32_t *)(lds + a.lds_rcnt);
+        s.queue = (GAS int32_t *)(gb + Y.queue) + (size_t)id * (size_t)(Y.S_max + 2);
+        const LAS int32_t *ctl = (const LAS int32_t *)(lds + a.lds_ctl);
+        for (;;) {
+            __syncthreads();
+            if (ctl[CTL_CMD] == CMD_DONE) break;
+            walk_candidates(s, ctl[CTL_N], ctl[CTL_BOTH] != 0);
+            __syncthreads();
+        }
+    }
+}
+
+// One replay per workgroup at a time.  In the LDS variant the workgroup may
+// hold helper waves (a.waves in all) that join the replaying wave's walk scans;
+// every wave learns the next replay from the control words after a workgroup
+// barrier, so all of them leave the loop together.
+template <bool L>
+__global__ void __launch_bounds__(L ? MAX_LOG_WAVES * WAVE : WAVE) log_kernel(LogKernelArgs a)
 {
     extern __shared__ uint8_t lds_dyn[];
-    const int32_t lane = threadIdx.x;
+    const int32_t lane = (int32_t)threadIdx.x & (WAVE - 1);
+    const int32_t wave = uni((int32_t)threadIdx.x / WAVE);
+    const int32_t nw = L ? a.waves : 1;
     uint8_t *base = a.slots + (size_t)blockIdx.x * (size_t)a.L.bytes;
+    LAS int32_t *ctl = (LAS int32_t *)(lds_dyn + a.lds_ctl);
+    if constexpr (L) {
+        if (wave > 0) {
+            // a helper's visited bitsets start clear (each walk clears its own)
+            LAS uint32_t *M = (LAS uint32_t *)(lds_dyn + a.lds_wm) + (size_t)wave * WAVE * a.wm_words;
+            for (int32_t i = lane; i < WAVE * a.wm_words; i += WAVE) M[i] = 0;
+        }
+    }
     for (;;) {
         uint32_t k = 0;
-        if (lane == 0) k = atomicAdd(a.queue, 1u);
-        k = (uint32_t)uni((int32_t)k);
+        if (wave == 0 && lane == 0) k = atomicAdd(a.queue, 1u);
+        if (nw > 1) {
+            if (wave == 0 && lane == 0) ctl[CTL_K] = (int32_t)k;
+            __syncthreads();
+            k = (uint32_t)uni(ctl[CTL_K]);
+        } else {
+            k = (uint32_t)uni((int32_t)k);
+        }
         if (k >= (uint32_t)a.n_sims) break;
-        run_sim<L>(a, a.order[k], base, lane, lds_dyn);
+        if (wave == 0) run_sim<L>(a, a.order[k], base, lane, lds_dyn, nw);
+        else help_walks<L>(a, base, lane, wave, lds_dyn);
     }
 }
 
@@ -987,7 +1092,8 @@ extern "C" hipError_t dtr_launch_log(const dtr::LogKernelArgs *args, hipStream_t
                                                    hipFuncAttributeMaxDynamicSharedMemorySize, args->lds_bytes);
                 if (e != hipSuccess) return e;
             }
-            hipLaunchKernelGGL(logk::log_kernel<true>, dim3(args->n_slots), dim3(WAVE), args->lds_bytes, stream, *args);
+            hipLaunchKernelGGL(logk::log_kernel<true>, dim3(args->n_slots), dim3(WAVE * args->waves), args->lds_bytes,
+                               stream, *args);
         }
         else
             hipLaunchKernelGGL(logk::log_kernel<false>, dim3(args->n_slots), dim3(WAVE), 0, stream, *args);
