@@ -267,6 +267,23 @@ int dtr_log_create(const dtr_log *logs, int32_t n_logs,
                    void *device_workspace, size_t workspace_bytes,
                    void *stream, dtr_sim **out);
 
+/* How a handle's simulations occupy the device, fixed at creation:
+ * n_slots          simulations that can be in flight (one workgroup each);
+ * waves_per_group  wavefronts per workgroup: 1, except for operator logs
+ *                  whose walk state is in LDS, where up to 4 (the first
+ *                  replays, the others join its e* / e_R walk scans);
+ * lds_bytes        dynamic LDS per workgroup (0: the kernels' static LDS only,
+ *                  or walk state in device memory).
+ * Returns DTR_EINVAL for a NULL argument.  No device work. */
+typedef struct {
+    int32_t n_slots;
+    int32_t waves_per_group;
+    int32_t lds_bytes;
+    int32_t reserved;            /* 0 */
+} dtr_launch_info;
+
+int dtr_sim_launch_info(const dtr_sim *sim, dtr_launch_info *out);
+
 /* Release the handle (not the caller's workspace).  NULL is ignored. */
 void dtr_sim_destroy(dtr_sim *sim);
 

@@ -568,6 +568,12 @@ int log_plan_make(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims,
 }
 
 size_t log_plan_total(const LogPlan *p) { return p->total; }
+void log_plan_info(const LogPlan *p, int32_t *n_slots, int32_t *waves, int32_t *lds_bytes)
+{
+    *n_slots = p->n_slots;
+    *waves = p->lds_bytes > 0 ? p->waves : 1;
+    *lds_bytes = p->lds_bytes;
+}
 size_t log_plan_result_off(const LogPlan *p) { return p->result_off; }
 void log_plan_free(LogPlan *p) { delete p; }
 

@@ -556,6 +556,21 @@ int dtr_log_create(const dtr_log *logs, int32_t n_logs, const dtr_sim_spec *sims
     return DTR_OK;
 }
 
+int dtr_sim_launch_info(const dtr_sim *h, dtr_launch_info *out)
+{
+    g_err.clear();
+    if (!h || !out) return fail(DTR_EINVAL, "null handle or output");
+    out->reserved = 0;
+    if (h->log) {
+        dtrhost::log_plan_info(h->log, &out->n_slots, &out->waves_per_group, &out->lds_bytes);
+    } else {
+        out->n_slots = h->plan.n_slots;
+        out->waves_per_group = 1;
+        out->lds_bytes = 0;
+    }
+    return DTR_OK;
+}
+
 #ifdef DTR_PROFILE
 // Phase timers of the last run (DTR_PROFILE builds only; not part of the
 // public header): PROF_FIELDS int64 per simulation.

@@ -35,5 +35,7 @@ size_t log_plan_result_off(const LogPlan *p);
 int log_plan_upload(LogPlan *p, uint8_t *ws, hipStream_t st);
 int log_plan_launch(const LogPlan *p, uint8_t *ws, hipStream_t st);
 void log_plan_free(LogPlan *p);
+// resident slots, waves per workgroup and dynamic LDS bytes of the launch
+void log_plan_info(const LogPlan *p, int32_t *n_slots, int32_t *waves, int32_t *lds_bytes);
 
 }  // namespace dtrhost

@@ -62,13 +62,14 @@ def lib():
         L.dtr_sim_create.argtypes = [vp, i32, vp, i32, vp, vp, sz, vp, C.POINTER(vp)]
         L.dtr_sim_run.argtypes = [vp, vp]
         L.dtr_sim_results.argtypes = [vp, vp, i32]
+        L.dtr_sim_launch_info.argtypes = [vp, vp]
         L.dtr_sim_destroy.argtypes = [vp]
         L.dtr_sim_destroy.restype = None
         L.dtr_sim_last_error.restype = C.c_char_p
         L.dtr_log_workspace_bytes.argtypes = [vp, i32, vp, i32, vp, C.POINTER(sz)]
         L.dtr_log_create.argtypes = [vp, i32, vp, i32, vp, vp, sz, vp, C.POINTER(vp)]
         for f in ("dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run", "dtr_sim_results",
-                  "dtr_log_workspace_bytes", "dtr_log_create"):
+                  "dtr_sim_launch_info", "dtr_log_workspace_bytes", "dtr_log_create"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -176,6 +177,17 @@ def dtr_sim_results(handle: int, n_sims: int) -> np.ndarray:
     return out
 
 
+class _LaunchInfo(C.Structure):
+    _fields_ = [("n_slots", C.c_int32), ("waves_per_group", C.c_int32), ("lds_bytes", C.c_int32),
+                ("reserved", C.c_int32)]
+
+
+def dtr_sim_launch_info(handle: int) -> dict:
+    out = _LaunchInfo()
+    _check(lib().dtr_sim_launch_info(C.c_void_p(handle), C.byref(out)))
+    return {"n_slots": out.n_slots, "waves_per_group": out.waves_per_group, "lds_bytes": out.lds_bytes}
+
+
 def dtr_sim_destroy(handle: int):
     if handle:
         lib().dtr_sim_destroy(C.c_void_p(handle))
@@ -215,6 +227,10 @@ class Simulator:
     def results(self) -> np.ndarray:
         with self.torch.cuda.device(self.device):
             return dtr_sim_results(self.handle, self.n_sims)
+
+    def launch_info(self) -> dict:
+        """Resident slots, waves per workgroup and dynamic LDS bytes."""
+        return dtr_sim_launch_info(self.handle)
 
     def close(self):
         if getattr(self, "handle", 0):

@@ -34,6 +34,16 @@ def test_struct_sizes_match_header():
     assert D.RESULT_DTYPE.itemsize == 104
 
 
+def test_launch_info_layout_and_null_arguments():
+    text = open(D.HEADER).read()
+    body = text[text.index("typedef struct {", text.index("dtr_sim_launch_info") - 900):text.index("} dtr_launch_info;")]
+    fields = [l.split()[1].rstrip(";") for l in body.splitlines() if l.strip().startswith("int32_t")]
+    assert fields == [f for f, _ in D._LaunchInfo._fields_]
+    assert C.sizeof(D._LaunchInfo) == 16
+    L = D.lib()
+    assert L.dtr_sim_launch_info(None, None) == D.DTR_EINVAL
+
+
 def _spec(h=W.H_LRU, b=10, trace=0):
     return W.make_specs([(trace, h, b, 0)])
 

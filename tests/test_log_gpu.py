@@ -164,3 +164,26 @@ def test_resnet_log_config_sampled(gpu, oracle_lib):
     specs = wl.specs[::8]
     print(f"resnet log: {len(specs)} sims", flush=True)
     compare(gpu.run_log(wl.traces, specs), oracle_lib.run_log(wl.traces, specs), specs, "resnet50log")
+
+
+def test_workgroup_shapes_of_the_lds_variant(gpu, oracle_lib):
+    """Logs of growing size take 4, 2 and 1 waves per workgroup (helper waves
+    in the walk scans while the LDS holds their bitsets and stacks), then the
+    device-memory variant; each shape against the oracle."""
+    seen = set()
+    for n_steps in (1500, 2300, 2500, 2700, 2900, 3100, 3600):
+        L = W.random_log(6000 + n_steps, n_steps=n_steps, n_const=3, max_size=20, max_cost=7, max_in=3, keep=3)
+        pk = unlimited_peaks(oracle_lib, [L])[0]
+        rows = [(0, h, max(1, int(pk * f)), 11, W.POLICY_EAGER) for h in (W.H_DTR, W.H_MSPS, W.H_EQ)
+                for f in (0.15, 0.4)]
+        specs = W.make_specs(rows)
+        sim = gpu.Simulator(None, specs, logs=[L])
+        info = sim.launch_info()
+        sim.run()
+        got = sim.results()
+        sim.close()
+        shape = (info["waves_per_group"], info["lds_bytes"] > 0)
+        print(f"log of {n_steps} steps: {info}", flush=True)
+        seen.add(shape)
+        compare(got, oracle_lib.run_log([L], specs), specs, f"log of {n_steps} steps, {info}")
+    assert {(4, True), (2, True), (1, True), (1, False)} <= seen, seen
