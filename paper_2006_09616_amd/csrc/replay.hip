@@ -796,49 +796,6 @@ __device__ __forceinline__ int64_t eq_cost_full(const Sim &s, const NS &N, int32
     return sum;
 }
 
-// e*(x): evicted ancestors through evicted parents, then (if `both`) evicted
-// descendants through evicted children; lane-private stamps make it a set.
-__device__ __forceinline__ int64_t estar_cost(const Sim &s, int32_t x, uint32_t ep, int64_t &count, bool both)
-{
-    const int32_t lane = s.lane;
-    GAS uint32_t *st = s.S.stamp;
-    GAS int32_t *q = s.S.queue;
-    int64_t sum = 0, cnt = 0;
-    int32_t head = 0, tail = 0;
-    q[(size_t)tail++ * WAVE + lane] = x;
-    while (head < tail) {
-        const int32_t u = q[(size_t)head++ * WAVE + lane];
-        const TRec ru = rec_v(s, u);
-        for (int32_t k = ru.in_b; k < ru.in_e; k++) {
-            const int32_t p = gld(s.t.in + k);
-            if (ts_sw(s.S.tst[p]) < 0) continue;
-            const size_t sp = (size_t)p * WAVE + lane;
-            if (st[sp] == ep) continue;
-            st[sp] = ep;
-            sum += gld(s.t.c0 + p);
-            cnt++;
-            q[(size_t)tail++ * WAVE + lane] = p;
-        }
-    }
-    head = tail = 0;
-    if (both) q[(size_t)tail++ * WAVE + lane] = x;
-    while (head < tail) {
-        const int32_t u = q[(size_t)head++ * WAVE + lane];
-        for (int32_t k = gld(s.t.ch_off + u), e = gld(s.t.ch_off + u + 1); k < e; k++) {
-            const int32_t c = gld(s.t.ch + k);
-            if (ts_sw(s.S.tst[c]) < 0) continue;
-            const size_t sc = (size_t)c * WAVE + lane;
-            if (st[sc] == ep) continue;
-            st[sc] = ep;
-            sum += gld(s.t.c0 + c);
-            cnt++;
-            q[(size_t)tail++ * WAVE + lane] = c;
-        }
-    }
-    count = cnt;
-    return sum;
-}
-
 __device__ __forceinline__ void clear_stamps(Sim &s)
 {
     __syncthreads();
@@ -984,6 +941,141 @@ __device__ __forceinline__ int64_t cached_sum(const LAS UfNode *NL, const int32_
     return t;
 }
 
+// e* (h_DTR, h_{e*}) or e_R (h_MSPS) of every pooled candidate, walked with
+// lane-private epoch stamps and queues.  Flattened: a lane takes the next pool
+// slot as soon as its previous walk ends (lanes are handed consecutive slots
+// in lane order), and every iteration expands one queued tensor per lane: its
+// record element brings the first NB_HEAD neighbours (parents first), whose
+// states and stamps are then read together.  A walk's members are the tensors
+// it queues (the candidate itself is queued at the start of each side only);
+// their costs are added when they are expanded.  Each walk takes the next
+// epoch of its lane; the scan advances the epoch by the most walks a lane made.
+template <int HC>
+__device__ __forceinline__ void walk_scan(Sim &s, const Filter &F, Best &best, int64_t &scored)
+{
+    const int32_t end = s.pool_end, lane = s.lane;
+    const int64_t T = s.T;
+    const bool both = s.cmode == CM_ESTAR;
+    GAS uint32_t *st = s.S.stamp;
+    GAS int32_t *q = s.S.queue;
+    int32_t next = 0;                     // next pool slot to hand out (uniform)
+    int32_t x = -1, slot = -1, head = 0, tail = 0, side = 0, deg = 0;
+    int64_t sum = 0, cnt = 0, c0x = 0, size = 0, last = 0, nscored = 0;
+    uint32_t walks = 0, ep = 0;
+    for (;;) {
+        const bool idle = x < 0;
+        const uint64_t mi = __ballot(idle);
+        if (mi && next < end) {
+            if (idle) {
+                const int32_t i = next + lane_rank(mi);
+                if (i < end) {
+                    const i32x4 *P = (const i32x4 *)&s.S.pool(i);
+                    const i32x4 q0 = P[0], q1 = P[1];
+                    bool ok = q0.x >= 0;
+                    const int64_t sz = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
+                    if (approx(HC)) {
+                        ok = ok && (uint64_t)sz >= F.min_size;
+                        if (F.sample) ok = ok && sample_draw(s, q0.x) < F.tau;
+                    }
+                    if (ok) {
+                        x = q0.x;
+                        slot = i;
+                        deg = q0.y >> 8;
+                        last = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
+                        size = sz;
+                        c0x = (int64_t)q1.z;
+                        side = 0;
+                        head = 0;
+                        tail = 1;
+                        q[lane] = x;
+                        sum = cnt = 0;
+                        walks++;
+                        ep = s.epoch + walks;
+                    }
+                }
+            }
+            next += __popcll(mi);
+        }
+        const uint64_t ma = __ballot(x >= 0);
+        if (!ma) {
+            if (next >= end) break;
+            continue;
+        }
+        bool fin = false;
+        if (x >= 0) {
+            if (head < tail) {
+                const int32_t u = q[(size_t)head * WAVE + lane];
+                const GAS i32x4 *R = (const GAS i32x4 *)&s.t.rec[u];
+                const i32x4 r0 = R[0], r1 = R[1], n0 = R[2], n1 = R[3];
+                if (head > 0) {           // a member (not the candidate)
+                    sum += (int64_t)r0.z;
+                    cnt++;
+                }
+                head++;
+                const int32_t np = r1.y - r1.x, dg = r1.w - r1.z, ab = r1.z;
+                const int32_t b = side == 0 ? 0 : np, e = side == 0 ? np : dg;
+                const int32_t nb[NB_HEAD] = {n0.x, n0.y, n0.z, n0.w, n1.x, n1.y, n1.z, n1.w};
+                // neighbours WB at a time: from the inline table below NB_HEAD,
+                // then from the adjacency list; every read is unconditional
+                // (clamped in range) so that a chunk's reads issue together
+                constexpr int WB = 4;
+                for (int32_t k0 = b; k0 < e; k0 += WB) {
+                    int32_t v[WB];
+                    uint64_t w[WB];
+                    uint32_t sv[WB];
+#pragma unroll
+                    for (int j = 0; j < WB; j++) {
+                        const int32_t k = min(k0 + j, e - 1);
+                        int32_t id = nb[0];
+#pragma unroll
+                        for (int t = 1; t < NB_HEAD; t++) id = k == t ? nb[t] : id;
+                        v[j] = k < NB_HEAD ? id : gld(s.t.adj + ab + k);
+                    }
+#pragma unroll
+                    for (int j = 0; j < WB; j++) {
+                        w[j] = s.S.tst[v[j]];
+                        sv[j] = st[(size_t)v[j] * WAVE + lane];
+                    }
+#pragma unroll
+                    for (int j = 0; j < WB; j++) {
+                        if (k0 + j < e && ts_sw(w[j]) >= 0 && sv[j] != ep) {
+                            st[(size_t)v[j] * WAVE + lane] = ep;
+                            q[(size_t)tail++ * WAVE + lane] = v[j];
+                        }
+                    }
+                }
+            } else if (side == 0 && both) {
+                side = 1;
+                head = 0;
+                tail = 1;
+                q[lane] = x;
+            } else {
+                fin = true;
+            }
+        }
+        // a finished walk is scored (every lane takes part in the reduction step)
+        if (__ballot(fin)) {
+            const uint64_t N = (uint64_t)(c0x + sum);
+            const uint64_t DA = s.use_m ? (uint64_t)size : 1;
+            const uint64_t DB = s.use_s ? (uint64_t)(T - last) : 1;
+            take(best, fin, fin ? score_est(N, DA, DB) : 0.0f, N, DA, DB, x, slot);
+        }
+        if (fin) {
+            s.nbr += cnt;
+            s.adj += deg;
+            nscored++;
+            x = -1;
+        }
+    }
+    uint32_t mw = walks;
+    for (int off = WAVE / 2; off >= 1; off >>= 1) mw = max(mw, (uint32_t)__shfl_xor((int32_t)mw, off, WAVE));
+    s.epoch += uni((int32_t)mw);
+    if (approx(HC)) {
+        for (int off = WAVE / 2; off >= 1; off >>= 1) nscored += __shfl_xor(nscored, off, WAVE);
+        scored += (int64_t)uni64(nscored);
+    }
+}
+
 template <int HC>
 __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filter &F, int64_t &scored)
 {
@@ -1001,195 +1093,183 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
     best.slot = -1;
     best.have = 0;
     constexpr int U = Round<HC>::value;
-    if (cls(HC) == HC_WALK && (uint64_t)s.epoch + (uint64_t)(end / WAVE) + 2 * U + 2 >= 0xffffffffull)
-        clear_stamps(s);
+    if (cls(HC) == HC_WALK && (uint64_t)s.epoch + (uint64_t)end + 2 >= 0xffffffffull) clear_stamps(s);
     // quads of the next round when it lies in global memory, read one round
     // ahead so that their latency overlaps this round's scoring (scans start
     // in LDS, so every global round has been read ahead by its predecessor)
     static_assert(POOL_LDS > 0, "the first round of a scan lies in LDS");
     i32x4 P0[U], P1[U], PC[U][KQ];
-    for (int32_t base = 0; base < end; base += WAVE * U) {
-        int32_t id[U], pd[U];
-        uint32_t slot[U];
-        int64_t last[U], size[U], c0[U];
-        int32_t ab[U];
-        int32_t nb[U][K];
-        bool ok[U];
-        // level 1: the 16-byte quads of each slot, all issued together, from
-        // LDS or global memory (a round never straddles the two)
-        i32x4 Q0[U], Q1[U], QC[U][KQ];
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            const int32_t i = base + u * WAVE + lane;
-            slot[u] = (uint32_t)(i < end ? i : base);
-        }
-        if (base < POOL_LDS) {
-#pragma unroll
+    if constexpr (cls(HC) == HC_WALK) {
+        walk_scan<HC>(s, F, best, scored);
+    } else {
+        for (int32_t base = 0; base < end; base += WAVE * U) {
+            int32_t id[U], pd[U];
+            uint32_t slot[U];
+            int64_t last[U], size[U], c0[U];
+            int32_t ab[U];
+            int32_t nb[U][K];
+            bool ok[U];
+            // level 1: the 16-byte quads of each slot, all issued together, from
+            // LDS or global memory (a round never straddles the two)
+            i32x4 Q0[U], Q1[U], QC[U][KQ];
+    #pragma unroll
             for (int u = 0; u < U; u++) {
-                Q0[u] = L4[PQ * slot[u]];
-                Q1[u] = L4[PQ * slot[u] + 1];
-#pragma unroll
-                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
+                const int32_t i = base + u * WAVE + lane;
+                slot[u] = (uint32_t)(i < end ? i : base);
             }
-        } else {
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                Q0[u] = P0[u];
-                Q1[u] = P1[u];
-#pragma unroll
-                for (int k = 0; k < KQ; k++) QC[u][k] = PC[u][k];
-            }
-        }
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            const int32_t i = base + u * WAVE + lane;
-            const i32x4 q0 = Q0[u], q1 = Q1[u];
-            id[u] = i < end ? q0.x : -1;
-            pd[u] = q0.y;
-            last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
-            size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
-            c0[u] = (int64_t)q1.z;
-            ab[u] = q1.w;
-#pragma unroll
-            for (int k = 0; k < KQ; k++) {
-                nb[u][4 * k] = QC[u][k].x;
-                nb[u][4 * k + 1] = QC[u][k].y;
-                nb[u][4 * k + 2] = QC[u][k].z;
-                nb[u][4 * k + 3] = QC[u][k].w;
-            }
-            ok[u] = id[u] >= 0;
-            if (approx(HC)) {
-                ok[u] = ok[u] && (uint64_t)size[u] >= F.min_size;
-                if (F.sample) ok[u] = ok[u] && sample_draw(s, id[u]) < F.tau;
-            }
-        }
-        const int32_t nbase = base + WAVE * U;
-        if (nbase < end && nbase >= POOL_LDS) {
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                const int32_t i = nbase + u * WAVE + lane;
-                const uint32_t ns = (uint32_t)(i < end ? i : nbase);
-                P0[u] = G4[PQ * ns];
-                P1[u] = G4[PQ * ns + 1];
-#pragma unroll
-                for (int k = 0; k < KQ; k++) PC[u][k] = cls(HC) == HC_EQ ? G4[PQ * ns + 2 + k] : 0;
-            }
-        }
-        uint64_t N[U], DA[U], DB[U];
-        if (cls(HC) == HC_EQ) {
-            const bool lds_nodes = s.uf_n <= UF_LDS;
-            // level 2: every cached node (unused entries hold node 0, the null
-            // node); level 3: its parent, so nodes one merge away resolve too
-            int64_t sum[U], ev[U];
-            bool slow[U];
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                const int32_t c = pd[u] & 0xFF;
-                // roots are their own parent, so the node two hops along (n2)
-                // is the set root whenever the cached node is at most one
-                // merge away from it; its cost is used unconditionally
-                bool deep = false;
-                // cache entries at or beyond every lane's count hold the null
-                // node (cost 0, its own root) and are skipped when the whole
-                // wave allows it
-                if (lds_nodes) {
-                    const LAS UfNode *NL = s.S.nodes.lds_l;
-                    if (!__ballot(c > 2)) sum[u] = cached_sum<2>(NL, nb[u], deep);
-                    else if (!__ballot(c > 4)) sum[u] = cached_sum<4>(NL, nb[u], deep);
-                    else sum[u] = cached_sum<K>(NL, nb[u], deep);
-                } else {
-                    int32_t r[K];
-                    int64_t cost[K];
-#pragma unroll
-                    for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
-#pragma unroll
-                    for (int k = 0; k < K; k++) {
-                        const UfNode n2 = s.S.nodes[r[k]];
-                        cost[k] = n2.cost;
-                        deep |= n2.parent != r[k];
-                    }
-                    int64_t t = 0;
-#pragma unroll
-                    for (int k = 0; k < K; k++) {
-                        bool dup = false;
-#pragma unroll
-                        for (int j = 0; j < k; j++) dup |= r[j] == r[k];
-                        t += dup ? 0 : cost[k];
-                    }
-                    sum[u] = t;
+            if (base < POOL_LDS) {
+    #pragma unroll
+                for (int u = 0; u < U; u++) {
+                    Q0[u] = L4[PQ * slot[u]];
+                    Q1[u] = L4[PQ * slot[u] + 1];
+    #pragma unroll
+                    for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
                 }
-                ev[u] = c;
-                slow[u] = ok[u] && (c > K || deep);
-            }
-            // rare: overflowed cache or a merged-away node -- exact recount
-            bool any_slow = false;
-#pragma unroll
-            for (int u = 0; u < U; u++) any_slow |= slow[u];
-#ifdef DTR_PROFILE
-            {
-                int32_t ns = 0;
-#pragma unroll
-                for (int u = 0; u < U; u++) ns += slow[u] ? 1 : 0;
-                s.prof_slow += ns;     // per lane; reduced at the end
-                for (int u = 0; u < U; u++) s.prof_global_nodes += ok[u] && (pd[u] & 0xFF) > K ? 1 : 0;
-            }
-#endif
-            if (__ballot(any_slow)) {
-                if (lds_nodes) {
-                    LdsNodes NL;
-                    NL.p = s.S.nodes.lds_l;
-#pragma unroll
-                    for (int u = 0; u < U; u++)
-                        if (slow[u]) sum[u] = eq_cost_full(s, NL, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
-                } else {
-                    AnyNodes NA;
-                    NA.n = s.S.nodes;
-#pragma unroll
-                    for (int u = 0; u < U; u++)
-                        if (slow[u]) sum[u] = eq_cost_full(s, NA, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+            } else {
+    #pragma unroll
+                for (int u = 0; u < U; u++) {
+                    Q0[u] = P0[u];
+                    Q1[u] = P1[u];
+    #pragma unroll
+                    for (int k = 0; k < KQ; k++) QC[u][k] = PC[u][k];
                 }
             }
-#pragma unroll
+    #pragma unroll
             for (int u = 0; u < U; u++) {
-                N[u] = (uint64_t)(c0[u] + sum[u]);
-                DA[u] = s.use_m ? (uint64_t)size[u] : 1;
-                DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
-                s.nbr += ok[u] ? ev[u] : 0;
-                s.adj += ok[u] ? (pd[u] >> 8) : 0;
+                const int32_t i = base + u * WAVE + lane;
+                const i32x4 q0 = Q0[u], q1 = Q1[u];
+                id[u] = i < end ? q0.x : -1;
+                pd[u] = q0.y;
+                last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
+                size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
+                c0[u] = (int64_t)q1.z;
+                ab[u] = q1.w;
+    #pragma unroll
+                for (int k = 0; k < KQ; k++) {
+                    nb[u][4 * k] = QC[u][k].x;
+                    nb[u][4 * k + 1] = QC[u][k].y;
+                    nb[u][4 * k + 2] = QC[u][k].z;
+                    nb[u][4 * k + 3] = QC[u][k].w;
+                }
+                ok[u] = id[u] >= 0;
+                if (approx(HC)) {
+                    ok[u] = ok[u] && (uint64_t)size[u] >= F.min_size;
+                    if (F.sample) ok[u] = ok[u] && sample_draw(s, id[u]) < F.tau;
+                }
             }
-        } else if (cls(HC) == HC_WALK) {
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                N[u] = 0;
-                DA[u] = DB[u] = 1;
-                if (!ok[u]) continue;
-                int64_t cnt;
-                const uint32_t ep = s.epoch + 1 + (uint32_t)u;
-                N[u] = (uint64_t)(c0[u] + estar_cost(s, id[u], ep, cnt, s.cmode == CM_ESTAR));
-                DA[u] = s.use_m ? (uint64_t)size[u] : 1;
-                DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
-                s.nbr += cnt;
-                s.adj += pd[u] >> 8;
+            const int32_t nbase = base + WAVE * U;
+            if (nbase < end && nbase >= POOL_LDS) {
+    #pragma unroll
+                for (int u = 0; u < U; u++) {
+                    const int32_t i = nbase + u * WAVE + lane;
+                    const uint32_t ns = (uint32_t)(i < end ? i : nbase);
+                    P0[u] = G4[PQ * ns];
+                    P1[u] = G4[PQ * ns + 1];
+    #pragma unroll
+                    for (int k = 0; k < KQ; k++) PC[u][k] = cls(HC) == HC_EQ ? G4[PQ * ns + 2 + k] : 0;
+                }
             }
-            s.epoch += U;
-        } else {
-#pragma unroll
-            for (int u = 0; u < U; u++) {
-                if (s.cmode == CM_RAND) {
-                    const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
-                    N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
-                    DA[u] = DB[u] = 1;
-                } else {
-                    N[u] = s.cmode == CM_LOCAL ? (uint64_t)c0[u] : 1;
+            uint64_t N[U], DA[U], DB[U];
+            if (cls(HC) == HC_EQ) {
+                const bool lds_nodes = s.uf_n <= UF_LDS;
+                // level 2: every cached node (unused entries hold node 0, the null
+                // node); level 3: its parent, so nodes one merge away resolve too
+                int64_t sum[U], ev[U];
+                bool slow[U];
+    #pragma unroll
+                for (int u = 0; u < U; u++) {
+                    const int32_t c = pd[u] & 0xFF;
+                    // roots are their own parent, so the node two hops along (n2)
+                    // is the set root whenever the cached node is at most one
+                    // merge away from it; its cost is used unconditionally
+                    bool deep = false;
+                    // cache entries at or beyond every lane's count hold the null
+                    // node (cost 0, its own root) and are skipped when the whole
+                    // wave allows it
+                    if (lds_nodes) {
+                        const LAS UfNode *NL = s.S.nodes.lds_l;
+                        if (!__ballot(c > 2)) sum[u] = cached_sum<2>(NL, nb[u], deep);
+                        else if (!__ballot(c > 4)) sum[u] = cached_sum<4>(NL, nb[u], deep);
+                        else sum[u] = cached_sum<K>(NL, nb[u], deep);
+                    } else {
+                        int32_t r[K];
+                        int64_t cost[K];
+    #pragma unroll
+                        for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
+    #pragma unroll
+                        for (int k = 0; k < K; k++) {
+                            const UfNode n2 = s.S.nodes[r[k]];
+                            cost[k] = n2.cost;
+                            deep |= n2.parent != r[k];
+                        }
+                        int64_t t = 0;
+    #pragma unroll
+                        for (int k = 0; k < K; k++) {
+                            bool dup = false;
+    #pragma unroll
+                            for (int j = 0; j < k; j++) dup |= r[j] == r[k];
+                            t += dup ? 0 : cost[k];
+                        }
+                        sum[u] = t;
+                    }
+                    ev[u] = c;
+                    slow[u] = ok[u] && (c > K || deep);
+                }
+                // rare: overflowed cache or a merged-away node -- exact recount
+                bool any_slow = false;
+    #pragma unroll
+                for (int u = 0; u < U; u++) any_slow |= slow[u];
+    #ifdef DTR_PROFILE
+                {
+                    int32_t ns = 0;
+    #pragma unroll
+                    for (int u = 0; u < U; u++) ns += slow[u] ? 1 : 0;
+                    s.prof_slow += ns;     // per lane; reduced at the end
+                    for (int u = 0; u < U; u++) s.prof_global_nodes += ok[u] && (pd[u] & 0xFF) > K ? 1 : 0;
+                }
+    #endif
+                if (__ballot(any_slow)) {
+                    if (lds_nodes) {
+                        LdsNodes NL;
+                        NL.p = s.S.nodes.lds_l;
+    #pragma unroll
+                        for (int u = 0; u < U; u++)
+                            if (slow[u]) sum[u] = eq_cost_full(s, NL, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+                    } else {
+                        AnyNodes NA;
+                        NA.n = s.S.nodes;
+    #pragma unroll
+                        for (int u = 0; u < U; u++)
+                            if (slow[u]) sum[u] = eq_cost_full(s, NA, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+                    }
+                }
+    #pragma unroll
+                for (int u = 0; u < U; u++) {
+                    N[u] = (uint64_t)(c0[u] + sum[u]);
                     DA[u] = s.use_m ? (uint64_t)size[u] : 1;
                     DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
+                    s.nbr += ok[u] ? ev[u] : 0;
+                    s.adj += ok[u] ? (pd[u] >> 8) : 0;
+                }
+            } else {
+    #pragma unroll
+                for (int u = 0; u < U; u++) {
+                    if (s.cmode == CM_RAND) {
+                        const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
+                        N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
+                        DA[u] = DB[u] = 1;
+                    } else {
+                        N[u] = s.cmode == CM_LOCAL ? (uint64_t)c0[u] : 1;
+                        DA[u] = s.use_m ? (uint64_t)size[u] : 1;
+                        DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
+                    }
                 }
             }
-        }
-#pragma unroll
-        for (int u = 0; u < U; u++) {
-            take(best, ok[u], score_est(N[u], DA[u], DB[u]), N[u], DA[u], DB[u], id[u], (int32_t)slot[u]);
-            if (approx(HC)) scored += __popcll(__ballot(ok[u]));
+    #pragma unroll
+            for (int u = 0; u < U; u++) {
+                take(best, ok[u], score_est(N[u], DA[u], DB[u]), N[u], DA[u], DB[u], id[u], (int32_t)slot[u]);
+                if (approx(HC)) scored += __popcll(__ballot(ok[u]));
+            }
         }
     }
     if (__ballot(bad)) { set_status(s, ST_CAPACITY); return -1; }
