@@ -27,7 +27,8 @@
 //    rematerialization subtracts c0 and detaches the tensor (split
 //    approximation); the node pool is compacted when full;
 //  * h_DTR / h_{e*}: each lane walks its candidate's evicted ancestors and
-//    descendants (e*, Appendix C.2) with lane-private epoch stamps.
+//    descendants (e*, Appendix C.2) with lane-private epoch stamps, taking the
+//    next candidate as soon as its walk ends.
 //
 // Scores N/D are compared exactly by 128-bit cross-multiplication; ties go to
 // the smaller tensor id.  Last-access times are not kept per tensor: a tensor
