@@ -210,3 +210,26 @@ def test_random_dag_full_size_sampled(gpu, oracle_lib):
     specs = w.specs[pick]
     print(f"random dag full size: sims {pick.tolist()}", flush=True)
     compare(gpu.run(w.traces, specs), oracle_lib.run(w.traces, specs), specs, "randdag100k-sampled")
+
+
+def test_treelstm_full_batch_sampled(gpu, oracle_lib):
+    """The full TreeLSTM batch (4096 traces x 8 budgets, 32768 simulations) in
+    one launch, as the benchmark times it: every simulation checked against
+    properties that hold at any size, every 256th against the oracle."""
+    w = W.make_config("treelstm4096")
+    print(f"treelstm full batch: {w.n_sims} sims", flush=True)
+    got = gpu.run(w.traces, w.specs)
+    ok = got["status"] == 0
+    assert (got["total_cost"] == got["base_cost"] + got["remat_cost"]).all()
+    assert (got["peak_memory"][ok] <= w.specs["budget"][ok]).all()
+    assert (got["final_memory"][ok] <= w.specs["budget"][ok]).all()
+    # a finished simulation executes every trace operation once, plus its rematerializations
+    base = np.array([int(t.op_cost.sum()) for t in w.traces])[w.specs["trace"]]
+    n_ops = np.array([t.n_ops for t in w.traces])[w.specs["trace"]]
+    assert (got["base_cost"][ok] == base[ok]).all()
+    assert (got["n_executed_ops"][ok] == n_ops[ok] + got["n_remats"][ok]).all()
+    assert (got["failed_op"][ok] == -1).all() and (got["failed_op"][~ok] >= 0).all()
+    assert set(np.unique(got["status"]).tolist()) <= {0, 1}
+    pick = np.arange(0, w.n_sims, 256)
+    sub = w.specs[pick]
+    compare(got[pick], oracle_lib.run(w.traces, sub, threads=16), sub, "treelstm4096-sampled")
