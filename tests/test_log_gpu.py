@@ -166,6 +166,26 @@ def test_resnet_log_config_sampled(gpu, oracle_lib):
     compare(gpu.run_log(wl.traces, specs), oracle_lib.run_log(wl.traces, specs), specs, "resnet50log")
 
 
+def test_resnet_log_full_batch_properties(gpu):
+    """All 1536 replays of the ResNet log in one launch, against properties
+    that hold at any size: a finished replay runs every operator (CALL,
+    MUTATE, CONSTANT) once at its listed cost, plus its rematerializations,
+    within its budget."""
+    wl = W.make_config("resnet50log")
+    L = wl.traces[0]
+    kind, value = np.asarray(L.kind), np.asarray(L.value)
+    n_ops = int(np.isin(kind, [W.LOG_CALL, W.LOG_MUTATE, W.LOG_CONSTANT]).sum())
+    base = int(value[np.isin(kind, [W.LOG_CALL, W.LOG_MUTATE])].sum())
+    got = gpu.run_log(wl.traces, wl.specs)
+    ok = got["status"] == 0
+    assert ok.any() and (~ok).any()
+    assert (got["total_cost"] == got["base_cost"] + got["remat_cost"]).all()
+    assert (got["base_cost"][ok] == base).all()
+    assert (got["n_executed_ops"][ok] == n_ops + got["n_remats"][ok]).all()
+    assert (got["peak_memory"][ok] <= wl.specs["budget"][ok]).all()
+    assert (got["failed_op"][ok] == -1).all() and (got["failed_op"][~ok] >= 0).all()
+
+
 def test_workgroup_shapes_of_the_lds_variant(gpu, oracle_lib):
     """Logs of growing size take 4, 2 and 1 waves per workgroup (helper waves
     in the walk scans while the LDS holds their bitsets and stacks), then the
