@@ -207,3 +207,22 @@ def test_workgroup_shapes_of_the_lds_variant(gpu, oracle_lib):
         seen.add(shape)
         compare(got, oracle_lib.run_log([L], specs), specs, f"log of {n_steps} steps, {info}")
     assert {(4, True), (2, True), (1, True), (1, False)} <= seen, seen
+
+
+def test_more_storages_than_16_bit_ids(gpu, oracle_lib):
+    """A log of 66000 storages (the Appendix A chain of 33000 layers written as
+    a log): its neighbour ids do not fit the LDS variant's 16 bits, so it
+    replays from device memory."""
+    L = W.log_from_trace(W.chain_trace(33000))
+    pk = W.log_peak(L)
+    rows = [(0, h, int(pk * f), 3, W.POLICY_EAGER) for h in (W.H_LRU, W.H_EQ, W.H_SIZE) for f in (0.97, 0.99)]
+    rows += [(0, h, int(pk * 0.99), 3, W.POLICY_EAGER) for h in (W.H_DTR, W.H_MSPS)]
+    specs = W.make_specs(rows)
+    sim = gpu.Simulator(None, specs, logs=[L])
+    info = sim.launch_info()
+    sim.run()
+    got = sim.results()
+    sim.close()
+    print(f"66000-storage log: {info}", flush=True)
+    assert info["lds_bytes"] == 0 and info["waves_per_group"] == 1
+    compare(got, oracle_lib.run_log([L], specs), specs, "66000-storage chain log")
