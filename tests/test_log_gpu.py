@@ -226,3 +226,18 @@ def test_more_storages_than_16_bit_ids(gpu, oracle_lib):
     print(f"66000-storage log: {info}", flush=True)
     assert info["lds_bytes"] == 0 and info["waves_per_group"] == 1
     compare(got, oracle_lib.run_log([L], specs), specs, "66000-storage chain log")
+
+
+def test_wide_operators_as_logs(gpu, oracle_lib):
+    """Operators with up to ~180 inputs and storages read by up to ~240
+    operators, written as logs (inputs checked over several 64-lane chunks)."""
+    logs, rows = [], []
+    for s in range(3):
+        tr = W.random_program(900 + s, n_ops=260, n_const=4, max_in=130, backward=s % 2 == 0, max_size=9,
+                              max_cost=6)
+        logs.append(W.log_from_trace(tr))
+        rows += rows_for(s, W.natural_peak(tr), s, HS, policies=(W.POLICY_EAGER, W.POLICY_BANISH),
+                         fracs=(0.8, 0.95, 0.995))
+    specs = W.make_specs(rows)
+    print(f"wide logs: {len(specs)} sims", flush=True)
+    compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "wide logs")

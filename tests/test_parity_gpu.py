@@ -233,3 +233,31 @@ def test_treelstm_full_batch_sampled(gpu, oracle_lib):
     pick = np.arange(0, w.n_sims, 256)
     sub = w.specs[pick]
     compare(got[pick], oracle_lib.run(w.traces, sub, threads=16), sub, "treelstm4096-sampled")
+
+
+def _wide_programs():
+    """Programs whose operators read up to ~180 inputs and whose tensors feed
+    up to ~240 operators: input locking, rematerialization checks, unlocking,
+    neighbour caches, merges and walks all run over several 64-lane chunks."""
+    return [W.random_program(900 + s, n_ops=260, n_const=4, max_in=130, backward=s % 2 == 0, max_size=9,
+                             max_cost=6) for s in range(3)]
+
+
+def _wide_rows(traces):
+    rows = []
+    for i, tr in enumerate(traces):
+        pk = W.natural_peak(tr)
+        for h in range(8):
+            for pol in (W.POLICY_EAGER, W.POLICY_BANISH):
+                if pol == W.POLICY_BANISH and h == W.H_EQ:
+                    continue
+                for f in (0.8, 0.95, 0.995):
+                    rows.append((i, h, int(pk * f), 7 + i, pol))
+    return rows
+
+
+def test_wide_operators(gpu, oracle_lib):
+    trs = _wide_programs()
+    specs = specs_of(_wide_rows(trs))
+    print(f"wide operators: {len(specs)} sims", flush=True)
+    compare(gpu.run(trs, specs), oracle_lib.run(trs, specs), specs, "wide operators")
