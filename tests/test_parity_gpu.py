@@ -1,5 +1,6 @@
 """GPU parity: the HIP path, called through the C ABI, against the CPU oracle,
 field by field and bit-exact (every quantity is an integer)."""
+import math
 import os
 
 import numpy as np
@@ -261,3 +262,19 @@ def test_wide_operators(gpu, oracle_lib):
     specs = specs_of(_wide_rows(trs))
     print(f"wide operators: {len(specs)} sims", flush=True)
     compare(gpu.run(trs, specs), oracle_lib.run(trs, specs), specs, "wide operators")
+
+
+def test_deep_rematerialization_chain(gpu, oracle_lib):
+    """The Appendix A chain at 2000 layers: at budget 2*ceil(sqrt(N)) under
+    the neighbourhood heuristics, and at budget 4 under h_DTR^eq, h_LRU and
+    h_size, where backward steps rematerialize the forward chain from its start
+    (remat stacks about N frames deep, ~1M rematerializations)."""
+    N = 2000
+    tr = W.chain_trace(N)
+    rows = [(0, h, 2 * math.ceil(math.sqrt(N)), 3) for h in (W.H_DTR, W.H_EQ, W.H_LRU, W.H_ESTAR, W.H_MSPS)]
+    rows += [(0, h, 4, 3) for h in (W.H_EQ, W.H_LRU, W.H_SIZE)]
+    specs = specs_of(rows)
+    print(f"deep chain: {len(specs)} sims", flush=True)
+    ref = oracle_lib.run([tr], specs, threads=16)
+    compare(gpu.run([tr], specs), ref, specs, "deep chain")
+    assert int(ref["n_remats"].max()) > 500_000
