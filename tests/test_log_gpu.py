@@ -241,3 +241,22 @@ def test_wide_operators_as_logs(gpu, oracle_lib):
     specs = W.make_specs(rows)
     print(f"wide logs: {len(specs)} sims", flush=True)
     compare(gpu.run_log(logs, specs), oracle_lib.run_log(logs, specs), specs, "wide logs")
+
+
+def test_deep_rematerialization_chain_logs(gpu, oracle_lib):
+    """The Appendix A chain written as logs, at 700 layers (walk state in LDS)
+    and 2000 layers (device memory): operator-call stacks about N frames deep
+    at budget 4."""
+    import math
+    for N in (700, 2000):
+        L = W.log_from_trace(W.chain_trace(N))
+        rows = [(0, h, 2 * math.ceil(math.sqrt(N)), 3) for h in (W.H_DTR, W.H_EQ, W.H_ESTAR, W.H_MSPS)]
+        rows += [(0, h, 4, 3) for h in (W.H_EQ, W.H_LRU)]
+        specs = W.make_specs(rows)
+        sim = gpu.Simulator(None, specs, logs=[L])
+        info = sim.launch_info()
+        sim.run()
+        got = sim.results()
+        sim.close()
+        print(f"chain log of {N} layers: {info}", flush=True)
+        compare(got, oracle_lib.run_log([L], specs, threads=16), specs, f"chain log {N}")
