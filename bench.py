@@ -100,35 +100,37 @@ def copy_probe(mib: int):
     print(json.dumps({"copy_probe_bytes": n, "copies": 3}))
 
 
-def search_study(wl, steps: int):
-    """The prototype's search approximations (ignore small candidates, sample
-    sqrt(n) of the pool; Appendix E) against exact search on the same batch:
-    OOM rate, total cost relative to exact search where both finish, scores
-    searched, and launch time."""
+def _timed(traces, specs, steps: int):
+    """Results and mean event-timed launch (ms) of one batch."""
     import torch
     from paper_2006_09616_amd import dtr as D
-    variants = {"exact": 0, "ignore_small": W.SEARCH_IGNORE_SMALL, "sample": W.SEARCH_SAMPLE,
-                "ignore_small+sample": W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE}
-    out, base = {}, None
-    for name, flags in variants.items():
-        specs = wl.specs.copy()
-        specs["search"] = flags
-        sim = D.Simulator(wl.traces, specs, device="cuda:0")
+    sim = D.Simulator(traces, specs, device="cuda:0")
+    sim.run()
+    torch.cuda.synchronize()
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    for i in range(steps):
+        ev0[i].record(sim.stream)
         sim.run()
-        torch.cuda.synchronize()
-        ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-        ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
-        for i in range(steps):
-            ev0[i].record(sim.stream)
-            sim.run()
-            ev1[i].record(sim.stream)
-        torch.cuda.synchronize()
-        ms = sum(a.elapsed_time(b) for a, b in zip(ev0, ev1)) / steps
-        res = sim.results()
-        sim.close()
+        ev1[i].record(sim.stream)
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in zip(ev0, ev1)) / steps
+    res = sim.results()
+    sim.close()
+    return res, ms
+
+
+def _variant_rows(traces, variants, steps: int, label: str):
+    """Each variant (name -> specs) timed; the first is the reference for the
+    total-cost ratios (simulations that finish under both), the OOM count
+    and the speedup."""
+    out, base = {}, None
+    for name, specs in variants.items():
+        res, ms = _timed(traces, specs, steps)
         ok = res["status"] == 0
-        row = {"launch_ms": ms, "oom_rate": float(np.mean(res["status"] == 1)),
-               "scores": int(res["n_scores"].sum()), "ops": int(res["n_executed_ops"].sum())}
+        row = {"sims": int(len(specs)), "launch_ms": ms, "oom_rate": float(np.mean(res["status"] == 1)),
+               "scores": int(res["n_scores"].sum()), "ops": int(res["n_executed_ops"].sum()),
+               "ops_per_s": int(res["n_executed_ops"].sum()) / (ms / 1e3)}
         if base is None:
             base = (res, ms)
         else:
@@ -136,11 +138,65 @@ def search_study(wl, steps: int):
             ratio = res["total_cost"][both] / base[0]["total_cost"][both]
             row.update(speedup=base[1] / ms, cost_ratio_mean=float(ratio.mean()) if both.any() else None,
                        cost_ratio_max=float(ratio.max()) if both.any() else None,
-                       scores_vs_exact=row["scores"] / max(1, int(base[0]["n_scores"].sum())),
+                       scores_vs_first=row["scores"] / max(1, int(base[0]["n_scores"].sum())),
                        newly_oom=int(((res["status"] == 1) & (base[0]["status"] == 0)).sum()))
         out[name] = row
-        print(f"[bench] search study {name}: {ms:.1f} ms, oom {row['oom_rate']:.4f}", file=sys.stderr, flush=True)
+        print(f"[bench] {label} {name}: {ms:.1f} ms, oom {row['oom_rate']:.4f}", file=sys.stderr, flush=True)
     return out
+
+
+def search_study(wl, steps: int):
+    """The prototype's search approximations (ignore small candidates, sample
+    sqrt(n) of the pool; Appendix E) against exact search on the same batch:
+    OOM rate, total cost relative to exact search where both finish, scores
+    searched, and launch time."""
+    variants = {}
+    for name, flags in {"exact": 0, "ignore_small": W.SEARCH_IGNORE_SMALL, "sample": W.SEARCH_SAMPLE,
+                        "ignore_small+sample": W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE}.items():
+        specs = wl.specs.copy()
+        specs["search"] = flags
+        variants[name] = specs
+    return _variant_rows(wl.traces, variants, steps, "search study")
+
+
+def _union_find(h: int) -> bool:
+    return h == W.H_EQ or (h >= W.H_FAMILY and (h - W.H_FAMILY) >> 2 == W.C_EQCLASS)
+
+
+def policy_study(wl, steps: int):
+    """The deallocation policies (Section 2 and Appendix C.5: eager eviction at
+    release, ignoring releases, banishing) on the same simulations, eager
+    first.  Union-find heuristics take no banishing, so their simulations are
+    left out of every variant."""
+    keep = np.array([not _union_find(int(h)) for h in wl.specs["heuristic"]])
+    if not keep.any():
+        sys.exit("--study policy needs simulations whose heuristic is not a union-find one")
+    variants = {}
+    for name, pol in {"eager": W.POLICY_EAGER, "ignore": W.POLICY_IGNORE, "banish": W.POLICY_BANISH}.items():
+        specs = wl.specs[keep].copy()
+        specs["policy"] = pol
+        variants[name] = specs
+    return _variant_rows(wl.traces, variants, steps, "policy study")
+
+
+def family_study(wl, steps: int):
+    """h_MSPS and the ablation family h'(s, m, c) = c / (m^[m] s^[s]) for every
+    cost measure c (e*, union-find neighbourhood, local, none; Section 4.1,
+    Appendix A.3) on the budgets of the batch's h_DTR simulations (all
+    simulations if it has none), h_DTR first."""
+    rows = wl.specs[wl.specs["heuristic"] == W.H_DTR]
+    if len(rows) == 0:
+        rows = wl.specs
+    variants = {}
+    names = {W.C_ESTAR: "e*", W.C_EQCLASS: "eq", W.C_LOCAL: "local", W.C_NONE: "none"}
+    for name, h in [("h_DTR", W.H_DTR), ("h_MSPS", W.H_MSPS)] + [
+            (f"h'(c={names[c]},s={st},m={m})", W.h_family(c, st, m))
+            for c in (W.C_ESTAR, W.C_EQCLASS, W.C_LOCAL, W.C_NONE) for st in (1, 0) for m in (1, 0)]:
+        specs = rows.copy()
+        specs["heuristic"] = h
+        specs["policy"] = W.POLICY_EAGER
+        variants[name] = specs
+    return _variant_rows(wl.traces, variants, steps, "family study")
 
 
 WORKLOADS = {
@@ -189,6 +245,9 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
     ap.add_argument("--search-study", action="store_true",
                     help="only compare the search approximations with exact search on the workload")
+    ap.add_argument("--study", choices=("search", "policy", "family"), default=None,
+                    help="only compare variants of the workload's simulations: search approximations, "
+                         "deallocation policies, or h_MSPS and the h'(s, m, c) family")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (counter calibration)")
     args = ap.parse_args()
@@ -210,11 +269,13 @@ def main():
     gen_s = time.perf_counter() - t0
     print(f"[bench] workload {wl.name}: {len(wl.traces)} traces, {wl.n_sims} sims, generated in {gen_s:.1f}s",
           file=sys.stderr, flush=True)
-    if args.search_study and is_log(wl):
-        sys.exit("--search-study runs on trace workloads")
-    if args.search_study:
+    study = "search" if args.search_study else args.study
+    if study and is_log(wl):
+        sys.exit("the studies run on trace workloads")
+    if study:
         torch.cuda.set_device(0)
-        print(json.dumps({"search_study": search_study(wl, args.steps), "workload": wl.name,
+        fn = {"search": search_study, "policy": policy_study, "family": family_study}[study]
+        print(json.dumps({f"{study}_study": fn(wl, args.steps), "workload": wl.name,
                           "n_sims": wl.n_sims, "n_gpus": 1}))
         return
     dev = torch.device("cuda:0")

@@ -43,3 +43,8 @@ def test_measured_traffic_is_gated_on_the_kernel_sources(monkeypatch):
         assert bench.measured_traffic("treelstm4096") == recorded
     monkeypatch.setattr(bench, "kernel_source_digest", lambda: "0" * 64)
     assert bench.measured_traffic("treelstm4096") is None
+
+
+def test_union_find_heuristics_are_recognised():
+    uf = [h for h in list(range(8)) + list(range(16, 32)) if bench._union_find(h)]
+    assert uf == [W.H_EQ] + [W.h_family(W.C_EQCLASS, s, m) for s in (0, 1) for m in (0, 1)]
