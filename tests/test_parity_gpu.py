@@ -278,3 +278,18 @@ def test_deep_rematerialization_chain(gpu, oracle_lib):
     ref = oracle_lib.run([tr], specs, threads=16)
     compare(gpu.run([tr], specs), ref, specs, "deep chain")
     assert int(ref["n_remats"].max()) > 500_000
+
+
+def test_search_approximations_on_large_pools(gpu, oracle_lib):
+    """The search approximations on TreeLSTM traces whose pools hold hundreds
+    to thousands of candidates (scan rounds beyond the LDS head), under
+    h_DTR^eq and h_LRU, at the 43%, 54% and 89% budgets of each tree."""
+    w = W.make_config("treelstm4096", n_trees=12)
+    flags = (W.SEARCH_IGNORE_SMALL, W.SEARCH_SAMPLE, W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE)
+    rows = [(int(w.specs["trace"][k]), h, int(w.specs["budget"][k]), 11 + k, W.POLICY_EAGER, sf)
+            for k in range(len(w.specs)) if k % 8 in (2, 3, 6) for sf in flags for h in (W.H_EQ, W.H_LRU)]
+    specs = specs_of(rows)
+    print(f"search on large pools: {len(specs)} sims", flush=True)
+    ref = oracle_lib.run(w.traces, specs, threads=16)
+    compare(gpu.run(w.traces, specs), ref, specs, "search, large pools")
+    assert float(ref["n_scores"].sum()) / max(1, int(ref["n_evictions"].sum())) > 256
