@@ -293,3 +293,21 @@ def test_search_approximations_on_large_pools(gpu, oracle_lib):
     ref = oracle_lib.run(w.traces, specs, threads=16)
     compare(gpu.run(w.traces, specs), ref, specs, "search, large pools")
     assert float(ref["n_scores"].sum()) / max(1, int(ref["n_evictions"].sum())) > 256
+
+
+def test_policies_on_model_traces(gpu, oracle_lib):
+    """Ignoring releases and banishing on the ResNet and transformer traces
+    (pools of hundreds of tensors, long release lists), every heuristic that
+    takes banishing, at 8 budgets spread over each trace's benchmark range."""
+    traces, rows = [], []
+    for name in ("resnet50blk", "transformer12"):
+        w = W.make_config(name)
+        traces.append(w.traces[0])
+        b = sorted(set(int(x) for x in w.specs["budget"]))
+        for bb in (b[len(b) * q // 8] for q in range(8)):
+            for h in (W.H_DTR, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_RAND, W.H_ESTAR, W.H_MSPS):
+                for pol in (W.POLICY_IGNORE, W.POLICY_BANISH):
+                    rows.append((len(traces) - 1, h, bb, 17 + h, pol))
+    specs = specs_of(rows)
+    print(f"policies on model traces: {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs), oracle_lib.run(traces, specs, threads=16), specs, "policies, model traces")
