@@ -260,3 +260,18 @@ def test_deep_rematerialization_chain_logs(gpu, oracle_lib):
         sim.close()
         print(f"chain log of {N} layers: {info}", flush=True)
         compare(got, oracle_lib.run_log([L], specs, threads=16), specs, f"chain log {N}")
+
+
+def test_resnet_log_policies(gpu, oracle_lib):
+    """Ignoring releases and banishing on the PyTorch-style ResNet log (views,
+    in-place operators, constants), at 8 budgets spread over its benchmark
+    range, for the heuristics that take banishing."""
+    wl = W.make_config("resnet50log")
+    b = sorted(set(int(x) for x in wl.specs["budget"]))
+    rows = [(0, h, b[len(b) * q // 8], 17 + h, pol) for q in range(8)
+            for h in (W.H_DTR, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_MSPS)
+            for pol in (W.POLICY_IGNORE, W.POLICY_BANISH)]
+    specs = W.make_specs(rows)
+    print(f"resnet log policies: {len(specs)} sims", flush=True)
+    compare(gpu.run_log(wl.traces, specs), oracle_lib.run_log(wl.traces, specs, threads=16), specs,
+            "resnet log policies")
