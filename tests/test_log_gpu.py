@@ -275,3 +275,18 @@ def test_resnet_log_policies(gpu, oracle_lib):
     print(f"resnet log policies: {len(specs)} sims", flush=True)
     compare(gpu.run_log(wl.traces, specs), oracle_lib.run_log(wl.traces, specs, threads=16), specs,
             "resnet log policies")
+
+
+def test_resnet_log_search_approximations(gpu, oracle_lib):
+    """The search approximations on the ResNet log (a pool of up to ~1300
+    storages; the LDS variant's walk scans with sampled candidate lists) at 5
+    budgets, under h_DTR, h_DTR^eq and h_LRU."""
+    wl = W.make_config("resnet50log")
+    b = sorted(set(int(x) for x in wl.specs["budget"]))
+    flags = (W.SEARCH_IGNORE_SMALL, W.SEARCH_SAMPLE, W.SEARCH_IGNORE_SMALL | W.SEARCH_SAMPLE)
+    rows = [(0, h, b[len(b) * q // 6], 23 + h, W.POLICY_EAGER, sf) for q in range(1, 6)
+            for h in (W.H_DTR, W.H_EQ, W.H_LRU) for sf in flags]
+    specs = W.make_specs(rows)
+    print(f"resnet log search: {len(specs)} sims", flush=True)
+    compare(gpu.run_log(wl.traces, specs), oracle_lib.run_log(wl.traces, specs, threads=16), specs,
+            "resnet log search")
