@@ -381,6 +381,23 @@ def _searched(prog, m, cands, search, seed):
     return keep if keep else big
 
 
+def visits(prog, m, x, heuristic):
+    """The work counters of scoring candidate x: (members of the walked
+    neighbourhood, neighbour slots examined).  e*(x) (h_DTR, h_{e*}, family
+    cost e*) or e_R(x) (h_MSPS): its size and x's degree; union-find cost
+    (h_DTR^eq, family cost eq): x's evicted parents and children, and its
+    degree; other heuristics: none."""
+    fc = (heuristic - 16) >> 2 if heuristic >= 16 else -1
+    deg = len(prog.parents[x]) + len(prog.children[x])
+    if heuristic in (0, 6) or fc == 0:
+        return len(evicted_closure(prog, m.state, x)), deg
+    if heuristic == 7:
+        return len(evicted_ancestors(prog, m.state, x)), deg
+    if heuristic == 1 or fc == 1:
+        return sum(m.state[n] == EVICTED for n in prog.parents[x] + prog.children[x]), deg
+    return 0, 0
+
+
 def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EAGER, search: int = 0) -> dict:
     """Heuristic-driven run of the same machine (h ids, policies and search
     flags as in the C-ABI)."""
@@ -389,6 +406,7 @@ def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EA
     fc, fs, fm = ((heuristic - 16) >> 2, ((heuristic - 16) >> 1) & 1, (heuristic - 16) & 1) if fam else (-1, 0, 0)
     m = Machine(prog, budget, track_uf=(heuristic == 1 or fc == 1), policy=policy)
     c = None if m.oom else m.run()
+    nbr = adj = 0
     while c is not None:
         best, bkey = None, None
         if search:
@@ -397,14 +415,22 @@ def simulate(trace, budget: int, heuristic: int, seed: int = 0, policy: int = EA
             key = score_key(prog, m, x, heuristic, seed, m.clock - m.last[x])
             if bkey is None or key < bkey or (key == bkey and x < best):
                 best, bkey = x, key
+            v = visits(prog, m, x, heuristic)
+            nbr += v[0]
+            adj += v[1]
         m.n_scores += len(c)
         m.evict(best)
         c = m.run()
     status = 1 if m.oom else (2 if m.overflow else 0)
+    # the operation being run when the simulation stopped: the bottom frame's
+    # (the number of operations while the output condition runs)
+    f0 = m.frames[0]
+    failed = -1 if status == 0 else (f0[1] if f0[0] == "op" else prog.F)
     return dict(total_cost=m.cost, remat_cost=m.remat_cost, base_cost=m.cost - m.remat_cost,
                 peak_memory=m.peak, final_memory=m.mem, n_executed_ops=m.n_exec,
                 n_remats=m.n_remat, n_evictions=m.n_evict, n_eager_evictions=m.n_eager,
-                n_scores=m.n_scores, status=status)
+                n_scores=m.n_scores, n_nbr_visits=nbr, n_adj_visits=adj, status=status,
+                failed_op=failed)
 
 
 def score_key(prog, m, x, heuristic, seed, s):

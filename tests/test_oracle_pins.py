@@ -82,6 +82,46 @@ def test_golden_lru_output_stamp(oracle_lib):
     assert p["remat_log"].tolist() == g["remat_log"]
 
 
+def _visit_class(h):
+    """Which visit counters a heuristic keeps: e*/e_R walks, union-find
+    neighbourhoods, or none."""
+    if h in (W.H_DTR, W.H_ESTAR, W.H_MSPS) or (h >= W.H_FAMILY and (h - W.H_FAMILY) >> 2 == W.C_ESTAR):
+        return "walk"
+    if h == W.H_EQ or (h >= W.H_FAMILY and (h - W.H_FAMILY) >> 2 == W.C_EQCLASS):
+        return "eq"
+    return "none"
+
+
+def clock_overflow_cases():
+    g = json.load(open(os.path.join(GOLDEN, "clock_overflow.json")))
+    assert g["cost"] == 1 << 28 and g["limit"] == 1 << 40
+    return [(c, W.plain_chain(c["chain"]["n_ops"], g["cost"], c["chain"]["last_reads_first"],
+                              c["chain"]["required"])) for c in g["cases"]]
+
+
+def test_golden_clock_overflow(oracle_lib):
+    """The clock guard: a trace operation, a rematerialization inside one, and
+    a rematerialization in the output condition reach 2^40 (hand-derived),
+    under every heuristic."""
+    O = oracle_lib
+    hs = [W.H_DTR, W.H_EQ, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_RAND, W.H_ESTAR, W.H_MSPS] + W.ALL_FAMILY
+    for case, tr in clock_overflow_cases():
+        for h in hs:
+            r = run1(O, tr, h, case["budget"], seed=h)
+            for k, v in case["expected"].items():
+                assert int(r[k]) == v, (case["name"], h, k)
+            nbr, adj = case["visits"][_visit_class(h)]
+            assert (int(r["n_nbr_visits"]), int(r["n_adj_visits"])) == (nbr, adj), (case["name"], h)
+        # the independent Python machine stops at the same point
+        for h in (W.H_DTR, W.H_EQ, W.H_LRU):
+            s = brute.simulate(tr, case["budget"], h, h)
+            r = run1(O, tr, h, case["budget"], seed=h)
+            assert all(int(r[k]) == v for k, v in s.items()), (case["name"], h)
+        # a budget of 1 cannot hold t_0 (locked) and t_1: out of memory at op 1
+        r = run1(O, tr, W.H_LRU, 1)
+        assert (int(r["status"]), int(r["failed_op"])) == (O.STATUS_OOM, 1)
+
+
 def test_golden_splitmix(oracle_lib):
     O = oracle_lib
     g = json.load(open(os.path.join(GOLDEN, "splitmix64_state0.json")))
@@ -283,7 +323,7 @@ def test_theorem32_adversary(oracle_lib):
 
 # ------------------------------------------------------------ brute force --
 
-@pytest.mark.parametrize("N", [2, 3, 4, 5, 6, 7])
+@pytest.mark.parametrize("N", [2, 3, 4, 5, 6, 7, 8, 9])
 def test_chain_brute_force_optimum(oracle_lib, N):
     O = oracle_lib
     tr = W.chain_trace(N)
@@ -383,6 +423,39 @@ def test_dtr_scores_match_scipy(oracle_lib):
             assert p["score_d"][x] == int(tr.tensor_size[x]) * (p["clock"] - int(p["last_access"][x]))
             assert p["clock"] - int(p["last_access"][x]) >= 1
     assert checked >= 3
+
+
+def test_visit_counters_match_scipy(oracle_lib):
+    """The work counters, decision by decision: under h_DTR the n_nbr_visits
+    added by an eviction decision is the sum over its candidates of |e*|
+    (scipy reachability) and n_adj_visits the sum of their degrees; under
+    h_DTR^eq, the number of their evicted parents and children."""
+    O = oracle_lib
+    tr = W.resnet_trace(seed=7, blocks=6)
+    adj = _adj(tr)
+    und = (adj + adj.T).tocsr()
+    deg = np.diff(adj.indptr) + np.diff(adj.T.tocsr().indptr)
+    peak = W.natural_peak(tr)
+    checked = 0
+    for h in (W.H_DTR, W.H_EQ):
+        prev = None
+        for k in range(0, 60):
+            p = O.run_probe(tr, spec(h, peak // 4), stop_at_eviction=k)
+            if p["result"]["status"] != O.STATUS_STOPPED:
+                break
+            nbr, dg = int(p["result"]["n_nbr_visits"]), int(p["result"]["n_adj_visits"])
+            ev = p["state"] == O.EVICTED
+            cand = np.nonzero(p["candidate"])[0]
+            if h == W.H_DTR:
+                want = sum(len(_reach(adj, ev, x) | _reach(adj.T.tocsr(), ev, x)) for x in cand)
+            else:
+                want = sum(int(ev[und.indices[und.indptr[x]:und.indptr[x + 1]]].sum()) for x in cand)
+            if prev is not None:
+                assert nbr - prev[0] == want, (h, k)
+                assert dg - prev[1] == int(deg[cand].sum()), (h, k)
+                checked += 1
+            prev = (nbr, dg)
+    assert checked >= 60
 
 
 def test_eq_scores_are_components_before_remat(oracle_lib):
