@@ -259,6 +259,130 @@ def chain_trace(N: int, size: int = 1, cost: int = 1) -> Trace:
                          np.full(N, cost, np.int64), name=f"chain{N}", meta=dict(N=N))
 
 
+def shared_weight_chain(N: int, weight_size: int = 1, constant: bool = True) -> Trace:
+    """The Appendix A chain in which every forward and gradient operator also
+    reads one weight W (one weight shared by every layer, as in the recurrent
+    and tree-structured models of Section 4).  Tensor ids as in chain_trace,
+    W is id 2N: a constant, or (constant=False) the output of a nullary
+    operator of cost 1 run first, so that W is evictable whenever no operator
+    holds it."""
+    tr = chain_trace(N)
+    n = tr.n_tensors
+    lists = [list(tr.inputs(o)) + [n] for o in range(tr.n_ops)]
+    outs, costs = tr.op_output.copy(), tr.op_cost.copy()
+    if not constant:
+        lists = [[]] + lists
+        outs = np.concatenate([[n], outs]).astype(np.int32)
+        costs = np.concatenate([[1], costs]).astype(np.int64)
+    off, flat = _csr(lists)
+    size = np.concatenate([tr.tensor_size, [weight_size]]).astype(np.int64)
+    flags = np.concatenate([tr.tensor_flags, [FLAG_CONSTANT if constant else 0]]).astype(np.uint8)
+    return Trace(f"chainW{N}" + ("" if constant else "op"), size, flags, outs, costs, off, flat,
+                 meta=dict(N=N, weight=n))
+
+
+def plain_chain(n_ops: int, cost: int, last_reads_first: bool = False, required=(-1,)) -> Trace:
+    """Forward-only chain t_0 = f_0(), t_i = f_i(t_{i-1}), unit sizes, every
+    operator of the given cost; with last_reads_first the last operator reads
+    (t_0, t_{n-2}).  `required` lists the tensor ids (negative: from the end)
+    that are required outputs."""
+    ins = [[]] + [[i - 1] for i in range(1, n_ops)]
+    if last_reads_first and n_ops >= 3:
+        ins[-1] = [0, n_ops - 2]
+    off, flat = _csr(ins)
+    flags = np.zeros(n_ops, np.uint8)
+    for t in required:
+        flags[t % n_ops] |= FLAG_REQUIRED
+    return Trace(f"plainchain{n_ops}", np.ones(n_ops, np.int64), flags, np.arange(n_ops, dtype=np.int32),
+                 np.full(n_ops, cost, np.int64), off, flat)
+
+
+def near_tie_program(seed: int, k: int = 24, fillers: int = 2048) -> Trace:
+    """Eviction decisions between large, nearly equal scores.  k tensors x_i
+    (sizes near 2^35 or 2^34, some equal, some exactly double another's with
+    double the cost; costs from 1 to 2^28, some equal) are made first, some
+    pairs are read together by one operator (equal last access), x's of equal
+    cost per byte are read one after another by cheap operators, then a chain
+    of `fillers` operators of cost 2^28 and size 1 moves the clock to about
+    2^39, so staleness values differ by 1 to 2^28 in about 2^39.  An operator
+    G then needs a third of the x memory, and every x is read again (in a
+    shuffled order) while G's output is still held, so the x's are evicted and
+    rematerialized by decisions among near-ties.  The budget of the workload is
+    the sum of the x sizes plus 4 (see near_tie_budgets)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    big = 1 << 35
+    sizes, costs, lists = [], [], []
+    for i in range(k):
+        r = rng.integers(0, 4)
+        if r == 0 and i >= 2:            # (2c, 2m) against an earlier (c, m): an exact tie of c/m
+            j = int(rng.integers(0, i))
+            if sizes[j] < big and 2 * costs[j] <= (1 << 28):
+                sizes.append(2 * sizes[j])
+                costs.append(2 * costs[j])
+            else:
+                sizes.append(sizes[j])
+                costs.append(costs[j])
+        elif r == 1 and i >= 1:          # a copy of an earlier (c, m)
+            j = int(rng.integers(0, i))
+            sizes.append(sizes[j])
+            costs.append(costs[j])
+        else:
+            base = big if rng.integers(0, 2) else big // 2
+            sizes.append(base - int(rng.integers(0, 1 << int(rng.integers(0, 31)))))
+            costs.append(int(rng.integers(1, (1 << 28) + 1)) if rng.integers(0, 2)
+                         else (1 << 19) * int(rng.integers(1, 9)) + int(rng.integers(0, 4)))
+        n_in = int(rng.integers(0, min(2, i) + 1))
+        lists.append(sorted(int(v) for v in rng.choice(i, size=n_in, replace=False)) if n_in else [])
+    out_size = list(sizes)
+    out_cost = list(costs)
+    # pairs read together (equal last access); outputs of size 1 released at once
+    for _ in range(k // 4):
+        a, b = sorted(int(v) for v in rng.choice(k, size=2, replace=False))
+        lists.append([a, b])
+        out_size.append(1)
+        out_cost.append(int(rng.integers(1, 1 << 20)))
+    # x's of equal (c, m) or (2c, 2m) read one after another by cheap
+    # operators: their staleness values end up a few units apart
+    same = [(a, b) for b in range(k) for a in range(b) if sizes[a] * costs[b] == sizes[b] * costs[a]]
+    for a, b in same[:6]:
+        for x in (a, b):
+            lists.append([x])
+            out_size.append(1)
+            out_cost.append(int(rng.integers(1, 65)))
+    # the filler chain
+    h0 = len(lists)
+    for j in range(fillers):
+        lists.append([] if j == 0 else [h0 + j - 1])
+        out_size.append(1)
+        out_cost.append(1 << 28)
+    g = len(lists)
+    lists.append([])              # nullary, so that rematerializing its output is cheap
+    out_size.append(int(sum(sizes)) // 3)
+    out_cost.append(int(rng.integers(1, 1 << 20)))
+    for i in rng.permutation(k):
+        lists.append([int(i)])
+        out_size.append(1)
+        out_cost.append(int(rng.integers(1, 1 << 20)))
+    lists.append([g])
+    out_size.append(1)
+    out_cost.append(1)
+    n = len(lists)
+    flags = np.zeros(n, np.uint8)
+    flags[g + 1:] = FLAG_REQUIRED
+    off, flat = _csr(lists)
+    return Trace(f"neartie{seed}", np.asarray(out_size, np.int64), flags, np.arange(n, dtype=np.int32),
+                 np.asarray(out_cost, np.int64), off, flat, meta=dict(seed=seed, k=k))
+
+
+def near_tie_budgets(tr: Trace) -> list:
+    """Budgets of a near_tie_program: the x memory plus 4 units, and that
+    less 1/16 and 1/8 of the largest x (more evictions per decision)."""
+    k = tr.meta["k"]
+    xs = tr.tensor_size[:k]
+    b = int(xs.sum()) + 4
+    return [b, b - int(xs.max()) // 16, b - int(xs.max()) // 8]
+
+
 def config_chain(N: int = 32) -> Workload:
     tr = chain_trace(N)
     peak = natural_peak(tr)
