@@ -304,10 +304,11 @@ def near_tie_program(seed: int, k: int = 24, fillers: int = 2048) -> Trace:
     pairs are read together by one operator (equal last access), x's of equal
     cost per byte are read one after another by cheap operators, then a chain
     of `fillers` operators of cost 2^28 and size 1 moves the clock to about
-    2^39, so staleness values differ by 1 to 2^28 in about 2^39.  An operator
-    G then needs a third of the x memory, and every x is read again (in a
-    shuffled order) while G's output is still held, so the x's are evicted and
-    rematerialized by decisions among near-ties.  The budget of the workload is
+    2^39, so staleness values differ by 1 to 2^28 in about 2^39.  Nullary
+    operators G then need a third of the x memory (pieces below 2^36), and
+    every x is read again (in a shuffled order) while the G outputs are still
+    held, so the x's are evicted and rematerialized by decisions among
+    near-ties.  The budget of the workload is
     the sum of the x sizes plus 4 (see near_tie_budgets)."""
     rng = np.random.Generator(np.random.PCG64(seed))
     big = 1 << 35
@@ -355,20 +356,26 @@ def near_tie_program(seed: int, k: int = 24, fillers: int = 2048) -> Trace:
         lists.append([] if j == 0 else [h0 + j - 1])
         out_size.append(1)
         out_cost.append(1 << 28)
+    # G: a third of the x memory, in pieces below the size limit of 2^36,
+    # made by nullary operators (so that rematerializing them is cheap)
     g = len(lists)
-    lists.append([])              # nullary, so that rematerializing its output is cheap
-    out_size.append(int(sum(sizes)) // 3)
-    out_cost.append(int(rng.integers(1, 1 << 20)))
+    need = int(sum(sizes)) // 3
+    n_g = -(-need // ((1 << 36) - 1))
+    for _ in range(n_g):
+        lists.append([])
+        out_size.append(need // n_g)
+        out_cost.append(int(rng.integers(1, 1 << 20)))
+    z = len(lists)
     for i in rng.permutation(k):
         lists.append([int(i)])
         out_size.append(1)
         out_cost.append(int(rng.integers(1, 1 << 20)))
-    lists.append([g])
+    lists.append(list(range(g, g + n_g)))
     out_size.append(1)
     out_cost.append(1)
     n = len(lists)
     flags = np.zeros(n, np.uint8)
-    flags[g + 1:] = FLAG_REQUIRED
+    flags[z:] = FLAG_REQUIRED
     off, flat = _csr(lists)
     return Trace(f"neartie{seed}", np.asarray(out_size, np.int64), flags, np.arange(n, dtype=np.int32),
                  np.asarray(out_cost, np.int64), off, flat, meta=dict(seed=seed, k=k))
