@@ -295,6 +295,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     L.ucap = need_uf ? 2 * (int64_t)n + 64 : 0;
     const size_t pc = (size_t)L.pcap;
     take(L.tst, 8 * n);
+    take(L.lockx, 4 * n);
     take(L.pool, sizeof(dtr::PoolSlot) * pc);
     take(L.nodes, sizeof(dtr::UfNode) * (size_t)L.ucap);
     take(L.uf_remap, need_uf ? 4 * ((size_t)L.ucap + dtr::UF_LDS) : 0);

@@ -88,7 +88,10 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 // largest trace of the batch (n_max tensors).  Offsets in bytes from the slot
 // base, each 256-byte aligned.
 //   tst       per-tensor state word: state/union-find node (32 bits), pool
-//             position (24 bits), lock count (8 bits)
+//             position (24 bits), lock count (8 bits; 255 = the count is in lockx)
+//   lockx     per-tensor lock count of tensors held 255 times or more (a
+//             weight read by every operation of a deep rematerialization
+//             stack); read and written only while the 8-bit field is saturated
 //   pool      evictable tensors, pcap 64-byte slots (dead slots are
 //             tombstoned and squeezed out): id, packed (degree << 8 | n), last
 //             access, size, c0, start of the neighbour range, and for
@@ -109,7 +112,7 @@ constexpr int POOL_LDS = 256;
 
 struct SlotLayout {
     int64_t bytes;           // stride between slots
-    int64_t tst;
+    int64_t tst, lockx;
     int64_t pool;
     int64_t nodes, uf_remap;
     int64_t stack;

@@ -59,7 +59,9 @@ constexpr int32_t S_UNCOMPUTED = -2;
 constexpr int32_t S_RESIDENT = -1;
 enum { POLICY_EAGER = 0, POLICY_IGNORE = 1, POLICY_BANISH = 2 };
 enum { SEARCH_IGNORE_SMALL = 1, SEARCH_SAMPLE = 2 };
-constexpr uint32_t MAX_LOCKS = 255;
+// lock counts of 255 and more live in the slot's lockx array (the 8-bit field
+// then reads LOCKS_SAT)
+constexpr uint32_t LOCKS_SAT = 255;
 constexpr uint8_t FLAG_CONST = 1;
 constexpr int K = NB_CACHE;
 constexpr int KQ = K / 4;        // 16-byte quads of cached nodes per pool slot
@@ -160,6 +162,7 @@ struct NodeStore {
 // rest in the slot's global array (same indices).
 struct Slot {
     GAS uint64_t *tst;
+    GAS int32_t *lockx;           // lock counts >= LOCKS_SAT
     PoolSlot *lpool;              // flat view of the LDS head
     LAS PoolSlot *lpool_l;
     GAS PoolSlot *gpool;
@@ -181,6 +184,7 @@ __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
     uint8_t *b = a.slots + (size_t)k * (size_t)a.L.bytes;
     Slot S;
     S.tst = (GAS uint64_t *)(b + a.L.tst);
+    S.lockx = (GAS int32_t *)(b + a.L.lockx);
     S.lpool = nullptr;
     S.lpool_l = nullptr;
     S.gpool = (GAS PoolSlot *)(b + a.L.pool);
@@ -806,10 +810,16 @@ __device__ __forceinline__ void clear_stamps(Sim &s)
 }
 
 // Scores are N / (da * db) with N < 2^64 and da * db < 2^76.  A float
-// estimate (relative error below 2^-21) decides every comparison whose two
-// estimates differ by more than a factor 1 -+ 2^-16; the rest (near ties,
-// exact ties, 0/0) are decided exactly by 128-bit cross-multiplication, so
-// the outcome is always that of the exact comparison.
+// estimate decides every comparison whose two estimates differ by more than a
+// factor 1 -+ 2^-16; the rest (near ties, exact ties, 0/0) are decided
+// exactly by 128-bit cross-multiplication, so the outcome is always that of
+// the exact comparison.  Error of the estimate: each u64f conversion rounds
+// twice (the high and low 32-bit halves, then the fused sum), under
+// (1 + 2^-24)^2 - 1 < 2^-22.9; the product da * db adds one rounding
+// (2^-24), v_rcp_f32 at most 1 ulp (2^-23) and the final product one
+// rounding (2^-24): in all below 3 * 2^-22.9 + 2^-23 + 2 * 2^-24 < 2^-20.4.
+// Two estimates within the margin can therefore never be ordered wrongly by
+// the float test: (1 - 2^-16) (1 + 2^-24) (1 + 2^-20.4)^2 < 1.
 constexpr float FILTER_LO = 1.0f - 0x1p-16f;
 constexpr float FILTER_HI = 1.0f + 0x1p-16f;
 
@@ -1359,29 +1369,28 @@ __device__ __forceinline__ void lock_inputs(Sim &s, const int32_t *ids, int32_t 
 {
     for (int32_t k0 = b; k0 < e; k0 += WAVE) {
         const int32_t k = k0 + s.lane;
-        bool killed = false, over = false;
+        bool killed = false;
         int32_t u = -1;
         uint64_t nw = 0;
         if (k < e) {
             u = head >= -1 && k0 == b && s.lane < NB_HEAD ? head : gld(ids + k);
             const uint64_t w = s.S.tst[u];
             const uint32_t l = ts_locks(w);
-            nw = ts_make(ts_sw(w), ts_pos(w), l + 1);
-            if (l >= MAX_LOCKS) over = true;
-            else {
-                if (ts_in_pool(w)) {
-                    s.S.pool((int32_t)ts_pos(w)).id = -1;
-                    killed = true;
-                }
-                s.S.tst[u] = nw;
+            // counts from LOCKS_SAT on are kept in lockx (the field stays saturated)
+            nw = l < LOCKS_SAT ? ts_make(ts_sw(w), ts_pos(w), l + 1) : w;
+            if (l + 1 == LOCKS_SAT) s.S.lockx[u] = (int32_t)LOCKS_SAT;
+            else if (l == LOCKS_SAT) s.S.lockx[u] = s.S.lockx[u] + 1;
+            if (ts_in_pool(w)) {
+                s.S.pool((int32_t)ts_pos(w)).id = -1;
+                killed = true;
             }
+            s.S.tst[u] = nw;
         }
         if (k0 == b) {
             f.u = u;
             f.w = nw;
         }
         s.pool_live -= __popcll(__ballot(killed));
-        if (__ballot(over)) set_status(s, ST_CAPACITY);
     }
 }
 
@@ -1412,9 +1421,21 @@ __device__ __forceinline__ void unlock_inputs(Sim &s, int32_t b, int32_t e, int6
                 w = s.S.tst[u];
             }
         }
-        const bool join = k < e && ts_locks(w) == 1 && ts_sw(w) == S_RESIDENT;
+        const uint32_t l = ts_locks(w);
+        const bool join = k < e && l == 1 && ts_sw(w) == S_RESIDENT;
         const int32_t slot = pool_append<HC>(s, join, u, last);
-        if (k < e) s.S.tst[u] = ts_make(ts_sw(w), join ? (uint32_t)slot : ts_pos(w), ts_locks(w) - 1);
+        if (k < e) {
+            uint32_t nl = l - 1;
+            if (l == LOCKS_SAT) {
+                // a saturated count leaves lockx once it drops below LOCKS_SAT
+                const int32_t c = s.S.lockx[u] - 1;
+                if (c >= (int32_t)LOCKS_SAT) {
+                    s.S.lockx[u] = c;
+                    nl = LOCKS_SAT;
+                }
+            }
+            s.S.tst[u] = ts_make(ts_sw(w), join ? (uint32_t)slot : ts_pos(w), nl);
+        }
     }
 }
 
