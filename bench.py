@@ -228,7 +228,7 @@ def cpu_baseline(wl, gpu_res, sample_every: int, threads: int):
     scores = int(ref["n_scores"].sum())
     match = sum(all(int(gpu_res[f][i]) == int(ref[f][k]) for f in O.RESULT_FIELDS)
                 for k, i in enumerate(idx))
-    return dict(value=ops / dt, unit="simulated tensor ops/s", cores=threads, kind="oracle",
+    return dict(value=ops / dt, unit="simulated tensor ops/s", cores=threads, nproc=os.cpu_count(), kind="oracle",
                 sample=f"every {sample_every}th simulation ({len(idx)} of {wl.n_sims}), "
                        f"{dt:.2f} s wall on {threads} threads",
                 scores_per_s=scores / dt, parity_sample=f"{match}/{len(idx)}")
@@ -241,8 +241,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--workload", default="treelstm4096", choices=sorted(WORKLOADS))
     ap.add_argument("--slots", type=int, default=0)
-    ap.add_argument("--cpu-sample", type=int, default=64, help="oracle on every k-th simulation (0: skip)")
-    ap.add_argument("--cpu-threads", type=int, default=min(16, os.cpu_count() or 1))
+    ap.add_argument("--cpu-sample", type=int, default=61,
+                    help="oracle on every k-th simulation (0: skip); 61 is coprime to the 8 budgets per tree")
+    ap.add_argument("--cpu-threads", type=int, default=os.cpu_count() or 1)
     ap.add_argument("--search-study", action="store_true",
                     help="only compare the search approximations with exact search on the workload")
     ap.add_argument("--study", choices=("search", "policy", "family"), default=None,

@@ -193,6 +193,19 @@ def test_determinism_across_slot_counts(gpu):
     assert a.tobytes() == b.tobytes() == c.tobytes()
 
 
+def test_determinism_under_shuffled_order(gpu):
+    """Each simulation's result depends on its spec alone: the batch shuffled
+    (so simulations land in other slots, other workgroups and another dispatch
+    order) gives the same result per simulation."""
+    w = W.make_config("resnet50blk")
+    t = W.make_config("treelstm4096", n_trees=64)
+    for wl in (w, t):
+        a = gpu.run(wl.traces, wl.specs)
+        perm = np.random.default_rng(3).permutation(wl.n_sims)
+        b = gpu.run(wl.traces, wl.specs[perm])
+        assert a[perm].tobytes() == b.tobytes(), wl.name
+
+
 def test_random_dag_replica_all_budgets(gpu, oracle_lib):
     """Random-DAG recipe (1-3 inputs from the previous 64 outputs, log-normal
     sizes) at 1000 forward ops, h_DTR at 12 budgets from 5% to 100%: the
@@ -216,7 +229,8 @@ def test_random_dag_full_size_sampled(gpu, oracle_lib):
 def test_treelstm_full_batch_sampled(gpu, oracle_lib):
     """The full TreeLSTM batch (4096 traces x 8 budgets, 32768 simulations) in
     one launch, as the benchmark times it: every simulation checked against
-    properties that hold at any size, every 256th against the oracle."""
+    properties that hold at any size, every 257th against the oracle (a stride
+    coprime to the 8 budgets per tree, so every budget level is sampled)."""
     w = W.make_config("treelstm4096")
     print(f"treelstm full batch: {w.n_sims} sims", flush=True)
     got = gpu.run(w.traces, w.specs)
@@ -231,7 +245,8 @@ def test_treelstm_full_batch_sampled(gpu, oracle_lib):
     assert (got["n_executed_ops"][ok] == n_ops[ok] + got["n_remats"][ok]).all()
     assert (got["failed_op"][ok] == -1).all() and (got["failed_op"][~ok] >= 0).all()
     assert set(np.unique(got["status"]).tolist()) <= {0, 1}
-    pick = np.arange(0, w.n_sims, 256)
+    pick = np.arange(0, w.n_sims, 257)
+    assert len(set((pick % 8).tolist())) == 8
     sub = w.specs[pick]
     compare(got[pick], oracle_lib.run(w.traces, sub, threads=16), sub, "treelstm4096-sampled")
 
@@ -311,3 +326,56 @@ def test_policies_on_model_traces(gpu, oracle_lib):
     specs = specs_of(rows)
     print(f"policies on model traces: {len(specs)} sims", flush=True)
     compare(gpu.run(traces, specs), oracle_lib.run(traces, specs, threads=16), specs, "policies, model traces")
+
+
+def test_clock_overflow_goldens(gpu, oracle_lib):
+    """The clock guard reached in a trace operation, in a rematerialization
+    inside one, and in the output condition (hand-derived goldens), under
+    every heuristic class and family member, bit-exact against the oracle."""
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "clock_overflow.json")))
+    traces = [W.plain_chain(c["chain"]["n_ops"], g["cost"], c["chain"]["last_reads_first"], c["chain"]["required"])
+              for c in g["cases"]]
+    hs = [W.H_DTR, W.H_EQ, W.H_LOCAL, W.H_LRU, W.H_SIZE, W.H_RAND, W.H_ESTAR, W.H_MSPS] + W.ALL_FAMILY
+    rows = [(i, h, c["budget"], 9 + h) for i, c in enumerate(g["cases"]) for h in hs]
+    specs = specs_of(rows)
+    got = gpu.run(traces, specs)
+    compare(got, oracle_lib.run(traces, specs), specs, "clock overflow")
+    for k, (i, h, _, _) in enumerate(rows):
+        for f, v in g["cases"][i]["expected"].items():
+            assert int(got[f][k]) == v, (g["cases"][i]["name"], h, f)
+
+
+def test_shared_weight_chains(gpu, oracle_lib):
+    """A chain whose every operator also reads one weight: at budgets 5-8 the
+    rematerialization stack holds the weight hundreds of times over (up to ~590
+    nested frames at N=600), as a constant and as an evictable operator output
+    (twice the size of a layer), bit-exact against the oracle."""
+    traces = [W.shared_weight_chain(600), W.shared_weight_chain(600, weight_size=2, constant=False),
+              W.shared_weight_chain(1000)]
+    rows = []
+    for i in range(len(traces)):
+        for h in (W.H_LRU, W.H_EQ, W.H_DTR, W.H_SIZE, W.H_LOCAL, W.H_MSPS):
+            for b in (5, 6, 7, 8) if i < 2 else (6,):
+                rows.append((i, h, b + (i == 1), 21 + i))
+    specs = specs_of(rows)
+    print(f"shared weight chains: {len(specs)} sims", flush=True)
+    ref = oracle_lib.run(traces, specs, threads=8)
+    assert (ref["status"] == 0).all()
+    compare(gpu.run(traces, specs), ref, specs, "shared weight chains")
+
+
+def test_near_ties_at_large_magnitude(gpu, oracle_lib):
+    """Scores that tie exactly or differ by less than 2^-16 (down to about
+    2^-39) at sizes near 2^35, costs up to 2^28 and staleness near 2^39:
+    decisions the kernel's float estimate cannot separate, which it must
+    hand to the exact 128-bit comparison (ties to the smaller id)."""
+    traces = [W.near_tie_program(s) for s in range(16)]
+    hs = [W.H_LOCAL, W.H_SIZE, W.H_LRU, W.H_EQ, W.H_DTR, W.H_ESTAR, W.H_MSPS,
+          W.h_family(W.C_LOCAL, 1, 0), W.h_family(W.C_EQCLASS, 0, 1), W.h_family(W.C_NONE, 1, 1)]
+    rows = [(i, h, b, i) for i, t in enumerate(traces) for h in hs for b in W.near_tie_budgets(t)]
+    specs = specs_of(rows)
+    print(f"near ties: {len(specs)} sims", flush=True)
+    ref = oracle_lib.run(traces, specs)
+    assert (ref["status"] == 0).all() and int(ref["n_evictions"].min()) > 0
+    compare(gpu.run(traces, specs), ref, specs, "near ties")
