@@ -164,7 +164,7 @@ typedef struct {
 /* Launch options (NULL = defaults). */
 typedef struct {
     int32_t slots;   /* simulations resident on the GPU at once (0 = 16 per CU) */
-    int32_t flags;   /* 0, or DTR_OPT_* bits (operator logs only)               */
+    int32_t flags;   /* 0, or DTR_OPT_* bits                                    */
 } dtr_sim_options;
 
 /* Operator-log replay keeps every per-simulation array in device memory even
@@ -172,6 +172,15 @@ typedef struct {
  * largest log fit in LDS (results are identical; a testing aid).  Rejected
  * for traces. */
 #define DTR_OPT_LOG_NO_LDS 1
+
+/* Traces only: the handle will run through dtr_sim_run_static, so its
+ * workspace holds the inputs and results alone (no per-simulation working
+ * memory); dtr_sim_run on it returns DTR_ESTATE.  Creation fails with
+ * DTR_EINVAL if one simulation's working memory exceeds the static scratch. */
+#define DTR_OPT_STATIC_SCRATCH 2
+
+/* Size of the library's static device array used by dtr_sim_run_static. */
+#define DTR_STATIC_SCRATCH_BYTES ((size_t)256 << 20)
 
 typedef struct dtr_sim dtr_sim;
 
@@ -194,6 +203,24 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces,
 /* Enqueue every simulation on `stream` (asynchronous, stream-ordered).  May be
  * called again; each call recomputes all results. */
 int dtr_sim_run(dtr_sim *sim, void *stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops): as dtr_sim_run, but every simulation's working
+ * memory (state words, evictable pool, union-find nodes, rematerialization
+ * stack, walk stamps and queues) and the work counters live in the
+ * library's own static device array of DTR_STATIC_SCRATCH_BYTES, one per
+ * device, held until the process ends, instead of in the handle's
+ * workspace.  The inputs (uploaded by dtr_sim_create) and the results stay
+ * in the handle's workspace; read them with dtr_sim_results.  As many
+ * simulations are resident at once as the handle's slot count allows and
+ * the array holds.  Allocates nothing and calls no allocating routine.
+ * Errors: DTR_EINVAL for a NULL or operator-log handle, or when one
+ * simulation's working memory exceeds the array; DTR_EHIP if a HIP call
+ * fails.  Every call on a device shares that device's array and overwrites
+ * it (the counters are cleared by a kernel at the start of each call):
+ * calls that overlap in time on one device race, so order them (for
+ * example on one stream). */
+int dtr_sim_run_static(dtr_sim *sim, void *stream);
 
 /* Copy n_sims results (== the batch size) into host_out, after synchronizing
  * the stream of the last run.  DTR_ESTATE if no run was enqueued. */

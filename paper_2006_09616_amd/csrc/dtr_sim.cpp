@@ -23,6 +23,7 @@
 #include "layout.h"
 
 extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream);
+extern "C" hipError_t dtr_static_scratch(void **ptr, size_t *bytes);
 
 namespace dtrhost {
 
@@ -83,6 +84,8 @@ namespace {
 
 using namespace dtrhost;
 
+// dtr_sim_run_static: work counters, then slots, in the static scratch
+constexpr size_t STATIC_HEADER = 256;
 constexpr int32_t MAX_TENSORS = 8000000;       // pool positions are packed in 24 bits
 constexpr int32_t MAX_DEGREE = (1 << 23) - 1;  // degrees are packed in 23 bits
 
@@ -247,6 +250,7 @@ struct Plan {
     size_t total = 0;
     dtr::SlotLayout L{};
     int32_t n_slots = 0;
+    bool static_only = false;        // runs only through dtr_sim_run_static: no slots in the workspace
     std::vector<int32_t> order;
     int32_t class_count[dtr::N_GROUPS] = {0, 0, 0, 0, 0, 0};
 };
@@ -267,7 +271,8 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
 {
     if (n_traces < 0 || n_sims < 0) return fail(DTR_EINVAL, "negative n_traces or n_sims");
     if ((n_traces > 0 && !traces) || (n_sims > 0 && !sims)) return fail(DTR_EINVAL, "null traces or sims");
-    if (opt && (opt->slots < 0 || opt->flags != 0)) return fail(DTR_EINVAL, "bad options");
+    if (opt && (opt->slots < 0 || (opt->flags & ~DTR_OPT_STATIC_SCRATCH))) return fail(DTR_EINVAL, "bad options");
+    p.static_only = opt && (opt->flags & DTR_OPT_STATIC_SCRATCH);
     p.traces.resize(n_traces);
     for (int32_t i = 0; i < n_traces; i++) {
         int rc = validate_and_derive(traces[i], i, p.traces[i]);
@@ -304,6 +309,9 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);
     take(L.pending, need_banish ? n : 0);
     L.bytes = (int64_t)o;
+    if (p.static_only && (size_t)L.bytes > DTR_STATIC_SCRATCH_BYTES - STATIC_HEADER)
+        return fail(DTR_EINVAL, "one simulation needs %lld bytes of working memory; the static scratch holds %zu",
+                    (long long)L.bytes, (size_t)(DTR_STATIC_SCRATCH_BYTES - STATIC_HEADER));
 
     int32_t cus = 0;
     int rc = device_cus(&cus);
@@ -352,7 +360,7 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     w += align_up(sizeof(int64_t) * dtr::PROF_FIELDS * std::max(1, n_sims));
 #endif
     p.slot_off = w;
-    w += (size_t)L.bytes * (size_t)p.n_slots;
+    if (!p.static_only) w += (size_t)L.bytes * (size_t)p.n_slots;
     p.total = w;
     return DTR_OK;
 }
@@ -463,6 +471,45 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec
     return DTR_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// Enqueue the replay kernels of a trace batch: slots from `slots` (at most
+// `max_slots` resident simulations), work counters at `queue`.
+int launch_traces(dtr_sim *h, void *stream, uint8_t *slots, uint32_t *queue, int64_t max_slots)
+{
+    const Plan &p = h->plan;
+    dtr::KernelArgs a[dtr::N_GROUPS];
+    int32_t first = 0;
+    const int32_t cap = (int32_t)std::max<int64_t>(1, std::min<int64_t>(p.n_slots, max_slots));
+    for (int c = 0; c < dtr::N_GROUPS; c++) {
+        a[c].traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
+        a[c].specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
+        a[c].order = (const int32_t *)(h->ws + p.order_off) + first;
+        a[c].results = (dtr::ResultDev *)(h->ws + p.result_off);
+        a[c].queue = queue + c;
+        a[c].slots = slots;
+        a[c].L = p.L;
+        a[c].n_sims = p.class_count[c];
+        a[c].n_slots = std::max(1, std::min(cap, p.class_count[c]));
+        a[c].prof = nullptr;
+#ifdef DTR_PROFILE
+        a[c].prof = (int64_t *)(h->ws + p.prof_off);
+#endif
+        first += p.class_count[c];
+    }
+    hipError_t e = dtr_launch_replay(a, (hipStream_t)stream);
+    if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
+    h->ran = true;
+    h->last_stream = (hipStream_t)stream;
+    return DTR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
 int dtr_sim_run(dtr_sim *h, void *stream)
 {
     g_err.clear();
@@ -475,29 +522,27 @@ int dtr_sim_run(dtr_sim *h, void *stream)
         h->last_stream = (hipStream_t)stream;
         return DTR_OK;
     }
-    dtr::KernelArgs a[dtr::N_GROUPS];
-    int32_t first = 0;
-    for (int c = 0; c < dtr::N_GROUPS; c++) {
-        a[c].traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
-        a[c].specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
-        a[c].order = (const int32_t *)(h->ws + p.order_off) + first;
-        a[c].results = (dtr::ResultDev *)(h->ws + p.result_off);
-        a[c].queue = (uint32_t *)h->ws + c;
-        a[c].slots = h->ws + p.slot_off;
-        a[c].L = p.L;
-        a[c].n_sims = p.class_count[c];
-        a[c].n_slots = std::max(1, std::min(p.n_slots, p.class_count[c]));
-        a[c].prof = nullptr;
-#ifdef DTR_PROFILE
-        a[c].prof = (int64_t *)(h->ws + p.prof_off);
-#endif
-        first += p.class_count[c];
-    }
-    hipError_t e = dtr_launch_replay(a, (hipStream_t)stream);
-    if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
-    h->ran = true;
-    h->last_stream = (hipStream_t)stream;
-    return DTR_OK;
+    if (p.static_only)
+        return fail(DTR_ESTATE, "the handle was created with DTR_OPT_STATIC_SCRATCH: run it with dtr_sim_run_static");
+    return launch_traces(h, stream, h->ws + p.slot_off, (uint32_t *)h->ws, p.n_slots);
+}
+
+int dtr_sim_run_static(dtr_sim *h, void *stream)
+{
+    g_err.clear();
+    if (!h) return fail(DTR_EINVAL, "null handle");
+    if (h->log) return fail(DTR_EINVAL, "dtr_sim_run_static runs traces only");
+    const Plan &p = h->plan;
+    if (h->n_sims == 0) { h->ran = true; h->last_stream = (hipStream_t)stream; return DTR_OK; }
+    void *base = nullptr;
+    size_t cap = 0;
+    const hipError_t e = dtr_static_scratch(&base, &cap);
+    if (e != hipSuccess) return fail(DTR_EHIP, "static scratch lookup failed: %s", hipGetErrorString(e));
+    if ((size_t)p.L.bytes > cap - STATIC_HEADER)
+        return fail(DTR_EINVAL, "one simulation needs %lld bytes of working memory; the static scratch holds %zu",
+                    (long long)p.L.bytes, cap - STATIC_HEADER);
+    const int64_t fit = (int64_t)((cap - STATIC_HEADER) / (size_t)p.L.bytes);
+    return launch_traces(h, stream, (uint8_t *)base + STATIC_HEADER, (uint32_t *)base, fit);
 }
 
 int dtr_sim_results(dtr_sim *h, dtr_sim_result *host_out, int32_t n_sims)
@@ -566,6 +611,9 @@ int dtr_sim_launch_info(const dtr_sim *h, dtr_launch_info *out)
         dtrhost::log_plan_info(h->log, &out->n_slots, &out->waves_per_group, &out->lds_bytes);
     } else {
         out->n_slots = h->plan.n_slots;
+        if (h->plan.static_only)
+            out->n_slots = (int32_t)std::max<int64_t>(1, std::min<int64_t>(
+                out->n_slots, (int64_t)((DTR_STATIC_SCRATCH_BYTES - STATIC_HEADER) / (size_t)h->plan.L.bytes)));
         out->waves_per_group = 1;
         out->lds_bytes = 0;
     }

@@ -37,6 +37,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
+#include "../../include/dtr_sim.h"
 #include "layout.h"
 
 namespace dtr {
@@ -1866,7 +1869,37 @@ __global__ void reset_kernel(uint32_t *queue, int32_t n)
     if ((int32_t)threadIdx.x < n) queue[threadIdx.x] = 0;
 }
 
+// Working memory of dtr_sim_run_static: the work counters (first 256 bytes),
+// then the simulation slots.  One copy per device, held until the process
+// ends; every static run on a device shares it.
+constexpr size_t STATIC_SCRATCH_BYTES = DTR_STATIC_SCRATCH_BYTES;
+static __device__ __align__(256) uint8_t scratch[STATIC_SCRATCH_BYTES];
+
 }  // namespace dtr
+
+// Device address and size of this device's static working memory.  The
+// address is looked up once per device (with that device current) and kept:
+// in host code the array's name is not a device address.
+extern "C" hipError_t dtr_static_scratch(void **ptr, size_t *bytes)
+{
+    constexpr int MAX_DEVICES = 64;
+    static std::mutex mu;
+    static void *addr[MAX_DEVICES] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= MAX_DEVICES) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(mu);
+    if (!addr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(dtr::scratch));
+        if (e != hipSuccess) return e;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    *bytes = dtr::STATIC_SCRATCH_BYTES;
+    return hipSuccess;
+}
 
 // Launch entry used by the host library (same shared object): args[g] holds
 // the simulations of group g = heuristic class (union-find; neighbourhood

@@ -22,6 +22,7 @@ HEADER = os.path.join(os.path.dirname(HERE), "include", "dtr_sim.h")
 DTR_OK, DTR_EINVAL, DTR_ETRACE, DTR_EHIP, DTR_ESTATE = 0, -1, -2, -3, -4
 STATUS_OK, STATUS_OOM, STATUS_CLOCK_OVERFLOW, STATUS_CAPACITY = 0, 1, 2, 3
 OPT_LOG_NO_LDS = 1
+OPT_STATIC_SCRATCH = 2
 
 RESULT_FIELDS = ["total_cost", "base_cost", "remat_cost", "peak_memory", "final_memory",
                  "n_executed_ops", "n_remats", "n_evictions", "n_eager_evictions", "n_scores",
@@ -61,6 +62,7 @@ def lib():
         L.dtr_sim_workspace_bytes.argtypes = [vp, i32, vp, i32, vp, C.POINTER(sz)]
         L.dtr_sim_create.argtypes = [vp, i32, vp, i32, vp, vp, sz, vp, C.POINTER(vp)]
         L.dtr_sim_run.argtypes = [vp, vp]
+        L.dtr_sim_run_static.argtypes = [vp, vp]
         L.dtr_sim_results.argtypes = [vp, vp, i32]
         L.dtr_sim_launch_info.argtypes = [vp, vp]
         L.dtr_sim_destroy.argtypes = [vp]
@@ -68,7 +70,7 @@ def lib():
         L.dtr_sim_last_error.restype = C.c_char_p
         L.dtr_log_workspace_bytes.argtypes = [vp, i32, vp, i32, vp, C.POINTER(sz)]
         L.dtr_log_create.argtypes = [vp, i32, vp, i32, vp, vp, sz, vp, C.POINTER(vp)]
-        for f in ("dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run", "dtr_sim_results",
+        for f in ("dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run", "dtr_sim_run_static", "dtr_sim_results",
                   "dtr_sim_launch_info", "dtr_log_workspace_bytes", "dtr_log_create"):
             getattr(L, f).restype = C.c_int
         _lib = L
@@ -171,6 +173,10 @@ def dtr_sim_run(handle: int, stream_ptr: int):
     _check(lib().dtr_sim_run(C.c_void_p(handle), C.c_void_p(stream_ptr)))
 
 
+def dtr_sim_run_static(handle: int, stream_ptr: int):
+    _check(lib().dtr_sim_run_static(C.c_void_p(handle), C.c_void_p(stream_ptr)))
+
+
 def dtr_sim_results(handle: int, n_sims: int) -> np.ndarray:
     out = np.zeros(n_sims, dtype=RESULT_DTYPE)
     _check(lib().dtr_sim_results(C.c_void_p(handle), out.ctypes.data, n_sims))
@@ -223,6 +229,11 @@ class Simulator:
     def run(self):
         with self.torch.cuda.device(self.device):
             dtr_sim_run(self.handle, self.stream.cuda_stream)
+
+    def run_static(self):
+        """Run with the library's static working memory (dtr_sim_run_static)."""
+        with self.torch.cuda.device(self.device):
+            dtr_sim_run_static(self.handle, self.stream.cuda_stream)
 
     def results(self) -> np.ndarray:
         with self.torch.cuda.device(self.device):

@@ -233,3 +233,18 @@ def test_log_options():
     with pytest.raises(D.DtrError) as e:
         D.dtr_sim_workspace_bytes([W.chain_trace(4)], sp, {"slots": 0, "flags": D.OPT_LOG_NO_LDS})
     assert e.value.code == D.DTR_EINVAL
+
+
+def test_static_scratch_option_limits():
+    """DTR_OPT_STATIC_SCRATCH is for traces only, and a batch whose one
+    simulation needs more working memory than the static array is rejected
+    when the workspace is sized (before any device work)."""
+    sp = W.make_specs([(0, W.H_DTR, 4, 0)])
+    with pytest.raises(D.DtrError) as e:
+        D.dtr_log_workspace_bytes([W.log_from_trace(W.chain_trace(4))], sp,
+                                  {"slots": 0, "flags": D.OPT_STATIC_SCRATCH})
+    assert e.value.code == D.DTR_EINVAL
+    big = W.chain_trace(300_000)                   # 600k tensors: lane-private walk state alone > 256 MiB
+    with pytest.raises(D.DtrError) as e:
+        D.dtr_sim_workspace_bytes([big], sp, {"slots": 0, "flags": D.OPT_STATIC_SCRATCH})
+    assert e.value.code == D.DTR_EINVAL and "static scratch" in str(e.value)
