@@ -1,5 +1,6 @@
 """Shape and validity checks of the seeded synthetic workloads."""
 import math
+import os
 
 import numpy as np
 import pytest
@@ -98,3 +99,19 @@ def test_resnet_log_uses_the_instruction_kinds():
     assert kinds >= {W.LOG_MEMORY, W.LOG_ALIAS, W.LOG_CALL, W.LOG_MUTATE, W.LOG_CONSTANT, W.LOG_COPY,
                      W.LOG_RELEASE}
     assert L.digest() == W.resnet_log(blocks=4).digest()
+
+
+def test_randdag100k_golden_matches_generator():
+    """The stored oracle results of the full random-DAG workload belong to
+    the trace and budgets the generator makes today."""
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "randdag100k_oracle.json")))
+    w = W.make_config("randdag100k")
+    assert w.traces[0].digest() == g["trace_sha256"]
+    assert int(w.peaks[0]) == g["peak"] and w.n_sims == g["n_budgets"]
+    pcts = []
+    for s in g["sims"]:
+        assert int(w.specs["budget"][s["index"]]) == s["budget"]
+        assert int(w.specs["seed"][s["index"]]) == s["seed"]
+        pcts.append(100 * s["budget"] / g["peak"])
+    assert min(pcts) <= 5.01 and max(pcts) >= 99.99 and len(pcts) >= 8
