@@ -234,6 +234,84 @@ def cpu_baseline(wl, gpu_res, sample_every: int, threads: int):
                 scores_per_s=scores / dt, parity_sample=f"{match}/{len(idx)}")
 
 
+RANDDAG_GOLDEN = os.path.join(ROOT, "tests", "golden", "randdag100k_oracle.json")
+
+
+def sub_workloads():
+    """The other benchmark configurations, each measured in the same run:
+    the Appendix A chain, the ResNet and transformer batches in full, and the
+    full-size random DAG (200k ops, h_DTR) at its stored oracle budgets from
+    48% to 100% of the peak (the lower budgets take the GPU several minutes
+    per simulation; their stored results are checked separately)."""
+    out = [W.make_config("chain32"), W.make_config("resnet50blk"), W.make_config("transformer12")]
+    g = json.load(open(RANDDAG_GOLDEN))
+    full = W.make_config("randdag100k")
+    rows = [r for r in g["sims"] if r["index"] >= 460]
+    pick = np.array([r["index"] for r in rows])
+    sub = W.Workload("randdag100k", full.traces, full.specs[pick], full.peaks,
+                     f"random DAG 100k fwd ops, h_DTR, budget indices {pick.tolist()} of 1024 (48%-100% of peak)")
+    sub.golden = rows
+    out.append(sub)
+    return out
+
+
+def measure_sub(wl, steps: int, threads: int) -> dict:
+    """One configuration: event-timed launches, throughput, algorithmic
+    scan bytes, and the oracle on the host cores (run in a thread while the
+    GPU works): on every simulation for the small batches, on the 90% budget
+    for the random DAG, whose other stored results serve as parity."""
+    import threading
+    import torch
+    from oracle import oracle as O
+    from paper_2006_09616_amd import dtr as D
+    golden = getattr(wl, "golden", None)
+    cpu_idx = np.array([k for k, r in enumerate(golden) if r["index"] == 921]) if golden else np.arange(wl.n_sims)
+    cpu = {}
+
+    def oracle_leg():
+        t0 = time.perf_counter()
+        cpu["ref"] = O.run(wl.traces, wl.specs[cpu_idx], threads=threads)
+        cpu["dt"] = time.perf_counter() - t0
+
+    th = threading.Thread(target=oracle_leg)
+    th.start()
+    sim = D.Simulator(wl.traces, wl.specs, device="cuda:0")
+    if not golden:
+        sim.run()
+        torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record(sim.stream)
+        sim.run()
+        b.record(sim.stream)
+    torch.cuda.synchronize()
+    ms = sum(a.elapsed_time(b) for a, b in ev) / steps
+    res = sim.results()
+    sim.close()
+    th.join()
+    ref, dt = cpu["ref"], cpu["dt"]
+    cpu_match = sum(all(int(res[f][i]) == int(ref[f][k]) for f in O.RESULT_FIELDS) for k, i in enumerate(cpu_idx))
+    if golden:
+        parity = sum(all(int(res[f][k]) == v for f, v in r["result"].items()) for k, r in enumerate(golden))
+        parity_of = "stored oracle results"
+    else:
+        parity, parity_of = cpu_match, "oracle in this run"
+    ops, scores = int(res["n_executed_ops"].sum()), int(res["n_scores"].sum())
+    nbytes = scan_bytes(wl.specs, res)
+    achieved = nbytes / (ms / 1e3) / 1e9
+    print(f"[bench] {wl.name}: {ms:.1f} ms per launch, parity {parity}/{wl.n_sims}, oracle {dt:.2f} s",
+          file=sys.stderr, flush=True)
+    return {"workload": wl.name, "description": wl.description, "n_sims": wl.n_sims, "launch_ms": ms,
+            "launches": steps, "ops_per_s": ops / (ms / 1e3), "scores_per_s": scores / (ms / 1e3),
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBS, "algorithmic_bytes_per_launch": nbytes},
+            "parity": f"{parity}/{wl.n_sims} bit-exact against the {parity_of}",
+            "cpu_baseline": {"value": int(ref["n_executed_ops"].sum()) / dt, "unit": "simulated tensor ops/s",
+                             "cores": threads, "nproc": os.cpu_count(), "kind": "oracle",
+                             "sample": f"{len(cpu_idx)} of {wl.n_sims} simulations, {dt:.2f} s wall",
+                             "parity_sample": f"{cpu_match}/{len(cpu_idx)}"}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -249,6 +327,8 @@ def main():
     ap.add_argument("--study", choices=("search", "policy", "family"), default=None,
                     help="only compare variants of the workload's simulations: search approximations, "
                          "deallocation policies, or h_MSPS and the h'(s, m, c) family")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other configurations (chain, ResNet, transformer, random DAG)")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB MiB three times (counter calibration)")
     args = ap.parse_args()
@@ -315,6 +395,10 @@ def main():
         print(f"[bench] cpu baseline: {cpu['sample']}, parity {cpu['parity_sample']}",
               file=sys.stderr, flush=True)
 
+    configs = None
+    if not args.no_configs and args.workload == "treelstm4096":
+        configs = [measure_sub(w, 1 if getattr(w, "golden", None) else 3, args.cpu_threads) for w in sub_workloads()]
+
     status = np.bincount(res["status"], minlength=4).tolist()
     out = {
         "metric": "simulated tensor ops/sec + eviction scores/sec (1 GPU), % peak HBM BW",
@@ -340,6 +424,7 @@ def main():
                      "kernel": "log_kernel" if log else "replay_kernel", "algorithmic_bytes_per_launch": nbytes,
                      "avg_launch_ms": avg_s * 1e3},
         "cpu_baseline": cpu,
+        "configs": configs,
     }
     print(json.dumps(out))
     sim.close()

@@ -173,6 +173,16 @@ typedef struct {
  * for traces. */
 #define DTR_OPT_LOG_NO_LDS 1
 
+/* Traces only, testing aids for the walk heuristics (h_DTR, h_{e*}, h_MSPS
+ * and the family members with the e* cost): bits 8-11 set the wavefronts per
+ * workgroup (1..8; 0 = chosen from the trace sizes), and
+ * DTR_OPT_WALK_QUEUE_SMALL gives each lane a queue of 16 members, so that
+ * larger neighbourhoods take the whole-wavefront walk.  Results are
+ * identical either way. */
+#define DTR_OPT_WALK_QUEUE_SMALL 4
+#define DTR_OPT_WALK_WAVES_SHIFT 8
+#define DTR_OPT_WALK_WAVES(w) ((w) << DTR_OPT_WALK_WAVES_SHIFT)
+
 /* Traces only: the handle will run through dtr_sim_run_static, so its
  * workspace holds the inputs and results alone (no per-simulation working
  * memory); dtr_sim_run on it returns DTR_ESTATE.  Creation fails with
@@ -297,8 +307,9 @@ int dtr_log_create(const dtr_log *logs, int32_t n_logs,
 /* How a handle's simulations occupy the device, fixed at creation:
  * n_slots          simulations that can be in flight (one workgroup each);
  * waves_per_group  wavefronts per workgroup: 1, except for operator logs
- *                  whose walk state is in LDS, where up to 4 (the first
- *                  replays, the others join its e* / e_R walk scans);
+ *                  whose walk state is in LDS (up to 4) and for traces with
+ *                  walk heuristics (up to 8): the first simulates, the
+ *                  others join its e* / e_R walk scans;
  * lds_bytes        dynamic LDS per workgroup (0: the kernels' static LDS only,
  *                  or walk state in device memory).
  * Returns DTR_EINVAL for a NULL argument.  No device work. */

@@ -271,7 +271,11 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
 {
     if (n_traces < 0 || n_sims < 0) return fail(DTR_EINVAL, "negative n_traces or n_sims");
     if ((n_traces > 0 && !traces) || (n_sims > 0 && !sims)) return fail(DTR_EINVAL, "null traces or sims");
-    if (opt && (opt->slots < 0 || (opt->flags & ~DTR_OPT_STATIC_SCRATCH))) return fail(DTR_EINVAL, "bad options");
+    if (opt && (opt->slots < 0 || (opt->flags & ~(DTR_OPT_STATIC_SCRATCH | DTR_OPT_WALK_QUEUE_SMALL |
+                                                  (15 << DTR_OPT_WALK_WAVES_SHIFT)))))
+        return fail(DTR_EINVAL, "bad options");
+    if (opt && ((opt->flags >> DTR_OPT_WALK_WAVES_SHIFT) & 15) > dtr::MAX_WALK_WAVES)
+        return fail(DTR_EINVAL, "at most %d wavefronts per walk workgroup", dtr::MAX_WALK_WAVES);
     p.static_only = opt && (opt->flags & DTR_OPT_STATIC_SCRATCH);
     p.traces.resize(n_traces);
     for (int32_t i = 0; i < n_traces; i++) {
@@ -305,8 +309,21 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     take(L.nodes, sizeof(dtr::UfNode) * (size_t)L.ucap);
     take(L.uf_remap, need_uf ? 4 * ((size_t)L.ucap + dtr::UF_LDS) : 0);
     take(L.stack, sizeof(dtr::StackFrame) * (size_t)(n + 1));
-    take(L.stamp, need_walk ? 4 * n * dtr::WAVE : 0);
-    take(L.queue, need_walk ? 4 * (n + 1) * dtr::WAVE : 0);
+    // walk heuristics: wavefronts per workgroup (more for large traces, whose
+    // pools are long), a visited bitmap and a member queue per lane
+    int32_t ww = opt ? (opt->flags >> DTR_OPT_WALK_WAVES_SHIFT) & 15 : 0;
+    if (ww == 0) ww = n_max >= 8192 ? dtr::MAX_WALK_WAVES : n_max >= 1024 ? 4 : 1;
+    L.walk_waves = need_walk ? ww : 1;
+    const size_t lanes = (size_t)L.walk_waves * dtr::WAVE;
+    L.vis_words = (int64_t)((n + 127) / 128 * 4);
+    L.vis_bytes = (int64_t)((n + 15) / 16 * 16);
+    L.wq_cap = (opt && (opt->flags & DTR_OPT_WALK_QUEUE_SMALL)) ? 16
+                                                                  : std::min<int64_t>((int64_t)n + 1, dtr::WALK_QUEUE_CAP);
+    take(L.vis, need_walk ? (size_t)L.vis_bytes * lanes : 0);
+    take(L.wq, need_walk ? 4 * (size_t)L.wq_cap * lanes : 0);
+    take(L.bigvis, need_walk ? 4 * (size_t)L.vis_words * (size_t)L.walk_waves : 0);
+    take(L.bigq, need_walk ? 4 * (n + 1) * (size_t)L.walk_waves : 0);
+    take(L.ovf, need_walk ? 4 * pc : 0);
     take(L.pending, need_banish ? n : 0);
     L.bytes = (int64_t)o;
     if (p.static_only && (size_t)L.bytes > DTR_STATIC_SCRATCH_BYTES - STATIC_HEADER)
@@ -316,7 +333,15 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     int32_t cus = 0;
     int rc = device_cus(&cus);
     if (rc) return rc;
-    int64_t slots = opt && opt->slots > 0 ? opt->slots : (int64_t)cus * 16;
+    // 16 one-wave workgroups per compute unit; a batch of walk heuristics
+    // alone needs no more slots than its larger workgroups can occupy
+    const bool walk_only = need_walk && !need_uf && [&] {
+        for (int32_t i = 0; i < n_sims; i++)
+            if (heuristic_class(sims[i].heuristic) != 1) return false;
+        return true;
+    }();
+    int64_t slots = opt && opt->slots > 0 ? opt->slots
+                                          : (int64_t)cus * (walk_only ? std::max<int64_t>(1, 16 / L.walk_waves) : 16);
     const int64_t cap_bytes = int64_t(48) << 30;     // bound slot memory
     slots = std::min<int64_t>(slots, std::max<int64_t>(1, cap_bytes / std::max<int64_t>(1, L.bytes)));
     slots = std::min<int64_t>(slots, std::max<int32_t>(1, n_sims));
@@ -611,10 +636,10 @@ int dtr_sim_launch_info(const dtr_sim *h, dtr_launch_info *out)
         dtrhost::log_plan_info(h->log, &out->n_slots, &out->waves_per_group, &out->lds_bytes);
     } else {
         out->n_slots = h->plan.n_slots;
+        out->waves_per_group = h->plan.class_count[1] + h->plan.class_count[4] > 0 ? (int32_t)h->plan.L.walk_waves : 1;
         if (h->plan.static_only)
             out->n_slots = (int32_t)std::max<int64_t>(1, std::min<int64_t>(
                 out->n_slots, (int64_t)((DTR_STATIC_SCRATCH_BYTES - STATIC_HEADER) / (size_t)h->plan.L.bytes)));
-        out->waves_per_group = 1;
         out->lds_bytes = 0;
     }
     return DTR_OK;

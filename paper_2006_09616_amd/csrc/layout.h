@@ -96,11 +96,18 @@ static_assert(sizeof(ResultDev) == 104, "result layout");
 //             tombstoned and squeezed out): id, packed (degree << 8 | n), last
 //             access, size, c0, start of the neighbour range, and for
 //             h_DTR^eq the union-find nodes of up to NB_CACHE evicted
-//             neighbours (n = NB_CACHE + 1 marks an overflowed cache)
+//             neighbours (n = NB_CACHE + 1 marks an overflowed cache); for
+//             the walk heuristics n is the parent count (255: at least 255)
+//             and the cache holds the first NB_HEAD neighbours
 //   nodes     union-find nodes {running cost, parent, size}
 //   stack     rematerialization frames (tensor, next input, the tensor's record,
 //             its first input ids)
-//   stamp/queue  lane-private walk state for e* (h_DTR, h_{e*})
+//   vis/wq    lane-private visited flags (one byte per tensor) and member
+//             queues (wq_cap entries) of the e* and e_R walks (h_DTR, h_{e*},
+//             h_MSPS), for every lane of the workgroup
+//   bigvis/bigq  each wavefront's visited bitmap and queue (n_max + 1
+//             entries) for walks that outgrow a lane's queue, which a whole
+//             wavefront then takes; ovf lists those candidates' pool slots
 //   pending   one byte per tensor: released, banishing deferred (banishing policy)
 constexpr int NB_CACHE = 8;
 // union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
@@ -116,19 +123,29 @@ struct SlotLayout {
     int64_t pool;
     int64_t nodes, uf_remap;
     int64_t stack;
-    int64_t stamp, queue;
+    int64_t vis, wq, bigvis, bigq, ovf;
     int64_t pending;
     int64_t pcap, ucap, n_max;
+    int64_t vis_words;       // 32-bit words of one wavefront's visited bitmap (a multiple of 4)
+    int64_t vis_bytes;       // bytes of one lane's visited flags (a multiple of 16)
+    int64_t wq_cap;          // entries of one lane's member queue
+    int64_t walk_waves;      // wavefronts per workgroup of the walk heuristics
 };
+// workgroups of the walk heuristics hold up to this many wavefronts: the
+// first runs the simulation, the others join its eviction scans
+constexpr int MAX_WALK_WAVES = 8;
+// a lane's member queue holds at most this many entries (walks that need
+// more are taken by a whole wavefront, a level at a time)
+constexpr int WALK_QUEUE_CAP = 256;
 
 struct __attribute__((aligned(16))) PoolSlot {
     int32_t id;              // tensor; -1 marks a dead slot
-    int32_t deg;             // degree << 8 | cached neighbour count
+    int32_t deg;             // degree << 8 | cached neighbour count (walks: parent count)
     int64_t last;            // last access
     int64_t size;
     int32_t c0;              // <= 2^28
     int32_t adj_b;           // start of the tensor's neighbour range
-    int32_t nb[NB_CACHE];    // cached union-find nodes of evicted neighbours
+    int32_t nb[NB_CACHE];    // cached union-find nodes of evicted neighbours (walks: first neighbours)
 };
 static_assert(sizeof(PoolSlot) == 64, "pool slot layout");
 

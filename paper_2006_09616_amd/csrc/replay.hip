@@ -172,10 +172,14 @@ struct Slot {
     NodeStore nodes;
     GAS int32_t *remap;
     GAS i32x4 *stack;             // StackFrame records, three quads each
-    GAS uint32_t *stamp;
-    GAS int32_t *queue;
+    GAS uint8_t *visb;            // walk heuristics: lane-private visited flags (a byte per tensor)
+    GAS int32_t *wq;              // and member queues
+    GAS uint32_t *bigvis;         // each wavefront's bitmap and queue for large walks
+    GAS int32_t *bigq;
+    GAS int32_t *ovf;             // pool slots of the candidates whose walk is large
     GAS uint8_t *pending;         // released, banishing deferred (banishing policy)
     int32_t pcap, ucap, n_max;
+    int32_t vis_words, vis_bytes, wq_cap;
     __device__ __forceinline__ PoolSlot &pool(int32_t i) const
     {
         return i < POOL_LDS ? lpool[i] : *(PoolSlot *)(gpool + i);
@@ -196,12 +200,18 @@ __device__ __forceinline__ Slot slot_at(const KernelArgs &a, int32_t k)
     S.nodes.glob = (UfNode *)(b + a.L.nodes);
     S.remap = (GAS int32_t *)(b + a.L.uf_remap);
     S.stack = (GAS i32x4 *)(b + a.L.stack);
-    S.stamp = (GAS uint32_t *)(b + a.L.stamp);
-    S.queue = (GAS int32_t *)(b + a.L.queue);
+    S.visb = (GAS uint8_t *)(b + a.L.vis);
+    S.wq = (GAS int32_t *)(b + a.L.wq);
+    S.bigvis = (GAS uint32_t *)(b + a.L.bigvis);
+    S.bigq = (GAS int32_t *)(b + a.L.bigq);
+    S.ovf = (GAS int32_t *)(b + a.L.ovf);
     S.pending = (GAS uint8_t *)(b + a.L.pending);
     S.pcap = (int32_t)a.L.pcap;
     S.ucap = (int32_t)a.L.ucap;
     S.n_max = (int32_t)a.L.n_max;
+    S.vis_words = (int32_t)a.L.vis_words;
+    S.vis_bytes = (int32_t)a.L.vis_bytes;
+    S.wq_cap = (int32_t)a.L.wq_cap;
     return S;
 }
 
@@ -220,7 +230,9 @@ struct Sim {
     int32_t pool_end, pool_live;
     int32_t uf_n, uf_limit;      // nodes in use; count that triggers a compaction
     int32_t status, cur_op;
-    uint32_t epoch;
+    int32_t nw;                   // wavefronts in the workgroup (walk heuristics)
+    int32_t trace_idx;
+    LAS struct WalkCtl *ctl;      // their control block in LDS
     int64_t evict_no;
     int64_t total, base, remat_cost, executed, remats, evictions, eager, scores;
     int64_t nbr, adj;     // per-lane partial sums, reduced at the end
@@ -265,9 +277,9 @@ __device__ __forceinline__ TRec rec_u(const Sim &s, int32_t x)
 }
 
 // per-lane read of a tensor's static record (two 16-byte global loads)
-__device__ __forceinline__ TRec rec_v(const Sim &s, int32_t x)
+__device__ __forceinline__ TRec rec_v_t(const TraceDev &t, int32_t x)
 {
-    const GAS u32x4 *p = (const GAS u32x4 *)&s.t.rec[x].r;
+    const GAS u32x4 *p = (const GAS u32x4 *)&t.rec[x].r;
     const u32x4 a = p[0], b = p[1];
     TRec r;
     r.size = (int64_t)((uint64_t)a.x | ((uint64_t)a.y << 32));
@@ -279,6 +291,8 @@ __device__ __forceinline__ TRec rec_v(const Sim &s, int32_t x)
     r.adj_e = (int32_t)b.w;
     return r;
 }
+
+__device__ __forceinline__ TRec rec_v(const Sim &s, int32_t x) { return rec_v_t(s.t, x); }
 
 // ------------------------------------------------------ neighbour cache --
 
@@ -382,6 +396,44 @@ __device__ __forceinline__ bool list_remove(const Sim &s, int32_t i, int32_t nd)
     return true;
 }
 
+// ------------------------------------------- walk workgroup control --
+
+// Control block of the walk heuristics' workgroup in LDS: what the simulating
+// wavefront posts for a scan, the shared candidate counter, the count of
+// large walks, and each wavefront's best candidate and work counters.
+struct WaveBest {
+    uint64_t N, da, db;
+    int32_t id, slot, have, pad;
+    int64_t nbr, adj, scored;
+};
+struct WalkCtl {
+    int32_t cmd, sim, end, both, use_m, use_s, sample, trace;
+    uint32_t ctr, ovf, ctr2, pad;
+    int64_t T, evict_no;
+    uint64_t min_size, tau, seed;
+    WaveBest res[MAX_WALK_WAVES];
+};
+enum { CMD_WALK = 1, CMD_DONE = 2 };
+
+// Order this wavefront's LDS and global accesses (what a workgroup barrier
+// gives a one-wave workgroup) without waiting for the other wavefronts.
+__device__ __forceinline__ void wave_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+}
+
+// the simulating wavefront's synchronization: wavefront-local for the walk
+// heuristics (their workgroups hold helper wavefronts), a workgroup barrier
+// otherwise (one-wave workgroups)
+template <int HC>
+__device__ __forceinline__ void slot_sync()
+{
+    if constexpr (cls(HC) == HC_WALK) wave_sync();
+    else __syncthreads();
+}
+
+
 // ---------------------------------------------------------------- pool --
 
 // Squeeze tombstones out of the pool (order preserved; positions updated).
@@ -393,30 +445,30 @@ __device__ __forceinline__ void pool_compact(Sim &s)
 #ifdef DTR_PROFILE
     s.prof_pool_compact++;
 #endif
-    __syncthreads();
+    slot_sync<HC>();
     for (int32_t base = 0; base < s.pool_end; base += WAVE) {
         const int32_t i = base + lane;
         const i32x4 *P = (const i32x4 *)&s.S.pool(i < s.pool_end ? i : 0);
         const i32x4 q0 = P[0], q1 = P[1];
         i32x4 qc[KQ];
 #pragma unroll
-        for (int k = 0; k < KQ; k++) qc[k] = cls(HC) == HC_EQ ? P[2 + k] : 0;
+        for (int k = 0; k < KQ; k++) qc[k] = cls(HC) != HC_SIMPLE ? P[2 + k] : 0;
         const int32_t x = i < s.pool_end ? q0.x : -1;
         const bool keep = x >= 0;
         const uint64_t m = __ballot(keep);
-        __syncthreads();
+        slot_sync<HC>();
         if (keep) {
             const int32_t j = kept + lane_rank(m);
             i32x4 *Q = (i32x4 *)&s.S.pool(j);
             Q[0] = q0;
             Q[1] = q1;
-            if (cls(HC) == HC_EQ)
+            if (cls(HC) != HC_SIMPLE)
 #pragma unroll
                 for (int k = 0; k < KQ; k++) Q[2 + k] = qc[k];
             s.S.tst[x] = ts_make(S_RESIDENT, (uint32_t)j, 0);
         }
         kept += __popcll(m);
-        __syncthreads();
+        slot_sync<HC>();
     }
     s.pool_end = kept;
 }
@@ -440,12 +492,13 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
         // the record and the first neighbours are one 64-byte element
         const GAS i32x4 *px = (const GAS i32x4 *)&s.t.rec[x];
         i32x4 hd[2];
-        if (cls(HC) == HC_EQ) {
+        if (cls(HC) != HC_SIMPLE) {
             hd[0] = px[2];
             hd[1] = px[3];
         }
         const TRec r = known ? *known : rec_v(s, x);
-        int32_t deg = (r.adj_e - r.adj_b) << 8;
+        // walk heuristics: the low byte holds the parent count (255: read the record)
+        int32_t deg = (r.adj_e - r.adj_b) << 8 | (cls(HC) == HC_WALK ? min(r.in_e - r.in_b, 255) : 0);
         NbCache nb;
         if (cls(HC) == HC_EQ) nb = list_build(s, r.adj_b, r.adj_e, deg, hd);
         i32x4 q0, q1;
@@ -461,6 +514,11 @@ __device__ __forceinline__ int32_t pool_append(Sim &s, bool want, int32_t x, int
         Q[0] = q0;
         Q[1] = q1;
         if (cls(HC) == HC_EQ) cache_store(s.S.pool(i), nb);
+        if (cls(HC) == HC_WALK) {
+            // the first neighbours, so that a walk starts from the slot alone
+            Q[2] = hd[0];
+            Q[3] = hd[1];
+        }
     }
     s.pool_end += cnt;
     s.pool_live += cnt;
@@ -804,14 +862,6 @@ __device__ __forceinline__ int64_t eq_cost_full(const Sim &s, const NS &N, int32
     return sum;
 }
 
-__device__ __forceinline__ void clear_stamps(Sim &s)
-{
-    __syncthreads();
-    for (size_t i = s.lane; i < (size_t)s.t.n * WAVE; i += WAVE) s.S.stamp[i] = 0;
-    __syncthreads();
-    s.epoch = 0;
-}
-
 // Scores are N / (da * db) with N < 2^64 and da * db < 2^76.  A float
 // estimate decides every comparison whose two estimates differ by more than a
 // factor 1 -+ 2^-16; the rest (near ties, exact ties, 0/0) are decided
@@ -955,138 +1005,499 @@ __device__ __forceinline__ int64_t cached_sum(const LAS UfNode *NL, const int32_
     return t;
 }
 
-// e* (h_DTR, h_{e*}) or e_R (h_MSPS) of every pooled candidate, walked with
-// lane-private epoch stamps and queues.  Flattened: a lane takes the next pool
-// slot as soon as its previous walk ends (lanes are handed consecutive slots
-// in lane order), and every iteration expands one queued tensor per lane: its
-// record element brings the first NB_HEAD neighbours (parents first), whose
-// states and stamps are then read together.  A walk's members are the tensors
-// it queues (the candidate itself is queued at the start of each side only);
-// their costs are added when they are expanded.  Each walk takes the next
-// epoch of its lane; the scan advances the epoch by the most walks a lane made.
-template <int HC>
-__device__ __forceinline__ void walk_scan(Sim &s, const Filter &F, Best &best, int64_t &scored)
+// ------------------------------------------------------------- e* walks --
+
+// What a walk scan needs to know, identical in every lane and wavefront.
+struct WalkParams {
+    int32_t end, both, use_m, use_s, sample;
+    int64_t T, evict_no;
+    uint64_t min_size, tau, seed;
+};
+
+// the search approximations' sampling draw of candidate x (Appendix E)
+__device__ __forceinline__ uint64_t sample_draw_at(uint64_t seed, int64_t evict_no, int32_t x)
 {
-    const int32_t end = s.pool_end, lane = s.lane;
-    const int64_t T = s.T;
-    const bool both = s.cmode == CM_ESTAR;
-    GAS uint32_t *st = s.S.stamp;
-    GAS int32_t *q = s.S.queue;
-    int32_t next = 0;                     // next pool slot to hand out (uniform)
-    int32_t x = -1, slot = -1, head = 0, tail = 0, side = 0, deg = 0;
-    int64_t sum = 0, cnt = 0, c0x = 0, size = 0, last = 0, nscored = 0;
-    uint32_t walks = 0, ep = 0;
+    const uint64_t key = ((uint64_t)evict_no << 32) + (uint64_t)(uint32_t)x;
+    return mix64((seed ^ 0xD6E8FEB86659FD93ull) + 0x9E3779B97F4A7C15ull * key);
+}
+
+// The evicted neighbourhood walks of one wavefront, one candidate per lane.
+// Each lane takes the next pool slot (from the workgroup's LDS counter when
+// wavefronts share the scan) as soon as its previous walk has ended, and
+// expands one tensor per iteration.  The candidate x comes from its pool slot
+// alone (which holds its first neighbours and parent count): its evicted
+// parents start its ancestors (e_R) and, for e*, its evicted children its
+// descendants.  Then each queued member: its record element brings its cost
+// c0 and first neighbours; an ancestor-side member follows its parents (the
+// first neighbours), a descendant-side member its children (read from the
+// adjacency list).  The two sides are disjoint in a DAG, so one visited flag
+// per tensor serves both: a byte per tensor and lane, so that marks need no
+// read-modify-write.  Up to NC neighbours are checked per iteration, their
+// reads issued together; a tensor with more relevant neighbours keeps its
+// cursor for the next iteration.  A member is marked and queued at once, so
+// the queue lists exactly the marked tensors and the flags are cleared from
+// it after the walk.  A walk ends, and is scored, in the iteration that
+// leaves its queue empty.  A walk that would outgrow the lane's queue is
+// abandoned (cleared) and its slot listed: those are walked afterwards by
+// whole wavefronts.
+template <int HC>
+__device__ void walk_lanes(const TraceDev &t, const Slot &S, GAS uint64_t *tst, const WalkParams &P,
+                           int32_t lane, int32_t lid, LAS uint32_t *ctr, LAS uint32_t *novf, Best &best,
+                           int64_t &nbr, int64_t &adj, int64_t &nscored)
+{
+    constexpr int NC = 8;                 // neighbours checked per iteration
+    GAS uint8_t *vis = S.visb + (size_t)lid * (size_t)S.vis_bytes;
+    GAS int32_t *q = S.wq + (size_t)lid * (size_t)S.wq_cap;
+    const GAS int32_t *sw = (const GAS int32_t *)tst;     // low words of the state words
+    const int32_t cap = S.wq_cap;
+    int32_t next = 0;                     // next pool slot (one wavefront alone)
+    bool drained = false;
+    int32_t x = -1, slot = 0, deg = 0, head = 0, tail = 0;
+    int64_t sum = 0, c0x = 0, size = 0, last = 0;
+    // the tensor being expanded: neighbour cursor k over [k, ke) of its
+    // adjacency (base ab, np parents first), side of the members it finds
+    // (-1: the candidate), and its first neighbours (from the pool slot or
+    // the record element), used while the cursor is at 0
+    int32_t k = 0, ke = 0, ab = 0, np = 0, sd = 0;
+    int32_t nb[NB_HEAD];
+#pragma unroll
+    for (int c = 0; c < NB_HEAD; c++) nb[c] = 0;
     for (;;) {
         const bool idle = x < 0;
         const uint64_t mi = __ballot(idle);
-        if (mi && next < end) {
-            if (idle) {
-                const int32_t i = next + lane_rank(mi);
-                if (i < end) {
-                    const i32x4 *P = (const i32x4 *)&s.S.pool(i);
-                    const i32x4 q0 = P[0], q1 = P[1];
-                    bool ok = q0.x >= 0;
-                    const int64_t sz = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
-                    if (approx(HC)) {
-                        ok = ok && (uint64_t)sz >= F.min_size;
-                        if (F.sample) ok = ok && sample_draw(s, q0.x) < F.tau;
-                    }
-                    if (ok) {
-                        x = q0.x;
-                        slot = i;
-                        deg = q0.y >> 8;
-                        last = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
-                        size = sz;
-                        c0x = (int64_t)q1.z;
-                        side = 0;
-                        head = 0;
-                        tail = 1;
-                        q[lane] = x;
-                        sum = cnt = 0;
-                        walks++;
-                        ep = s.epoch + walks;
-                    }
-                }
-            }
-            next += __popcll(mi);
-        }
-        const uint64_t ma = __ballot(x >= 0);
-        if (!ma) {
-            if (next >= end) break;
-            continue;
-        }
-        bool fin = false;
-        if (x >= 0) {
-            if (head < tail) {
-                const int32_t u = q[(size_t)head * WAVE + lane];
-                const GAS i32x4 *R = (const GAS i32x4 *)&s.t.rec[u];
-                const i32x4 r0 = R[0], r1 = R[1], n0 = R[2], n1 = R[3];
-                if (head > 0) {           // a member (not the candidate)
-                    sum += (int64_t)r0.z;
-                    cnt++;
-                }
-                head++;
-                const int32_t np = r1.y - r1.x, dg = r1.w - r1.z, ab = r1.z;
-                const int32_t b = side == 0 ? 0 : np, e = side == 0 ? np : dg;
-                const int32_t nb[NB_HEAD] = {n0.x, n0.y, n0.z, n0.w, n1.x, n1.y, n1.z, n1.w};
-                // neighbours WB at a time: from the inline table below NB_HEAD,
-                // then from the adjacency list; every read is unconditional
-                // (clamped in range) so that a chunk's reads issue together
-                constexpr int WB = 4;
-                for (int32_t k0 = b; k0 < e; k0 += WB) {
-                    int32_t v[WB];
-                    uint64_t w[WB];
-                    uint32_t sv[WB];
-#pragma unroll
-                    for (int j = 0; j < WB; j++) {
-                        const int32_t k = min(k0 + j, e - 1);
-                        int32_t id = nb[0];
-#pragma unroll
-                        for (int t = 1; t < NB_HEAD; t++) id = k == t ? nb[t] : id;
-                        v[j] = k < NB_HEAD ? id : gld(s.t.adj + ab + k);
-                    }
-#pragma unroll
-                    for (int j = 0; j < WB; j++) {
-                        w[j] = s.S.tst[v[j]];
-                        sv[j] = st[(size_t)v[j] * WAVE + lane];
-                    }
-#pragma unroll
-                    for (int j = 0; j < WB; j++) {
-                        if (k0 + j < e && ts_sw(w[j]) >= 0 && sv[j] != ep) {
-                            st[(size_t)v[j] * WAVE + lane] = ep;
-                            q[(size_t)tail++ * WAVE + lane] = v[j];
-                        }
-                    }
-                }
-            } else if (side == 0 && both) {
-                side = 1;
-                head = 0;
-                tail = 1;
-                q[lane] = x;
+        uint32_t i = 0xffffffffu;
+        if (mi && !drained) {
+            uint32_t b;
+            if (ctr) {
+                const int32_t first = __ffsll((long long)mi) - 1;
+                uint32_t got = 0;
+                if (lane == first) got = atomicAdd((uint32_t *)ctr, (uint32_t)__popcll(mi));
+                b = (uint32_t)__builtin_amdgcn_readlane((int32_t)got, first);
             } else {
-                fin = true;
+                b = (uint32_t)next;
+                next += __popcll(mi);
             }
+            if (b + (uint32_t)__popcll(mi) >= (uint32_t)P.end) drained = true;
+            if (idle) i = b + (uint32_t)lane_rank(mi);
+        } else if (!__ballot(x >= 0)) {
+            break;
         }
-        // a finished walk is scored (every lane takes part in the reduction step)
+        if (i < (uint32_t)P.end) {
+            i32x4 q0, q1, h0, h1;
+            if (i < (uint32_t)POOL_LDS) {
+                const LAS i32x4 *PS = (const LAS i32x4 *)S.lpool_l + PQ * i;
+                q0 = PS[0]; q1 = PS[1]; h0 = PS[2]; h1 = PS[3];
+            } else {
+                const GAS i32x4 *PS = (const GAS i32x4 *)S.gpool + PQ * (size_t)i;
+                q0 = PS[0]; q1 = PS[1]; h0 = PS[2]; h1 = PS[3];
+            }
+            bool ok = q0.x >= 0;
+            const int64_t sz = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
+            if (approx(HC)) {
+                ok = ok && (uint64_t)sz >= P.min_size;
+                if (P.sample) ok = ok && sample_draw_at(P.seed, P.evict_no, q0.x) < P.tau;
+            }
+            if (ok) {
+                x = q0.x;
+                slot = (int32_t)i;
+                deg = q0.y >> 8;
+                last = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
+                size = sz;
+                c0x = (int64_t)q1.z;
+                head = tail = 0;
+                sum = 0;
+                np = q0.y & 0xFF;
+                if (np == 255) {                // 255 or more parents: the record has the count
+                    const TRec r = rec_v_t(t, x);
+                    np = r.in_e - r.in_b;
+                }
+                ab = q1.w;
+                k = 0;
+                ke = P.both ? deg : np;
+                sd = -1;
+                nb[0] = h0.x; nb[1] = h0.y; nb[2] = h0.z; nb[3] = h0.w;
+                nb[4] = h1.x; nb[5] = h1.y; nb[6] = h1.z; nb[7] = h1.w;
+            }
+        } else if (x >= 0 && k >= ke) {
+            // the next queued member
+            const int32_t e = q[head++];
+            const int32_t u = e & 0x7fffffff;
+            const GAS i32x4 *R = (const GAS i32x4 *)&t.rec[u];
+            const i32x4 r0 = R[0], r1 = R[1], n0 = R[2], n1 = R[3];
+            sum += (int64_t)r0.z;
+            np = r1.y - r1.x;
+            ab = r1.z;
+            sd = (int32_t)((uint32_t)e >> 31);
+            k = sd == 0 ? 0 : np;
+            ke = sd == 0 ? np : r1.w - r1.z;
+            nb[0] = n0.x; nb[1] = n0.y; nb[2] = n0.z; nb[3] = n0.w;
+            nb[4] = n1.x; nb[5] = n1.y; nb[6] = n1.z; nb[7] = n1.w;
+        }
+        bool over = false;
+        if (x >= 0 && k < ke) {
+            // up to NC neighbours from the cursor: the first NB_HEAD from the
+            // registers when the cursor is at 0, the rest from the adjacency
+            // list; a lane reads only the neighbours in its range
+            int32_t v[NC], st[NC];
+            uint8_t seen[NC];
+#pragma unroll
+            for (int j = 0; j < NC; j++) {
+                v[j] = (k == 0 && j < NB_HEAD) ? nb[j] : 0;
+                if (k + j < ke && !(k == 0 && j < NB_HEAD)) v[j] = gld(t.adj + ab + k + j);
+            }
+#pragma unroll
+            for (int j = 0; j < NC; j++) {
+                st[j] = -1;
+                seen[j] = 1;
+                if (k + j < ke) {
+                    st[j] = sw[2 * (size_t)v[j]];
+                    seen[j] = vis[v[j]];
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < NC; j++) {
+                if (st[j] >= 0 && !seen[j]) {
+                    if (tail >= cap) {
+                        over = true;
+                    } else {
+                        vis[v[j]] = 1;
+                        const int32_t s2 = sd >= 0 ? sd : (k + j < np ? 0 : 1);
+                        q[tail++] = v[j] | (s2 << 31);
+                    }
+                }
+            }
+            k += NC;
+        }
+        // the walk ends with the expansion that leaves nothing to expand
+        const bool fin = x >= 0 && !over && k >= ke && head == tail;
         if (__ballot(fin)) {
             const uint64_t N = (uint64_t)(c0x + sum);
-            const uint64_t DA = s.use_m ? (uint64_t)size : 1;
-            const uint64_t DB = s.use_s ? (uint64_t)(T - last) : 1;
+            const uint64_t DA = P.use_m ? (uint64_t)size : 1;
+            const uint64_t DB = P.use_s ? (uint64_t)(P.T - last) : 1;
             take(best, fin, fin ? score_est(N, DA, DB) : 0.0f, N, DA, DB, x, slot);
         }
+        if (over) {
+            // listed for a whole-wavefront walk (its members are recounted there)
+            const uint32_t kk = atomicAdd((uint32_t *)novf, 1u);
+            S.ovf[kk] = slot;
+        }
         if (fin) {
-            s.nbr += cnt;
-            s.adj += deg;
+            nbr += tail;
+            adj += deg;
             nscored++;
+        }
+        if (fin || over) {
+            // every set flag of the lane belongs to this walk; entries read 8 at a time
+            for (int32_t j0 = 0; j0 < tail; j0 += 8) {
+                int32_t e[8];
+#pragma unroll
+                for (int j = 0; j < 8; j++) e[j] = q[min(j0 + j, tail - 1)];
+#pragma unroll
+                for (int j = 0; j < 8; j++) vis[e[j] & 0x7fffffff] = 0;
+            }
             x = -1;
+            k = ke = 0;
         }
     }
-    uint32_t mw = walks;
-    for (int off = WAVE / 2; off >= 1; off >>= 1) mw = max(mw, (uint32_t)__shfl_xor((int32_t)mw, off, WAVE));
-    s.epoch += uni((int32_t)mw);
-    if (approx(HC)) {
-        for (int off = WAVE / 2; off >= 1; off >>= 1) nscored += __shfl_xor(nscored, off, WAVE);
-        scored += (int64_t)uni64(nscored);
+}
+
+// A whole wavefront walks the evicted neighbourhood of candidate x (uniform)
+// with its own bitmap bv and queue bq, a level of up to 64 queued tensors at
+// a time: each lane expands one (its record element brings c0 and the first
+// neighbours), claims evicted neighbours with an atomic OR on the bitmap, and
+// claimed ones are appended in lane order.  Returns the summed c0 of the
+// members (uniform); *count gets their number.
+__device__ int64_t walk_wave(const TraceDev &t, GAS uint64_t *tst, GAS uint32_t *bv, GAS int32_t *bq, int32_t x,
+                             bool both, int32_t lane, int64_t *count)
+{
+    constexpr int WB = 8;
+    int32_t tail = 0;
+    int64_t sum = 0;
+    // lane's tensor u (or -1) and the side of the members it finds (-1: the
+    // candidate, parents to side 0 and children to side 1)
+    auto expand = [&](int32_t u, int32_t side) {
+        int32_t kb = 0, ke = 0, np = 0, ab = 0;
+        int32_t nb[NB_HEAD];
+#pragma unroll
+        for (int c = 0; c < NB_HEAD; c++) nb[c] = 0;
+        if (u >= 0) {
+            const GAS i32x4 *R = (const GAS i32x4 *)&t.rec[u];
+            const i32x4 r0 = R[0], r1 = R[1], n0 = R[2], n1 = R[3];
+            if (side >= 0) sum += (int64_t)r0.z;
+            np = r1.y - r1.x;
+            ab = r1.z;
+            const int32_t dg = r1.w - r1.z;
+            kb = side == 1 ? np : 0;
+            ke = side < 0 ? (both ? dg : np) : (side == 0 ? np : dg);
+            nb[0] = n0.x; nb[1] = n0.y; nb[2] = n0.z; nb[3] = n0.w;
+            nb[4] = n1.x; nb[5] = n1.y; nb[6] = n1.z; nb[7] = n1.w;
+        }
+        for (int32_t c0 = 0; __ballot(kb + c0 < ke); c0 += WB) {
+            int32_t v[WB];
+            bool claim[WB];
+            uint64_t w[WB];
+#pragma unroll
+            for (int j = 0; j < WB; j++) {
+                const int32_t kc = min(kb + c0 + j, max(ke - 1, 0));
+                int32_t id = nb[0];
+#pragma unroll
+                for (int c = 1; c < NB_HEAD; c++) id = kc == c ? nb[c] : id;
+                v[j] = kc < NB_HEAD ? id : gld(t.adj + ab + kc);
+            }
+#pragma unroll
+            for (int j = 0; j < WB; j++) w[j] = tst[v[j]];
+#pragma unroll
+            for (int j = 0; j < WB; j++) {
+                claim[j] = false;
+                if (kb + c0 + j < ke && ts_sw(w[j]) >= 0) {
+                    const uint32_t bit = 1u << (v[j] & 31);
+                    claim[j] = !(atomicOr((uint32_t *)(bv + (v[j] >> 5)), bit) & bit);
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < WB; j++) {
+                const uint64_t m = __ballot(claim[j]);
+                if (claim[j]) {
+                    const int32_t s2 = side >= 0 ? side : (kb + c0 + j < np ? 0 : 1);
+                    bq[tail + lane_rank(m)] = v[j] | (s2 << 31);
+                }
+                tail += __popcll(m);
+            }
+        }
+    };
+    expand(lane == 0 ? x : -1, -1);
+    wave_sync();
+    for (int32_t head = 0; head < tail;) {
+        const int32_t hi = min(tail, head + WAVE);
+        int32_t u = -1, side = 0;
+        if (head + lane < hi) {
+            const int32_t e = bq[head + lane];
+            u = e & 0x7fffffff;
+            side = (int32_t)((uint32_t)e >> 31);
+        }
+        head = hi;
+        expand(u, side);
+        wave_sync();
+    }
+    for (int32_t j = lane; j < tail; j += WAVE) bv[(bq[j] & 0x7fffffff) >> 5] = 0u;
+    wave_sync();
+    for (int off = WAVE / 2; off >= 1; off >>= 1) sum += __shfl_xor(sum, off, WAVE);
+    *count = tail;
+    return uni64(sum);
+}
+
+// The listed walks, each by a whole wavefront: wavefronts take them from the
+// shared counter ctr2 (this wavefront alone when ctr2 is null) and keep the
+// best in `best` (lane 0 takes each result).
+template <int HC>
+__device__ void walk_listed(const TraceDev &t, const Slot &S, GAS uint64_t *tst, const WalkParams &P, int32_t lane,
+                            int32_t wave, int32_t n_ovf, LAS uint32_t *ctr2, Best &best, int64_t &nbr,
+                            int64_t &adj, int64_t &nscored)
+{
+    GAS uint32_t *bv = S.bigvis + (size_t)wave * (size_t)S.vis_words;
+    GAS int32_t *bq = S.bigq + (size_t)wave * (size_t)(S.n_max + 1);
+    for (int32_t own = 0;;) {
+        int32_t k;
+        if (ctr2) {
+            uint32_t got = 0;
+            if (lane == 0) got = atomicAdd((uint32_t *)ctr2, 1u);
+            k = uni((int32_t)got);
+        } else {
+            k = own++;
+        }
+        if (k >= n_ovf) break;
+        const int32_t sl = uni(gld(S.ovf + k));
+        const i32x4 *PS = (const i32x4 *)&S.pool(sl);
+        const i32x4 q0 = PS[0], q1 = PS[1];
+        const int32_t x = uni(q0.x);
+        const int64_t last = uni64((int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z));
+        const int64_t size = uni64((int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x));
+        const int64_t c0x = (int64_t)uni(q1.z);
+        int64_t cnt = 0;
+        const int64_t sum = walk_wave(t, tst, bv, bq, x, P.both, lane, &cnt);
+        const uint64_t N = (uint64_t)(c0x + sum);
+        const uint64_t DA = P.use_m ? (uint64_t)size : 1;
+        const uint64_t DB = P.use_s ? (uint64_t)(P.T - last) : 1;
+        const bool me = lane == 0;
+        take(best, me, score_est(N, DA, DB), N, DA, DB, x, sl);
+        if (me) {
+            nbr += cnt;
+            adj += uni(q0.y >> 8);
+            nscored++;
+        }
+    }
+}
+
+// the wavefront's best (exact lexicographic minimum of score and id over its
+// lanes), uniform
+__device__ WaveBest wave_best(const Best &best)
+{
+    WaveBest r;
+    float mn = best.have ? best.sc : __builtin_inff();
+    for (int off = WAVE / 2; off >= 1; off >>= 1) mn = fminf(mn, __shfl_xor(mn, off, WAVE));
+    const float thr = mn * FILTER_HI;
+    uint64_t m = __ballot(best.have && !(best.sc > thr));     // NaN estimates stay in
+    r.have = m ? 1 : 0;
+    r.N = 0;
+    r.da = r.db = 1;
+    r.id = 0x7fffffff;
+    r.slot = -1;
+    r.pad = 0;
+    r.nbr = r.adj = r.scored = 0;
+    while (m) {
+        const int32_t j = __ffsll((long long)m) - 1;
+        m &= m - 1;
+        const uint64_t cN = readlane64(best.N, j), cda = readlane64(best.da, j), cdb = readlane64(best.db, j);
+        const int32_t cid = __builtin_amdgcn_readlane(best.id, j), cslot = __builtin_amdgcn_readlane(best.slot, j);
+        if (r.slot < 0 || better_exact(cN, cda, cdb, cid, r.N, r.da, r.db, r.id)) {
+            r.N = cN;
+            r.da = cda;
+            r.db = cdb;
+            r.id = cid;
+            r.slot = cslot;
+        }
+    }
+    return r;
+}
+
+__device__ __forceinline__ int64_t wave_sum(int64_t v)
+{
+    for (int off = WAVE / 2; off >= 1; off >>= 1) v += __shfl_xor(v, off, WAVE);
+    return uni64(v);
+}
+
+// The walk scan of the simulating wavefront.  Helper wavefronts (if any) are
+// given the scan's parameters at a workgroup barrier; all wavefronts walk
+// candidates lane by lane from the shared counter; after a second barrier
+// they take the listed (large) walks one per wavefront; after a third, the
+// helpers' bests enter this wavefront's lanes 1.. and their counters are
+// added.
+template <int HC>
+__device__ void walk_scan(Sim &s, const Filter &F, Best &best, int64_t &scored)
+{
+    WalkParams P;
+    P.end = s.pool_end;
+    P.both = s.cmode == CM_ESTAR;
+    P.use_m = s.use_m;
+    P.use_s = s.use_s;
+    P.sample = F.sample;
+    P.T = s.T;
+    P.evict_no = s.evict_no;
+    P.min_size = F.min_size;
+    P.tau = F.tau;
+    P.seed = s.seed;
+    LAS WalkCtl *C = s.ctl;
+    const bool multi = s.nw > 1;
+    if (s.lane == 0) {
+        C->ovf = 0;
+        C->ctr = 0;
+        C->ctr2 = 0;
+    }
+    if (multi) {
+        if (s.lane == 0) {
+            C->cmd = CMD_WALK;
+            C->trace = s.trace_idx;
+            C->end = P.end;
+            C->both = P.both;
+            C->use_m = P.use_m;
+            C->use_s = P.use_s;
+            C->sample = P.sample;
+            C->T = P.T;
+            C->evict_no = P.evict_no;
+            C->min_size = P.min_size;
+            C->tau = P.tau;
+            C->seed = P.seed;
+        }
+        __syncthreads();
+    } else {
+        wave_sync();
+    }
+    int64_t nbr = 0, adj = 0, nscored = 0;
+#ifdef DTR_PROFILE
+    // walk heuristics: cycles of this wavefront's own walks, of the wait for
+    // the helpers, of the whole-wavefront walks, and their number
+    const int64_t w1 = (int64_t)__builtin_readcyclecounter();
+#endif
+    walk_lanes<HC>(s.t, s.S, s.S.tst, P, s.lane, s.lane, multi ? (LAS uint32_t *)&C->ctr : nullptr,
+                   (LAS uint32_t *)&C->ovf, best, nbr, adj, nscored);
+#ifdef DTR_PROFILE
+    const int64_t w2 = (int64_t)__builtin_readcyclecounter();
+#endif
+    if (multi) __syncthreads();
+    else wave_sync();
+#ifdef DTR_PROFILE
+    const int64_t w3 = (int64_t)__builtin_readcyclecounter();
+#endif
+    walk_listed<HC>(s.t, s.S, s.S.tst, P, s.lane, 0, uni((int32_t)C->ovf), multi ? (LAS uint32_t *)&C->ctr2 : nullptr,
+                    best, nbr, adj, nscored);
+#ifdef DTR_PROFILE
+    const int64_t w4 = (int64_t)__builtin_readcyclecounter();
+    s.prof_rounds += w2 - w1;
+    if (s.lane == 0) {
+        s.prof_slow += w3 - w2;
+        s.prof_global_nodes += w4 - w3;
+    }
+    s.prof_uf_compact += uni((int32_t)C->ovf);
+#endif
+    if (multi) {
+        __syncthreads();
+        // the helpers' bests, one per lane 1..nw-1
+        const int32_t w = s.lane < s.nw ? s.lane : 0;
+        const bool h = w >= 1 && C->res[w].have;
+        const uint64_t N = h ? C->res[w].N : 0, da = h ? C->res[w].da : 1, db = h ? C->res[w].db : 1;
+        const int32_t id = h ? C->res[w].id : 0, sl = h ? C->res[w].slot : 0;
+        if (__ballot(h)) take(best, h, h ? score_est(N, da, db) : 0.0f, N, da, db, id, sl);
+        if (w >= 1) {
+            nbr += C->res[w].nbr;
+            adj += C->res[w].adj;
+            nscored += C->res[w].scored;
+        }
+    }
+    s.nbr += nbr;
+    s.adj += adj;
+    if (approx(HC)) scored += wave_sum(nscored);
+}
+
+// A helper wavefront of a walk heuristic's workgroup: joins the simulating
+// wavefront's walk scans (the three workgroup barriers of each) until it is
+// released at the end of the simulation.
+template <int HC>
+__device__ void help_walks(const KernelArgs &a, const Slot &S, int32_t lane, int32_t wave, LAS WalkCtl *C)
+{
+    for (;;) {
+        __syncthreads();
+        if (C->cmd == CMD_DONE) break;
+        WalkParams P;
+        P.end = C->end;
+        P.both = C->both;
+        P.use_m = C->use_m;
+        P.use_s = C->use_s;
+        P.sample = C->sample;
+        P.T = C->T;
+        P.evict_no = C->evict_no;
+        P.min_size = C->min_size;
+        P.tau = C->tau;
+        P.seed = C->seed;
+        const TraceDev t = a.traces[C->trace];
+        Best best;
+        best.sc = best.lo = best.hi = 0.0f;
+        best.N = 0;
+        best.da = best.db = 1;
+        best.id = 0x7fffffff;
+        best.slot = -1;
+        best.have = 0;
+        int64_t nbr = 0, adj = 0, nscored = 0;
+        walk_lanes<HC>(t, S, S.tst, P, lane, wave * WAVE + lane, (LAS uint32_t *)&C->ctr, (LAS uint32_t *)&C->ovf,
+                       best, nbr, adj, nscored);
+        __syncthreads();
+        walk_listed<HC>(t, S, S.tst, P, lane, wave, uni((int32_t)C->ovf), (LAS uint32_t *)&C->ctr2, best, nbr, adj,
+                        nscored);
+        WaveBest r = wave_best(best);
+        r.nbr = wave_sum(nbr);
+        r.adj = wave_sum(adj);
+        r.scored = wave_sum(nscored);
+        if (lane == 0) *(WaveBest *)&C->res[wave] = r;
+        __syncthreads();
     }
 }
 
@@ -1107,7 +1518,6 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
     best.slot = -1;
     best.have = 0;
     constexpr int U = Round<HC>::value;
-    if (cls(HC) == HC_WALK && (uint64_t)s.epoch + (uint64_t)end + 2 >= 0xffffffffull) clear_stamps(s);
     // quads of the next round when it lies in global memory, read one round
     // ahead so that their latency overlaps this round's scoring (scans start
     // in LDS, so every global round has been read ahead by its predecessor)
@@ -1327,7 +1737,7 @@ __device__ __forceinline__ bool allocate(Sim &s, int64_t sz)
 #ifdef DTR_PROFILE
         const int64_t c0_ = (int64_t)__builtin_readcyclecounter();
         s.prof_scans++;
-        s.prof_rounds += (s.pool_end + WAVE * Round<HC>::value - 1) / (WAVE * Round<HC>::value);
+        if (cls(HC) != HC_WALK) s.prof_rounds += (s.pool_end + WAVE * Round<HC>::value - 1) / (WAVE * Round<HC>::value);
 #endif
         int32_t slot = -1;
         int64_t scored = 0;
@@ -1716,12 +2126,15 @@ __device__ __forceinline__ bool release(Sim &s, int32_t o)
 }
 
 template <int HC>
-__device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const Slot &S, int32_t lane)
+__device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const Slot &S, int32_t lane, LAS WalkCtl *ctl)
 {
     Sim s;
     const SpecDev sp = a.specs[sim];
     s.t = a.traces[sp.trace];
     s.S = S;
+    s.trace_idx = sp.trace;
+    s.nw = cls(HC) == HC_WALK ? (int32_t)a.L.walk_waves : 1;
+    s.ctl = ctl;
     s.h = sp.heuristic;
     s.policy = sp.policy;
     s.search = sp.search;
@@ -1750,7 +2163,6 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.uf_limit = UF_LDS;
     s.status = ST_OK;
     s.cur_op = 0;
-    s.epoch = 0;
     s.evict_no = 0;
     s.total = s.base = s.remat_cost = s.executed = s.remats = s.evictions = s.eager = s.scores = 0;
     s.nbr = s.adj = 0;
@@ -1766,7 +2178,6 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
         s.S.tst[x] = ts_make((gld(s.t.flags + x) & FLAG_CONST) ? S_CONST : S_UNCOMPUTED, 0, 0);
     if (cls(HC) != HC_EQ && s.policy == POLICY_BANISH)
         for (int32_t x = lane; x < n; x += WAVE) s.S.pending[x] = 0;
-    if (cls(HC) == HC_WALK) clear_stamps(s);
     if (cls(HC) == HC_EQ && lane == 0) {
         UfNode z;
         z.cost = 0;
@@ -1774,7 +2185,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
         z.size = 1;
         s.S.nodes[0] = z;
     }
-    __syncthreads();
+    slot_sync<HC>();
     s.mem = s.t.const_mem;
     s.peak = s.mem;
 
@@ -1841,26 +2252,61 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
         r.failed_op = s.status == ST_OK ? -1 : s.cur_op;
         a.results[sim] = r;
     }
-    __syncthreads();
+    if (s.nw > 1) {
+        // release the helper wavefronts from this simulation
+        if (lane == 0) ctl->cmd = CMD_DONE;
+        __syncthreads();
+    } else {
+        slot_sync<HC>();
+    }
 }
 
+// One simulation per workgroup at a time, taken from the work counter.  The
+// workgroups of the walk heuristics may hold helper wavefronts (a.L.walk_waves
+// in all) that join the simulating wavefront's walk scans; every wavefront
+// learns the next simulation from the control block after a workgroup
+// barrier, so all of them leave the loop together.
 template <int HC>
-__global__ void __launch_bounds__(WAVE) replay_kernel(KernelArgs a)
+__global__ void __launch_bounds__(cls(HC) == HC_WALK ? MAX_WALK_WAVES * WAVE : WAVE) replay_kernel(KernelArgs a)
 {
-    __shared__ UfNode lds_nodes[cls(HC) == HC_EQ ? UF_LDS : 1];
+    // union-find nodes (h_DTR^eq), or the walk control block (walk heuristics)
+    __shared__ UfNode lds_nodes[cls(HC) == HC_EQ ? UF_LDS : (sizeof(WalkCtl) + sizeof(UfNode) - 1) / sizeof(UfNode)];
     __shared__ PoolSlot lds_pool[POOL_LDS];
-    const int32_t lane = threadIdx.x;
+    const int32_t lane = (int32_t)threadIdx.x & (WAVE - 1);
+    const int32_t wave = uni((int32_t)threadIdx.x / WAVE);
+    const int32_t nw = cls(HC) == HC_WALK ? (int32_t)a.L.walk_waves : 1;
     Slot S = slot_at(a, blockIdx.x);
     S.nodes.lds = lds_nodes;
     S.nodes.lds_l = (LAS UfNode *)lds_nodes;
     S.lpool = lds_pool;
     S.lpool_l = (LAS PoolSlot *)lds_pool;
+    LAS WalkCtl *ctl = (LAS WalkCtl *)lds_nodes;
+    if (cls(HC) == HC_WALK) {
+        // visited bitmaps start clear (every walk clears what it set)
+        // (the flags 16 bytes at a time: vis_bytes is a multiple of 16)
+        GAS u32x4 *V = (GAS u32x4 *)(S.visb + (size_t)(wave * WAVE) * (size_t)S.vis_bytes);
+        for (size_t i = lane; i < (size_t)WAVE * (size_t)S.vis_bytes / 16; i += WAVE) V[i] = u32x4{0u, 0u, 0u, 0u};
+        GAS uint32_t *B = S.bigvis + (size_t)wave * (size_t)S.vis_words;
+        for (int32_t i = lane; i < S.vis_words; i += WAVE) B[i] = 0u;
+        wave_sync();
+    }
     for (;;) {
         uint32_t k = 0;
-        if (lane == 0) k = atomicAdd(a.queue, 1u);
-        k = (uint32_t)uni((int32_t)k);
+        if (wave == 0 && lane == 0) k = atomicAdd(a.queue, 1u);
+        if (nw > 1) {
+            if (wave == 0 && lane == 0) ctl->sim = (int32_t)k;
+            __syncthreads();
+            k = (uint32_t)uni(ctl->sim);
+        } else {
+            k = (uint32_t)uni((int32_t)k);
+        }
         if (k >= (uint32_t)a.n_sims) break;
-        run_sim<HC>(a, a.order[k], S, lane);
+        if constexpr (cls(HC) == HC_WALK) {
+            if (wave == 0) run_sim<HC>(a, a.order[k], S, lane, ctl);
+            else help_walks<HC>(a, S, lane, wave, ctl);
+        } else {
+            run_sim<HC>(a, a.order[k], S, lane, ctl);
+        }
     }
 }
 
@@ -1911,12 +2357,13 @@ extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t
     hipLaunchKernelGGL(reset_kernel, dim3(1), dim3(WAVE), 0, stream, args[0].queue, N_GROUPS);
     const dim3 blk(WAVE);
     if (args[0].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_EQ>, dim3(args[0].n_slots), blk, 0, stream, args[0]);
-    if (args[1].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_WALK>, dim3(args[1].n_slots), blk, 0, stream, args[1]);
+    const dim3 wblk(WAVE * (uint32_t)args[1].L.walk_waves);
+    if (args[1].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_WALK>, dim3(args[1].n_slots), wblk, 0, stream, args[1]);
     if (args[2].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_SIMPLE>, dim3(args[2].n_slots), blk, 0, stream, args[2]);
     if (args[3].n_sims > 0)
         hipLaunchKernelGGL(replay_kernel<HC_EQ | HC_APPROX>, dim3(args[3].n_slots), blk, 0, stream, args[3]);
     if (args[4].n_sims > 0)
-        hipLaunchKernelGGL(replay_kernel<HC_WALK | HC_APPROX>, dim3(args[4].n_slots), blk, 0, stream, args[4]);
+        hipLaunchKernelGGL(replay_kernel<HC_WALK | HC_APPROX>, dim3(args[4].n_slots), wblk, 0, stream, args[4]);
     if (args[5].n_sims > 0)
         hipLaunchKernelGGL(replay_kernel<HC_SIMPLE | HC_APPROX>, dim3(args[5].n_slots), blk, 0, stream, args[5]);
     return hipGetLastError();

@@ -23,6 +23,12 @@ DTR_OK, DTR_EINVAL, DTR_ETRACE, DTR_EHIP, DTR_ESTATE = 0, -1, -2, -3, -4
 STATUS_OK, STATUS_OOM, STATUS_CLOCK_OVERFLOW, STATUS_CAPACITY = 0, 1, 2, 3
 OPT_LOG_NO_LDS = 1
 OPT_STATIC_SCRATCH = 2
+OPT_WALK_QUEUE_SMALL = 4
+
+
+def opt_walk_waves(w: int) -> int:
+    """Option bits: w wavefronts per workgroup of the walk heuristics."""
+    return w << 8
 
 RESULT_FIELDS = ["total_cost", "base_cost", "remat_cost", "peak_memory", "final_memory",
                  "n_executed_ops", "n_remats", "n_evictions", "n_eager_evictions", "n_scores",
@@ -255,9 +261,9 @@ class Simulator:
             pass
 
 
-def run(traces, specs, device: str = "cuda", slots: int = 0) -> np.ndarray:
+def run(traces, specs, device: str = "cuda", slots: int = 0, flags: int = 0) -> np.ndarray:
     """Simulate every spec on the GPU and return the results (numpy)."""
-    sim = Simulator(traces, specs, device=device, slots=slots)
+    sim = Simulator(traces, specs, device=device, slots=slots, flags=flags)
     try:
         sim.run()
         return sim.results()

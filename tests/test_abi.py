@@ -244,7 +244,7 @@ def test_static_scratch_option_limits():
         D.dtr_log_workspace_bytes([W.log_from_trace(W.chain_trace(4))], sp,
                                   {"slots": 0, "flags": D.OPT_STATIC_SCRATCH})
     assert e.value.code == D.DTR_EINVAL
-    big = W.chain_trace(300_000)                   # 600k tensors: lane-private walk state alone > 256 MiB
+    big = W.chain_trace(600_000)                   # 1.2M tensors: pool, remat stack and walk state > 256 MiB
     with pytest.raises(D.DtrError) as e:
         D.dtr_sim_workspace_bytes([big], sp, {"slots": 0, "flags": D.OPT_STATIC_SCRATCH})
     assert e.value.code == D.DTR_EINVAL and "static scratch" in str(e.value)

@@ -215,15 +215,25 @@ def test_random_dag_replica_all_budgets(gpu, oracle_lib):
     compare(gpu.run(w.traces, w.specs), oracle_lib.run(w.traces, w.specs), w.specs, "randdag1k")
 
 
-def test_random_dag_full_size_sampled(gpu, oracle_lib):
-    """The full 100k-forward-op trace (200k ops), in the launch configuration of
-    the full batch, on the sampled budgets the exact-e* oracle finishes in
-    seconds (the top of the 1024-budget range)."""
+def test_random_dag_full_size_goldens(gpu):
+    """The full 100k-forward-op random DAG (200k ops, h_DTR with exact e*)
+    against stored oracle results (tests/golden/randdag100k_oracle.json,
+    written by a script that calls only the oracle): the stored budgets from
+    48% to 100% of the peak, in one launch of the batch's kernel shape (8
+    wavefronts per workgroup).  The lower stored budgets (5% to 34%) take the
+    GPU several minutes per simulation and are not run here."""
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "randdag100k_oracle.json")))
     w = W.make_config("randdag100k")
-    pick = np.array([1023, 1012, 1000])
+    assert w.traces[0].digest() == g["trace_sha256"]
+    rows = [r for r in g["sims"] if r["index"] >= 460]
+    pick = np.array([r["index"] for r in rows])
     specs = w.specs[pick]
-    print(f"random dag full size: sims {pick.tolist()}", flush=True)
-    compare(gpu.run(w.traces, specs), oracle_lib.run(w.traces, specs), specs, "randdag100k-sampled")
+    print(f"random dag full size: budget indices {pick.tolist()}", flush=True)
+    got = gpu.run(w.traces, specs)
+    bad = [(r["index"], f, int(got[f][k]), v) for k, r in enumerate(rows) for f, v in r["result"].items()
+           if int(got[f][k]) != v]
+    assert not bad, f"randdag100k goldens: {bad[:6]}"
 
 
 def test_treelstm_full_batch_sampled(gpu, oracle_lib):
@@ -379,3 +389,38 @@ def test_near_ties_at_large_magnitude(gpu, oracle_lib):
     ref = oracle_lib.run(traces, specs)
     assert (ref["status"] == 0).all() and int(ref["n_evictions"].min()) > 0
     compare(gpu.run(traces, specs), ref, specs, "near ties")
+
+
+WALK_H = [W.H_DTR, W.H_ESTAR, W.H_MSPS, W.h_family(W.C_ESTAR, 1, 0), W.h_family(W.C_ESTAR, 0, 0)]
+
+
+@pytest.mark.parametrize("waves,small", [(1, True), (2, False), (8, False), (8, True)])
+def test_walk_workgroup_shapes(gpu, oracle_lib, waves, small):
+    """The e* / e_R walks with 1, 2 or 8 wavefronts sharing each eviction
+    scan, and with lane queues of 16 members (so that larger neighbourhoods
+    take the whole-wavefront walk), on random programs, the ResNet trace and
+    a chain of 300 layers, every walk heuristic and policy."""
+    traces, rows = [], []
+    for s in range(24):
+        tr = W.random_program(2100 + s, n_ops=20 + (s * 23) % 150, n_const=s % 3, backward=s % 2 == 0,
+                              max_in=1 + s % 4, max_size=1 + s % 25, max_cost=1 + s % 9)
+        traces.append(tr)
+        peak = W.natural_peak(tr)
+        for h in WALK_H:
+            for frac in (0.25, 0.5, 0.8):
+                rows.append((len(traces) - 1, h, max(1, int(peak * frac)), s, W.POLICY_EAGER if s % 3 else W.POLICY_BANISH))
+    rn = W.make_config("resnet50blk")
+    traces.append(rn.traces[0])
+    for k in range(0, 256, 51):
+        rows.append((len(traces) - 1, W.H_DTR, int(rn.specs["budget"][k]), 0))
+    traces.append(W.chain_trace(300))
+    for b in (2 * 18, 60):
+        for h in (W.H_DTR, W.H_ESTAR, W.H_MSPS):
+            rows.append((len(traces) - 1, h, b, 0))
+    specs = specs_of(rows)
+    flags = gpu.opt_walk_waves(waves) | (gpu.OPT_WALK_QUEUE_SMALL if small else 0)
+    print(f"walk shapes {waves} waves, small queues {small}: {len(specs)} sims", flush=True)
+    ref = oracle_lib.run(traces, specs)
+    if small:
+        assert int(ref["n_nbr_visits"].max()) > 0
+    compare(gpu.run(traces, specs, flags=flags), ref, specs, f"walk {waves} waves small={small}")
