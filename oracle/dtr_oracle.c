@@ -199,8 +199,25 @@ static int graph_build(graph *g, const oracle_trace *tr)
 
 /* ------------------------------------------------------------ simulator -- */
 
+typedef struct sim sim;
+
+/* How the simulator sees the dependency graph: parents and children of a
+ * node and its local cost c0, and what banishing a released node does.  A
+ * trace has the static graph of its operators (below); the log section
+ * supplies the storage graph of a replay, which grows as operators first
+ * run. */
 typedef struct {
+    int64_t (*n_par)(const sim *s, int32_t u);
+    int32_t (*par_at)(const sim *s, int32_t u, int64_t k);
+    int64_t (*n_ch)(const sim *s, int32_t u);
+    int32_t (*ch_at)(const sim *s, int32_t u, int64_t k);
+    int64_t (*c0_of)(const sim *s, int32_t u);
+    void (*try_banish)(sim *s, int32_t t);
+} graph_view;
+
+struct sim {
     const graph *g;
+    const graph_view *view;
     const oracle_trace *tr;
     int heuristic;
     int policy;
@@ -242,7 +259,7 @@ typedef struct {
     int32_t *queue;
 
     oracle_probe *probe;
-} sim;
+};
 
 static int32_t uf_new(sim *s)
 {
@@ -305,15 +322,12 @@ static int is_evictable(const sim *s, int32_t t)
            !(s->tr->tensor_flags[t] & O_FLAG_CONSTANT);
 }
 
-static void log_try_banish(sim *s, int32_t st);
-
 /* Banish t if none of its children is evicted and no operation in progress
  * holds it (Appendix C.4): its memory is reclaimed if resident, it leaves the
  * graph for good, and every resident child is pinned.  Otherwise t stays
  * pending and is retried when one of its children is rematerialized. */
-static void try_banish(sim *s, int32_t t)
+static void trace_try_banish(sim *s, int32_t t)
 {
-    if (s->logp) { log_try_banish(s, t); return; }
     const graph *g = s->g;
     int blocked = s->locks[t] > 0;
     for (int64_t e = g->ch_off[t]; e < g->ch_off[t + 1] && !blocked; e++)
@@ -327,6 +341,33 @@ static void try_banish(sim *s, int32_t t)
         if (s->state[g->ch[e]] == ST_RESIDENT) s->pinned[g->ch[e]] = 1;
 }
 
+/* A trace's graph is static: the parents of u are the inputs of its parent
+ * operation, its children the outputs of the operations reading u, its cost
+ * c0 that of its parent operation. */
+static int64_t trace_n_par(const sim *s, int32_t u)
+{
+    int32_t o = s->g->producer[u];
+    return o < 0 ? 0 : s->tr->op_input_offsets[o + 1] - s->tr->op_input_offsets[o];
+}
+static int32_t trace_par_at(const sim *s, int32_t u, int64_t k)
+{
+    return s->tr->op_inputs[s->tr->op_input_offsets[s->g->producer[u]] + k];
+}
+static int64_t trace_n_ch(const sim *s, int32_t u) { return s->g->ch_off[u + 1] - s->g->ch_off[u]; }
+static int32_t trace_ch_at(const sim *s, int32_t u, int64_t k) { return s->g->ch[s->g->ch_off[u] + k]; }
+static int64_t trace_c0_of(const sim *s, int32_t u) { return s->g->c0[u]; }
+
+static const graph_view TRACE_VIEW = {trace_n_par, trace_par_at, trace_n_ch, trace_ch_at, trace_c0_of,
+                                      trace_try_banish};
+
+/* the graph as the current simulation sees it */
+static int64_t n_par(const sim *s, int32_t u) { return s->view->n_par(s, u); }
+static int32_t par_at(const sim *s, int32_t u, int64_t k) { return s->view->par_at(s, u, k); }
+static int64_t n_ch(const sim *s, int32_t u) { return s->view->n_ch(s, u); }
+static int32_t ch_at(const sim *s, int32_t u, int64_t k) { return s->view->ch_at(s, u, k); }
+static int64_t c0_of(const sim *s, int32_t u) { return s->view->c0_of(s, u); }
+static void try_banish(sim *s, int32_t t) { s->view->try_banish(s, t); }
+
 /* deallocation of t after its last reader (Section 2, Appendix C.5) */
 static void release(sim *s, int32_t t)
 {
@@ -336,32 +377,6 @@ static void release(sim *s, int32_t t)
         try_banish(s, t);
     }
 }
-
-/* Neighbours and local cost of node u.  A trace's graph is static: parents
- * are the inputs of u's parent operation, children the outputs of the
- * operations reading u.  A log's storage graph is the one that exists now. */
-static int64_t n_par(const sim *s, int32_t u)
-{
-    if (s->logp) return s->npar[u];
-    int32_t o = s->g->producer[u];
-    return o < 0 ? 0 : s->tr->op_input_offsets[o + 1] - s->tr->op_input_offsets[o];
-}
-static int32_t par_at(const sim *s, int32_t u, int64_t k)
-{
-    if (s->logp) return s->dpar[u][k];
-    return s->tr->op_inputs[s->tr->op_input_offsets[s->g->producer[u]] + k];
-}
-static int64_t n_ch(const sim *s, int32_t u)
-{
-    if (s->logp) return s->nch[u];
-    return s->g->ch_off[u + 1] - s->g->ch_off[u];
-}
-static int32_t ch_at(const sim *s, int32_t u, int64_t k)
-{
-    if (s->logp) return s->dch[u][k];
-    return s->g->ch[s->g->ch_off[u] + k];
-}
-static int64_t c0_of(const sim *s, int32_t u) { return s->logp ? s->dc0[u] : s->g->c0[u]; }
 
 /* e_R(x) (Section 4.1): evicted tensors reachable from x through evicted
  * parents only, i.e. those that rematerializing x would rematerialize.
@@ -771,6 +786,7 @@ static int run_one(const oracle_trace *tr, const graph *g, const oracle_spec *sp
     sim s;
     memset(&s, 0, sizeof(s));
     s.g = g;
+    s.view = &TRACE_VIEW;
     s.tr = tr;
     s.heuristic = sp->heuristic;
     s.policy = sp->policy;
@@ -897,6 +913,7 @@ int64_t oracle_estar(const oracle_trace *tr, const uint8_t *state, int32_t x, in
     sim s;
     memset(&s, 0, sizeof(s));
     s.g = &g;
+    s.view = &TRACE_VIEW;
     s.tr = tr;
     size_t nn = (size_t)(tr->n_tensors > 0 ? tr->n_tensors : 1);
     s.state = malloc(nn);
@@ -1338,6 +1355,17 @@ static void log_try_banish(sim *s, int32_t st)
     }
 }
 
+/* A replay's storage graph as of now (Appendix C.2, indexed by time): the
+ * parents and children created so far and the cost of the tensors created so
+ * far. */
+static int64_t log_n_par(const sim *s, int32_t u) { return s->npar[u]; }
+static int32_t log_par_at(const sim *s, int32_t u, int64_t k) { return s->dpar[u][k]; }
+static int64_t log_n_ch(const sim *s, int32_t u) { return s->nch[u]; }
+static int32_t log_ch_at(const sim *s, int32_t u, int64_t k) { return s->dch[u][k]; }
+static int64_t log_c0_of(const sim *s, int32_t u) { return s->dc0[u]; }
+
+static const graph_view LOG_VIEW = {log_n_par, log_par_at, log_n_ch, log_ch_at, log_c0_of, log_try_banish};
+
 static int push32(int32_t **v, int64_t *n, int64_t *cap, int32_t e)
 {
     if (*n == *cap) {
@@ -1462,6 +1490,7 @@ static int run_one_log(const log_prog *L, const oracle_spec *sp, int64_t *result
     sim s;
     memset(&s, 0, sizeof(s));
     s.g = &L->g;
+    s.view = &LOG_VIEW;
     s.tr = &L->meta;
     s.logp = L;
     s.heuristic = sp->heuristic;
