@@ -22,7 +22,8 @@
 #include "host.h"
 #include "layout.h"
 
-extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream);
+extern "C" hipError_t dtr_launch_reset(uint32_t *queue, hipStream_t stream);
+extern "C" hipError_t dtr_launch_group(const dtr::KernelArgs *a, int32_t group, hipStream_t stream);
 extern "C" hipError_t dtr_static_scratch(void **ptr, size_t *bytes);
 
 namespace dtrhost {
@@ -401,7 +402,20 @@ struct dtr_sim {
     hipStream_t last_stream = nullptr;
     bool ran = false;
     int32_t n_sims = 0;
-    ~dtr_sim() { dtrhost::log_plan_free(log); }
+    // a batch with simulations in several groups runs each group's kernel on
+    // a stream of its own (default priority), forked from and joined back to
+    // the caller's stream by events, so that the groups overlap
+    hipStream_t aux[dtr::N_GROUPS] = {};
+    hipEvent_t fork = nullptr, join[dtr::N_GROUPS] = {};
+    ~dtr_sim()
+    {
+        dtrhost::log_plan_free(log);
+        for (int g = 0; g < dtr::N_GROUPS; g++) {
+            if (aux[g]) (void)hipStreamDestroy(aux[g]);
+            if (join[g]) (void)hipEventDestroy(join[g]);
+        }
+        if (fork) (void)hipEventDestroy(fork);
+    }
 };
 
 extern "C" {
@@ -486,6 +500,20 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec
     }
     if (n_sims) std::memcpy(H + p.order_off, p.order.data(), sizeof(int32_t) * n_sims);
     hipStream_t st = (hipStream_t)stream;
+    int groups = 0;
+    for (int c = 0; c < dtr::N_GROUPS; c++) groups += p.class_count[c] > 0;
+    if (groups > 1) {
+        bool okk = hipEventCreateWithFlags(&h->fork, hipEventDisableTiming) == hipSuccess;
+        for (int c = 0; okk && c < dtr::N_GROUPS; c++)
+            if (p.class_count[c] > 0)
+                okk = hipStreamCreateWithFlags(&h->aux[c], hipStreamNonBlocking) == hipSuccess &&
+                      hipEventCreateWithFlags(&h->join[c], hipEventDisableTiming) == hipSuccess;
+        if (!okk) {
+            rc = fail(DTR_EHIP, "stream or event creation failed");
+            delete h;
+            return rc;
+        }
+    }
     if (hipMemcpyAsync(h->ws, H, p.tables_bytes, hipMemcpyHostToDevice, st) != hipSuccess ||
         hipStreamSynchronize(st) != hipSuccess) {
         rc = fail(DTR_EHIP, "upload of %zu bytes failed", p.tables_bytes);
@@ -501,33 +529,70 @@ int dtr_sim_create(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec
 namespace {
 
 // Enqueue the replay kernels of a trace batch: slots from `slots` (at most
-// `max_slots` resident simulations), work counters at `queue`.
+// `max_slots` resident simulations), work counters at `queue`.  When several
+// groups have simulations, the slots are shared out in proportion to their
+// simulations and each group's kernel runs on its own stream.
 int launch_traces(dtr_sim *h, void *stream, uint8_t *slots, uint32_t *queue, int64_t max_slots)
 {
     const Plan &p = h->plan;
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t total = std::max<int64_t>(1, std::min<int64_t>(p.n_slots, max_slots));
+    int32_t groups[dtr::N_GROUPS], ng = 0;
+    for (int c = 0; c < dtr::N_GROUPS; c++)
+        if (p.class_count[c] > 0) groups[ng++] = c;
+    // concurrent groups take disjoint slot ranges, each at least one slot;
+    // with fewer slots than groups the groups run one after another on the
+    // caller's stream, each over every slot
+    const bool fan = ng > 1 && h->fork && total >= ng;
+    int64_t share[dtr::N_GROUPS] = {0, 0, 0, 0, 0, 0};
+    for (int k = 0; k < ng; k++) {
+        const int c = groups[k];
+        share[c] = !fan ? total : std::max<int64_t>(1, total * p.class_count[c] / std::max(1, h->n_sims));
+        share[c] = std::min<int64_t>(share[c], p.class_count[c]);
+    }
+    for (; fan;) {      // trim the largest shares until the ranges fit
+        int64_t sum = 0;
+        int big = -1;
+        for (int k = 0; k < ng; k++) {
+            sum += share[groups[k]];
+            if (share[groups[k]] > 1 && (big < 0 || share[groups[k]] > share[big])) big = groups[k];
+        }
+        if (sum <= total) break;
+        share[big]--;
+    }
     dtr::KernelArgs a[dtr::N_GROUPS];
     int32_t first = 0;
-    const int32_t cap = (int32_t)std::max<int64_t>(1, std::min<int64_t>(p.n_slots, max_slots));
+    int64_t off = 0;
     for (int c = 0; c < dtr::N_GROUPS; c++) {
         a[c].traces = (const dtr::TraceDev *)(h->ws + p.desc_off);
         a[c].specs = (const dtr::SpecDev *)(h->ws + p.spec_off);
         a[c].order = (const int32_t *)(h->ws + p.order_off) + first;
         a[c].results = (dtr::ResultDev *)(h->ws + p.result_off);
         a[c].queue = queue + c;
-        a[c].slots = slots;
+        a[c].slots = slots + (size_t)off * (size_t)p.L.bytes;
         a[c].L = p.L;
         a[c].n_sims = p.class_count[c];
-        a[c].n_slots = std::max(1, std::min(cap, p.class_count[c]));
+        a[c].n_slots = (int32_t)std::max<int64_t>(1, share[c]);
         a[c].prof = nullptr;
 #ifdef DTR_PROFILE
         a[c].prof = (int64_t *)(h->ws + p.prof_off);
 #endif
         first += p.class_count[c];
+        if (fan) off += share[c];
     }
-    hipError_t e = dtr_launch_replay(a, (hipStream_t)stream);
+    hipError_t e = dtr_launch_reset(queue, st);
+    if (e == hipSuccess && fan) e = hipEventRecord(h->fork, st);
+    for (int k = 0; e == hipSuccess && k < ng; k++) {
+        const int c = groups[k];
+        hipStream_t gs = fan && k > 0 ? h->aux[c] : st;
+        if (gs != st) e = hipStreamWaitEvent(gs, h->fork, 0);
+        if (e == hipSuccess) e = dtr_launch_group(&a[c], c, gs);
+        if (e == hipSuccess && gs != st) e = hipEventRecord(h->join[c], gs);
+        if (e == hipSuccess && gs != st) e = hipStreamWaitEvent(st, h->join[c], 0);
+    }
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     h->ran = true;
-    h->last_stream = (hipStream_t)stream;
+    h->last_stream = st;
     return DTR_OK;
 }
 

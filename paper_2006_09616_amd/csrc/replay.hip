@@ -2347,24 +2347,31 @@ extern "C" hipError_t dtr_static_scratch(void **ptr, size_t *bytes)
     return hipSuccess;
 }
 
-// Launch entry used by the host library (same shared object): args[g] holds
-// the simulations of group g = heuristic class (union-find; neighbourhood
-// walk; none) + 3 if the search approximations are on, each with its own
-// work counter; empty groups are skipped.
-extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *args, hipStream_t stream)
+// Launch entries used by the host library (same shared object): the work
+// counters of the groups are cleared by a kernel, then each group g (heuristic
+// class: union-find; neighbourhood walk; none; + 3 with the search
+// approximations) runs its own kernel specialisation, each on the stream the
+// host gives it (the groups use disjoint slots, so they may run at once).
+extern "C" hipError_t dtr_launch_reset(uint32_t *queue, hipStream_t stream)
 {
     using namespace dtr;
-    hipLaunchKernelGGL(reset_kernel, dim3(1), dim3(WAVE), 0, stream, args[0].queue, N_GROUPS);
-    const dim3 blk(WAVE);
-    if (args[0].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_EQ>, dim3(args[0].n_slots), blk, 0, stream, args[0]);
-    const dim3 wblk(WAVE * (uint32_t)args[1].L.walk_waves);
-    if (args[1].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_WALK>, dim3(args[1].n_slots), wblk, 0, stream, args[1]);
-    if (args[2].n_sims > 0) hipLaunchKernelGGL(replay_kernel<HC_SIMPLE>, dim3(args[2].n_slots), blk, 0, stream, args[2]);
-    if (args[3].n_sims > 0)
-        hipLaunchKernelGGL(replay_kernel<HC_EQ | HC_APPROX>, dim3(args[3].n_slots), blk, 0, stream, args[3]);
-    if (args[4].n_sims > 0)
-        hipLaunchKernelGGL(replay_kernel<HC_WALK | HC_APPROX>, dim3(args[4].n_slots), wblk, 0, stream, args[4]);
-    if (args[5].n_sims > 0)
-        hipLaunchKernelGGL(replay_kernel<HC_SIMPLE | HC_APPROX>, dim3(args[5].n_slots), blk, 0, stream, args[5]);
+    hipLaunchKernelGGL(reset_kernel, dim3(1), dim3(WAVE), 0, stream, queue, N_GROUPS);
+    return hipGetLastError();
+}
+
+extern "C" hipError_t dtr_launch_group(const dtr::KernelArgs *a, int32_t group, hipStream_t stream)
+{
+    using namespace dtr;
+    if (a->n_sims <= 0) return hipSuccess;
+    const dim3 grid(a->n_slots), blk(WAVE), wblk(WAVE * (uint32_t)a->L.walk_waves);
+    switch (group) {
+    case 0: hipLaunchKernelGGL(replay_kernel<HC_EQ>, grid, blk, 0, stream, *a); break;
+    case 1: hipLaunchKernelGGL(replay_kernel<HC_WALK>, grid, wblk, 0, stream, *a); break;
+    case 2: hipLaunchKernelGGL(replay_kernel<HC_SIMPLE>, grid, blk, 0, stream, *a); break;
+    case 3: hipLaunchKernelGGL(replay_kernel<HC_EQ | HC_APPROX>, grid, blk, 0, stream, *a); break;
+    case 4: hipLaunchKernelGGL(replay_kernel<HC_WALK | HC_APPROX>, grid, wblk, 0, stream, *a); break;
+    case 5: hipLaunchKernelGGL(replay_kernel<HC_SIMPLE | HC_APPROX>, grid, blk, 0, stream, *a); break;
+    default: return hipErrorInvalidValue;
+    }
     return hipGetLastError();
 }

@@ -18,7 +18,8 @@
 #include "dtr_sim.h"
 
 namespace dtr { struct KernelArgs; struct LogKernelArgs; }
-extern "C" hipError_t dtr_launch_replay(const dtr::KernelArgs *, hipStream_t) { return hipErrorNoDevice; }
+extern "C" hipError_t dtr_launch_reset(uint32_t *, hipStream_t) { return hipErrorNoDevice; }
+extern "C" hipError_t dtr_launch_group(const dtr::KernelArgs *, int32_t, hipStream_t) { return hipErrorNoDevice; }
 extern "C" hipError_t dtr_launch_log(const dtr::LogKernelArgs *, hipStream_t) { return hipErrorNoDevice; }
 extern "C" hipError_t dtr_static_scratch(void **, size_t *) { return hipErrorNoDevice; }
 
