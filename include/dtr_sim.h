@@ -305,11 +305,14 @@ int dtr_log_create(const dtr_log *logs, int32_t n_logs,
                    void *stream, dtr_sim **out);
 
 /* How a handle's simulations occupy the device, fixed at creation:
- * n_slots          simulations that can be in flight (one workgroup each);
+ * n_slots          simulations that can be in flight (one workgroup each,
+ *                  except under exact h_DTR^eq: one wavefront each);
  * waves_per_group  wavefronts per workgroup: 1, except for operator logs
  *                  whose walk state is in LDS (up to 4) and for traces with
  *                  walk heuristics (up to 8): the first simulates, the
- *                  others join its e* / e_R walk scans;
+ *                  others join its e* / e_R walk scans; else 4 for traces
+ *                  with exact h_DTR^eq simulations (a simulation per
+ *                  wavefront);
  * lds_bytes        dynamic LDS per workgroup (0: the kernels' static LDS only,
  *                  or walk state in device memory).
  * Returns DTR_EINVAL for a NULL argument.  No device work. */

@@ -350,17 +350,23 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
 
     // grouped by heuristic class (one kernel specialisation each), then the
     // likely heaviest first: the tightest budget relative to the trace's
-    // no-eviction peak, then the longest trace
+    // no-eviction peak (in steps of 1/1024 of the peak, so that budgets set
+    // at one fraction of their traces' peaks tie), then the longest trace,
+    // then the exact ratio
     auto cls = [&](int32_t i) { return heuristic_class(sims[i].heuristic) + (sims[i].search ? 3 : 0); };
     p.order.resize(n_sims);
     std::iota(p.order.begin(), p.order.end(), 0);
     std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {
         if (cls(a) != cls(b)) return cls(a) < cls(b);
         const Derived &ta = p.traces[sims[a].trace], &tb = p.traces[sims[b].trace];
-        const unsigned __int128 ra = (unsigned __int128)(uint64_t)sims[a].budget * (uint64_t)std::max<int64_t>(1, tb.peak);
-        const unsigned __int128 rb = (unsigned __int128)(uint64_t)sims[b].budget * (uint64_t)std::max<int64_t>(1, ta.peak);
-        if (ra != rb) return ra < rb;
+        const uint64_t pa = (uint64_t)std::max<int64_t>(1, ta.peak), pb = (uint64_t)std::max<int64_t>(1, tb.peak);
+        const unsigned __int128 qa = (unsigned __int128)(uint64_t)sims[a].budget * 1024u / pa;
+        const unsigned __int128 qb = (unsigned __int128)(uint64_t)sims[b].budget * 1024u / pb;
+        if (qa != qb) return qa < qb;
         if (ta.F != tb.F) return ta.F > tb.F;
+        const unsigned __int128 ra = (unsigned __int128)(uint64_t)sims[a].budget * pb;
+        const unsigned __int128 rb = (unsigned __int128)(uint64_t)sims[b].budget * pa;
+        if (ra != rb) return ra < rb;
         return sims[a].budget < sims[b].budget;
     });
     for (int c = 0; c < dtr::N_GROUPS; c++) p.class_count[c] = 0;
@@ -701,7 +707,9 @@ int dtr_sim_launch_info(const dtr_sim *h, dtr_launch_info *out)
         dtrhost::log_plan_info(h->log, &out->n_slots, &out->waves_per_group, &out->lds_bytes);
     } else {
         out->n_slots = h->plan.n_slots;
-        out->waves_per_group = h->plan.class_count[1] + h->plan.class_count[4] > 0 ? (int32_t)h->plan.L.walk_waves : 1;
+        out->waves_per_group = h->plan.class_count[1] + h->plan.class_count[4] > 0 ? (int32_t)h->plan.L.walk_waves
+                               : h->plan.class_count[0] > 0                      ? dtr::EQ_WAVES
+                                                                                 : 1;
         if (h->plan.static_only)
             out->n_slots = (int32_t)std::max<int64_t>(1, std::min<int64_t>(
                 out->n_slots, (int64_t)((DTR_STATIC_SCRATCH_BYTES - STATIC_HEADER) / (size_t)h->plan.L.bytes)));

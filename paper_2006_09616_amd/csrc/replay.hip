@@ -414,6 +414,7 @@ struct WalkCtl {
     WaveBest res[MAX_WALK_WAVES];
 };
 enum { CMD_WALK = 1, CMD_DONE = 2 };
+constexpr int CTL_NODES = (int)((sizeof(WalkCtl) + sizeof(UfNode) - 1) / sizeof(UfNode));
 
 // Order this wavefront's LDS and global accesses (what a workgroup barrier
 // gives a one-wave workgroup) without waiting for the other wavefronts.
@@ -423,13 +424,17 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_wave_barrier();
 }
 
-// the simulating wavefront's synchronization: wavefront-local for the walk
-// heuristics (their workgroups hold helper wavefronts), a workgroup barrier
-// otherwise (one-wave workgroups)
+// wavefronts per workgroup that hold simulations of their own (each with its
+// own LDS pool and node arrays): the exact h_DTR^eq kernel's four, else one
+__host__ __device__ constexpr int lds_waves(int hc) { return hc == HC_EQ ? EQ_WAVES : 1; }
+
+// the simulating wavefront's synchronization: wavefront-local where its
+// workgroup holds other wavefronts (walk heuristics, h_DTR^eq), a workgroup
+// barrier otherwise (one-wave workgroups)
 template <int HC>
 __device__ __forceinline__ void slot_sync()
 {
-    if constexpr (cls(HC) == HC_WALK) wave_sync();
+    if constexpr (cls(HC) == HC_WALK || lds_waves(HC) > 1) wave_sync();
     else __syncthreads();
 }
 
@@ -601,9 +606,9 @@ __device__ __forceinline__ void uf_compact(Sim &s)
 #ifdef DTR_PROFILE
     s.prof_uf_compact++;
 #endif
-    __syncthreads();
+    wave_sync();
     for (int32_t i = lane; i < s.uf_n; i += WAVE) R[i] = -1;
-    __syncthreads();
+    wave_sync();
     for (int32_t x = lane; x < n; x += WAVE) {
         const uint64_t w = s.S.tst[x];
         const int32_t v = ts_sw(w);
@@ -614,14 +619,14 @@ __device__ __forceinline__ void uf_compact(Sim &s)
             R[r] = 0;
         }
     }
-    __syncthreads();
+    wave_sync();
     int32_t kept = 1;                    // node 0 stays the null node
     for (int32_t base = 0; base < s.uf_n; base += WAVE) {
         const int32_t i = base + lane;
         const bool keep = i > 0 && i < s.uf_n && R[i] == 0;
         const int64_t c = keep ? N[i].cost : 0;
         const uint64_t m = __ballot(keep);
-        __syncthreads();
+        wave_sync();
         if (keep) {
             const int32_t ni = kept + lane_rank(m);
             R[i] = ni;
@@ -632,13 +637,13 @@ __device__ __forceinline__ void uf_compact(Sim &s)
             N[ni] = nd;
         }
         kept += __popcll(m);
-        __syncthreads();
+        wave_sync();
     }
     for (int32_t x = lane; x < n; x += WAVE) {
         const uint64_t w = s.S.tst[x];
         if (ts_sw(w) >= 0) s.S.tst[x] = ts_make(R[ts_pos(w)], 0, ts_locks(w));
     }
-    __syncthreads();
+    wave_sync();
     s.uf_n = kept;
     // stay inside LDS while the live sets fit comfortably, else double
     s.uf_limit = kept + 256 <= UF_LDS ? UF_LDS : min(UF_LDS + s.S.ucap, 2 * kept + 256);
@@ -652,7 +657,7 @@ __device__ __forceinline__ void uf_compact(Sim &s)
             ps.deg = deg;
         }
     }
-    __syncthreads();
+    wave_sync();
 }
 
 // ------------------------------------------------------------ eviction --
@@ -1501,14 +1506,195 @@ __device__ void help_walks(const KernelArgs &a, const Slot &S, int32_t lane, int
     }
 }
 
+// Score the pool rounds of a scan (each WAVE * U entries) into this
+// wavefront's per-lane bests; `bad` is set on a broken forest.  Rounds in
+// global memory are read one round ahead, so that their latency overlaps the
+// scoring of the round before (scans start in LDS).
 template <int HC>
-__device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filter &F, int64_t &scored)
+__device__ __forceinline__ void scan_rounds(Sim &s, const Filter &F, Best &best, int64_t &scored, bool &bad)
 {
     const int32_t end = s.pool_end;
     const int32_t lane = s.lane;
     const int64_t T = s.T;
     const LAS i32x4 *L4 = (const LAS i32x4 *)s.S.lpool_l;
     const GAS i32x4 *G4 = (const GAS i32x4 *)s.S.gpool;
+    constexpr int U = Round<HC>::value;
+    static_assert(POOL_LDS > 0, "the first round of a scan lies in LDS");
+    i32x4 P0[U], P1[U], PC[U][KQ];
+    for (int32_t base = 0; base < end; base += WAVE * U) {
+        int32_t id[U], pd[U];
+        uint32_t slot[U];
+        int64_t last[U], size[U], c0[U];
+        int32_t ab[U];
+        int32_t nb[U][K];
+        bool ok[U];
+        // level 1: the 16-byte quads of each slot, all issued together, from
+        // LDS or global memory (a round never straddles the two)
+        i32x4 Q0[U], Q1[U], QC[U][KQ];
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int32_t i = base + u * WAVE + lane;
+            slot[u] = (uint32_t)(i < end ? i : base);
+        }
+        if (base < POOL_LDS) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                Q0[u] = L4[PQ * slot[u]];
+                Q1[u] = L4[PQ * slot[u] + 1];
+#pragma unroll
+                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                Q0[u] = P0[u];
+                Q1[u] = P1[u];
+#pragma unroll
+                for (int k = 0; k < KQ; k++) QC[u][k] = PC[u][k];
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            const int32_t i = base + u * WAVE + lane;
+            const i32x4 q0 = Q0[u], q1 = Q1[u];
+            id[u] = i < end ? q0.x : -1;
+            pd[u] = q0.y;
+            last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
+            size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
+            c0[u] = (int64_t)q1.z;
+            ab[u] = q1.w;
+#pragma unroll
+            for (int k = 0; k < KQ; k++) {
+                nb[u][4 * k] = QC[u][k].x;
+                nb[u][4 * k + 1] = QC[u][k].y;
+                nb[u][4 * k + 2] = QC[u][k].z;
+                nb[u][4 * k + 3] = QC[u][k].w;
+            }
+            ok[u] = id[u] >= 0;
+            if (approx(HC)) {
+                ok[u] = ok[u] && (uint64_t)size[u] >= F.min_size;
+                if (F.sample) ok[u] = ok[u] && sample_draw(s, id[u]) < F.tau;
+            }
+        }
+        const int32_t nbase = base + WAVE * U;
+        if (nbase < end && nbase >= POOL_LDS) {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int32_t i = nbase + u * WAVE + lane;
+                const uint32_t ns = (uint32_t)(i < end ? i : nbase);
+                P0[u] = G4[PQ * ns];
+                P1[u] = G4[PQ * ns + 1];
+#pragma unroll
+                for (int k = 0; k < KQ; k++) PC[u][k] = cls(HC) == HC_EQ ? G4[PQ * ns + 2 + k] : 0;
+            }
+        }
+        uint64_t N[U], DA[U], DB[U];
+        if (cls(HC) == HC_EQ) {
+            const bool lds_nodes = s.uf_n <= UF_LDS;
+            // level 2: every cached node (unused entries hold node 0, the null
+            // node); level 3: its parent, so nodes one merge away resolve too
+            int64_t sum[U], ev[U];
+            bool slow[U];
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                const int32_t c = pd[u] & 0xFF;
+                // roots are their own parent, so the node two hops along (n2)
+                // is the set root whenever the cached node is at most one
+                // merge away from it; its cost is used unconditionally
+                bool deep = false;
+                // cache entries at or beyond every lane's count hold the null
+                // node (cost 0, its own root) and are skipped when the whole
+                // wave allows it
+                if (lds_nodes) {
+                    const LAS UfNode *NL = s.S.nodes.lds_l;
+                    if (!__ballot(c > 2)) sum[u] = cached_sum<2>(NL, nb[u], deep);
+                    else if (!__ballot(c > 4)) sum[u] = cached_sum<4>(NL, nb[u], deep);
+                    else sum[u] = cached_sum<K>(NL, nb[u], deep);
+                } else {
+                    int32_t r[K];
+                    int64_t cost[K];
+#pragma unroll
+                    for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
+#pragma unroll
+                    for (int k = 0; k < K; k++) {
+                        const UfNode n2 = s.S.nodes[r[k]];
+                        cost[k] = n2.cost;
+                        deep |= n2.parent != r[k];
+                    }
+                    int64_t t = 0;
+#pragma unroll
+                    for (int k = 0; k < K; k++) {
+                        bool dup = false;
+#pragma unroll
+                        for (int j = 0; j < k; j++) dup |= r[j] == r[k];
+                        t += dup ? 0 : cost[k];
+                    }
+                    sum[u] = t;
+                }
+                ev[u] = c;
+                slow[u] = ok[u] && (c > K || deep);
+            }
+            // rare: overflowed cache or a merged-away node -- exact recount
+            bool any_slow = false;
+#pragma unroll
+            for (int u = 0; u < U; u++) any_slow |= slow[u];
+#ifdef DTR_PROFILE
+            {
+                int32_t ns = 0;
+#pragma unroll
+                for (int u = 0; u < U; u++) ns += slow[u] ? 1 : 0;
+                s.prof_slow += ns;     // per lane; reduced at the end
+                for (int u = 0; u < U; u++) s.prof_global_nodes += ok[u] && (pd[u] & 0xFF) > K ? 1 : 0;
+            }
+#endif
+            if (__ballot(any_slow)) {
+                if (lds_nodes) {
+                    LdsNodes NL;
+                    NL.p = s.S.nodes.lds_l;
+#pragma unroll
+                    for (int u = 0; u < U; u++)
+                        if (slow[u]) sum[u] = eq_cost_full(s, NL, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+                } else {
+                    AnyNodes NA;
+                    NA.n = s.S.nodes;
+#pragma unroll
+                    for (int u = 0; u < U; u++)
+                        if (slow[u]) sum[u] = eq_cost_full(s, NA, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                N[u] = (uint64_t)(c0[u] + sum[u]);
+                DA[u] = s.use_m ? (uint64_t)size[u] : 1;
+                DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
+                s.nbr += ok[u] ? ev[u] : 0;
+                s.adj += ok[u] ? (pd[u] >> 8) : 0;
+            }
+        } else {
+#pragma unroll
+            for (int u = 0; u < U; u++) {
+                if (s.cmode == CM_RAND) {
+                    const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
+                    N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
+                    DA[u] = DB[u] = 1;
+                } else {
+                    N[u] = s.cmode == CM_LOCAL ? (uint64_t)c0[u] : 1;
+                    DA[u] = s.use_m ? (uint64_t)size[u] : 1;
+                    DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < U; u++) {
+            take(best, ok[u], score_est(N[u], DA[u], DB[u]), N[u], DA[u], DB[u], id[u], (int32_t)slot[u]);
+            if (approx(HC)) scored += __popcll(__ballot(ok[u]));
+        }
+    }
+}
+
+template <int HC>
+__device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filter &F, int64_t &scored)
+{
     bool bad = false;
     Best best;
     best.sc = best.lo = best.hi = 0.0f;
@@ -1517,185 +1703,8 @@ __device__ __forceinline__ int32_t scan(Sim &s, int32_t &victim_slot, const Filt
     best.id = 0x7fffffff;
     best.slot = -1;
     best.have = 0;
-    constexpr int U = Round<HC>::value;
-    // quads of the next round when it lies in global memory, read one round
-    // ahead so that their latency overlaps this round's scoring (scans start
-    // in LDS, so every global round has been read ahead by its predecessor)
-    static_assert(POOL_LDS > 0, "the first round of a scan lies in LDS");
-    i32x4 P0[U], P1[U], PC[U][KQ];
-    if constexpr (cls(HC) == HC_WALK) {
-        walk_scan<HC>(s, F, best, scored);
-    } else {
-        for (int32_t base = 0; base < end; base += WAVE * U) {
-            int32_t id[U], pd[U];
-            uint32_t slot[U];
-            int64_t last[U], size[U], c0[U];
-            int32_t ab[U];
-            int32_t nb[U][K];
-            bool ok[U];
-            // level 1: the 16-byte quads of each slot, all issued together, from
-            // LDS or global memory (a round never straddles the two)
-            i32x4 Q0[U], Q1[U], QC[U][KQ];
-    #pragma unroll
-            for (int u = 0; u < U; u++) {
-                const int32_t i = base + u * WAVE + lane;
-                slot[u] = (uint32_t)(i < end ? i : base);
-            }
-            if (base < POOL_LDS) {
-    #pragma unroll
-                for (int u = 0; u < U; u++) {
-                    Q0[u] = L4[PQ * slot[u]];
-                    Q1[u] = L4[PQ * slot[u] + 1];
-    #pragma unroll
-                    for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
-                }
-            } else {
-    #pragma unroll
-                for (int u = 0; u < U; u++) {
-                    Q0[u] = P0[u];
-                    Q1[u] = P1[u];
-    #pragma unroll
-                    for (int k = 0; k < KQ; k++) QC[u][k] = PC[u][k];
-                }
-            }
-    #pragma unroll
-            for (int u = 0; u < U; u++) {
-                const int32_t i = base + u * WAVE + lane;
-                const i32x4 q0 = Q0[u], q1 = Q1[u];
-                id[u] = i < end ? q0.x : -1;
-                pd[u] = q0.y;
-                last[u] = (int64_t)(((uint64_t)(uint32_t)q0.w << 32) | (uint32_t)q0.z);
-                size[u] = (int64_t)(((uint64_t)(uint32_t)q1.y << 32) | (uint32_t)q1.x);
-                c0[u] = (int64_t)q1.z;
-                ab[u] = q1.w;
-    #pragma unroll
-                for (int k = 0; k < KQ; k++) {
-                    nb[u][4 * k] = QC[u][k].x;
-                    nb[u][4 * k + 1] = QC[u][k].y;
-                    nb[u][4 * k + 2] = QC[u][k].z;
-                    nb[u][4 * k + 3] = QC[u][k].w;
-                }
-                ok[u] = id[u] >= 0;
-                if (approx(HC)) {
-                    ok[u] = ok[u] && (uint64_t)size[u] >= F.min_size;
-                    if (F.sample) ok[u] = ok[u] && sample_draw(s, id[u]) < F.tau;
-                }
-            }
-            const int32_t nbase = base + WAVE * U;
-            if (nbase < end && nbase >= POOL_LDS) {
-    #pragma unroll
-                for (int u = 0; u < U; u++) {
-                    const int32_t i = nbase + u * WAVE + lane;
-                    const uint32_t ns = (uint32_t)(i < end ? i : nbase);
-                    P0[u] = G4[PQ * ns];
-                    P1[u] = G4[PQ * ns + 1];
-    #pragma unroll
-                    for (int k = 0; k < KQ; k++) PC[u][k] = cls(HC) == HC_EQ ? G4[PQ * ns + 2 + k] : 0;
-                }
-            }
-            uint64_t N[U], DA[U], DB[U];
-            if (cls(HC) == HC_EQ) {
-                const bool lds_nodes = s.uf_n <= UF_LDS;
-                // level 2: every cached node (unused entries hold node 0, the null
-                // node); level 3: its parent, so nodes one merge away resolve too
-                int64_t sum[U], ev[U];
-                bool slow[U];
-    #pragma unroll
-                for (int u = 0; u < U; u++) {
-                    const int32_t c = pd[u] & 0xFF;
-                    // roots are their own parent, so the node two hops along (n2)
-                    // is the set root whenever the cached node is at most one
-                    // merge away from it; its cost is used unconditionally
-                    bool deep = false;
-                    // cache entries at or beyond every lane's count hold the null
-                    // node (cost 0, its own root) and are skipped when the whole
-                    // wave allows it
-                    if (lds_nodes) {
-                        const LAS UfNode *NL = s.S.nodes.lds_l;
-                        if (!__ballot(c > 2)) sum[u] = cached_sum<2>(NL, nb[u], deep);
-                        else if (!__ballot(c > 4)) sum[u] = cached_sum<4>(NL, nb[u], deep);
-                        else sum[u] = cached_sum<K>(NL, nb[u], deep);
-                    } else {
-                        int32_t r[K];
-                        int64_t cost[K];
-    #pragma unroll
-                        for (int k = 0; k < K; k++) r[k] = s.S.nodes[nb[u][k]].parent;
-    #pragma unroll
-                        for (int k = 0; k < K; k++) {
-                            const UfNode n2 = s.S.nodes[r[k]];
-                            cost[k] = n2.cost;
-                            deep |= n2.parent != r[k];
-                        }
-                        int64_t t = 0;
-    #pragma unroll
-                        for (int k = 0; k < K; k++) {
-                            bool dup = false;
-    #pragma unroll
-                            for (int j = 0; j < k; j++) dup |= r[j] == r[k];
-                            t += dup ? 0 : cost[k];
-                        }
-                        sum[u] = t;
-                    }
-                    ev[u] = c;
-                    slow[u] = ok[u] && (c > K || deep);
-                }
-                // rare: overflowed cache or a merged-away node -- exact recount
-                bool any_slow = false;
-    #pragma unroll
-                for (int u = 0; u < U; u++) any_slow |= slow[u];
-    #ifdef DTR_PROFILE
-                {
-                    int32_t ns = 0;
-    #pragma unroll
-                    for (int u = 0; u < U; u++) ns += slow[u] ? 1 : 0;
-                    s.prof_slow += ns;     // per lane; reduced at the end
-                    for (int u = 0; u < U; u++) s.prof_global_nodes += ok[u] && (pd[u] & 0xFF) > K ? 1 : 0;
-                }
-    #endif
-                if (__ballot(any_slow)) {
-                    if (lds_nodes) {
-                        LdsNodes NL;
-                        NL.p = s.S.nodes.lds_l;
-    #pragma unroll
-                        for (int u = 0; u < U; u++)
-                            if (slow[u]) sum[u] = eq_cost_full(s, NL, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
-                    } else {
-                        AnyNodes NA;
-                        NA.n = s.S.nodes;
-    #pragma unroll
-                        for (int u = 0; u < U; u++)
-                            if (slow[u]) sum[u] = eq_cost_full(s, NA, ab[u], ab[u] + (pd[u] >> 8), ev[u], bad);
-                    }
-                }
-    #pragma unroll
-                for (int u = 0; u < U; u++) {
-                    N[u] = (uint64_t)(c0[u] + sum[u]);
-                    DA[u] = s.use_m ? (uint64_t)size[u] : 1;
-                    DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
-                    s.nbr += ok[u] ? ev[u] : 0;
-                    s.adj += ok[u] ? (pd[u] >> 8) : 0;
-                }
-            } else {
-    #pragma unroll
-                for (int u = 0; u < U; u++) {
-                    if (s.cmode == CM_RAND) {
-                        const uint64_t key = ((uint64_t)s.evict_no << 32) + (uint64_t)(uint32_t)id[u];
-                        N[u] = mix64(s.seed + 0x9E3779B97F4A7C15ull * key);
-                        DA[u] = DB[u] = 1;
-                    } else {
-                        N[u] = s.cmode == CM_LOCAL ? (uint64_t)c0[u] : 1;
-                        DA[u] = s.use_m ? (uint64_t)size[u] : 1;
-                        DB[u] = s.use_s ? (uint64_t)(T - last[u]) : 1;
-                    }
-                }
-            }
-    #pragma unroll
-            for (int u = 0; u < U; u++) {
-                take(best, ok[u], score_est(N[u], DA[u], DB[u]), N[u], DA[u], DB[u], id[u], (int32_t)slot[u]);
-                if (approx(HC)) scored += __popcll(__ballot(ok[u]));
-            }
-        }
-    }
+    if constexpr (cls(HC) == HC_WALK) walk_scan<HC>(s, F, best, scored);
+    else scan_rounds<HC>(s, F, best, scored, bad);
     if (__ballot(bad)) { set_status(s, ST_CAPACITY); return -1; }
     // cross-lane minimum: the smallest estimate bounds the winner; only the
     // lanes within the filter margin of it (usually one) are compared exactly
@@ -2126,14 +2135,15 @@ __device__ __forceinline__ bool release(Sim &s, int32_t o)
 }
 
 template <int HC>
-__device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const Slot &S, int32_t lane, LAS WalkCtl *ctl)
+__device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const Slot &S, int32_t lane, LAS WalkCtl *ctl,
+                                       int32_t nw)
 {
     Sim s;
     const SpecDev sp = a.specs[sim];
     s.t = a.traces[sp.trace];
     s.S = S;
     s.trace_idx = sp.trace;
-    s.nw = cls(HC) == HC_WALK ? (int32_t)a.L.walk_waves : 1;
+    s.nw = nw;
     s.ctl = ctl;
     s.h = sp.heuristic;
     s.policy = sp.policy;
@@ -2261,19 +2271,51 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     }
 }
 
-// One simulation per workgroup at a time, taken from the work counter.  The
-// workgroups of the walk heuristics may hold helper wavefronts (a.L.walk_waves
-// in all) that join the simulating wavefront's walk scans; every wavefront
-// learns the next simulation from the control block after a workgroup
-// barrier, so all of them leave the loop together.
+// The exact h_DTR^eq kernel: every wavefront takes simulations from the work
+// counter on its own, in its own slot and LDS arrays, with no workgroup
+// barrier (four to a workgroup: LDS is allocated per workgroup, so one
+// allocation serves four simulations).
 template <int HC>
-__global__ void __launch_bounds__(cls(HC) == HC_WALK ? MAX_WALK_WAVES * WAVE : WAVE) replay_kernel(KernelArgs a)
+__device__ __forceinline__ void eq_waves(const KernelArgs &a, UfNode *lds_nodes, PoolSlot *lds_pool, int32_t lane,
+                                         int32_t wave)
 {
-    // union-find nodes (h_DTR^eq), or the walk control block (walk heuristics)
-    __shared__ UfNode lds_nodes[cls(HC) == HC_EQ ? UF_LDS : (sizeof(WalkCtl) + sizeof(UfNode) - 1) / sizeof(UfNode)];
-    __shared__ PoolSlot lds_pool[POOL_LDS];
+    const int32_t slot = (int32_t)blockIdx.x * lds_waves(HC) + wave;
+    if (slot >= a.n_slots) return;
+    Slot S = slot_at(a, slot);
+    S.nodes.lds = lds_nodes + wave * UF_LDS;
+    S.nodes.lds_l = (LAS UfNode *)lds_nodes + wave * UF_LDS;
+    S.lpool = lds_pool + wave * POOL_LDS;
+    S.lpool_l = (LAS PoolSlot *)lds_pool + wave * POOL_LDS;
+    for (;;) {
+        uint32_t k = 0;
+        if (lane == 0) k = atomicAdd(a.queue, 1u);
+        k = (uint32_t)uni((int32_t)k);
+        if (k >= (uint32_t)a.n_sims) break;
+        run_sim<HC>(a, a.order[k], S, lane, nullptr, 1);
+    }
+}
+
+// One simulation per workgroup at a time, taken from the work counter (the
+// exact h_DTR^eq kernel: one per wavefront, as above).  The workgroups of the
+// walk heuristics may hold helper wavefronts (a.L.walk_waves in all) that
+// join the simulating wavefront's walk scans; every wavefront learns the next
+// simulation from the control block after a workgroup barrier, so all of them
+// leave the loop together.
+template <int HC>
+__global__ void __launch_bounds__(cls(HC) == HC_WALK ? MAX_WALK_WAVES * WAVE : lds_waves(HC) * WAVE)
+    __attribute__((amdgpu_waves_per_eu(2))) replay_kernel(KernelArgs a)
+{
+    constexpr int LW = lds_waves(HC);
+    // union-find nodes (h_DTR^eq: one array per wavefront), or the walk
+    // control block (walk heuristics)
+    __shared__ UfNode lds_nodes[cls(HC) == HC_EQ ? UF_LDS * LW : CTL_NODES];
+    __shared__ PoolSlot lds_pool[POOL_LDS * LW];
     const int32_t lane = (int32_t)threadIdx.x & (WAVE - 1);
     const int32_t wave = uni((int32_t)threadIdx.x / WAVE);
+    if constexpr (LW > 1) {
+        eq_waves<HC>(a, lds_nodes, lds_pool, lane, wave);
+        return;
+    }
     const int32_t nw = cls(HC) == HC_WALK ? (int32_t)a.L.walk_waves : 1;
     Slot S = slot_at(a, blockIdx.x);
     S.nodes.lds = lds_nodes;
@@ -2302,10 +2344,10 @@ __global__ void __launch_bounds__(cls(HC) == HC_WALK ? MAX_WALK_WAVES * WAVE : W
         }
         if (k >= (uint32_t)a.n_sims) break;
         if constexpr (cls(HC) == HC_WALK) {
-            if (wave == 0) run_sim<HC>(a, a.order[k], S, lane, ctl);
+            if (wave == 0) run_sim<HC>(a, a.order[k], S, lane, ctl, nw);
             else help_walks<HC>(a, S, lane, wave, ctl);
         } else {
-            run_sim<HC>(a, a.order[k], S, lane, ctl);
+            run_sim<HC>(a, a.order[k], S, lane, ctl, 1);
         }
     }
 }
@@ -2364,8 +2406,10 @@ extern "C" hipError_t dtr_launch_group(const dtr::KernelArgs *a, int32_t group, 
     using namespace dtr;
     if (a->n_sims <= 0) return hipSuccess;
     const dim3 grid(a->n_slots), blk(WAVE), wblk(WAVE * (uint32_t)a->L.walk_waves);
+    // the exact h_DTR^eq kernel: EQ_WAVES slots per workgroup
+    const dim3 egrid((a->n_slots + EQ_WAVES - 1) / EQ_WAVES), eblk(WAVE * EQ_WAVES);
     switch (group) {
-    case 0: hipLaunchKernelGGL(replay_kernel<HC_EQ>, grid, blk, 0, stream, *a); break;
+    case 0: hipLaunchKernelGGL(replay_kernel<HC_EQ>, egrid, eblk, 0, stream, *a); break;
     case 1: hipLaunchKernelGGL(replay_kernel<HC_WALK>, grid, wblk, 0, stream, *a); break;
     case 2: hipLaunchKernelGGL(replay_kernel<HC_SIMPLE>, grid, blk, 0, stream, *a); break;
     case 3: hipLaunchKernelGGL(replay_kernel<HC_EQ | HC_APPROX>, grid, blk, 0, stream, *a); break;

@@ -248,3 +248,4 @@ def test_static_scratch_option_limits():
     with pytest.raises(D.DtrError) as e:
         D.dtr_sim_workspace_bytes([big], sp, {"slots": 0, "flags": D.OPT_STATIC_SCRATCH})
     assert e.value.code == D.DTR_EINVAL and "static scratch" in str(e.value)
+

@@ -424,3 +424,49 @@ def test_walk_workgroup_shapes(gpu, oracle_lib, waves, small):
     if small:
         assert int(ref["n_nbr_visits"].max()) > 0
     compare(gpu.run(traces, specs, flags=flags), ref, specs, f"walk {waves} waves small={small}")
+
+
+_EQ_BATCH = {}
+
+
+def _eq_batch(oracle_lib):
+    """TreeLSTM traces at tight budgets (pools of several rounds), the ResNet
+    trace, wide operators (overflowed neighbour caches) and random programs,
+    under h_DTR^eq and the union-find members of the h' family; the oracle's
+    results computed once."""
+    if not _EQ_BATCH:
+        tl = W.make_config("treelstm4096", n_trees=24)
+        rn = W.make_config("resnet50blk")
+        traces, rows = list(tl.traces), []
+        for k in range(tl.n_sims):
+            t, h, b, seed = (int(v) for v in tuple(tl.specs[k])[:4])
+            rows.append((t, h, b, seed))
+        traces.append(rn.traces[0])
+        for k in range(0, 256, 37):
+            rows.append((len(traces) - 1, W.H_EQ, int(rn.specs["budget"][k]), 0))
+        for tr in _wide_programs()[:6]:
+            traces.append(tr)
+            peak = W.natural_peak(tr)
+            for frac in (0.3, 0.6):
+                rows.append((len(traces) - 1, W.H_EQ, max(1, int(peak * frac)), 0))
+        for s in range(12):
+            tr = W.random_program(3300 + s, n_ops=40 + (s * 37) % 200, n_const=s % 3, backward=True,
+                                  max_in=1 + s % 5, max_size=1 + s % 30, max_cost=1 + s % 9)
+            traces.append(tr)
+            peak = W.natural_peak(tr)
+            for h in (W.H_EQ, W.h_family(W.C_EQCLASS, 1, 0), W.h_family(W.C_EQCLASS, 0, 1),
+                      W.h_family(W.C_EQCLASS, 0, 0)):
+                rows.append((len(traces) - 1, h, max(1, int(peak * 0.35)), s))
+        specs = specs_of(rows)
+        _EQ_BATCH.update(traces=traces, specs=specs, ref=oracle_lib.run(traces, specs))
+    return _EQ_BATCH["traces"], _EQ_BATCH["specs"], _EQ_BATCH["ref"]
+
+
+@pytest.mark.parametrize("slots", [1, 5, 0])
+def test_eq_wavefront_slots(gpu, oracle_lib, slots):
+    """The exact h_DTR^eq kernel runs a simulation per wavefront, four
+    wavefronts (slots) to a workgroup: one slot, five (a workgroup with one
+    slot used and three idle wavefronts) and the default count."""
+    traces, specs, ref = _eq_batch(oracle_lib)
+    print(f"h_DTR^eq batch, slots={slots}: {len(specs)} sims", flush=True)
+    compare(gpu.run(traces, specs, slots=slots), ref, specs, f"eq slots={slots}")
