@@ -10,6 +10,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, f) for f in ("dtr_sim.cpp", "dtr_log.cpp", "replay.hip", "replay_log.hip")]
 OUT = os.path.join(HERE, "libdtrsim.so")
+# the same sources with the in-kernel cycle timers (profile.py); never the product
+OUT_PROFILE = os.path.join(HERE, "libdtrsim_prof.so")
 ARCH = "gfx950"
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
@@ -18,9 +20,10 @@ FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
          "-I", os.path.join(ROOT, "include")]
 
 
-def build(verbose: bool = False) -> str:
-    tmp = OUT + ".tmp"
-    cmd = ["hipcc", *FLAGS, "-o", tmp, *SOURCES]
+def build(verbose: bool = False, profile: bool = False) -> str:
+    out = OUT_PROFILE if profile else OUT
+    tmp = out + ".tmp"
+    cmd = ["hipcc", *FLAGS, *(["-DDTR_PROFILE"] if profile else []), "-o", tmp, *SOURCES]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -29,8 +32,8 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("hipcc failed:\n" + "\n".join(noise))
     if verbose and noise:
         print("\n".join(noise), file=sys.stderr)
-    os.replace(tmp, OUT)
-    return OUT
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
