@@ -14,6 +14,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <map>
 #include <numeric>
 #include <string>
 #include <vector>
@@ -349,16 +350,36 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     p.n_slots = (int32_t)std::max<int64_t>(1, slots);
 
     // grouped by heuristic class (one kernel specialisation each), then the
-    // likely heaviest first: the tightest budget relative to the trace's
-    // no-eviction peak (in steps of 1/1024 of the peak, so that budgets set
-    // at one fraction of their traces' peaks tie), then the longest trace,
-    // then the exact ratio
+    // Likely heaviest first: each trace's tightest simulation (budget relative
+    // to the trace's no-eviction peak, in steps of 1/1024 of the peak, so
+    // that budgets set at one fraction of their traces' peaks tie) before the
+    // rest, those by tightness, then the longest trace, then the exact ratio;
+    // then the rest trace by trace (longest first), each trace's tightest
+    // first, so that the simulations of one trace run side by side and share
+    // its tables in the caches.
     auto cls = [&](int32_t i) { return heuristic_class(sims[i].heuristic) + (sims[i].search ? 3 : 0); };
+    auto bucket = [&](int32_t i) {
+        const uint64_t pk = (uint64_t)std::max<int64_t>(1, p.traces[sims[i].trace].peak);
+        return (unsigned __int128)(uint64_t)sims[i].budget * 1024u / pk;
+    };
+    std::map<std::pair<int32_t, int32_t>, unsigned __int128> tightest;     // (trace, group) -> bucket
+    for (int32_t i = 0; i < n_sims; i++) {
+        const auto key = std::make_pair(sims[i].trace, cls(i));
+        const auto it = tightest.find(key);
+        if (it == tightest.end() || bucket(i) < it->second) tightest[key] = bucket(i);
+    }
+    std::vector<uint8_t> first(n_sims);
+    for (int32_t i = 0; i < n_sims; i++) first[i] = bucket(i) == tightest[std::make_pair(sims[i].trace, cls(i))];
     p.order.resize(n_sims);
     std::iota(p.order.begin(), p.order.end(), 0);
     std::stable_sort(p.order.begin(), p.order.end(), [&](int32_t a, int32_t b) {
         if (cls(a) != cls(b)) return cls(a) < cls(b);
+        if (first[a] != first[b]) return first[a] > first[b];
         const Derived &ta = p.traces[sims[a].trace], &tb = p.traces[sims[b].trace];
+        if (!first[a]) {
+            if (ta.F != tb.F) return ta.F > tb.F;
+            if (sims[a].trace != sims[b].trace) return sims[a].trace < sims[b].trace;
+        }
         const uint64_t pa = (uint64_t)std::max<int64_t>(1, ta.peak), pb = (uint64_t)std::max<int64_t>(1, tb.peak);
         const unsigned __int128 qa = (unsigned __int128)(uint64_t)sims[a].budget * 1024u / pa;
         const unsigned __int128 qb = (unsigned __int128)(uint64_t)sims[b].budget * 1024u / pb;
