@@ -64,7 +64,8 @@ def scan_bytes(specs, res) -> int:
 # (FETCH_SIZE, WRITE_SIZE) and scaled by the same counters on a plain device
 # copy of known size; valid only for the kernel sources it was measured on.
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "replay_kernel_eq_treelstm4096_traffic.md")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_2006_09616_amd", "csrc", f) for f in ("replay.hip", "layout.h")]
+# (the host library too: its dispatch order decides which simulations share the caches)
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2006_09616_amd", "csrc", f) for f in ("replay.hip", "layout.h", "dtr_sim.cpp")]
 
 
 def kernel_source_digest() -> str:
