@@ -236,6 +236,16 @@ int dtr_sim_run_static(dtr_sim *sim, void *stream);
  * the stream of the last run.  DTR_ESTATE if no run was enqueued. */
 int dtr_sim_results(dtr_sim *sim, dtr_sim_result *host_out, int32_t n_sims);
 
+/* Progress of the handle's last trace run, which may still be in flight:
+ * the operations executed so far by its simulations under the e*-walking
+ * heuristics (h_DTR, h_{e*}, h_MSPS and the h' members with c = e*), each
+ * simulation counted in whole steps of 4096 operations (a lower bound; the
+ * other heuristics and operator logs count 0).  It reads a device counter on
+ * a stream of the handle's own (created at the first call), so it returns
+ * without waiting for the run; for progress reports of long runs.
+ * DTR_EINVAL for a NULL argument; *ops_done = 0 before any run. */
+int dtr_sim_progress(dtr_sim *sim, int64_t *ops_done);
+
 /* ---- operator logs (Appendix C.6) ------------------------------------------
  * A log is a sequence of instructions over integer names 0..n_names-1, as
  * parallel arrays (one entry per instruction):

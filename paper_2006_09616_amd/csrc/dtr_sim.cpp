@@ -434,6 +434,8 @@ struct dtr_sim {
     // the caller's stream by events, so that the groups overlap
     hipStream_t aux[dtr::N_GROUPS] = {};
     hipEvent_t fork = nullptr, join[dtr::N_GROUPS] = {};
+    uint32_t *last_queue = nullptr;       // counter block of the last trace run
+    hipStream_t progress_stream = nullptr;  // dtr_sim_progress's reads
     ~dtr_sim()
     {
         dtrhost::log_plan_free(log);
@@ -442,6 +444,7 @@ struct dtr_sim {
             if (join[g]) (void)hipEventDestroy(join[g]);
         }
         if (fork) (void)hipEventDestroy(fork);
+        if (progress_stream) (void)hipStreamDestroy(progress_stream);
     }
 };
 
@@ -596,6 +599,7 @@ int launch_traces(dtr_sim *h, void *stream, uint8_t *slots, uint32_t *queue, int
         a[c].order = (const int32_t *)(h->ws + p.order_off) + first;
         a[c].results = (dtr::ResultDev *)(h->ws + p.result_off);
         a[c].queue = queue + c;
+        a[c].progress = (unsigned long long *)((uint8_t *)queue + dtr::PROGRESS_OFFSET);
         a[c].slots = slots + (size_t)off * (size_t)p.L.bytes;
         a[c].L = p.L;
         a[c].n_sims = p.class_count[c];
@@ -620,6 +624,7 @@ int launch_traces(dtr_sim *h, void *stream, uint8_t *slots, uint32_t *queue, int
     if (e != hipSuccess) return fail(DTR_EHIP, "kernel launch failed: %s", hipGetErrorString(e));
     h->ran = true;
     h->last_stream = st;
+    h->last_queue = queue;
     return DTR_OK;
 }
 
@@ -675,6 +680,25 @@ int dtr_sim_results(dtr_sim *h, dtr_sim_result *host_out, int32_t n_sims)
                        hipMemcpyDeviceToHost, h->last_stream) != hipSuccess ||
         hipStreamSynchronize(h->last_stream) != hipSuccess)
         return fail(DTR_EHIP, "result copy failed");
+    return DTR_OK;
+}
+
+int dtr_sim_progress(dtr_sim *h, int64_t *ops_done)
+{
+    g_err.clear();
+    if (!h || !ops_done) return fail(DTR_EINVAL, "null handle or output");
+    *ops_done = 0;
+    if (h->log || !h->last_queue) return DTR_OK;
+    if (!h->progress_stream && hipStreamCreateWithFlags(&h->progress_stream, hipStreamNonBlocking) != hipSuccess) {
+        h->progress_stream = nullptr;
+        return fail(DTR_EHIP, "stream creation failed");
+    }
+    unsigned long long v = 0;
+    if (hipMemcpyAsync(&v, (uint8_t *)h->last_queue + dtr::PROGRESS_OFFSET, sizeof v, hipMemcpyDeviceToHost,
+                       h->progress_stream) != hipSuccess ||
+        hipStreamSynchronize(h->progress_stream) != hipSuccess)
+        return fail(DTR_EHIP, "progress read failed");
+    *ops_done = (int64_t)v;
     return DTR_OK;
 }
 

@@ -171,6 +171,11 @@ struct __attribute__((aligned(16))) UfNode {
 // (union-find neighbourhood, neighbourhood walk, none), plus 3 with the
 // search approximations on
 constexpr int N_GROUPS = 6;
+// work-counter block at the head of the working memory: one 32-bit counter
+// per group, then (at byte PROGRESS_OFFSET) the 64-bit progress counter
+constexpr int PROGRESS_OFFSET = 32;
+constexpr int COUNTER_WORDS = PROGRESS_OFFSET / 4 + 2;
+constexpr int PROGRESS_STEP = 4096;
 
 struct KernelArgs {
     const TraceDev *traces;
@@ -178,6 +183,7 @@ struct KernelArgs {
     const int32_t *order;    // sims, longest first
     ResultDev *results;
     uint32_t *queue;         // work counter, zeroed before each run
+    unsigned long long *progress;   // walk heuristics' executed operations, in steps of PROGRESS_STEP
     uint8_t *slots;
     SlotLayout L;
     int32_t n_sims;

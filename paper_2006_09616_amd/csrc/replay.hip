@@ -233,6 +233,7 @@ struct Sim {
     int32_t nw;                   // wavefronts in the workgroup (walk heuristics)
     int32_t trace_idx;
     LAS struct WalkCtl *ctl;      // their control block in LDS
+    unsigned long long *progress; // the launch's progress counter (walk heuristics)
     int64_t evict_no;
     int64_t total, base, remat_cost, executed, remats, evictions, eager, scores;
     int64_t nbr, adj;     // per-lane partial sums, reduced at the end
@@ -1886,6 +1887,8 @@ __device__ __forceinline__ bool execute(Sim &s, int32_t t, const TRec &rt, bool 
     s.T += c;
     s.total += c;
     s.executed++;
+    if (cls(HC) == HC_WALK && (s.executed & (PROGRESS_STEP - 1)) == 0 && s.lane == 0)
+        atomicAdd(s.progress, (unsigned long long)PROGRESS_STEP);
     if (remat) { s.remats++; s.remat_cost += c; }
     else s.base += c;
     s.mem += rt.size;
@@ -2143,6 +2146,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
     s.t = a.traces[sp.trace];
     s.S = S;
     s.trace_idx = sp.trace;
+    s.progress = a.progress;
     s.nw = nw;
     s.ctl = ctl;
     s.h = sp.heuristic;
@@ -2397,7 +2401,7 @@ extern "C" hipError_t dtr_static_scratch(void **ptr, size_t *bytes)
 extern "C" hipError_t dtr_launch_reset(uint32_t *queue, hipStream_t stream)
 {
     using namespace dtr;
-    hipLaunchKernelGGL(reset_kernel, dim3(1), dim3(WAVE), 0, stream, queue, N_GROUPS);
+    hipLaunchKernelGGL(reset_kernel, dim3(1), dim3(WAVE), 0, stream, queue, COUNTER_WORDS);
     return hipGetLastError();
 }
 

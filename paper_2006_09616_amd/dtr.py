@@ -70,6 +70,7 @@ def lib():
         L.dtr_sim_run.argtypes = [vp, vp]
         L.dtr_sim_run_static.argtypes = [vp, vp]
         L.dtr_sim_results.argtypes = [vp, vp, i32]
+        L.dtr_sim_progress.argtypes = [vp, C.POINTER(C.c_int64)]
         L.dtr_sim_launch_info.argtypes = [vp, vp]
         L.dtr_sim_destroy.argtypes = [vp]
         L.dtr_sim_destroy.restype = None
@@ -77,7 +78,7 @@ def lib():
         L.dtr_log_workspace_bytes.argtypes = [vp, i32, vp, i32, vp, C.POINTER(sz)]
         L.dtr_log_create.argtypes = [vp, i32, vp, i32, vp, vp, sz, vp, C.POINTER(vp)]
         for f in ("dtr_sim_workspace_bytes", "dtr_sim_create", "dtr_sim_run", "dtr_sim_run_static", "dtr_sim_results",
-                  "dtr_sim_launch_info", "dtr_log_workspace_bytes", "dtr_log_create"):
+                  "dtr_sim_progress", "dtr_sim_launch_info", "dtr_log_workspace_bytes", "dtr_log_create"):
             getattr(L, f).restype = C.c_int
         _lib = L
     return _lib
@@ -189,6 +190,12 @@ def dtr_sim_results(handle: int, n_sims: int) -> np.ndarray:
     return out
 
 
+def dtr_sim_progress(handle: int) -> int:
+    v = C.c_int64(0)
+    _check(lib().dtr_sim_progress(C.c_void_p(handle), C.byref(v)))
+    return int(v.value)
+
+
 class _LaunchInfo(C.Structure):
     _fields_ = [("n_slots", C.c_int32), ("waves_per_group", C.c_int32), ("lds_bytes", C.c_int32),
                 ("reserved", C.c_int32)]
@@ -244,6 +251,16 @@ class Simulator:
     def results(self) -> np.ndarray:
         with self.torch.cuda.device(self.device):
             return dtr_sim_results(self.handle, self.n_sims)
+
+    def progress(self) -> int:
+        """Operations executed so far by the last run's walk-heuristic
+        simulations, in steps of 4096 each (dtr_sim_progress; no wait)."""
+        with self.torch.cuda.device(self.device):
+            return dtr_sim_progress(self.handle)
+
+    def done(self) -> bool:
+        """Whether the work enqueued on the handle's stream has finished."""
+        return bool(self.stream.query())
 
     def launch_info(self) -> dict:
         """Resident slots, waves per workgroup and dynamic LDS bytes."""

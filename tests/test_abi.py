@@ -249,3 +249,10 @@ def test_static_scratch_option_limits():
         D.dtr_sim_workspace_bytes([big], sp, {"slots": 0, "flags": D.OPT_STATIC_SCRATCH})
     assert e.value.code == D.DTR_EINVAL and "static scratch" in str(e.value)
 
+
+def test_progress_null_arguments():
+    """dtr_sim_progress rejects a NULL handle or output without device work."""
+    L = D.lib()
+    v = C.c_int64(7)
+    assert L.dtr_sim_progress(None, C.byref(v)) == D.DTR_EINVAL
+    assert L.dtr_sim_progress(None, None) == D.DTR_EINVAL
