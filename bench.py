@@ -366,9 +366,20 @@ def main():
     sim = D.Simulator(None if log else wl.traces, wl.specs, device="cuda:0", slots=args.slots,
                       logs=wl.traces if log else None)
     stream = sim.stream
+    def wait(label):
+        # a launch that lasts minutes reports the operations its walk
+        # simulations have executed so far (dtr_sim_progress) while it runs
+        t = time.perf_counter()
+        while not log and not sim.done():
+            time.sleep(0.05 if time.perf_counter() - t < 30 else 20)
+            if time.perf_counter() - t >= 30:
+                print(f"[bench] {label}: {time.perf_counter() - t:.0f} s, {sim.progress()} operations executed",
+                      file=sys.stderr, flush=True)
+        torch.cuda.synchronize()
+
     for i in range(args.warmup):
         sim.run()
-        torch.cuda.synchronize()
+        wait(f"warmup {i + 1}")
         print(f"[bench] warmup {i + 1}/{args.warmup} done", file=sys.stderr, flush=True)
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
     ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -378,7 +389,7 @@ def main():
         starts[i].record(stream)
         sim.run()
         ends[i].record(stream)
-    torch.cuda.synchronize()
+    wait("timed steps")
     wall = time.perf_counter() - w0
     launch_ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
     res = sim.results()
@@ -389,6 +400,15 @@ def main():
     achieved = nbytes / avg_s / 1e9
     print(f"[bench] {args.steps} steps, kernel avg {avg_s * 1e3:.2f} ms, wall {wall:.3f}s",
           file=sys.stderr, flush=True)
+
+    golden = None
+    if wl.name.startswith("randdag") and os.path.exists(RANDDAG_GOLDEN):
+        # the stored oracle results at 9 of the batch's budgets
+        g = json.load(open(RANDDAG_GOLDEN))
+        if g["trace_sha256"] == wl.traces[0].digest() and g["n_budgets"] == wl.n_sims:
+            ok = sum(all(int(res[f][r["index"]]) == v for f, v in r["result"].items()) for r in g["sims"])
+            golden = f"{ok}/{len(g['sims'])} bit-exact against the stored oracle results"
+            print(f"[bench] stored oracle results: {golden}", file=sys.stderr, flush=True)
 
     cpu = None
     if args.cpu_sample > 0:
@@ -434,6 +454,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "configs": configs,
+        **({"parity_stored": golden} if golden else {}),
     }
     print(json.dumps(out))
     sim.close()
