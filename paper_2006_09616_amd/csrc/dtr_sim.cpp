@@ -335,8 +335,9 @@ int make_plan(const dtr_trace *traces, int32_t n_traces, const dtr_sim_spec *sim
     int32_t cus = 0;
     int rc = device_cus(&cus);
     if (rc) return rc;
-    // 16 one-wave workgroups per compute unit; a batch of walk heuristics
-    // alone needs no more slots than its larger workgroups can occupy
+    // 16 slots per compute unit (at least as many as any kernel keeps
+    // resident: 8 under h_DTR^eq, one per wavefront); a batch of walk
+    // heuristics alone needs no more slots than its larger workgroups occupy
     const bool walk_only = need_walk && !need_uf && [&] {
         for (int32_t i = 0; i < n_sims; i++)
             if (heuristic_class(sims[i].heuristic) != 1) return false;
