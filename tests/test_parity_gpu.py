@@ -186,11 +186,15 @@ def test_treelstm_subset(gpu, oracle_lib):
 
 
 def test_determinism_across_slot_counts(gpu):
+    """The mixed ResNet batch (three kernel groups): with 2 slots the groups
+    run one after another over both, with 7 or more side by side on streams
+    of their own over disjoint slots; the results are the same."""
     w = W.make_config("resnet50blk")
     a = gpu.run(w.traces, w.specs, slots=7)
     b = gpu.run(w.traces, w.specs, slots=1000)
     c = gpu.run(w.traces, w.specs)
-    assert a.tobytes() == b.tobytes() == c.tobytes()
+    d = gpu.run(w.traces, w.specs, slots=2)
+    assert a.tobytes() == b.tobytes() == c.tobytes() == d.tobytes()
 
 
 def test_determinism_under_shuffled_order(gpu):
@@ -280,6 +284,9 @@ def test_progress_counter(gpu):
     walk = np.isin(specs["heuristic"], [W.H_DTR, W.H_ESTAR, W.H_MSPS])
     expect = int((res["n_executed_ops"][walk] // 4096 * 4096).sum())
     assert expect > 0
+    assert sim.progress() == expect
+    sim.run_static()                    # the counter of the static working memory
+    assert sim.results().tobytes() == res.tobytes()
     assert sim.progress() == expect
     sim.close()
 
