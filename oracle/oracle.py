@@ -28,7 +28,14 @@ UNCOMPUTED, RESIDENT, EVICTED, BANISHED = 0, 1, 2, 3
 
 
 def build(force: bool = False) -> str:
-    """Compile the oracle with gcc (plain C11, pthreads)."""
+    """Compile the oracle with gcc (plain C11, pthreads).
+
+    ``DTR_ORACLE_LIB`` names another build of the same interface to load
+    instead (the mutation test runs the pins against deliberately broken
+    copies of the source this way)."""
+    other = os.environ.get("DTR_ORACLE_LIB")
+    if other:
+        return other
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < os.path.getmtime(SRC):
         tmp = LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-fPIC", "-shared",
