@@ -113,10 +113,10 @@ constexpr int NB_CACHE = 8;
 // union-find node ids below UF_LDS live in LDS (16 bytes each per wavefront),
 // the rest in the slot's global node array
 constexpr int UF_LDS = 512;
-// pool slots below POOL_LDS live in LDS (64 bytes each per wavefront), the
-// rest in the slot's global pool array (which keeps the same indices); with
-// 16 KB of LDS per h_DTR^eq wavefront a compute unit holds as many of them as
-// its registers allow (two per SIMD)
+// pool slots below POOL_LDS live in LDS (64 bytes each, padded to 80, per
+// wavefront), the rest in the slot's global pool array (which keeps the same
+// indices); with 18 KB of LDS per h_DTR^eq wavefront a compute unit holds as
+// many of them as its registers allow (two per SIMD)
 constexpr int POOL_LDS = 128;
 // wavefronts per workgroup of the exact h_DTR^eq kernel, each running its own
 // simulations with its own LDS arrays

@@ -161,13 +161,20 @@ struct NodeStore {
     }
 };
 
+// LDS pool slots are padded to 80 bytes, so the 16-byte reads of 64
+// consecutive slots fall in distinct bank groups
+constexpr int PQL = PQ + 1;
+struct __attribute__((aligned(16))) PoolSlotL {
+    PoolSlot s;
+    i32x4 pad;
+};
 // Evictable pool: slots below POOL_LDS in this wavefront's LDS array, the
 // rest in the slot's global array (same indices).
 struct Slot {
     GAS uint64_t *tst;
     GAS int32_t *lockx;           // lock counts >= LOCKS_SAT
-    PoolSlot *lpool;              // flat view of the LDS head
-    LAS PoolSlot *lpool_l;
+    PoolSlotL *lpool;             // flat view of the LDS head
+    LAS PoolSlotL *lpool_l;
     GAS PoolSlot *gpool;
     NodeStore nodes;
     GAS int32_t *remap;
@@ -182,7 +189,7 @@ struct Slot {
     int32_t vis_words, vis_bytes, wq_cap;
     __device__ __forceinline__ PoolSlot &pool(int32_t i) const
     {
-        return i < POOL_LDS ? lpool[i] : *(PoolSlot *)(gpool + i);
+        return i < POOL_LDS ? lpool[i].s : *(PoolSlot *)(gpool + i);
     }
 };
 
@@ -1091,7 +1098,7 @@ __device__ void walk_lanes(const TraceDev &t, const Slot &S, GAS uint64_t *tst, 
         if (i < (uint32_t)P.end) {
             i32x4 q0, q1, h0, h1;
             if (i < (uint32_t)POOL_LDS) {
-                const LAS i32x4 *PS = (const LAS i32x4 *)S.lpool_l + PQ * i;
+                const LAS i32x4 *PS = (const LAS i32x4 *)S.lpool_l + PQL * i;
                 q0 = PS[0]; q1 = PS[1]; h0 = PS[2]; h1 = PS[3];
             } else {
                 const GAS i32x4 *PS = (const GAS i32x4 *)S.gpool + PQ * (size_t)i;
@@ -1540,10 +1547,10 @@ __device__ __forceinline__ void scan_rounds(Sim &s, const Filter &F, Best &best,
         if (base < POOL_LDS) {
 #pragma unroll
             for (int u = 0; u < U; u++) {
-                Q0[u] = L4[PQ * slot[u]];
-                Q1[u] = L4[PQ * slot[u] + 1];
+                Q0[u] = L4[PQL * slot[u]];
+                Q1[u] = L4[PQL * slot[u] + 1];
 #pragma unroll
-                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQ * slot[u] + 2 + k] : 0;
+                for (int k = 0; k < KQ; k++) QC[u][k] = cls(HC) == HC_EQ ? L4[PQL * slot[u] + 2 + k] : 0;
             }
         } else {
 #pragma unroll
@@ -2280,7 +2287,7 @@ __device__ __forceinline__ void run_sim(const KernelArgs &a, int32_t sim, const 
 // barrier (four to a workgroup: LDS is allocated per workgroup, so one
 // allocation serves four simulations).
 template <int HC>
-__device__ __forceinline__ void eq_waves(const KernelArgs &a, UfNode *lds_nodes, PoolSlot *lds_pool, int32_t lane,
+__device__ __forceinline__ void eq_waves(const KernelArgs &a, UfNode *lds_nodes, PoolSlotL *lds_pool, int32_t lane,
                                          int32_t wave)
 {
     const int32_t slot = (int32_t)blockIdx.x * lds_waves(HC) + wave;
@@ -2289,7 +2296,7 @@ __device__ __forceinline__ void eq_waves(const KernelArgs &a, UfNode *lds_nodes,
     S.nodes.lds = lds_nodes + wave * UF_LDS;
     S.nodes.lds_l = (LAS UfNode *)lds_nodes + wave * UF_LDS;
     S.lpool = lds_pool + wave * POOL_LDS;
-    S.lpool_l = (LAS PoolSlot *)lds_pool + wave * POOL_LDS;
+    S.lpool_l = (LAS PoolSlotL *)lds_pool + wave * POOL_LDS;
     for (;;) {
         uint32_t k = 0;
         if (lane == 0) k = atomicAdd(a.queue, 1u);
@@ -2313,7 +2320,7 @@ __global__ void __launch_bounds__(cls(HC) == HC_WALK ? MAX_WALK_WAVES * WAVE : l
     // union-find nodes (h_DTR^eq: one array per wavefront), or the walk
     // control block (walk heuristics)
     __shared__ UfNode lds_nodes[cls(HC) == HC_EQ ? UF_LDS * LW : CTL_NODES];
-    __shared__ PoolSlot lds_pool[POOL_LDS * LW];
+    __shared__ PoolSlotL lds_pool[POOL_LDS * LW];
     const int32_t lane = (int32_t)threadIdx.x & (WAVE - 1);
     const int32_t wave = uni((int32_t)threadIdx.x / WAVE);
     if constexpr (LW > 1) {
@@ -2325,7 +2332,7 @@ __global__ void __launch_bounds__(cls(HC) == HC_WALK ? MAX_WALK_WAVES * WAVE : l
     S.nodes.lds = lds_nodes;
     S.nodes.lds_l = (LAS UfNode *)lds_nodes;
     S.lpool = lds_pool;
-    S.lpool_l = (LAS PoolSlot *)lds_pool;
+    S.lpool_l = (LAS PoolSlotL *)lds_pool;
     LAS WalkCtl *ctl = (LAS WalkCtl *)lds_nodes;
     if (cls(HC) == HC_WALK) {
         // visited bitmaps start clear (every walk clears what it set)
