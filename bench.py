@@ -219,22 +219,39 @@ def is_log(wl) -> bool:
     return isinstance(wl.traces[0], W.Log)
 
 
-def cpu_baseline(wl, gpu_res, sample_every: int, threads: int):
-    """The oracle, as it stands, on every sample_every-th simulation."""
+def ordinal(n: int) -> str:
+    """1st, 2nd, 3rd, 4th, ..., 11th, 12th, 13th, ..., 21st, 61st."""
+    suffix = "th" if 10 <= n % 100 <= 20 else {1: "st", 2: "nd", 3: "rd"}.get(n % 10, "th")
+    return f"{n}{suffix}"
+
+
+def cpu_baseline(wl, gpu_res, sample_every: int, threads: int, single_every: int = 29):
+    """The oracle, as it stands, on every sample_every-th simulation, and its
+    single-core rate on every single_every-th of those (29 keeps the stride
+    coprime to the 8 budgets per tree whenever sample_every is)."""
     from oracle import oracle as O
+    run = O.run_log if is_log(wl) else O.run
     idx = np.arange(0, wl.n_sims, sample_every)
     specs = wl.specs[idx]
     t0 = time.perf_counter()
-    ref = (O.run_log if is_log(wl) else O.run)(wl.traces, specs, threads=threads)
+    ref = run(wl.traces, specs, threads=threads)
     dt = time.perf_counter() - t0
     ops = int(ref["n_executed_ops"].sum())
     scores = int(ref["n_scores"].sum())
     match = sum(all(int(gpu_res[f][i]) == int(ref[f][k]) for f in O.RESULT_FIELDS)
                 for k, i in enumerate(idx))
-    return dict(value=ops / dt, unit="simulated tensor ops/s", cores=threads, nproc=os.cpu_count(), kind="oracle",
-                sample=f"every {sample_every}th simulation ({len(idx)} of {wl.n_sims}), "
-                       f"{dt:.2f} s wall on {threads} threads",
-                scores_per_s=scores / dt, parity_sample=f"{match}/{len(idx)}")
+    out = dict(value=ops / dt, unit="simulated tensor ops/s", cores=threads, nproc=os.cpu_count(), kind="oracle",
+               sample=f"every {ordinal(sample_every)} simulation ({len(idx)} of {wl.n_sims}), "
+                      f"{dt:.2f} s wall on {threads} threads",
+               scores_per_s=scores / dt, parity_sample=f"{match}/{len(idx)}")
+    idx1 = idx[::single_every]
+    t0 = time.perf_counter()
+    ref1 = run(wl.traces, wl.specs[idx1], threads=1)
+    dt1 = max(time.perf_counter() - t0, 1e-9)
+    out["single_thread"] = dict(value=int(ref1["n_executed_ops"].sum()) / dt1, unit="simulated tensor ops/s",
+                                sample=f"every {ordinal(sample_every * single_every)} simulation ({len(idx1)} of "
+                                       f"{wl.n_sims}), {dt1:.2f} s on 1 thread")
+    return out
 
 
 RANDDAG_GOLDEN = os.path.join(ROOT, "tests", "golden", "randdag100k_oracle.json")

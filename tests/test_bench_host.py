@@ -48,3 +48,22 @@ def test_measured_traffic_is_gated_on_the_kernel_sources(monkeypatch):
 def test_union_find_heuristics_are_recognised():
     uf = [h for h in list(range(8)) + list(range(16, 32)) if bench._union_find(h)]
     assert uf == [W.H_EQ] + [W.h_family(W.C_EQCLASS, s, m) for s in (0, 1) for m in (0, 1)]
+
+
+def test_cpu_baseline_reports_both_rates_and_parity(oracle_lib):
+    wl = W.make_config("chain32")
+    ref = oracle_lib.run(wl.traces, wl.specs, threads=1)
+    cpu = bench.cpu_baseline(wl, ref, 1, 2, single_every=2)
+    assert cpu["kind"] == "oracle" and cpu["cores"] == 2
+    assert cpu["parity_sample"] == f"{wl.n_sims}/{wl.n_sims}"
+    assert cpu["value"] > 0 and cpu["single_thread"]["value"] > 0
+    assert "1 thread" in cpu["single_thread"]["sample"]
+    # a planted difference in the GPU side's results is counted
+    bad = ref.copy()
+    bad["total_cost"][0] += 1
+    assert bench.cpu_baseline(wl, bad, 1, 2)["parity_sample"] == f"{wl.n_sims - 1}/{wl.n_sims}"
+
+
+def test_ordinals():
+    assert [bench.ordinal(n) for n in (1, 2, 3, 4, 11, 12, 13, 21, 61, 111, 1769)] == \
+        ["1st", "2nd", "3rd", "4th", "11th", "12th", "13th", "21st", "61st", "111th", "1769th"]
